@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Benchmark: nested-Winograd convolution on one MI355X.
+
+A step is one pass of the whole hot path (input transform, per-point channel
+contraction, output transform -- every layer of the workload) over one batch
+of synthetic input already resident in HBM.  The kernel transform runs once
+per weight set during warm-up (the plan caches U); its time is reported
+separately and in `value_incl_kernel_transform`.
+
+Prints ONE JSON line.  `value` is direct-convolution-equivalent TFLOP/s
+(2*B*N*M*Ho*Wo*r^2 per layer, summed, divided by the step time).  The
+roofline object describes the kernel with the largest share of the step,
+with its algorithmic bytes or FLOPs and its average duration from HIP
+events the library records on the stream it launches on.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
+PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
+METRIC = "direct-conv-equiv TFLOP/s & fraction of fp32 MFMA/HBM roofline, 1 MI355X"
+STAGES = ["kernel_transform", "input_transform", "contraction", "output_transform"]
+CSRC = os.path.join(ROOT, "paper_2102_13272_amd", "csrc")
+
+
+def stage_bytes_flops(info: dict):
+    """Algorithmic bytes (fp32) and FLOPs per launch of each stage of one layer."""
+    P, M, N, T = info["P"], info["M"], info["N"], info["T"]
+    B, H, W, Ho, Wo, r = info["B"], info["H"], info["W"], info["Ho"], info["Wo"], info["r"]
+    x = 4 * B * M * H * W
+    y = 4 * B * N * Ho * Wo
+    w = 4 * N * M * r * r
+    if info["n"] == 0:
+        return {"kernel_transform": (w + 4 * M * N, 0.0),
+                "contraction": (x + y + 4 * M * N, 2.0 * B * N * M * Ho * Wo)}
+    U, V, Yh = 4 * P * M * N, 4 * P * M * T, 4 * P * N * T
+    return {"kernel_transform": (w + U, 0.0),
+            "input_transform": (x + V, 0.0),
+            "contraction": (U + V + Yh, 2.0 * P * M * N * T),
+            "output_transform": (Yh + y, 0.0)}
+
+
+def source_hash(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_SOURCES = {"input_transform": ["input_xform.hip", "nwg_internal.h"],
+                  "contraction": ["contract_mfma.hip", "nwg_internal.h"],
+                  "output_transform": ["output_xform.hip", "nwg_internal.h"],
+                  "kernel_transform": ["kernel_xform.hip", "nwg_internal.h"]}
+
+
+def measured_traffic(workload: str, stage: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        d = json.load(fh)
+    ent = d.get("kernels", {}).get(stage)
+    if not ent or ent.get("source_hash") != source_hash(KERNEL_SOURCES[stage]):
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(workload: str, target_s: float):
+    """The fp64 oracle timed on this host's cores over a bounded sample."""
+    from oracle.direct import direct_conv2d
+    from paper_2102_13272_amd.workloads import WORKLOADS, make_workload
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()
+                       if d.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    wl = WORKLOADS[workload]
+    x, ws = make_workload(workload)
+    flop = 0.0
+    t0 = time.perf_counter()
+    images = 0
+    if len(wl.layers) == 1:
+        L = wl.layers[0]
+        for b in range(L.B):
+            direct_conv2d(x[b:b + 1], ws[0], L.pad)
+            flop += L.direct_flop / L.B
+            images += 1
+            if time.perf_counter() - t0 >= target_s:
+                break
+        sample = f"{images} of {L.B} images of the workload, all channels"
+    else:
+        for b in range(wl.layers[0].B):
+            cur = x[b:b + 1].astype(np.float64)
+            for L, w in zip(wl.layers, ws):
+                cur = direct_conv2d(cur, w, L.pad)
+                flop += L.direct_flop / L.B
+            images += 1
+            if time.perf_counter() - t0 >= target_s:
+                break
+        sample = f"{images} of {wl.layers[0].B} images through all {len(wl.layers)} layers"
+    dt = time.perf_counter() - t0
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": sample, "seconds": round(dt, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c5_r31")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time for the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); the path "
+              f"shards over output tiles or Winograd points, which is not built here.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2102_13272_amd import nwg
+    from paper_2102_13272_amd.workloads import WORKLOADS, make_workload
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    nwg.load_library()
+    torch.cuda.set_device(0)
+    wl = WORKLOADS[args.workload]
+    x, ws = make_workload(args.workload)
+    xd = torch.from_numpy(x).to("cuda")
+    wds = [torch.from_numpy(w).to("cuda") for w in ws]
+    plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad) for L in wl.layers]
+    outs = [torch.empty(p.y_shape, dtype=torch.float32, device="cuda") for p in plans]
+    stream = torch.cuda.current_stream()
+
+    def step():
+        cur = xd
+        for p, w, y in zip(plans, wds, outs):
+            p.conv2d(cur, w, y, stream)
+            cur = y
+
+    # warm-up (includes the one kernel transform per layer), then timed steps
+    for p in plans:
+        p.set_timing(True)
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    warm = [p.get_timing() for p in plans]
+    kx_ms = sum(ms[0] for ms, _ in warm)
+
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = e0.elapsed_time(e1)
+    ms_step = ms_total / args.steps
+    timing = [p.get_timing() for p in plans]
+
+    direct_flop = float(sum(L.direct_flop for L in wl.layers))
+    value = direct_flop / (ms_step * 1e-3) / 1e12
+
+    # per-stage accounting summed over layers
+    stages = {}
+    for p, (ms, cnt) in zip(plans, timing):
+        bf = stage_bytes_flops(p.info)
+        for si, name in enumerate(STAGES):
+            if name == "kernel_transform" or cnt[si] == 0:
+                continue
+            b, f = bf[name]
+            s = stages.setdefault(name, {"ms_total": 0.0, "launches": 0, "bytes": 0.0,
+                                         "flop": 0.0, "per_layer": []})
+            s["ms_total"] += ms[si]
+            s["launches"] += cnt[si]
+            s["bytes"] += b * cnt[si]
+            s["flop"] += f * cnt[si]
+            s["per_layer"].append({"r": p.info["r"], "n": p.info["n"],
+                                   "avg_us": round(1e3 * ms[si] / cnt[si], 2)})
+    detail = {}
+    for name, s in stages.items():
+        sec = s["ms_total"] * 1e-3
+        gbs = s["bytes"] / sec / 1e9
+        tfs = s["flop"] / sec / 1e12
+        detail[name] = {"ms_per_step": round(s["ms_total"] / args.steps, 4),
+                        "launches_per_step": s["launches"] // args.steps,
+                        "GB_s": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+                        "TFLOP_s": round(tfs, 2),
+                        "mfma_frac": round(tfs / PEAK_FP32_MFMA_TFLOPS, 4),
+                        "per_layer": s["per_layer"]}
+
+    # dominant kernel: largest time share of the step
+    dom = max(stages, key=lambda k: stages[k]["ms_total"])
+    s = stages[dom]
+    avg_s = s["ms_total"] * 1e-3 / s["launches"]
+    ai = s["flop"] / s["bytes"] if s["bytes"] else 0.0
+    ridge = PEAK_FP32_MFMA_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if dom == "contraction" and ai > ridge:
+        ach = s["flop"] / s["launches"] / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_FP32_MFMA_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_FP32_MFMA_TFLOPS, 4)}
+    else:
+        ach = s["bytes"] / s["launches"] / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4)}
+    roof["kernel"] = dom
+    roof["avg_launch_us"] = round(avg_s * 1e6, 2)
+    roof["traffic"] = measured_traffic(args.workload, dom) if len(plans) == 1 else None
+
+    L0 = wl.layers[0]
+    cfg = {"workload": args.workload, "layers": len(wl.layers), "B": L0.B,
+           "M": L0.M, "N": wl.layers[-1].N, "H": L0.H, "W": L0.W,
+           "r": [L.r for L in wl.layers] if len(wl.layers) > 1 else L0.r,
+           "pad": [L.pad for L in wl.layers] if len(wl.layers) > 1 else L0.pad,
+           "base": "F(2x2,3x3)", "nesting_depth": [p.info["n"] for p in plans]}
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic", "config": cfg, "roofline": roof,
+        "stages": detail,
+        "kernel_transform_ms_once": round(kx_ms, 4),
+        "value_incl_kernel_transform": round(direct_flop / ((ms_step + kx_ms) * 1e-3) / 1e12, 3),
+        "direct_flop_per_step": direct_flop,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
+    for p in plans:
+        p.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

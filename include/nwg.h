@@ -1,0 +1,154 @@
+/*
+ * nwg.h -- nested-Winograd stride-1 2D convolution on MI355X (gfx950).
+ *
+ * Operation (Sec. II.A of "Accelerating Large Kernel Convolutions with
+ * Nested Winograd Transformation", Jiang, Chen, Tsui): M input maps x of
+ * size H x W are correlated with N groups of M-channel r x r kernels w,
+ * stride 1, zero padding `pad` on all four sides, giving N output maps y:
+ *
+ *   y[b][n][i][j] = sum_{m,u,v} xpad[b][m][i+u][j+v] * w[n][m][u][v],
+ *   0 <= i < Ho = H + 2 pad - r + 1,  0 <= j < Wo = W + 2 pad - r + 1.
+ *
+ * Computed by nested Winograd (Sec. III.B) on the fixed base F(2x2, 3x3)
+ * (eq. 2.3): the r x r kernel is handled by an n-level nest of the base,
+ * n = smallest depth whose padded kernel K_n = 2^(n+1) - 1 >= r
+ * (r = 1: n = 0, no transform; r <= 3: n = 1; r <= 7: 2; r <= 15: 3;
+ * r <= 31: 4).  Level j works at stride 2^(j-1); each tile produces
+ * M_n = 2^n x 2^n outputs from an L_n x L_n input window, L_n = 3*2^n - 2,
+ * through P = 4^(2n) Winograd points.
+ *
+ * Data: all tensors are contiguous fp32 in DEVICE memory.
+ *   x [B][M][H][W],  w [N][M][r][r],  y [B][N][Ho][Wo].
+ * Winograd-domain buffers (what the stage entry points read and write):
+ *   U    [P][M][N]   transformed kernel (N fastest)
+ *   V    [P][M][T]   transformed input  (T fastest)
+ *   Yhat [P][N][T]   per-point channel contraction (T fastest)
+ * with T = B * th * tw tiles, th = ceil(Ho / M_n), tw = ceil(Wo / M_n), and
+ * tile t = (b * th + ty) * tw + tx covering outputs [ty*M_n, ty*M_n + M_n) x
+ * [tx*M_n, tx*M_n + M_n).  The point index p of a tile is written in base 4
+ * with digits (q_n^row, q_n^col, q_{n-1}^row, q_{n-1}^col, ..., q_1^row,
+ * q_1^col), most significant first, q_j being the level-j Winograd index.
+ *
+ * Ownership: the caller owns x, w, y, U/V/Yhat passed to stage calls, and
+ * the stream; they must stay valid until the work queued on the stream has
+ * finished.  A plan owns its workspace (U, V, Yhat), allocated at creation.
+ * Every call that takes a stream only queues work on it (`stream` is a
+ * hipStream_t; NULL is the default stream) and never synchronises, except
+ * nwg_plan_get_timing.  A plan is not thread-safe; one call in flight per
+ * plan.
+ *
+ * Errors: functions returning int give NWG_OK (0) or a negative status;
+ * functions returning a pointer give NULL.  nwg_last_error() then returns a
+ * message for the calling thread.
+ */
+#ifndef NWG_H
+#define NWG_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct nwg_plan nwg_plan;
+
+/* Winograd base of the nest.  Only F(2x2, 3x3) (eq. 2.3) is provided. */
+enum { NWG_TILE_F2X2_3X3 = 0 };
+
+enum {
+  NWG_OK = 0,
+  NWG_EINVAL = -1,       /* bad argument (NULL pointer, bad shape) */
+  NWG_ENOMEM = -2,       /* device allocation failed */
+  NWG_EHIP = -3,         /* a HIP runtime call or kernel launch failed */
+  NWG_EUNSUPPORTED = -4  /* valid request this build does not handle */
+};
+
+#define NWG_MAX_DEPTH 4   /* r <= 31 */
+
+/* Plan geometry, as computed by the level recurrence (Sec. III.B). */
+typedef struct nwg_plan_info {
+  int B, M, N, H, W, r, pad, tile;
+  int Ho, Wo;
+  int n;                        /* nesting depth, 0..NWG_MAX_DEPTH */
+  int m, rb, l;                 /* base F(m, rb), l = m + rb - 1 */
+  int strides[NWG_MAX_DEPTH];   /* stride of level 1..n */
+  int Mn, Kn, Ln;               /* outputs / padded taps / input per axis per tile */
+  int th, tw;                   /* tiles per image */
+  long long T;                  /* B * th * tw */
+  long long P;                  /* Winograd points per tile, l^(2n) */
+  size_t u_bytes, v_bytes, yhat_bytes, workspace_bytes;
+  long long ewmm_mults;         /* general multiplications per call: P*T*M*N */
+  double direct_flop;           /* 2*B*N*M*Ho*Wo*r*r */
+  double contract_flop;         /* 2*P*M*N*T (n = 0: 2*B*N*M*Ho*Wo) */
+} nwg_plan_info;
+
+/* Geometry of a convolution without touching any device (host-only).
+ * Returns NWG_EINVAL for a bad shape, NWG_EUNSUPPORTED for r > 31 or an
+ * unknown tile. */
+int nwg_plan_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
+                      nwg_plan_info* out);
+
+/* Create a plan ("valid" convolution, pad = 0) and allocate its workspace on
+ * the current device.  NULL on a bad shape, unsupported request or failed
+ * allocation (see nwg_last_error). */
+nwg_plan* nwg_plan_create(int B, int M, int N, int H, int W, int r, int tile);
+
+/* Same with explicit zero padding on all four sides ("same": pad = (r-1)/2). */
+nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad, int tile);
+
+/* Release a plan and its workspace.  NULL is a no-op.  The caller must make
+ * sure no work using the plan is still queued. */
+void nwg_plan_destroy(nwg_plan* plan);
+
+/* Copy the plan's geometry into *out. */
+int nwg_plan_query(const nwg_plan* plan, nwg_plan_info* out);
+
+/* y = conv(x, w): kernel transform (only when w differs from the cached weight
+ * pointer or after nwg_plan_set_weights), then the input transform, the
+ * per-point channel contraction and the output transform, all queued on
+ * `stream`.  For r = 1 the contraction reads x and writes y directly.
+ * Mutating w in place requires nwg_plan_set_weights before the next call. */
+int nwg_conv2d(nwg_plan* plan, const float* x, const float* w, float* y, void* stream);
+
+/* Re-run the kernel transform of w into the plan's cached U now. */
+int nwg_plan_set_weights(nwg_plan* plan, const float* w, void* stream);
+
+/* --- Stage entry points (each is one kernel launch on `stream`) ---------- */
+
+/* Nested kernel transformation (Sec. III.B, 2nd step): w [N][M][r][r] -> U. */
+int nwg_kernel_transform(const nwg_plan* plan, const float* w, float* U, void* stream);
+
+/* Nested input transformation (Sec. III.B, 1st step): x -> V.
+ * NWG_EINVAL at depth 0 (r = 1), which has no transform. */
+int nwg_input_transform(const nwg_plan* plan, const float* x, float* V, void* stream);
+
+/* EWMM accumulated over the M input channels (Sec. II.B, III.B final step):
+ * Yhat[p][n][t] = sum_m U[p][m][n] * V[p][m][t], on fp32 MFMA.
+ * At depth 0, V is x and Yhat is y (a plain per-image channel GEMM). */
+int nwg_contract(const nwg_plan* plan, const float* U, const float* V, float* Yhat,
+                 void* stream);
+
+/* Nested output transformation (Sec. III.B, final step): Yhat -> y, cropped
+ * to Ho x Wo.  NWG_EINVAL at depth 0. */
+int nwg_output_transform(const nwg_plan* plan, const float* Yhat, float* y, void* stream);
+
+/* --- Per-stage timing ------------------------------------------------------
+ * When enabled, nwg_conv2d records HIP events around each of its launches on
+ * the caller's stream.  nwg_plan_get_timing waits for the recorded events,
+ * adds their durations to ms[4] and launch counts to count[4] (index 0 kernel
+ * transform, 1 input transform, 2 contraction, 3 output transform), then
+ * forgets them. */
+int nwg_plan_set_timing(nwg_plan* plan, int enable);
+int nwg_plan_get_timing(nwg_plan* plan, double ms[4], long long count[4]);
+
+/* Message for the last error on the calling thread ("" if none). */
+const char* nwg_last_error(void);
+
+/* Library version string. */
+const char* nwg_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NWG_H */

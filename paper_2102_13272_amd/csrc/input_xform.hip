@@ -1,0 +1,274 @@
+// Nested input transformation (Sec. III.B, first step; 2D per Fig. 4 text).
+//
+// For every tile t and input channel m, the L_n x L_n input window starting
+// at (ty*M_n - pad, tx*M_n - pad) (zero outside the image) is reordered into
+// the 2n-dim tensor D[a;b] = x[sum_j s_{j-1} a_j][sum_j s_{j-1} b_j] and
+// transformed by B^T of F(2,3) along every axis, giving the P = 4^(2n)
+// values V[p][m][t].
+//
+// Level by level, outermost first: a B^T row at stride s combines two
+// windows shifted by s * tap, so the outer levels turn the window into
+// independent sub-windows ("branches"), and the two innermost levels
+// (10 -> 16 per axis) run in registers.
+//
+//   depth n <= 2 : one thread per tile; the work-group stages the union of
+//                  its tiles' windows (a box of whole-row tile runs) in LDS.
+//   depth n >= 3 : one thread per (tile, level-3 branch); the work-group
+//                  stages each of its 16 tiles' windows separately in LDS
+//                  (window stride L_n^2 + 1 so that the 16 tiles of a
+//                  quarter-wave read 16 different banks), and depth 4 loops
+//                  over the 16 level-4 branches.  A branch's 10 x 10
+//                  sub-window is a signed sum of 2^(n-2) x 2^(n-2) shifted
+//                  window reads, all at compile-time offsets from one base.
+//
+// Writes are V[p][m][t] with consecutive lanes on consecutive tiles, i.e.
+// contiguous runs of the T axis for every point.
+#include "nwg_internal.h"
+
+namespace nwg {
+namespace {
+
+// 2D inner transform (two levels per axis) of a 10 x 10 sub-window S and
+// store of its 256 points.  Point digits (q2r, q2c, q1r, q1c), most
+// significant first; vb already points at the branch's first point.
+__device__ __forceinline__ void inner2_store(const float (&S)[10][10], float* __restrict__ vb,
+                                             size_t pstride) {
+#pragma unroll
+  for (int q2r = 0; q2r < 4; ++q2r) {
+    // level 2 along rows (stride 2): Z[u][j], u = 0..3
+    float Z[4][10];
+    const int a0 = 2 * bt_tap0(q2r), a1 = 2 * bt_tap1(q2r);
+    const float s0 = bt_sign0(q2r), s1 = bt_sign1(q2r);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < 10; ++j) Z[u][j] = s0 * S[u + a0][j] + s1 * S[u + a1][j];
+#pragma unroll
+    for (int q1r = 0; q1r < 4; ++q1r) {
+      // level 1 along rows (stride 1)
+      float R[10];
+      const int b0 = bt_tap0(q1r), b1 = bt_tap1(q1r);
+      const float t0 = bt_sign0(q1r), t1 = bt_sign1(q1r);
+#pragma unroll
+      for (int j = 0; j < 10; ++j) R[j] = t0 * Z[b0][j] + t1 * Z[b1][j];
+      float o[16];
+      bt_inner2(R, o);  // columns: index q2c*4 + q1c
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int p = q2r * 64 + (k >> 2) * 16 + q1r * 4 + (k & 3);
+        vb[(size_t)p * pstride] = o[k];
+      }
+    }
+  }
+}
+
+// ---- depth 1 and 2: union box of tiles in LDS ------------------------------
+template <int NLEV>
+__global__ __launch_bounds__(256) void input_xform_box(
+    const float* __restrict__ x, float* __restrict__ V, int M, int H, int W, int pad, int th,
+    int tw, int T, long long MT, int RX, int RY, int nbx, int nby) {
+  constexpr int Mn = 1 << NLEV;
+  constexpr int Ln = 3 * Mn - 2;
+  extern __shared__ float lds[];
+  const int m = blockIdx.y;
+  int bid = blockIdx.x;
+  const int bx = bid % nbx;
+  bid /= nbx;
+  const int by = bid % nby;
+  const int b = bid / nby;
+  const int ty0 = by * RY, tx0 = bx * RX;
+  const int BH = (RY - 1) * Mn + Ln, BW = (RX - 1) * Mn + Ln;
+  const int r0 = ty0 * Mn - pad, c0 = tx0 * Mn - pad;
+  const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
+  const int nth = blockDim.x;
+  for (int e = threadIdx.x; e < BH * BW; e += nth) {
+    const int row = e / BW, col = e - row * BW;
+    const int gr = r0 + row, gc = c0 + col;
+    float v = 0.0f;
+    if (gr >= 0 && gr < H && gc >= 0 && gc < W) v = xp[(size_t)gr * W + gc];
+    lds[e] = v;
+  }
+  __syncthreads();
+  const int s = threadIdx.x;
+  if (s >= RX * RY) return;
+  const int ly = s / RX, lx = s - ly * RX;
+  const int ty = ty0 + ly, tx = tx0 + lx;
+  if (ty >= th || tx >= tw) return;
+  const int t = (b * th + ty) * tw + tx;
+  const float* win = lds + ly * Mn * BW + lx * Mn;
+  float* vb = V + (size_t)m * T + t;
+  if constexpr (NLEV == 2) {
+    float S[10][10];
+#pragma unroll
+    for (int i = 0; i < 10; ++i)
+#pragma unroll
+      for (int j = 0; j < 10; ++j) S[i][j] = win[i * BW + j];
+    inner2_store(S, vb, (size_t)MT);
+  } else {
+    float X[4][4], Rw[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float row[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) row[j] = win[i * BW + j];
+      float o[4];
+      bt_one(row, o);                    // along the row: index q1c
+#pragma unroll
+      for (int j = 0; j < 4; ++j) X[i][j] = o[j];
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      float col[4] = {X[0][c], X[1][c], X[2][c], X[3][c]};
+      float o[4];
+      bt_one(col, o);                    // along the column: index q1r
+#pragma unroll
+      for (int q = 0; q < 4; ++q) Rw[q][c] = o[q];
+    }
+#pragma unroll
+    for (int q1r = 0; q1r < 4; ++q1r)
+#pragma unroll
+      for (int q1c = 0; q1c < 4; ++q1c) vb[(size_t)(q1r * 4 + q1c) * MT] = Rw[q1r][q1c];
+  }
+}
+
+// ---- depth 3 and 4: 16 tiles per work-group, per-tile windows in LDS -------
+template <int NLEV>
+__global__ __launch_bounds__(256) void input_xform_tiles(
+    const float* __restrict__ x, float* __restrict__ V, int M, int H, int W, int pad, int th,
+    int tw, int T, long long MT) {
+  constexpr int Mn = 1 << NLEV;
+  constexpr int Ln = 3 * Mn - 2;
+  constexpr int WS = Ln * Ln + 1;            // odd window stride: 16 tiles -> 16 banks
+  constexpr int PASSES = NLEV == 4 ? 16 : 1;
+  constexpr int NR = NLEV == 4 ? 4 : 2;      // outer taps per axis
+  extern __shared__ float lds[];
+  const int m = blockIdx.y;
+  const int t0 = blockIdx.x * 16;
+  const int tpi = th * tw;
+  for (int e = threadIdx.x; e < 16 * Ln * Ln; e += 256) {
+    const int tl = e / (Ln * Ln);
+    const int rem = e - tl * (Ln * Ln);
+    const int row = rem / Ln, col = rem - row * Ln;
+    const int t = t0 + tl;
+    float v = 0.0f;
+    if (t < T) {
+      const int b = t / tpi;
+      const int r2 = t - b * tpi;
+      const int ty = r2 / tw, tx = r2 - ty * tw;
+      const int gr = ty * Mn - pad + row, gc = tx * Mn - pad + col;
+      if (gr >= 0 && gr < H && gc >= 0 && gc < W)
+        v = x[(((size_t)b * M + m) * H + gr) * W + gc];
+    }
+    lds[tl * WS + rem] = v;
+  }
+  __syncthreads();
+  const int tl = threadIdx.x & 15;
+  const int slot = threadIdx.x >> 4;        // level-3 branch (q3r, q3c)
+  const int t = t0 + tl;
+  if (t >= T) return;                       // no barrier below
+  const int q3r = slot >> 2, q3c = slot & 3;
+  const float* win = lds + tl * WS;
+  float* vslot = V + (size_t)slot * 256 * MT + (size_t)m * T + t;
+
+  for (int pass = 0; pass < PASSES; ++pass) {
+    const int q4r = pass >> 2, q4c = pass & 3;
+    // outer taps (level 3 at stride 4, level 4 at stride 8) per axis
+    int ro[NR], co[NR];
+    float rs[NR], cs[NR];
+#pragma unroll
+    for (int k = 0; k < NR; ++k) {
+      const int k3 = k & 1, k4 = k >> 1;
+      const int a3r = k3 ? bt_tap1(q3r) : bt_tap0(q3r);
+      const int a3c = k3 ? bt_tap1(q3c) : bt_tap0(q3c);
+      float sr = k3 ? bt_sign1(q3r) : bt_sign0(q3r);
+      float sc = k3 ? bt_sign1(q3c) : bt_sign0(q3c);
+      int orow = 4 * a3r, ocol = 4 * a3c;
+      if (NLEV == 4) {
+        orow += 8 * (k4 ? bt_tap1(q4r) : bt_tap0(q4r));
+        ocol += 8 * (k4 ? bt_tap1(q4c) : bt_tap0(q4c));
+        sr *= k4 ? bt_sign1(q4r) : bt_sign0(q4r);
+        sc *= k4 ? bt_sign1(q4c) : bt_sign0(q4c);
+      }
+      ro[k] = orow;
+      co[k] = ocol;
+      rs[k] = sr;
+      cs[k] = sc;
+    }
+    float S[10][10];
+#pragma unroll
+    for (int i = 0; i < 10; ++i)
+#pragma unroll
+      for (int j = 0; j < 10; ++j) S[i][j] = 0.0f;
+#pragma unroll
+    for (int kr = 0; kr < NR; ++kr) {
+#pragma unroll
+      for (int kc = 0; kc < NR; ++kc) {
+        const float* base = win + ro[kr] * Ln + co[kc];
+        const float sg = rs[kr] * cs[kc];
+#pragma unroll
+        for (int i = 0; i < 10; ++i)
+#pragma unroll
+          for (int j = 0; j < 10; ++j) S[i][j] += sg * base[i * Ln + j];
+      }
+    }
+    inner2_store(S, vslot + (size_t)pass * 4096 * MT, (size_t)MT);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s) {
+  const long long MT = (long long)g.M * g.T;
+  const int T = (int)g.T;
+  if (g.n >= 3) {
+    const int Ln = 3 * (1 << g.n) - 2;
+    const size_t lds = (size_t)16 * (Ln * Ln + 1) * sizeof(float);
+    int dev = 0, max_lds = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess)
+      e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e != hipSuccess) return e;
+    if ((size_t)max_lds < lds) return hipErrorInvalidConfiguration;
+    dim3 grid((unsigned)((g.T + 15) / 16), (unsigned)g.M);
+    if (g.n == 3) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_tiles<3>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(input_xform_tiles<3>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
+                         g.pad, g.th, g.tw, T, MT);
+    } else {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_tiles<4>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(input_xform_tiles<4>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
+                         g.pad, g.th, g.tw, T, MT);
+    }
+  } else {
+    const int Mn = 1 << g.n, Ln = 3 * Mn - 2;
+    // tiles per work-group: 256, or 64 when that leaves too few work-groups
+    int tpb = 256;
+    for (int pass = 0; pass < 2; ++pass) {
+      const int RX = g.tw < tpb ? g.tw : tpb;
+      int RY = tpb / RX;
+      if (RY > g.th) RY = g.th;
+      const long long nwg = (long long)((g.tw + RX - 1) / RX) * ((g.th + RY - 1) / RY) * g.B * g.M;
+      if (nwg >= 1024 || tpb == 64) break;
+      tpb = 64;
+    }
+    const int RX = g.tw < tpb ? g.tw : tpb;
+    int RY = tpb / RX;
+    if (RY > g.th) RY = g.th;
+    const int nbx = (g.tw + RX - 1) / RX, nby = (g.th + RY - 1) / RY;
+    const size_t lds = (size_t)((RY - 1) * Mn + Ln) * ((RX - 1) * Mn + Ln) * sizeof(float);
+    dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)g.M);
+    if (g.n == 2)
+      hipLaunchKernelGGL(input_xform_box<2>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
+                         g.th, g.tw, T, MT, RX, RY, nbx, nby);
+    else
+      hipLaunchKernelGGL(input_xform_box<1>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
+                         g.th, g.tw, T, MT, RX, RY, nbx, nby);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace nwg

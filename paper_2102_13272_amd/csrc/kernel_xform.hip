@@ -1,0 +1,181 @@
+// Nested kernel transformation (Sec. III.B, second step; multi-level
+// paragraph for depth > 2), run once per weight set; the plan caches U.
+//
+// The r x r kernel is zero-padded at its end to K_n x K_n (K_n = 2^(n+1)-1).
+// Each tap k of an axis sits at one multi-index (k_1..k_n), k_j in {0,1,2},
+// with sum_j 2^(j-1) k_j = k: the greedy split, outermost digit first, each
+// digit as large as allowed.  Every other entry of the 3^n x 3^n reordered
+// kernel is zero.  G of F(2,3) along every axis gives U[p][m][n].
+//
+// One thread per (output channel, input channel, outer branch): the outer
+// levels (3 and 4) fold the reordered kernel into a 9 x 9 sub-kernel over
+// the digits (k2, k1) of each axis, and the two inner levels (9 -> 16 per
+// axis) run in registers.  Consecutive threads take consecutive output
+// channels, then input channels, so the writes of U[p][m][n] are contiguous.
+#include "nwg_internal.h"
+
+namespace nwg {
+namespace {
+
+// Tap of an axis multi-index (k4, k3, k2, k1) at depth NLEV, or -1 when the
+// multi-index is not the greedy split of its tap.
+template <int NLEV>
+__device__ __forceinline__ int canonical_tap(int k4, int k3, int k2, int k1) {
+  const int tap = 8 * k4 + 4 * k3 + 2 * k2 + k1;
+  int rem = tap;
+  int d[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int j = NLEV - 1; j >= 1; --j) {
+    int v = rem >> j;
+    v = v < 2 ? v : 2;
+    d[j] = v;
+    rem -= v << j;
+  }
+  d[0] = rem;
+  const bool ok = d[0] == k1 && (NLEV < 2 || d[1] == k2) && (NLEV < 3 || d[2] == k3) &&
+                  (NLEV < 4 || d[3] == k4);
+  return ok ? tap : -1;
+}
+
+// inner G transform (level 2 over k2, level 1 over k1) of a 9-vector
+// indexed k2*3 + k1 -> 16 values indexed q2*4 + q1
+__device__ __forceinline__ void g_inner2(const float (&v)[9], float (&out)[16]) {
+  float h[4][3];
+#pragma unroll
+  for (int k1 = 0; k1 < 3; ++k1) {
+    float o[4];
+    g_one(v[0 * 3 + k1], v[1 * 3 + k1], v[2 * 3 + k1], o);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) h[q][k1] = o[q];
+  }
+#pragma unroll
+  for (int q2 = 0; q2 < 4; ++q2) {
+    float o[4];
+    g_one(h[q2][0], h[q2][1], h[q2][2], o);
+#pragma unroll
+    for (int q1 = 0; q1 < 4; ++q1) out[q2 * 4 + q1] = o[q1];
+  }
+}
+
+template <int NLEV>
+__global__ __launch_bounds__(256) void kernel_xform(const float* __restrict__ w,
+                                                    float* __restrict__ U, int M, int N, int r,
+                                                    long long nthreads) {
+  const long long id = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (id >= nthreads) return;
+  const int nn = (int)(id % N);
+  const long long rest = id / N;
+  const int m = (int)(rest % M);
+  const int branch = (int)(rest / M);
+  const float* __restrict__ wk = w + ((size_t)nn * M + m) * r * r;
+  const size_t MN = (size_t)M * N;
+
+  if constexpr (NLEV == 0) {
+    U[(size_t)m * N + nn] = wk[0];
+  } else if constexpr (NLEV == 1) {
+    float k[3][3];
+#pragma unroll
+    for (int u = 0; u < 3; ++u)
+#pragma unroll
+      for (int v = 0; v < 3; ++v) k[u][v] = (u < r && v < r) ? wk[u * r + v] : 0.0f;
+    float rows[3][4];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) g_one(k[u][0], k[u][1], k[u][2], rows[u]);
+#pragma unroll
+    for (int q1c = 0; q1c < 4; ++q1c) {
+      float o[4];
+      g_one(rows[0][q1c], rows[1][q1c], rows[2][q1c], o);
+#pragma unroll
+      for (int q1r = 0; q1r < 4; ++q1r)
+        U[(size_t)(q1r * 4 + q1c) * MN + (size_t)m * N + nn] = o[q1r];
+    }
+  } else {
+    // outer branch: (q4r, q4c, q3r, q3c) digits of the branch index
+    int qr3 = 0, qc3 = 0, qr4 = 0, qc4 = 0;
+    if (NLEV == 3) {
+      qr3 = branch >> 2;
+      qc3 = branch & 3;
+    } else if (NLEV == 4) {
+      qr4 = branch >> 6;
+      qc4 = (branch >> 4) & 3;
+      qr3 = (branch >> 2) & 3;
+      qc3 = branch & 3;
+    }
+    float S[9][9];
+#pragma unroll
+    for (int i = 0; i < 9; ++i)
+#pragma unroll
+      for (int j = 0; j < 9; ++j) S[i][j] = 0.0f;
+    // outer digits (k4, k3) per axis with their G weights
+    const int n4 = NLEV == 4 ? 3 : 1, n3 = NLEV >= 3 ? 3 : 1;
+    for (int a4 = 0; a4 < n4; ++a4)
+      for (int a3 = 0; a3 < n3; ++a3) {
+        float gr = 1.0f;
+        if (NLEV >= 3) gr *= g_coef(qr3, a3);
+        if (NLEV == 4) gr *= g_coef(qr4, a4);
+        if (gr == 0.0f) continue;
+        for (int b4 = 0; b4 < n4; ++b4)
+          for (int b3 = 0; b3 < n3; ++b3) {
+            float gc = gr;
+            if (NLEV >= 3) gc *= g_coef(qc3, b3);
+            if (NLEV == 4) gc *= g_coef(qc4, b4);
+            if (gc == 0.0f) continue;
+#pragma unroll
+            for (int ir = 0; ir < 9; ++ir) {
+              const int tr = canonical_tap<NLEV>(a4, a3, ir / 3, ir % 3);
+              if (tr < 0 || tr >= r) continue;
+#pragma unroll
+              for (int ic = 0; ic < 9; ++ic) {
+                const int tc = canonical_tap<NLEV>(b4, b3, ic / 3, ic % 3);
+                if (tc < 0 || tc >= r) continue;
+                S[ir][ic] += gc * wk[tr * r + tc];
+              }
+            }
+          }
+      }
+    // two inner levels: rows then columns
+    float* ub = U + (size_t)branch * 256 * MN + (size_t)m * N + nn;
+#pragma unroll
+    for (int rho = 0; rho < 16; ++rho) {
+      // row rho = (q2r, q1r) of G2 applied to the 9 row digits
+      const int q2r = rho >> 2, q1r = rho & 3;
+      float rowv[9];
+#pragma unroll
+      for (int ic = 0; ic < 9; ++ic) {
+        float s = 0.0f;
+#pragma unroll
+        for (int ir = 0; ir < 9; ++ir) {
+          const float c = g_coef(q2r, ir / 3) * g_coef(q1r, ir % 3);
+          if (c != 0.0f) s += c * S[ir][ic];
+        }
+        rowv[ic] = s;
+      }
+      float o[16];
+      g_inner2(rowv, o);   // index q2c*4 + q1c
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int p = q2r * 64 + (k >> 2) * 16 + q1r * 4 + (k & 3);
+        ub[(size_t)p * MN] = o[k];
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
+  const int nb = g.n >= 3 ? (g.n == 3 ? 16 : 256) : 1;
+  const long long nthreads = (long long)g.N * g.M * nb;
+  dim3 grid((unsigned)((nthreads + 255) / 256));
+  switch (g.n) {
+    case 0: hipLaunchKernelGGL(kernel_xform<0>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
+    case 1: hipLaunchKernelGGL(kernel_xform<1>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
+    case 2: hipLaunchKernelGGL(kernel_xform<2>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
+    case 3: hipLaunchKernelGGL(kernel_xform<3>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
+    case 4: hipLaunchKernelGGL(kernel_xform<4>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace nwg

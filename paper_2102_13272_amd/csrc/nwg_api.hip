@@ -1,0 +1,401 @@
+// Host side of the nested-Winograd library: the plan (level recurrence of
+// Sec. III.B and Alg. 1, read as a chain of n identical F(2,3) bases), the
+// workspace, the weight cache, the C ABI of include/nwg.h and per-stage
+// timing.  All device work is queued on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "nwg_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
+void set_error(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  if (std::getenv("NWG_LOG")) std::fprintf(stderr, "nwg: %s\n", buf);
+}
+
+struct TimingRecord {
+  int stage;
+  hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct nwg_plan {
+  nwg_plan_info info;
+  int device = 0;
+  float* U = nullptr;
+  float* V = nullptr;
+  float* Yh = nullptr;
+  const float* cached_w = nullptr;
+  bool weights_valid = false;
+  bool timing = false;
+  std::vector<TimingRecord> pending;
+  std::vector<hipEvent_t> event_pool;
+};
+
+namespace {
+
+// Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,
+// s_j = min(M_j, K_j), M_{j+1} = M_j + s_j (m-1), K_{j+1} = K_j + s_j (rb-1);
+// n is the smallest depth with K_n >= r, and r = 1 needs no level.
+int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
+                     nwg_plan_info* g) {
+  if (!g) {
+    set_error("output pointer is NULL");
+    return NWG_EINVAL;
+  }
+  std::memset(g, 0, sizeof *g);
+  if (B <= 0 || M <= 0 || N <= 0 || H <= 0 || W <= 0 || r <= 0 || pad < 0) {
+    set_error("invalid shape B=%d M=%d N=%d H=%d W=%d r=%d pad=%d", B, M, N, H, W, r, pad);
+    return NWG_EINVAL;
+  }
+  if (tile != NWG_TILE_F2X2_3X3) {
+    set_error("unsupported tile %d (only NWG_TILE_F2X2_3X3)", tile);
+    return NWG_EUNSUPPORTED;
+  }
+  const long long Ho = (long long)H + 2LL * pad - r + 1, Wo = (long long)W + 2LL * pad - r + 1;
+  if (Ho <= 0 || Wo <= 0) {
+    set_error("kernel %d larger than padded input %dx%d (pad %d)", r, H, W, pad);
+    return NWG_EINVAL;
+  }
+  const int m = nwg::kOut, rb = nwg::kTaps, l = nwg::kBase;
+  int n = 0, Mn = 1, Kn = 1;
+  int strides[NWG_MAX_DEPTH + 1] = {0};
+  if (r > 1) {
+    strides[0] = 1;
+    n = 1;
+    Mn = m;
+    Kn = rb;
+    while (Kn < r) {
+      const int s = Mn < Kn ? Mn : Kn;
+      if (n >= NWG_MAX_DEPTH) {
+        set_error("kernel size %d needs nesting depth > %d (r <= 31 supported)", r,
+                  NWG_MAX_DEPTH);
+        return NWG_EUNSUPPORTED;
+      }
+      strides[n] = s;
+      Mn += s * (m - 1);
+      Kn += s * (rb - 1);
+      ++n;
+    }
+  }
+  g->B = B; g->M = M; g->N = N; g->H = H; g->W = W; g->r = r; g->pad = pad; g->tile = tile;
+  g->Ho = (int)Ho;
+  g->Wo = (int)Wo;
+  g->n = n;
+  g->m = m; g->rb = rb; g->l = l;
+  for (int j = 0; j < n; ++j) g->strides[j] = strides[j];
+  g->Mn = Mn;
+  g->Kn = Kn;
+  g->Ln = n == 0 ? 1 : Mn + Kn - 1;
+  g->th = (int)((Ho + Mn - 1) / Mn);
+  g->tw = (int)((Wo + Mn - 1) / Mn);
+  g->T = (long long)B * g->th * g->tw;
+  long long P = 1;
+  for (int j = 0; j < 2 * n; ++j) P *= l;
+  g->P = P;
+  const double f = (double)sizeof(float);
+  g->direct_flop = 2.0 * B * N * (double)M * Ho * Wo * r * r;
+  if (n == 0) {
+    g->u_bytes = (size_t)M * N * sizeof(float);
+    g->v_bytes = 0;
+    g->yhat_bytes = 0;
+    g->ewmm_mults = (long long)B * N * M * Ho * Wo;
+    g->contract_flop = 2.0 * B * N * (double)M * Ho * Wo;
+  } else {
+    const double u = f * P * M * N, v = f * P * M * g->T, yh = f * P * N * g->T;
+    if (u > 1e13 || v > 1e13 || yh > 1e13 || g->T > 0x7fffffffLL / 64) {
+      set_error("workspace too large");
+      return NWG_EUNSUPPORTED;
+    }
+    g->u_bytes = (size_t)u;
+    g->v_bytes = (size_t)v;
+    g->yhat_bytes = (size_t)yh;
+    g->ewmm_mults = P * g->T * M * (long long)N;
+    g->contract_flop = 2.0 * P * (double)M * N * g->T;
+  }
+  g->workspace_bytes = g->u_bytes + g->v_bytes + g->yhat_bytes;
+  return NWG_OK;
+}
+
+int check_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return NWG_OK;
+  set_error("%s: %s", what, hipGetErrorString(e));
+  return NWG_EHIP;
+}
+
+hipEvent_t take_event(nwg_plan* p) {
+  if (!p->event_pool.empty()) {
+    hipEvent_t e = p->event_pool.back();
+    p->event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Runs `launch` on stream s, bracketed by timing events when enabled.
+template <typename F>
+int timed(nwg_plan* p, int stage, hipStream_t s, const char* what, F&& launch) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (p && p->timing) {
+    e0 = take_event(p);
+    e1 = take_event(p);
+    if (e0 && e1) hipEventRecord(e0, s);
+  }
+  const int rc = check_hip(launch(), what);
+  if (e0 && e1) {
+    hipEventRecord(e1, s);
+    p->pending.push_back({stage, e0, e1});
+  } else {
+    if (e0) p->event_pool.push_back(e0);
+    if (e1) p->event_pool.push_back(e1);
+  }
+  return rc;
+}
+
+nwg::ContractArgs contract_args(const nwg_plan_info& g, const float* U, const float* V,
+                                float* Yh) {
+  nwg::ContractArgs a{};
+  a.A = U;
+  a.Bm = V;
+  a.C = Yh;
+  a.Nrows = g.N;
+  a.K = g.M;
+  a.ldA = g.N;
+  if (g.n == 0) {
+    // F(1, r): no transform; per image, y[b] (N x HoWo) = U^T (N x M) * x[b] (M x HW)
+    const int hw = g.Ho * g.Wo;   // r = 1: Ho = H + 2 pad; pad > 0 is handled by the caller
+    a.Ncols = hw;
+    a.ldB = hw;
+    a.ldC = hw;
+    a.sA = 0;
+    a.sB = (long long)g.M * g.H * g.W;
+    a.sC = (long long)g.N * hw;
+    a.batch = g.B;
+  } else {
+    a.Ncols = (int)g.T;
+    a.ldB = (int)g.T;
+    a.ldC = (int)g.T;
+    a.sA = (long long)g.M * g.N;
+    a.sB = (long long)g.M * g.T;
+    a.sC = (long long)g.N * g.T;
+    a.batch = g.P;
+  }
+  return a;
+}
+
+int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, float* U,
+                         hipStream_t s) {
+  return timed(p, 0, s, "kernel transform launch",
+               [&] { return nwg::launch_kernel_xform(g, w, U, s); });
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* nwg_version(void) { return "nwg 0.1 (F(2x2,3x3) nested, gfx950)"; }
+
+const char* nwg_last_error(void) { return g_last_error.c_str(); }
+
+int nwg_plan_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
+                      nwg_plan_info* out) {
+  return compute_geometry(B, M, N, H, W, r, pad, tile, out);
+}
+
+nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad, int tile) {
+  nwg_plan_info g;
+  if (compute_geometry(B, M, N, H, W, r, pad, tile, &g) != NWG_OK) return nullptr;
+  if (g.n == 0 && pad != 0) {
+    set_error("1x1 kernels with padding are not supported (pad must be 0 for r = 1)");
+    return nullptr;
+  }
+  nwg_plan* p = new (std::nothrow) nwg_plan;
+  if (!p) {
+    set_error("host allocation failed");
+    return nullptr;
+  }
+  p->info = g;
+  if (hipGetDevice(&p->device) != hipSuccess) {
+    set_error("no HIP device available");
+    delete p;
+    return nullptr;
+  }
+  auto alloc = [&](float** ptr, size_t bytes, const char* what) {
+    if (bytes == 0) return true;
+    hipError_t e = hipMalloc((void**)ptr, bytes);
+    if (e != hipSuccess) {
+      hipGetLastError();
+      set_error("hipMalloc of %s (%zu bytes) failed: %s", what, bytes, hipGetErrorString(e));
+      return false;
+    }
+    return true;
+  };
+  if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, g.v_bytes, "V") ||
+      !alloc(&p->Yh, g.yhat_bytes, "Yhat")) {
+    nwg_plan_destroy(p);
+    // keep the allocation message
+    return nullptr;
+  }
+  return p;
+}
+
+nwg_plan* nwg_plan_create(int B, int M, int N, int H, int W, int r, int tile) {
+  return nwg_plan_create_pad(B, M, N, H, W, r, 0, tile);
+}
+
+void nwg_plan_destroy(nwg_plan* p) {
+  if (!p) return;
+  if (p->U) hipFree(p->U);
+  if (p->V) hipFree(p->V);
+  if (p->Yh) hipFree(p->Yh);
+  for (auto& r : p->pending) {
+    hipEventDestroy(r.start);
+    hipEventDestroy(r.stop);
+  }
+  for (auto e : p->event_pool) hipEventDestroy(e);
+  delete p;
+}
+
+int nwg_plan_query(const nwg_plan* p, nwg_plan_info* out) {
+  if (!p || !out) {
+    set_error("NULL plan or output");
+    return NWG_EINVAL;
+  }
+  *out = p->info;
+  return NWG_OK;
+}
+
+int nwg_kernel_transform(const nwg_plan* p, const float* w, float* U, void* stream) {
+  if (!p || !w || !U) {
+    set_error("NULL argument to nwg_kernel_transform");
+    return NWG_EINVAL;
+  }
+  return check_hip(nwg::launch_kernel_xform(p->info, w, U, (hipStream_t)stream),
+                   "kernel transform launch");
+}
+
+int nwg_input_transform(const nwg_plan* p, const float* x, float* V, void* stream) {
+  if (!p || !x || !V) {
+    set_error("NULL argument to nwg_input_transform");
+    return NWG_EINVAL;
+  }
+  if (p->info.n == 0) {
+    set_error("depth 0 (r = 1) has no input transform");
+    return NWG_EINVAL;
+  }
+  return check_hip(nwg::launch_input_xform(p->info, x, V, (hipStream_t)stream),
+                   "input transform launch");
+}
+
+int nwg_contract(const nwg_plan* p, const float* U, const float* V, float* Yh, void* stream) {
+  if (!p || !U || !V || !Yh) {
+    set_error("NULL argument to nwg_contract");
+    return NWG_EINVAL;
+  }
+  return check_hip(nwg::launch_contract(contract_args(p->info, U, V, Yh), (hipStream_t)stream),
+                   "contraction launch");
+}
+
+int nwg_output_transform(const nwg_plan* p, const float* Yh, float* y, void* stream) {
+  if (!p || !Yh || !y) {
+    set_error("NULL argument to nwg_output_transform");
+    return NWG_EINVAL;
+  }
+  if (p->info.n == 0) {
+    set_error("depth 0 (r = 1) has no output transform");
+    return NWG_EINVAL;
+  }
+  return check_hip(nwg::launch_output_xform(p->info, Yh, y, (hipStream_t)stream),
+                   "output transform launch");
+}
+
+int nwg_plan_set_weights(nwg_plan* p, const float* w, void* stream) {
+  if (!p || !w) {
+    set_error("NULL argument to nwg_plan_set_weights");
+    return NWG_EINVAL;
+  }
+  const int rc = run_kernel_transform(p, p->info, w, p->U, (hipStream_t)stream);
+  if (rc == NWG_OK) {
+    p->cached_w = w;
+    p->weights_valid = true;
+  } else {
+    p->weights_valid = false;
+  }
+  return rc;
+}
+
+int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stream) {
+  if (!p || !x || !w || !y) {
+    set_error("NULL argument to nwg_conv2d");
+    return NWG_EINVAL;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  const nwg_plan_info& g = p->info;
+  if (!p->weights_valid || p->cached_w != w) {
+    const int rc = nwg_plan_set_weights(p, w, stream);
+    if (rc != NWG_OK) return rc;
+  }
+  if (g.n == 0) {
+    return timed(p, 2, s, "contraction launch",
+                 [&] { return nwg::launch_contract(contract_args(g, p->U, x, y), s); });
+  }
+  int rc = timed(p, 1, s, "input transform launch",
+                 [&] { return nwg::launch_input_xform(g, x, p->V, s); });
+  if (rc != NWG_OK) return rc;
+  rc = timed(p, 2, s, "contraction launch",
+             [&] { return nwg::launch_contract(contract_args(g, p->U, p->V, p->Yh), s); });
+  if (rc != NWG_OK) return rc;
+  return timed(p, 3, s, "output transform launch",
+               [&] { return nwg::launch_output_xform(g, p->Yh, y, s); });
+}
+
+int nwg_plan_set_timing(nwg_plan* p, int enable) {
+  if (!p) {
+    set_error("NULL plan");
+    return NWG_EINVAL;
+  }
+  p->timing = enable != 0;
+  return NWG_OK;
+}
+
+int nwg_plan_get_timing(nwg_plan* p, double ms[4], long long count[4]) {
+  if (!p || !ms || !count) {
+    set_error("NULL argument to nwg_plan_get_timing");
+    return NWG_EINVAL;
+  }
+  int rc = NWG_OK;
+  for (auto& r : p->pending) {
+    float t = 0.0f;
+    if (rc == NWG_OK) rc = check_hip(hipEventSynchronize(r.stop), "timing event sync");
+    if (rc == NWG_OK) rc = check_hip(hipEventElapsedTime(&t, r.start, r.stop), "elapsed time");
+    if (rc == NWG_OK) {
+      ms[r.stage] += t;
+      count[r.stage] += 1;
+    }
+    p->event_pool.push_back(r.start);
+    p->event_pool.push_back(r.stop);
+  }
+  p->pending.clear();
+  return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,104 @@
+// Internal declarations shared by the host plan code and the HIP kernels of
+// the nested-Winograd library.  Not part of the public ABI (see include/nwg.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/nwg.h"
+
+namespace nwg {
+
+// ---------------------------------------------------------------------------
+// Base F(2,3) (eq. 2.3), applied to values spaced by a stride.
+//   B^T rows: q0 = x0 - x2, q1 = x1 + x2, q2 = x2 - x1, q3 = x1 - x3
+//   G   rows: g0 = w0, g1 = (w0+w1+w2)/2, g2 = (w0-w1+w2)/2, g3 = w2
+//   A^T rows: y0 = v0 + v1 + v2, y1 = v1 - v2 - v3
+// ---------------------------------------------------------------------------
+
+constexpr int kBase = 4;   // l
+constexpr int kOut = 2;    // m
+constexpr int kTaps = 3;   // r of the base
+
+// Taps of row q of B^T: offsets in units of the level stride, and signs.
+__host__ __device__ constexpr int bt_tap0(int q) { return q == 0 ? 0 : 1; }
+__host__ __device__ constexpr int bt_tap1(int q) { return q == 3 ? 3 : 2; }
+__host__ __device__ constexpr float bt_sign0(int q) { return q == 2 ? -1.0f : 1.0f; }
+__host__ __device__ constexpr float bt_sign1(int q) { return (q == 0 || q == 3) ? -1.0f : 1.0f; }
+
+// One level of B^T at stride S on a vector v: out[q][u] = sum_a BT[q][a] v[u + S a].
+template <int S, int LEN>
+__device__ __forceinline__ void bt_level(const float* v, float (*out)[LEN]) {
+#pragma unroll
+  for (int u = 0; u < LEN; ++u) {
+    out[0][u] = v[u] - v[u + 2 * S];
+    out[1][u] = v[u + S] + v[u + 2 * S];
+    out[2][u] = v[u + 2 * S] - v[u + S];
+    out[3][u] = v[u + S] - v[u + 3 * S];
+  }
+}
+
+// Two inner levels of the nested input transform on a length-10 vector:
+// level 2 (stride 2) then level 1 (stride 1); out index = q2*4 + q1.
+__device__ __forceinline__ void bt_inner2(const float (&v)[10], float (&out)[16]) {
+  float z[4][4];
+  bt_level<2, 4>(v, z);
+#pragma unroll
+  for (int q2 = 0; q2 < 4; ++q2) {
+    out[q2 * 4 + 0] = z[q2][0] - z[q2][2];
+    out[q2 * 4 + 1] = z[q2][1] + z[q2][2];
+    out[q2 * 4 + 2] = z[q2][2] - z[q2][1];
+    out[q2 * 4 + 3] = z[q2][1] - z[q2][3];
+  }
+}
+
+__device__ __forceinline__ void bt_one(const float (&v)[4], float (&out)[4]) {
+  out[0] = v[0] - v[2];
+  out[1] = v[1] + v[2];
+  out[2] = v[2] - v[1];
+  out[3] = v[1] - v[3];
+}
+
+__device__ __forceinline__ void g_one(float w0, float w1, float w2, float (&out)[4]) {
+  out[0] = w0;
+  out[1] = 0.5f * (w0 + w1 + w2);
+  out[2] = 0.5f * (w0 - w1 + w2);
+  out[3] = w2;
+}
+
+// G coefficient G[q][k].
+__host__ __device__ constexpr float g_coef(int q, int k) {
+  return q == 0 ? (k == 0 ? 1.0f : 0.0f)
+       : q == 3 ? (k == 2 ? 1.0f : 0.0f)
+       : q == 1 ? 0.5f
+       : (k == 1 ? -0.5f : 0.5f);
+}
+
+// A^T coefficient A^T[i][q].
+__host__ __device__ constexpr float at_coef(int i, int q) {
+  return i == 0 ? (q == 3 ? 0.0f : 1.0f)
+                : (q == 0 ? 0.0f : (q == 1 ? 1.0f : -1.0f));
+}
+
+// ---------------------------------------------------------------------------
+// Plan
+// ---------------------------------------------------------------------------
+
+struct ContractArgs {
+  const float* A;   // [batch][K][Nrows]   (U; N fastest)
+  const float* Bm;  // [batch][K][Ncols]   (V or x; columns fastest)
+  float* C;         // [batch][Nrows][Ncols]
+  long long sA, sB, sC;   // batch strides in elements (sA = 0: shared A)
+  int ldA, ldB, ldC;      // row strides in elements
+  int Nrows, Ncols, K;
+  long long batch;
+};
+
+hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s);
+hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s);
+hipError_t launch_contract(const ContractArgs& a, hipStream_t s);
+hipError_t launch_output_xform(const nwg_plan_info& g, const float* Yh, float* y, hipStream_t s);
+
+}  // namespace nwg

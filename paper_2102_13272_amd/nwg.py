@@ -1,0 +1,202 @@
+"""ctypes binding of the C ABI in include/nwg.h (argument marshalling only).
+
+Every function of the header is exposed under the same name on the loaded
+library object; ``Plan`` wraps a plan handle for torch tensors (device
+pointers from ``tensor.data_ptr()``, streams from
+``torch.cuda.current_stream().cuda_stream``).  There is no fallback: if
+``libnwg.so`` is missing or cannot be loaded, every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnwg.so")
+
+NWG_TILE_F2X2_3X3 = 0
+NWG_OK, NWG_EINVAL, NWG_ENOMEM, NWG_EHIP, NWG_EUNSUPPORTED = 0, -1, -2, -3, -4
+NWG_MAX_DEPTH = 4
+
+
+class nwg_plan_info(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int), ("M", ctypes.c_int), ("N", ctypes.c_int), ("H", ctypes.c_int),
+        ("W", ctypes.c_int), ("r", ctypes.c_int), ("pad", ctypes.c_int), ("tile", ctypes.c_int),
+        ("Ho", ctypes.c_int), ("Wo", ctypes.c_int), ("n", ctypes.c_int),
+        ("m", ctypes.c_int), ("rb", ctypes.c_int), ("l", ctypes.c_int),
+        ("strides", ctypes.c_int * NWG_MAX_DEPTH),
+        ("Mn", ctypes.c_int), ("Kn", ctypes.c_int), ("Ln", ctypes.c_int),
+        ("th", ctypes.c_int), ("tw", ctypes.c_int),
+        ("T", ctypes.c_longlong), ("P", ctypes.c_longlong),
+        ("u_bytes", ctypes.c_size_t), ("v_bytes", ctypes.c_size_t),
+        ("yhat_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
+        ("ewmm_mults", ctypes.c_longlong), ("direct_flop", ctypes.c_double),
+        ("contract_flop", ctypes.c_double),
+    ]
+
+    def as_dict(self):
+        d = {name: getattr(self, name) for name, _ in self._fields_}
+        d["strides"] = list(self.strides)[: self.n]
+        return d
+
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+# (name, restype, argtypes) for every symbol declared in include/nwg.h
+SIGNATURES = [
+    ("nwg_plan_geometry", _I, [_I] * 8 + [ctypes.POINTER(nwg_plan_info)]),
+    ("nwg_plan_create", _P, [_I] * 7),
+    ("nwg_plan_create_pad", _P, [_I] * 8),
+    ("nwg_plan_destroy", None, [_P]),
+    ("nwg_plan_query", _I, [_P, ctypes.POINTER(nwg_plan_info)]),
+    ("nwg_conv2d", _I, [_P, _P, _P, _P, _P]),
+    ("nwg_plan_set_weights", _I, [_P, _P, _P]),
+    ("nwg_kernel_transform", _I, [_P, _P, _P, _P]),
+    ("nwg_input_transform", _I, [_P, _P, _P, _P]),
+    ("nwg_contract", _I, [_P, _P, _P, _P, _P]),
+    ("nwg_output_transform", _I, [_P, _P, _P, _P]),
+    ("nwg_plan_set_timing", _I, [_P, _I]),
+    ("nwg_plan_get_timing", _I, [_P, ctypes.POINTER(ctypes.c_double),
+                                 ctypes.POINTER(ctypes.c_longlong)]),
+    ("nwg_last_error", ctypes.c_char_p, []),
+    ("nwg_version", ctypes.c_char_p, []),
+]
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class NwgError(RuntimeError):
+    pass
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libnwg.so (once) and declare every entry point; raises if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise NwgError(f"{path} is missing: build it with `python -c 'import __graft_entry__ as g; "
+                       f"g.build()'` (no CPU fallback exists)")
+    lib = ctypes.CDLL(path)
+    for name, res, args in SIGNATURES:
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load_library().nwg_last_error().decode()
+
+
+def _check(rc: int, what: str):
+    if rc != NWG_OK:
+        raise NwgError(f"{what} failed ({rc}): {last_error()}")
+
+
+def plan_geometry(B, M, N, H, W, r, pad=0, tile=NWG_TILE_F2X2_3X3) -> dict:
+    """Host-only geometry of a convolution (no device is touched)."""
+    info = nwg_plan_info()
+    _check(load_library().nwg_plan_geometry(B, M, N, H, W, r, pad, tile, ctypes.byref(info)),
+           "nwg_plan_geometry")
+    return info.as_dict()
+
+
+def _ptr(t) -> int:
+    return int(t.data_ptr())
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+class Plan:
+    """A plan handle; tensors are torch float32 CUDA (HIP) tensors, contiguous."""
+
+    def __init__(self, B, M, N, H, W, r, pad=0, tile=NWG_TILE_F2X2_3X3):
+        lib = load_library()
+        self._lib = lib
+        self.handle = lib.nwg_plan_create_pad(B, M, N, H, W, r, pad, tile)
+        if not self.handle:
+            raise NwgError(f"nwg_plan_create_pad failed: {last_error()}")
+        info = nwg_plan_info()
+        _check(lib.nwg_plan_query(self.handle, ctypes.byref(info)), "nwg_plan_query")
+        self.info = info.as_dict()
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self._lib.nwg_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # shapes of the Winograd-domain buffers (elements)
+    @property
+    def u_shape(self):
+        i = self.info
+        return (i["P"] if i["n"] else 1, i["M"], i["N"])
+
+    @property
+    def v_shape(self):
+        i = self.info
+        return (i["P"], i["M"], i["T"])
+
+    @property
+    def yhat_shape(self):
+        i = self.info
+        return (i["P"], i["N"], i["T"])
+
+    @property
+    def y_shape(self):
+        i = self.info
+        return (i["B"], i["N"], i["Ho"], i["Wo"])
+
+    def conv2d(self, x, w, y, stream=None):
+        _check(self._lib.nwg_conv2d(self.handle, _ptr(x), _ptr(w), _ptr(y), _stream(stream)),
+               "nwg_conv2d")
+
+    def set_weights(self, w, stream=None):
+        _check(self._lib.nwg_plan_set_weights(self.handle, _ptr(w), _stream(stream)),
+               "nwg_plan_set_weights")
+
+    def kernel_transform(self, w, U, stream=None):
+        _check(self._lib.nwg_kernel_transform(self.handle, _ptr(w), _ptr(U), _stream(stream)),
+               "nwg_kernel_transform")
+
+    def input_transform(self, x, V, stream=None):
+        _check(self._lib.nwg_input_transform(self.handle, _ptr(x), _ptr(V), _stream(stream)),
+               "nwg_input_transform")
+
+    def contract(self, U, V, Yh, stream=None):
+        _check(self._lib.nwg_contract(self.handle, _ptr(U), _ptr(V), _ptr(Yh), _stream(stream)),
+               "nwg_contract")
+
+    def output_transform(self, Yh, y, stream=None):
+        _check(self._lib.nwg_output_transform(self.handle, _ptr(Yh), _ptr(y), _stream(stream)),
+               "nwg_output_transform")
+
+    def set_timing(self, enable: bool):
+        _check(self._lib.nwg_plan_set_timing(self.handle, int(bool(enable))), "nwg_plan_set_timing")
+
+    def get_timing(self):
+        """Wait for recorded stages; returns (ms[4], count[4]) summed since the last call."""
+        ms = (ctypes.c_double * 4)()
+        cnt = (ctypes.c_longlong * 4)()
+        _check(self._lib.nwg_plan_get_timing(self.handle, ms, cnt), "nwg_plan_get_timing")
+        return list(ms), list(cnt)

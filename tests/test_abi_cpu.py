@@ -1,0 +1,121 @@
+"""CPU checks of the C ABI: the library loads, exports every declared symbol,
+and its host-side plan geometry matches the oracle's level recurrence
+(two independent implementations of Sec. III.B's nesting).  No device work.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle.nested import base_f23, nesting_levels
+from paper_2102_13272_amd import nwg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nwg.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(nwg_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = nwg.load_library()
+    declared = _declared_functions()
+    assert len(declared) >= 15
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(n for n, _, _ in nwg.SIGNATURES) == declared
+    assert lib.nwg_version().decode().startswith("nwg")
+
+
+def test_info_struct_layout_matches_header():
+    # the binding's struct must have the same fields, in order, as the header
+    text = open(HEADER).read()
+    body = text[text.index("typedef struct nwg_plan_info"):text.index("} nwg_plan_info;")]
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    names = []
+    for decl in body.split(";")[:-1]:
+        decl = decl.split("{")[-1]
+        for part in decl.split(","):
+            m = re.search(r"([A-Za-z_][A-Za-z_0-9]*)\s*(\[[^\]]*\])?\s*$", part.strip())
+            if m:
+                names.append(m.group(1))
+    assert names == [f for f, _ in nwg.nwg_plan_info._fields_]
+
+
+@pytest.mark.parametrize("r", list(range(1, 32)))
+def test_geometry_matches_oracle_levels(r):
+    B, M, N, H, W = 2, 3, 5, 40, 37
+    pad = (r - 1) // 2
+    g = nwg.plan_geometry(B, M, N, H, W, r, pad)
+    lv = nesting_levels(base_f23(), r)
+    assert g["n"] == lv.n and g["Mn"] == lv.Mn and g["Kn"] == lv.Kn
+    assert g["strides"] == lv.strides
+    if lv.n:
+        assert g["Ln"] == lv.Ln
+    Ho, Wo = H + 2 * pad - r + 1, W + 2 * pad - r + 1
+    assert (g["Ho"], g["Wo"]) == (Ho, Wo)
+    th, tw = -(-Ho // lv.Mn), -(-Wo // lv.Mn)
+    assert (g["th"], g["tw"], g["T"]) == (th, tw, B * th * tw)
+    P = 4 ** (2 * lv.n)
+    assert g["P"] == P
+    if lv.n:
+        assert g["u_bytes"] == 4 * P * M * N
+        assert g["v_bytes"] == 4 * P * M * B * th * tw
+        assert g["yhat_bytes"] == 4 * P * N * B * th * tw
+        assert g["ewmm_mults"] == P * B * th * tw * M * N
+    assert g["direct_flop"] == 2 * B * N * M * Ho * Wo * r * r
+
+
+def test_geometry_of_the_five_workloads():
+    from paper_2102_13272_amd.workloads import WORKLOADS
+    expect = {"c1_r4_valid": [(2, 16, 256)], "c2_r7": [(2, 256, 256)], "c3_r13": [(3, 392, 4096)],
+              "c5_r31": [(4, 256, 65536)],
+              "c4_sr_stack": [(2, 16384, 256), (0, 65536, 1)] + [(1, 65536, 16)] * 4
+              + [(0, 65536, 1), (3, 4096, 4096)]}
+    for name, wl in WORKLOADS.items():
+        got = []
+        for L in wl.layers:
+            g = nwg.plan_geometry(L.B, L.M, L.N, L.H, L.W, L.r, L.pad)
+            got.append((g["n"], g["T"] if g["n"] else g["Ho"] * g["Wo"], g["P"]))
+        assert got == expect[name], name
+    g = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15)
+    assert g["workspace_bytes"] == (4 + 8 + 8) * 2 ** 30
+
+
+@pytest.mark.parametrize("args,rc", [
+    ((0, 1, 1, 8, 8, 3, 0, 0), nwg.NWG_EINVAL),       # empty batch
+    ((1, 0, 1, 8, 8, 3, 0, 0), nwg.NWG_EINVAL),
+    ((1, 1, 0, 8, 8, 3, 0, 0), nwg.NWG_EINVAL),
+    ((1, 1, 1, 0, 8, 3, 0, 0), nwg.NWG_EINVAL),
+    ((1, 1, 1, 8, 8, 0, 0, 0), nwg.NWG_EINVAL),
+    ((1, 1, 1, 8, 8, 3, -1, 0), nwg.NWG_EINVAL),
+    ((1, 1, 1, 4, 4, 9, 0, 0), nwg.NWG_EINVAL),       # kernel larger than the input
+    ((1, 1, 1, 64, 64, 32, 0, 0), nwg.NWG_EUNSUPPORTED),  # depth 5
+    ((1, 1, 1, 8, 8, 3, 1, 7), nwg.NWG_EUNSUPPORTED),    # unknown tile
+])
+def test_geometry_rejects_bad_arguments(args, rc):
+    lib = nwg.load_library()
+    info = nwg.nwg_plan_info()
+    assert lib.nwg_plan_geometry(*args, ctypes.byref(info)) == rc
+    assert lib.nwg_last_error().decode() != ""
+
+
+def test_null_arguments_are_rejected_without_a_device():
+    lib = nwg.load_library()
+    assert lib.nwg_plan_query(None, None) == nwg.NWG_EINVAL
+    assert lib.nwg_conv2d(None, None, None, None, None) == nwg.NWG_EINVAL
+    assert lib.nwg_contract(None, None, None, None, None) == nwg.NWG_EINVAL
+    assert lib.nwg_plan_set_timing(None, 1) == nwg.NWG_EINVAL
+    lib.nwg_plan_destroy(None)                       # NULL-safe
+
+
+def test_no_silent_fallback_without_device():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(nwg.NwgError):
+        nwg.Plan(1, 1, 1, 8, 8, 3)

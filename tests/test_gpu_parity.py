@@ -1,0 +1,169 @@
+"""GPU parity of the HIP nested-Winograd path against the CPU oracle.
+
+End to end: y from nwg_conv2d against the fp64 direct convolution
+(rel-L2 <= 1e-4, max-abs <= 1e-3 max|y|).  Stage by stage: the library's
+U, V, Yhat against the CPU nested reference, re-ordered to the library's
+documented point order.  All inputs are seeded and synthetic.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle.direct import direct_conv2d
+from oracle.nested import (ewmm, geometry, input_transform, kernel_transform, output_transform,
+                           point_permutation)
+from paper_2102_13272_amd import nwg
+from paper_2102_13272_amd.workloads import make_case
+from tests.gpu_util import assert_close, dev, run_conv
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    nwg.load_library()          # raises if the HIP library is missing: no fallback
+
+
+# B, M, N, H, W, r, pad -- depths 0..4, ragged tiles, odd channel counts, B > 1
+E2E = [
+    (2, 3, 5, 9, 7, 1, 0),
+    (1, 4, 4, 16, 16, 4, 0),
+    (1, 5, 3, 11, 13, 2, 0),
+    (2, 5, 5, 19, 17, 3, 1),
+    (1, 1, 7, 23, 21, 5, 2),
+    (3, 6, 4, 17, 30, 7, 3),
+    (1, 9, 1, 21, 18, 9, 4),
+    (2, 7, 9, 29, 26, 13, 6),
+    (1, 3, 2, 15, 15, 15, 0),
+    (1, 2, 3, 40, 35, 31, 15),
+    (1, 17, 20, 31, 31, 31, 0),   # a single output pixel
+    (1, 33, 18, 24, 24, 16, 0),
+]
+
+
+@pytest.mark.parametrize("case", E2E, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
+def test_conv2d_matches_direct_oracle(case):
+    B, M, N, H, W, r, pad = case
+    L, x, w = make_case(B, M, N, H, W, r, pad, seed=sum(case))
+    print(f"case {case}", flush=True)
+    y = run_conv(x, w, pad)
+    assert_close(y, direct_conv2d(x, w, pad), what=str(case))
+
+
+def _to_lib_points(a, n):
+    """oracle [..., P1, P1] -> [..., P] in the library's point order."""
+    perm = point_permutation(n)
+    return a[..., perm[:, 0], perm[:, 1]]
+
+
+STAGES = [(1, 3, 4, 12, 10, 3, 1), (2, 4, 3, 13, 11, 6, 2), (1, 3, 5, 20, 19, 11, 5),
+          (1, 2, 3, 24, 20, 31, 15)]
+
+
+@pytest.mark.parametrize("case", STAGES, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
+def test_stages_match_cpu_nested_reference(case):
+    B, M, N, H, W, r, pad = case
+    L, x, w = make_case(B, M, N, H, W, r, pad, seed=7 + r)
+    print(f"stages {case}", flush=True)
+    g = geometry(x.shape, w.shape, pad)
+    n = g.lv.n
+    U_ref = kernel_transform(w, g)                      # (N, M, P1, P1)
+    V_ref = input_transform(x, g)                       # (B, th, tw, M, P1, P1)
+    Yh_ref = ewmm(U_ref, V_ref)                         # (B, th, tw, N, P1, P1)
+    T = B * g.th * g.tw
+    U_lib = _to_lib_points(U_ref, n).transpose(2, 1, 0)                    # (P, M, N)
+    V_lib = _to_lib_points(V_ref.reshape(T, M, g.lv.P1, g.lv.P1), n).transpose(2, 1, 0)
+    Yh_lib = _to_lib_points(Yh_ref.reshape(T, N, g.lv.P1, g.lv.P1), n).transpose(2, 1, 0)
+
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        assert plan.info["P"] == U_lib.shape[0] and plan.info["T"] == T
+        U = torch.empty(plan.u_shape, device="cuda")
+        V = torch.empty(plan.v_shape, device="cuda")
+        Yh = torch.empty(plan.yhat_shape, device="cuda")
+        y = torch.empty(plan.y_shape, device="cuda")
+        plan.kernel_transform(dev(w), U)
+        plan.input_transform(dev(x), V)
+        torch.cuda.synchronize()
+        assert_close(U.cpu().numpy(), U_lib, rel_tol=1e-6, abs_frac=1e-6, what="U")
+        assert_close(V.cpu().numpy(), V_lib, rel_tol=1e-6, abs_frac=1e-6, what="V")
+        # contraction alone, on the oracle's transformed operands
+        plan.contract(dev(U_lib), dev(V_lib), Yh)
+        torch.cuda.synchronize()
+        assert_close(Yh.cpu().numpy(), Yh_lib, rel_tol=1e-5, abs_frac=1e-5, what="Yhat")
+        # output transform alone, on the oracle's Yhat
+        plan.output_transform(dev(Yh_lib), y)
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), output_transform(Yh_ref, g), rel_tol=1e-6, abs_frac=1e-6,
+                     what="y")
+
+
+@pytest.mark.parametrize("N,M,T,depth", [(1, 32, 4096, 1), (5, 5, 100, 1), (128, 128, 256, 1),
+                                         (64, 64, 392, 1), (3, 7, 33, 1), (32, 1, 300, 1),
+                                         (17, 33, 129, 1), (128, 20, 64, 0), (5, 32, 1000, 0),
+                                         (32, 5, 4096, 0)])
+def test_contraction_matches_numpy(N, M, T, depth):
+    """Yhat[p] = U[p]^T V[p] for ragged shapes, through nwg_contract.
+
+    Depth 1 (P = 16 points) uses B = T images of 2x2 with r = 2 (one tile
+    each); depth 0 (r = 1) uses one image of 1 x T, where V is x and Yhat is y.
+    """
+    rng = np.random.default_rng(N * 1000 + M * 10 + T)
+    plan = nwg.Plan(1, M, N, 1, T, 1, 0) if depth == 0 else nwg.Plan(T, M, N, 2, 2, 2, 0)
+    P = plan.info["P"]
+    assert P == (1 if depth == 0 else 16) and (depth == 0 or plan.info["T"] == T)
+    U = rng.standard_normal((P, M, N))
+    V = rng.standard_normal((P, M, T))
+    ref = np.einsum("pmn,pmt->pnt", U, V)
+    Yh = torch.empty((P, N, T), device="cuda")
+    plan.contract(dev(U), dev(V), Yh)
+    torch.cuda.synchronize()
+    assert_close(Yh.cpu().numpy(), ref, rel_tol=1e-5, abs_frac=1e-5, what="contract")
+    plan.close()
+
+
+def test_weight_cache_follows_pointer_and_set_weights():
+    B, M, N, H, W, r, pad = 1, 3, 4, 14, 14, 5, 2
+    _, x, w1 = make_case(B, M, N, H, W, r, pad, seed=1)
+    _, _, w2 = make_case(B, M, N, H, W, r, pad, seed=2)
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        xd = dev(x)
+        wd1, wd2 = dev(w1), dev(w2)
+        y = torch.empty(plan.y_shape, device="cuda")
+        plan.conv2d(xd, wd1, y)
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w1, pad), what="w1")
+        plan.conv2d(xd, wd2, y)                      # new pointer: re-transformed
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w2, pad), what="w2")
+        wd2.copy_(wd1)                                # in place: cache is stale by contract
+        plan.set_weights(wd2)
+        plan.conv2d(xd, wd2, y)
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w1, pad), what="set_weights")
+
+
+def test_depth0_stage_calls_are_rejected():
+    with nwg.Plan(1, 2, 2, 8, 8, 1, 0) as plan:
+        x = torch.zeros((1, 2, 8, 8), device="cuda")
+        with pytest.raises(nwg.NwgError):
+            plan.input_transform(x, x)
+        with pytest.raises(nwg.NwgError):
+            plan.output_transform(x, x)
+
+
+def test_timing_records_each_stage():
+    B, M, N, H, W, r, pad = 1, 8, 8, 32, 32, 7, 3
+    _, x, w = make_case(B, M, N, H, W, r, pad, seed=3)
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        xd, wd = dev(x), dev(w)
+        y = torch.empty(plan.y_shape, device="cuda")
+        plan.set_timing(True)
+        for _ in range(3):
+            plan.conv2d(xd, wd, y)
+        ms, cnt = plan.get_timing()
+        assert cnt == [1, 3, 3, 3]
+        assert all(t > 0 for t in ms)
+        ms2, cnt2 = plan.get_timing()
+        assert cnt2 == [0, 0, 0, 0]
