@@ -44,7 +44,8 @@ def stage_bytes_flops(info: dict):
     if info["n"] == 0:
         return {"kernel_transform": (w + 4 * M * N, 0.0),
                 "contraction": (x + y + 4 * M * N, 2.0 * B * N * M * Ho * Wo)}
-    U, V, Yh = 4 * P * M * N, 4 * P * M * T, 4 * P * N * T
+    # Z: the contraction's output after the first output level, P/4 values per (n, t)
+    U, V, Yh = 4 * P * M * N, 4 * P * M * T, 4 * (P // 4) * N * T
     return {"kernel_transform": (w + U, 0.0),
             "input_transform": (x + V, 0.0),
             "contraction": (U + V + Yh, 2.0 * P * M * N * T),

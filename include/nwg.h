@@ -19,19 +19,25 @@
  *
  * Data: all tensors are contiguous fp32 in DEVICE memory.
  *   x [B][M][H][W],  w [N][M][r][r],  y [B][N][Ho][Wo].
- * Winograd-domain buffers (what the stage entry points read and write):
- *   U    [P][M][N]   transformed kernel (N fastest)
- *   V    [P][M][T]   transformed input  (T fastest)
- *   Yhat [P][N][T]   per-point channel contraction (T fastest)
+ * Winograd-domain buffers (what the stage entry points read and write),
+ * "quad-interleaved": the level-1 column digit is the innermost axis, so
+ * each (channel, tile) entry is a 16-byte float4 quad:
+ *   U [P/4][M][N][4]  transformed kernel, U[p/4][m][n][p%4]
+ *   V [P/4][M][T][4]  transformed input,  V[p/4][m][t][p%4]
+ *   Z [P/16][N][T][4] channel contraction after the first output level:
+ *       Z[g][n][t][2*i1r + i1c] = sum over the 16 points p = 16g + 4 q1r + q1c
+ *       of A^T[i1r][q1r] A^T[i1c][q1c] sum_m U[p][m][n] V[p][m][t]
  * with T = B * th * tw tiles, th = ceil(Ho / M_n), tw = ceil(Wo / M_n), and
  * tile t = (b * th + ty) * tw + tx covering outputs [ty*M_n, ty*M_n + M_n) x
  * [tx*M_n, tx*M_n + M_n).  The point index p of a tile is written in base 4
  * with digits (q_n^row, q_n^col, q_{n-1}^row, q_{n-1}^col, ..., q_1^row,
  * q_1^col), most significant first, q_j being the level-j Winograd index.
+ * At depth 0 (r = 1) there is no transform: U is [M][N] and the contraction
+ * maps x to y directly.  All buffers must be 16-byte aligned.
  *
- * Ownership: the caller owns x, w, y, U/V/Yhat passed to stage calls, and
+ * Ownership: the caller owns x, w, y, U/V/Z passed to stage calls, and
  * the stream; they must stay valid until the work queued on the stream has
- * finished.  A plan owns its workspace (U, V, Yhat), allocated at creation.
+ * finished.  A plan owns its workspace (U, V, Z), allocated at creation.
  * Every call that takes a stream only queues work on it (`stream` is a
  * hipStream_t; NULL is the default stream) and never synchronises, except
  * nwg_plan_get_timing.  A plan is not thread-safe; one call in flight per
@@ -76,7 +82,7 @@ typedef struct nwg_plan_info {
   int th, tw;                   /* tiles per image */
   long long T;                  /* B * th * tw */
   long long P;                  /* Winograd points per tile, l^(2n) */
-  size_t u_bytes, v_bytes, yhat_bytes, workspace_bytes;
+  size_t u_bytes, v_bytes, yhat_bytes, workspace_bytes;   /* yhat_bytes: Z */
   long long ewmm_mults;         /* general multiplications per call: P*T*M*N */
   double direct_flop;           /* 2*B*N*M*Ho*Wo*r*r */
   double contract_flop;         /* 2*P*M*N*T (n = 0: 2*B*N*M*Ho*Wo) */
@@ -115,22 +121,24 @@ int nwg_plan_set_weights(nwg_plan* plan, const float* w, void* stream);
 
 /* --- Stage entry points (each is one kernel launch on `stream`) ---------- */
 
-/* Nested kernel transformation (Sec. III.B, 2nd step): w [N][M][r][r] -> U. */
+/* Nested kernel transformation (Sec. III.B, 2nd step): w [N][M][r][r] -> U
+ * (u_bytes). */
 int nwg_kernel_transform(const nwg_plan* plan, const float* w, float* U, void* stream);
 
-/* Nested input transformation (Sec. III.B, 1st step): x -> V.
+/* Nested input transformation (Sec. III.B, 1st step): x -> V (v_bytes).
  * NWG_EINVAL at depth 0 (r = 1), which has no transform. */
 int nwg_input_transform(const nwg_plan* plan, const float* x, float* V, void* stream);
 
-/* EWMM accumulated over the M input channels (Sec. II.B, III.B final step):
- * Yhat[p][n][t] = sum_m U[p][m][n] * V[p][m][t], on fp32 MFMA.
- * At depth 0, V is x and Yhat is y (a plain per-image channel GEMM). */
-int nwg_contract(const nwg_plan* plan, const float* U, const float* V, float* Yhat,
+/* EWMM accumulated over the M input channels (Sec. II.B, III.B final step),
+ * on fp32 MFMA, followed by the first level of the nested output
+ * transformation: U, V -> Z (yhat_bytes).  At depth 0, V is x and Z is y
+ * (a plain per-image channel GEMM). */
+int nwg_contract(const nwg_plan* plan, const float* U, const float* V, float* Z,
                  void* stream);
 
-/* Nested output transformation (Sec. III.B, final step): Yhat -> y, cropped
- * to Ho x Wo.  NWG_EINVAL at depth 0. */
-int nwg_output_transform(const nwg_plan* plan, const float* Yhat, float* y, void* stream);
+/* Nested output transformation (Sec. III.B, final step), levels 2..n:
+ * Z -> y, cropped to Ho x Wo.  NWG_EINVAL at depth 0. */
+int nwg_output_transform(const nwg_plan* plan, const float* Z, float* y, void* stream);
 
 /* --- Per-stage timing ------------------------------------------------------
  * When enabled, nwg_conv2d records HIP events around each of its launches on

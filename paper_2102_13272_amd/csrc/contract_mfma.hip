@@ -1,27 +1,38 @@
 // Winograd-domain channel contraction: the EWMM of Sec. III.B accumulated
-// over the M input channels (Sec. II.B), i.e. for every Winograd point p
+// over the M input channels (Sec. II.B), fused with the first (innermost)
+// level of the nested output transformation.
 //
-//     Yhat[p] (N x T) = U[p]^T (N x M) * V[p] (M x T)
+// For every Winograd point p,   Yhat[p] (N x T) = U[p]^T (N x M) * V[p] (M x T),
+// a batch of P independent GEMMs -- the one dense contraction of the method,
+// on fp32 MFMA (v_mfma_f32_16x16x4f32, fp32 accumulate).  The 16 points of a
+// level-1 group g (digits q1r, q1c) are then reduced by A^T along both axes
+// in registers:
 //
-// a batch of P independent GEMMs, the one dense contraction of the method.
-// It runs on fp32 MFMA (v_mfma_f32_16x16x4f32, fp32 accumulate).
+//     Z[g][n][t][2*i1r + i1c] = sum_{q1r,q1c} A^T[i1r][q1r] A^T[i1c][q1c] Yhat[16g + 4q1r + q1c][n][t]
 //
-// Work-group: 256 threads (4 wave64s) own a BM x BN block of one point's
-// output; each wave owns a (BM/WM) x (BN/WN) sub-block of 16x16 MFMA tiles.
-// The K loop moves BK = 16 channels per step through double-buffered LDS:
-// the next step's global loads are issued before the current step's MFMAs
-// and written to the other buffer afterwards, so one barrier per step
-// suffices.  LDS rows are padded to a stride of 16 or 48 (mod 64) floats so
-// that the four 16-lane groups of an MFMA operand read hit disjoint banks.
+// so the contraction writes P/4 values per (n, t) instead of P.
+//
+// Layouts (quad-interleaved: the level-1 column digit q1c is innermost):
+//   U [P/4][M][N][4],  V [P/4][M][T][4],  Z [P/16][N][T][4].
+//
+// Work-group: 256 threads (4 wave64s) own a BM x BN block of one group's
+// output.  For each q1r the K loop (BK = 16 channels per step) streams the
+// four points q1c = 0..3 together through double-buffered LDS as float4
+// quads; one ds_read_b128 yields the MFMA operand of all four points, and
+// four accumulator sets take the four GEMMs.  After the K loop the four
+// products are folded into the 2x2 level-1 outputs.
 //
 // Operand lane maps of v_mfma_f32_16x16x4f32 (wave64):
 //   A (16x4):  lane l holds A[l%16][l/16]
 //   B (4x16):  lane l holds B[l/16][l%16]
 //   D (16x16): lane l, register v holds D[4*(l/16)+v][l%16]
 //
-// Work-groups are numbered so that consecutive blocks of the same point land
-// on the same XCD (the dispatcher deals work-groups round-robin over the 8
-// XCDs), keeping each point's U and V tiles in one L2.
+// Work-groups are numbered so that the blocks of one group land on the same
+// XCD (the dispatcher deals work-groups round-robin over the 8 XCDs),
+// keeping the group's U and V tiles in one L2.
+//
+// Depth 0 (r = 1) has no transform: a plain per-image GEMM kernel below
+// takes y[b] = U^T x[b] with the same MFMA tiling.
 #include "nwg_internal.h"
 
 namespace nwg {
@@ -31,19 +42,186 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBK = 16;
 
-__host__ __device__ constexpr int lds_stride(int cols) {
-  return ((cols + 16) % 32 == 16) ? cols + 16 : cols + 32;
-}
-
 __device__ __forceinline__ long long xcd_remap(long long i, long long G) {
   const long long q = G / 8, rem = G % 8;
   const long long xcd = i % 8, slot = i / 8;
   return xcd < rem ? xcd * (q + 1) + slot : rem * (q + 1) + (xcd - rem) * q + slot;
 }
 
+// ---------------------------------------------------------------------------
+// Fused contraction + level-1 output transform (depth >= 1)
+// ---------------------------------------------------------------------------
+
+// BK x COLS tile of float4 quads from a [K][ncols] quad matrix into LDS.
+template <int COLS>
+struct QuadLoader {
+  static constexpr int ELEMS = kBK * COLS;
+  static constexpr int PER = (ELEMS + 255) / 256;
+  float4 reg[PER];
+
+  __device__ __forceinline__ void load(const float4* __restrict__ src, int ld, int k0, int c0,
+                                       int K, int ncols) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 256;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (e < ELEMS) {
+        const int k = e / COLS, col = e % COLS;
+        const int gk = k0 + k, gc = c0 + col;
+        if (gk < K && gc < ncols) v = src[(size_t)gk * ld + gc];
+      }
+      reg[i] = v;
+    }
+  }
+
+  __device__ __forceinline__ void store(float4 (*dst)[COLS]) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + i * 256;
+      if (e < ELEMS) dst[e / COLS][e % COLS] = reg[i];
+    }
+  }
+};
+
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(256) void contract_fused(const float4* __restrict__ U,
+                                                      const float4* __restrict__ V,
+                                                      float4* __restrict__ Z, int M, int N, int T,
+                                                      int ntb, int nnb) {
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 16, FN = WTN / 16;
+  static_assert(WM * WN == 4, "four waves");
+  static_assert(FM >= 1 && FN >= 1, "wave tile at least 16x16");
+  __shared__ float4 As[2][kBK][BM];
+  __shared__ float4 Bs[2][kBK][BN];
+
+  long long bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int tb = (int)(bid % ntb);
+  bid /= ntb;
+  const int nb = (int)(bid % nnb);
+  const long long g = bid / nnb;
+  const int n0 = nb * BM, c0 = tb * BN;
+  const size_t quadU = (size_t)M * N, quadV = (size_t)M * T;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int lr = lane & 15, lk = lane >> 4;
+
+  floatx4 out[4][FM][FN];   // [2*i1r + i1c]
+#pragma unroll
+  for (int o = 0; o < 4; ++o)
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) out[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  QuadLoader<BM> la;
+  QuadLoader<BN> lb;
+  const int nk = (M + kBK - 1) / kBK;
+
+  for (int q1r = 0; q1r < 4; ++q1r) {
+    const float4* __restrict__ Uq = U + (size_t)(4 * g + q1r) * quadU;
+    const float4* __restrict__ Vq = V + (size_t)(4 * g + q1r) * quadV;
+    floatx4 acc[4][FM][FN];   // [q1c]
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[c][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    la.load(Uq, N, 0, n0, M, N);
+    lb.load(Vq, T, 0, c0, M, T);
+    la.store(As[0]);
+    lb.store(Bs[0]);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int cur = kt & 1;
+      const bool more = kt + 1 < nk;
+      if (more) {
+        la.load(Uq, N, (kt + 1) * kBK, n0, M, N);
+        lb.load(Vq, T, (kt + 1) * kBK, c0, M, T);
+      }
+#pragma unroll
+      for (int kk = 0; kk < kBK / 4; ++kk) {
+        float4 af[FM], bf[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) af[i] = As[cur][kk * 4 + lk][wm * WTM + i * 16 + lr];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) bf[j] = Bs[cur][kk * 4 + lk][wn * WTN + j * 16 + lr];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            acc[0][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].x, bf[j].x, acc[0][i][j], 0, 0, 0);
+            acc[1][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].y, bf[j].y, acc[1][i][j], 0, 0, 0);
+            acc[2][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].z, bf[j].z, acc[2][i][j], 0, 0, 0);
+            acc[3][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].w, bf[j].w, acc[3][i][j], 0, 0, 0);
+          }
+      }
+      if (more) {
+        la.store(As[cur ^ 1]);
+        lb.store(Bs[cur ^ 1]);
+      }
+      __syncthreads();
+    }
+    // level 1 along columns (q1c -> i1c), then along rows with A^T[i1r][q1r]
+    const float r0 = at_coef(0, q1r), r1 = at_coef(1, q1r);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const floatx4 z0 = acc[0][i][j] + acc[1][i][j] + acc[2][i][j];
+        const floatx4 z1 = acc[1][i][j] - acc[2][i][j] - acc[3][i][j];
+        out[0][i][j] += r0 * z0;
+        out[1][i][j] += r0 * z1;
+        out[2][i][j] += r1 * z0;
+        out[3][i][j] += r1 * z1;
+      }
+  }
+
+  float4* __restrict__ Zg = Z + (size_t)g * N * T;
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = n0 + wm * WTM + i * 16 + lk * 4 + v;
+      if (row >= N) continue;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = c0 + wn * WTN + j * 16 + lr;
+        if (col < T)
+          Zg[(size_t)row * T + col] =
+              make_float4(out[0][i][j][v], out[1][i][j][v], out[2][i][j][v], out[3][i][j][v]);
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_fused(const float* U, const float* V, float* Z, int M, int N, int T,
+                        long long G, hipStream_t s) {
+  const int ntb = (T + BN - 1) / BN;
+  const int nnb = (N + BM - 1) / BM;
+  const long long blocks = (long long)ntb * nnb * G;
+  if (blocks <= 0 || blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+  if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN>), dim3((unsigned)blocks), dim3(256), 0, s,
+                     (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Plain GEMM for depth 0: C[b] (N x HW) = A^T (N x M) * B[b] (M x HW)
+// ---------------------------------------------------------------------------
+
+__host__ __device__ constexpr int lds_stride(int cols) {
+  return ((cols + 16) % 32 == 16) ? cols + 16 : cols + 32;
+}
+
 template <int COLS, int SROW>
 struct TileLoader {
-  // BK x COLS tile of a row-major [K][ld] matrix into LDS [BK][SROW].
   static constexpr int CHUNKS = kBK * COLS / 4;
   static constexpr int PER = (CHUNKS + 255) / 256;
   float4 reg[PER];
@@ -88,13 +266,12 @@ struct TileLoader {
 };
 
 template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(256) void contract_mfma(ContractArgs a, int ntb, int nnb,
-                                                     int vecA, int vecB) {
+__global__ __launch_bounds__(256) void gemm_mfma(ContractArgs a, int ntb, int nnb, int vecA,
+                                                 int vecB) {
   constexpr int SA = lds_stride(BM), SB = lds_stride(BN);
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int FM = WTM / 16, FN = WTN / 16;
   static_assert(WM * WN == 4, "four waves");
-  static_assert(FM >= 1 && FN >= 1, "wave tile at least 16x16");
   __shared__ __attribute__((aligned(16))) float As[2][kBK][SA];
   __shared__ __attribute__((aligned(16))) float Bs[2][kBK][SB];
 
@@ -172,7 +349,7 @@ __global__ __launch_bounds__(256) void contract_mfma(ContractArgs a, int ntb, in
 }
 
 template <int BM, int BN, int WM, int WN>
-hipError_t launch_tile(const ContractArgs& a, hipStream_t s) {
+hipError_t launch_gemm(const ContractArgs& a, hipStream_t s) {
   const int ntb = (a.Ncols + BN - 1) / BN;
   const int nnb = (a.Nrows + BM - 1) / BM;
   const long long blocks = (long long)ntb * nnb * a.batch;
@@ -180,21 +357,26 @@ hipError_t launch_tile(const ContractArgs& a, hipStream_t s) {
   auto aligned = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
   const int vecA = (a.ldA % 4 == 0) && (a.Nrows % 4 == 0) && (a.sA % 4 == 0) && aligned(a.A);
   const int vecB = (a.ldB % 4 == 0) && (a.Ncols % 4 == 0) && (a.sB % 4 == 0) && aligned(a.Bm);
-  hipLaunchKernelGGL((contract_mfma<BM, BN, WM, WN>), dim3((unsigned)blocks), dim3(256), 0, s, a,
+  hipLaunchKernelGGL((gemm_mfma<BM, BN, WM, WN>), dim3((unsigned)blocks), dim3(256), 0, s, a,
                      ntb, nnb, vecA, vecB);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_contract(const ContractArgs& a, hipStream_t s) {
-  const int N = a.Nrows, T = a.Ncols;
-  auto cols_waste = [T](int bn) { return ((T + bn - 1) / bn) * bn; };
-  const bool bn64 = cols_waste(64) < cols_waste(128);
-  if (N <= 16) return launch_tile<16, 128, 1, 4>(a, s);
-  if (N <= 32) return launch_tile<32, 128, 1, 4>(a, s);
-  if (N <= 64) return bn64 ? launch_tile<64, 64, 2, 2>(a, s) : launch_tile<64, 128, 2, 2>(a, s);
-  return bn64 ? launch_tile<128, 64, 2, 2>(a, s) : launch_tile<128, 128, 2, 2>(a, s);
+hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s) {
+  const int N = a.Nrows;
+  if (N <= 16) return launch_gemm<16, 128, 1, 4>(a, s);
+  if (N <= 32) return launch_gemm<32, 128, 1, 4>(a, s);
+  if (N <= 64) return launch_gemm<64, 128, 2, 2>(a, s);
+  return launch_gemm<128, 128, 2, 2>(a, s);
+}
+
+hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
+                                 long long G, hipStream_t s) {
+  if (N <= 16) return launch_fused<16, 128, 1, 4>(U, V, Z, M, N, T, G, s);
+  if (N <= 32) return launch_fused<32, 128, 1, 4>(U, V, Z, M, N, T, G, s);
+  return launch_fused<64, 64, 2, 2>(U, V, Z, M, N, T, G, s);
 }
 
 }  // namespace nwg

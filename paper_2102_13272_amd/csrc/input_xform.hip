@@ -15,24 +15,29 @@
 //                  its tiles' windows (a box of whole-row tile runs) in LDS.
 //   depth n >= 3 : one thread per (tile, level-3 branch); the work-group
 //                  stages each of its 16 tiles' windows separately in LDS
-//                  (window stride L_n^2 + 1 so that the 16 tiles of a
-//                  quarter-wave read 16 different banks), and depth 4 loops
-//                  over the 16 level-4 branches.  A branch's 10 x 10
-//                  sub-window is a signed sum of 2^(n-2) x 2^(n-2) shifted
-//                  window reads, all at compile-time offsets from one base.
+//                  (odd window stride, so that the 16 tiles of a
+//                  quarter-wave read 16 different banks).  At depth 4 the
+//                  work-group also owns one level-4 row branch q4r: the
+//                  fill already applies that B^T row along the window's
+//                  rows (46 -> 22 rows), and the threads loop over the four
+//                  level-4 column branches.  A branch's 10 x 10 sub-window
+//                  is then a signed sum of 2 x 2 (depth 3) or 2 x 4 (depth
+//                  4) shifted window reads at compile-time offsets.
 //
-// Writes are V[p][m][t] with consecutive lanes on consecutive tiles, i.e.
-// contiguous runs of the T axis for every point.
+// V is quad-interleaved, V[p/4][m][t][p%4] (p%4 is the level-1 column digit
+// q1c): every thread stores float4 quads, and the consecutive tiles of a
+// quarter-wave write 256 contiguous bytes.
 #include "nwg_internal.h"
 
 namespace nwg {
 namespace {
 
 // 2D inner transform (two levels per axis) of a 10 x 10 sub-window S and
-// store of its 256 points.  Point digits (q2r, q2c, q1r, q1c), most
-// significant first; vb already points at the branch's first point.
-__device__ __forceinline__ void inner2_store(const float (&S)[10][10], float* __restrict__ vb,
-                                             size_t pstride) {
+// store of its 256 points as 64 quads.  Point digits (q2r, q2c, q1r, q1c),
+// most significant first; vb points at the branch's first quad for this
+// (m, t), qstride is the distance between quads (M*T float4).
+__device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* __restrict__ vb,
+                                             size_t qstride) {
 #pragma unroll
   for (int q2r = 0; q2r < 4; ++q2r) {
     // level 2 along rows (stride 2): Z[u][j], u = 0..3
@@ -54,9 +59,10 @@ __device__ __forceinline__ void inner2_store(const float (&S)[10][10], float* __
       float o[16];
       bt_inner2(R, o);  // columns: index q2c*4 + q1c
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const int p = q2r * 64 + (k >> 2) * 16 + q1r * 4 + (k & 3);
-        vb[(size_t)p * pstride] = o[k];
+      for (int q2c = 0; q2c < 4; ++q2c) {
+        const int quad = q2r * 16 + q2c * 4 + q1r;
+        vb[(size_t)quad * qstride] =
+            make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
       }
     }
   }
@@ -65,8 +71,8 @@ __device__ __forceinline__ void inner2_store(const float (&S)[10][10], float* __
 // ---- depth 1 and 2: union box of tiles in LDS ------------------------------
 template <int NLEV>
 __global__ __launch_bounds__(256) void input_xform_box(
-    const float* __restrict__ x, float* __restrict__ V, int M, int H, int W, int pad, int th,
-    int tw, int T, long long MT, int RX, int RY, int nbx, int nby) {
+    const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
+    int tw, int T, long long qstride, int RX, int RY, int nbx, int nby) {
   constexpr int Mn = 1 << NLEV;
   constexpr int Ln = 3 * Mn - 2;
   extern __shared__ float lds[];
@@ -96,14 +102,14 @@ __global__ __launch_bounds__(256) void input_xform_box(
   if (ty >= th || tx >= tw) return;
   const int t = (b * th + ty) * tw + tx;
   const float* win = lds + ly * Mn * BW + lx * Mn;
-  float* vb = V + (size_t)m * T + t;
+  float4* vb = V + (size_t)m * T + t;
   if constexpr (NLEV == 2) {
     float S[10][10];
 #pragma unroll
     for (int i = 0; i < 10; ++i)
 #pragma unroll
       for (int j = 0; j < 10; ++j) S[i][j] = win[i * BW + j];
-    inner2_store(S, vb, (size_t)MT);
+    inner2_store(S, vb, (size_t)qstride);
   } else {
     float X[4][4], Rw[4][4];
 #pragma unroll
@@ -126,38 +132,52 @@ __global__ __launch_bounds__(256) void input_xform_box(
     }
 #pragma unroll
     for (int q1r = 0; q1r < 4; ++q1r)
-#pragma unroll
-      for (int q1c = 0; q1c < 4; ++q1c) vb[(size_t)(q1r * 4 + q1c) * MT] = Rw[q1r][q1c];
+      vb[(size_t)q1r * qstride] = make_float4(Rw[q1r][0], Rw[q1r][1], Rw[q1r][2], Rw[q1r][3]);
   }
 }
 
 // ---- depth 3 and 4: 16 tiles per work-group, per-tile windows in LDS -------
 template <int NLEV>
 __global__ __launch_bounds__(256) void input_xform_tiles(
-    const float* __restrict__ x, float* __restrict__ V, int M, int H, int W, int pad, int th,
-    int tw, int T, long long MT) {
+    const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
+    int tw, int T, long long qstride) {
   constexpr int Mn = 1 << NLEV;
   constexpr int Ln = 3 * Mn - 2;
-  constexpr int WS = Ln * Ln + 1;            // odd window stride: 16 tiles -> 16 banks
-  constexpr int PASSES = NLEV == 4 ? 16 : 1;
-  constexpr int NR = NLEV == 4 ? 4 : 2;      // outer taps per axis
+  constexpr int ROWS = 22;                   // L_3: rows left after the level-4 row branch
+  constexpr int COLS = Ln;
+  constexpr int WS = ROWS * COLS + 1;        // odd window stride: 16 tiles -> 16 banks
+  constexpr int NCT = NLEV == 4 ? 4 : 2;     // column taps of the outer levels
   extern __shared__ float lds[];
   const int m = blockIdx.y;
+  const int q4r = blockIdx.z;                // level-4 row branch (depth 4), else 0
   const int t0 = blockIdx.x * 16;
   const int tpi = th * tw;
-  for (int e = threadIdx.x; e < 16 * Ln * Ln; e += 256) {
-    const int tl = e / (Ln * Ln);
-    const int rem = e - tl * (Ln * Ln);
-    const int row = rem / Ln, col = rem - row * Ln;
+  // fill: per tile, rows u in [0,22) of the window after the level-4 row
+  // transform (depth 4) or the window itself (depth 3)
+  const int a4a = 8 * bt_tap0(q4r), a4b = 8 * bt_tap1(q4r);
+  const float s4a = bt_sign0(q4r), s4b = bt_sign1(q4r);
+  for (int e = threadIdx.x; e < 16 * ROWS * COLS; e += 256) {
+    const int tl = e / (ROWS * COLS);
+    const int rem = e - tl * (ROWS * COLS);
+    const int row = rem / COLS, col = rem - row * COLS;
     const int t = t0 + tl;
     float v = 0.0f;
     if (t < T) {
       const int b = t / tpi;
       const int r2 = t - b * tpi;
       const int ty = r2 / tw, tx = r2 - ty * tw;
-      const int gr = ty * Mn - pad + row, gc = tx * Mn - pad + col;
-      if (gr >= 0 && gr < H && gc >= 0 && gc < W)
-        v = x[(((size_t)b * M + m) * H + gr) * W + gc];
+      const int gc = tx * Mn - pad + col;
+      const float* xp = x + ((size_t)b * M + m) * H * W;
+      if (gc >= 0 && gc < W) {
+        const int gr0 = ty * Mn - pad + row;
+        if (NLEV == 4) {
+          const int ga = gr0 + a4a, gb = gr0 + a4b;
+          if (ga >= 0 && ga < H) v += s4a * xp[(size_t)ga * W + gc];
+          if (gb >= 0 && gb < H) v += s4b * xp[(size_t)gb * W + gc];
+        } else {
+          if (gr0 >= 0 && gr0 < H) v = xp[(size_t)gr0 * W + gc];
+        }
+      }
     }
     lds[tl * WS + rem] = v;
   }
@@ -168,80 +188,74 @@ __global__ __launch_bounds__(256) void input_xform_tiles(
   if (t >= T) return;                       // no barrier below
   const int q3r = slot >> 2, q3c = slot & 3;
   const float* win = lds + tl * WS;
-  float* vslot = V + (size_t)slot * 256 * MT + (size_t)m * T + t;
+  const int ro0 = 4 * bt_tap0(q3r), ro1 = 4 * bt_tap1(q3r);
+  const float rs0 = bt_sign0(q3r), rs1 = bt_sign1(q3r);
+  constexpr int PASSES = NLEV == 4 ? 4 : 1;
 
   for (int pass = 0; pass < PASSES; ++pass) {
-    const int q4r = pass >> 2, q4c = pass & 3;
-    // outer taps (level 3 at stride 4, level 4 at stride 8) per axis
-    int ro[NR], co[NR];
-    float rs[NR], cs[NR];
+    const int q4c = pass;
+    // column taps: level 3 (stride 4) and, at depth 4, level 4 (stride 8)
+    int co[NCT];
+    float cs[NCT];
 #pragma unroll
-    for (int k = 0; k < NR; ++k) {
+    for (int k = 0; k < NCT; ++k) {
       const int k3 = k & 1, k4 = k >> 1;
-      const int a3r = k3 ? bt_tap1(q3r) : bt_tap0(q3r);
-      const int a3c = k3 ? bt_tap1(q3c) : bt_tap0(q3c);
-      float sr = k3 ? bt_sign1(q3r) : bt_sign0(q3r);
-      float sc = k3 ? bt_sign1(q3c) : bt_sign0(q3c);
-      int orow = 4 * a3r, ocol = 4 * a3c;
+      co[k] = 4 * (k3 ? bt_tap1(q3c) : bt_tap0(q3c));
+      cs[k] = k3 ? bt_sign1(q3c) : bt_sign0(q3c);
       if (NLEV == 4) {
-        orow += 8 * (k4 ? bt_tap1(q4r) : bt_tap0(q4r));
-        ocol += 8 * (k4 ? bt_tap1(q4c) : bt_tap0(q4c));
-        sr *= k4 ? bt_sign1(q4r) : bt_sign0(q4r);
-        sc *= k4 ? bt_sign1(q4c) : bt_sign0(q4c);
+        co[k] += 8 * (k4 ? bt_tap1(q4c) : bt_tap0(q4c));
+        cs[k] *= k4 ? bt_sign1(q4c) : bt_sign0(q4c);
       }
-      ro[k] = orow;
-      co[k] = ocol;
-      rs[k] = sr;
-      cs[k] = sc;
     }
     float S[10][10];
 #pragma unroll
-    for (int i = 0; i < 10; ++i)
+    for (int i = 0; i < 10; ++i) {
 #pragma unroll
-      for (int j = 0; j < 10; ++j) S[i][j] = 0.0f;
+      for (int j = 0; j < 10; ++j) {
+        float a = 0.0f, c = 0.0f;
 #pragma unroll
-    for (int kr = 0; kr < NR; ++kr) {
-#pragma unroll
-      for (int kc = 0; kc < NR; ++kc) {
-        const float* base = win + ro[kr] * Ln + co[kc];
-        const float sg = rs[kr] * cs[kc];
-#pragma unroll
-        for (int i = 0; i < 10; ++i)
-#pragma unroll
-          for (int j = 0; j < 10; ++j) S[i][j] += sg * base[i * Ln + j];
+        for (int k = 0; k < NCT; ++k) {
+          a += cs[k] * win[(ro0 + i) * COLS + co[k] + j];
+          c += cs[k] * win[(ro1 + i) * COLS + co[k] + j];
+        }
+        S[i][j] = rs0 * a + rs1 * c;
       }
     }
-    inner2_store(S, vslot + (size_t)pass * 4096 * MT, (size_t)MT);
+    // 256-point block of this branch: (q4r, q4c, q3r, q3c) at depth 4, (q3r, q3c) at depth 3
+    const int branch = NLEV == 4 ? (q4r * 64 + q4c * 16 + slot) : slot;
+    inner2_store(S, V + (size_t)branch * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
   }
 }
 
 }  // namespace
 
-hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s) {
-  const long long MT = (long long)g.M * g.T;
+hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf, hipStream_t s) {
+  float4* V = reinterpret_cast<float4*>(Vf);
+  if ((uintptr_t)Vf & 15) return hipErrorInvalidValue;
+  const long long qstride = (long long)g.M * g.T;   // float4 quads between consecutive quads
   const int T = (int)g.T;
   if (g.n >= 3) {
     const int Ln = 3 * (1 << g.n) - 2;
-    const size_t lds = (size_t)16 * (Ln * Ln + 1) * sizeof(float);
+    const size_t lds = (size_t)16 * (22 * Ln + 1) * sizeof(float);
     int dev = 0, max_lds = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess)
       e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (e != hipSuccess) return e;
     if ((size_t)max_lds < lds) return hipErrorInvalidConfiguration;
-    dim3 grid((unsigned)((g.T + 15) / 16), (unsigned)g.M);
+    dim3 grid((unsigned)((g.T + 15) / 16), (unsigned)g.M, g.n == 4 ? 4u : 1u);
     if (g.n == 3) {
       e = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_tiles<3>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       if (e != hipSuccess) return e;
       hipLaunchKernelGGL(input_xform_tiles<3>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
-                         g.pad, g.th, g.tw, T, MT);
+                         g.pad, g.th, g.tw, T, qstride);
     } else {
       e = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_tiles<4>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       if (e != hipSuccess) return e;
       hipLaunchKernelGGL(input_xform_tiles<4>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
-                         g.pad, g.th, g.tw, T, MT);
+                         g.pad, g.th, g.tw, T, qstride);
     }
   } else {
     const int Mn = 1 << g.n, Ln = 3 * Mn - 2;
@@ -263,10 +277,10 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, 
     dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)g.M);
     if (g.n == 2)
       hipLaunchKernelGGL(input_xform_box<2>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
-                         g.th, g.tw, T, MT, RX, RY, nbx, nby);
+                         g.th, g.tw, T, qstride, RX, RY, nbx, nby);
     else
       hipLaunchKernelGGL(input_xform_box<1>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
-                         g.th, g.tw, T, MT, RX, RY, nbx, nby);
+                         g.th, g.tw, T, qstride, RX, RY, nbx, nby);
   }
   return hipGetLastError();
 }

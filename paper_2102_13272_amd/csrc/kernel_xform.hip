@@ -10,8 +10,10 @@
 // One thread per (output channel, input channel, outer branch): the outer
 // levels (3 and 4) fold the reordered kernel into a 9 x 9 sub-kernel over
 // the digits (k2, k1) of each axis, and the two inner levels (9 -> 16 per
-// axis) run in registers.  Consecutive threads take consecutive output
-// channels, then input channels, so the writes of U[p][m][n] are contiguous.
+// axis) run in registers.  U is quad-interleaved, U[p/4][m][n][p%4] (p%4 is
+// the level-1 column digit), written as float4; consecutive threads take
+// consecutive output channels, then input channels, so the writes are
+// contiguous.  Depth 0 (r = 1) stores U[m][n] = w[n][m][0][0].
 #include "nwg_internal.h"
 
 namespace nwg {
@@ -81,14 +83,18 @@ __global__ __launch_bounds__(256) void kernel_xform(const float* __restrict__ w,
     float rows[3][4];
 #pragma unroll
     for (int u = 0; u < 3; ++u) g_one(k[u][0], k[u][1], k[u][2], rows[u]);
+    float o[4][4];   // [q1r][q1c]
 #pragma unroll
     for (int q1c = 0; q1c < 4; ++q1c) {
-      float o[4];
-      g_one(rows[0][q1c], rows[1][q1c], rows[2][q1c], o);
+      float c[4];
+      g_one(rows[0][q1c], rows[1][q1c], rows[2][q1c], c);
 #pragma unroll
-      for (int q1r = 0; q1r < 4; ++q1r)
-        U[(size_t)(q1r * 4 + q1c) * MN + (size_t)m * N + nn] = o[q1r];
+      for (int q1r = 0; q1r < 4; ++q1r) o[q1r][q1c] = c[q1r];
     }
+    float4* U4 = reinterpret_cast<float4*>(U);
+#pragma unroll
+    for (int q1r = 0; q1r < 4; ++q1r)
+      U4[(size_t)q1r * MN + (size_t)m * N + nn] = make_float4(o[q1r][0], o[q1r][1], o[q1r][2], o[q1r][3]);
   } else {
     // outer branch: (q4r, q4c, q3r, q3c) digits of the branch index
     int qr3 = 0, qc3 = 0, qr4 = 0, qc4 = 0;
@@ -133,8 +139,8 @@ __global__ __launch_bounds__(256) void kernel_xform(const float* __restrict__ w,
             }
           }
       }
-    // two inner levels: rows then columns
-    float* ub = U + (size_t)branch * 256 * MN + (size_t)m * N + nn;
+    // two inner levels: rows then columns; 64 quads per branch
+    float4* ub = reinterpret_cast<float4*>(U) + (size_t)branch * 64 * MN + (size_t)m * N + nn;
 #pragma unroll
     for (int rho = 0; rho < 16; ++rho) {
       // row rho = (q2r, q1r) of G2 applied to the 9 row digits
@@ -153,9 +159,10 @@ __global__ __launch_bounds__(256) void kernel_xform(const float* __restrict__ w,
       float o[16];
       g_inner2(rowv, o);   // index q2c*4 + q1c
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const int p = q2r * 64 + (k >> 2) * 16 + q1r * 4 + (k & 3);
-        ub[(size_t)p * MN] = o[k];
+      for (int q2c = 0; q2c < 4; ++q2c) {
+        const int quad = q2r * 16 + q2c * 4 + q1r;
+        ub[(size_t)quad * MN] =
+            make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
       }
     }
   }

@@ -119,7 +119,8 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     g->ewmm_mults = (long long)B * N * M * Ho * Wo;
     g->contract_flop = 2.0 * B * N * (double)M * Ho * Wo;
   } else {
-    const double u = f * P * M * N, v = f * P * M * g->T, yh = f * P * N * g->T;
+    // the contraction writes the level-1 output transform of Yhat: P/4 values per (n, t)
+    const double u = f * P * M * N, v = f * P * M * g->T, yh = f * (P / 4) * N * g->T;
     if (u > 1e13 || v > 1e13 || yh > 1e13 || g->T > 0x7fffffffLL / 64) {
       set_error("workspace too large");
       return NWG_EUNSUPPORTED;
@@ -171,35 +172,30 @@ int timed(nwg_plan* p, int stage, hipStream_t s, const char* what, F&& launch) {
   return rc;
 }
 
-nwg::ContractArgs contract_args(const nwg_plan_info& g, const float* U, const float* V,
-                                float* Yh) {
+// Depth 0 (r = 1, pad = 0): per image, y[b] (N x HW) = U^T (N x M) * x[b] (M x HW).
+nwg::ContractArgs depth0_args(const nwg_plan_info& g, const float* U, const float* x, float* y) {
   nwg::ContractArgs a{};
+  const int hw = g.Ho * g.Wo;
   a.A = U;
-  a.Bm = V;
-  a.C = Yh;
+  a.Bm = x;
+  a.C = y;
   a.Nrows = g.N;
   a.K = g.M;
   a.ldA = g.N;
-  if (g.n == 0) {
-    // F(1, r): no transform; per image, y[b] (N x HoWo) = U^T (N x M) * x[b] (M x HW)
-    const int hw = g.Ho * g.Wo;   // r = 1: Ho = H + 2 pad; pad > 0 is handled by the caller
-    a.Ncols = hw;
-    a.ldB = hw;
-    a.ldC = hw;
-    a.sA = 0;
-    a.sB = (long long)g.M * g.H * g.W;
-    a.sC = (long long)g.N * hw;
-    a.batch = g.B;
-  } else {
-    a.Ncols = (int)g.T;
-    a.ldB = (int)g.T;
-    a.ldC = (int)g.T;
-    a.sA = (long long)g.M * g.N;
-    a.sB = (long long)g.M * g.T;
-    a.sC = (long long)g.N * g.T;
-    a.batch = g.P;
-  }
+  a.Ncols = hw;
+  a.ldB = hw;
+  a.ldC = hw;
+  a.sA = 0;
+  a.sB = (long long)g.M * g.H * g.W;
+  a.sC = (long long)g.N * hw;
+  a.batch = g.B;
   return a;
+}
+
+hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* V, float* Z,
+                           hipStream_t s) {
+  if (g.n == 0) return nwg::launch_gemm_depth0(depth0_args(g, U, V, Z), s);
+  return nwg::launch_contract_fused(U, V, Z, g.M, g.N, (int)g.T, g.P / 16, s);
 }
 
 int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, float* U,
@@ -311,7 +307,7 @@ int nwg_contract(const nwg_plan* p, const float* U, const float* V, float* Yh, v
     set_error("NULL argument to nwg_contract");
     return NWG_EINVAL;
   }
-  return check_hip(nwg::launch_contract(contract_args(p->info, U, V, Yh), (hipStream_t)stream),
+  return check_hip(launch_contract(p->info, U, V, Yh, (hipStream_t)stream),
                    "contraction launch");
 }
 
@@ -356,13 +352,13 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
   }
   if (g.n == 0) {
     return timed(p, 2, s, "contraction launch",
-                 [&] { return nwg::launch_contract(contract_args(g, p->U, x, y), s); });
+                 [&] { return launch_contract(g, p->U, x, y, s); });
   }
   int rc = timed(p, 1, s, "input transform launch",
                  [&] { return nwg::launch_input_xform(g, x, p->V, s); });
   if (rc != NWG_OK) return rc;
   rc = timed(p, 2, s, "contraction launch",
-             [&] { return nwg::launch_contract(contract_args(g, p->U, p->V, p->Yh), s); });
+             [&] { return launch_contract(g, p->U, p->V, p->Yh, s); });
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",
                [&] { return nwg::launch_output_xform(g, p->Yh, y, s); });

@@ -98,7 +98,11 @@ struct ContractArgs {
 
 hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s);
 hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s);
-hipError_t launch_contract(const ContractArgs& a, hipStream_t s);
+// depth 0: y[b] = U^T x[b]
+hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s);
+// depth >= 1: Z = level-1 A^T of (U^T V per point); G = P / 16 groups
+hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
+                                 long long G, hipStream_t s);
 hipError_t launch_output_xform(const nwg_plan_info& g, const float* Yh, float* y, hipStream_t s);
 
 }  // namespace nwg

@@ -1,103 +1,71 @@
-// Nested output transformation (Sec. III.B, final step; 2D per Fig. 4 text).
+// Nested output transformation (Sec. III.B, final step; 2D per Fig. 4 text),
+// levels 2..n.  Level 1 is already applied by the contraction, which writes
 //
-// For every tile t and output channel n, the P = 4^(2n) values Yhat[p][n][t]
-// are transformed by A^T of F(2,3) along every axis, giving the output
-// reordered tensor Y[i;k] (i_j, k_j in {0,1}), which is flattened to the
-// M_n x M_n output tile: row sum_j s_{j-1} i_j, column sum_j s_{j-1} k_j,
-// with s_{j-1} = 2^(j-1).  Outputs beyond Ho x Wo are cropped.
+//     Z[g][n][t][2*i1r + i1c],   g = p / 16 (the point's digits above level 1).
 //
-// Reads are Yhat[p][n][t] with consecutive lanes on consecutive tiles
-// (contiguous runs of the T axis).  Each thread reduces the 256 points of
-// one branch through the two innermost levels in registers (16 -> 4 per
-// axis).  At depth >= 3 the 16 level-3 branches of a tile sit in 16
-// different threads; their 4x4 partial outputs go through LDS, where the
-// level-3 A^T combines them, and at depth 4 the level-4 A^T accumulates the
-// 16 level-4 branches in registers over 16 passes.
+// For every tile t and output channel n this applies A^T of F(2,3) along
+// both axes for levels 2..n, giving the output reordered tensor Y[i;k]
+// (i_j, k_j in {0,1}), flattened to the M_n x M_n output tile: row
+// sum_j 2^(j-1) i_j, column sum_j 2^(j-1) k_j.  Outputs beyond Ho x Wo are
+// cropped.
+//
+// Reads are float4 quads Z[g][n][t] with consecutive lanes on consecutive
+// tiles: 256 contiguous bytes per quarter-wave.  Each thread reduces the
+// 16 level-2 groups of one branch in registers (4x4 partial tile).  At depth
+// >= 3 the 16 level-3 branches of a tile sit in 16 different threads; their
+// partial tiles go through LDS, where the level-3 A^T combines them, and at
+// depth 4 the level-4 A^T accumulates the 16 level-4 branches in registers
+// over 16 passes.
 #include "nwg_internal.h"
 
 namespace nwg {
 namespace {
 
-// Two inner levels for one branch: 256 points -> 4x4 partial tile.
-// po[rr][cc], rr = i1r + 2*i2r, cc = i1c + 2*i2c.  yb points at the branch's
-// first point; points are (q2r, q2c, q1r, q1c), most significant first.
-__device__ __forceinline__ void inner2_reduce(const float* __restrict__ yb, size_t pstride,
+// Level 2 for one branch: 16 quads (q2r, q2c) -> 4x4 partial tile
+// po[rr][cc], rr = i1r + 2*i2r, cc = i1c + 2*i2c.  zb points at the branch's
+// first quad for this (n, t); gstride is the distance between groups.
+__device__ __forceinline__ void level2_reduce(const float4* __restrict__ zb, size_t gstride,
                                               float (&po)[4][4]) {
+  float4 v[4][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int q2r = 0; q2r < 4; ++q2r)
 #pragma unroll
-    for (int k = 0; k < 4; ++k) po[i][k] = 0.0f;
+    for (int q2c = 0; q2c < 4; ++q2c) v[q2r][q2c] = zb[(size_t)(q2r * 4 + q2c) * gstride];
+  // along columns: h[q2r][i2c] (float4 over (i1r, i1c))
+  float4 h[4][2];
 #pragma unroll
-  for (int q2r = 0; q2r < 4; ++q2r) {
+  for (int q = 0; q < 4; ++q) {
+    h[q][0] = v[q][0] + v[q][1] + v[q][2];
+    h[q][1] = v[q][1] - v[q][2] - v[q][3];
+  }
 #pragma unroll
-    for (int q2c = 0; q2c < 4; ++q2c) {
-      float v[4][4];
-#pragma unroll
-      for (int q1r = 0; q1r < 4; ++q1r)
-#pragma unroll
-        for (int q1c = 0; q1c < 4; ++q1c)
-          v[q1r][q1c] = yb[(size_t)(q2r * 64 + q2c * 16 + q1r * 4 + q1c) * pstride];
-      // level 1 along columns then rows: 4x4 -> 2x2
-      float h[4][2];
-#pragma unroll
-      for (int q1r = 0; q1r < 4; ++q1r) {
-        h[q1r][0] = v[q1r][0] + v[q1r][1] + v[q1r][2];
-        h[q1r][1] = v[q1r][1] - v[q1r][2] - v[q1r][3];
-      }
-      float e[2][2];
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        e[0][c] = h[0][c] + h[1][c] + h[2][c];
-        e[1][c] = h[1][c] - h[2][c] - h[3][c];
-      }
-      // level 2: add with A^T[i2r][q2r] * A^T[i2c][q2c]
-#pragma unroll
-      for (int i2r = 0; i2r < 2; ++i2r)
-#pragma unroll
-        for (int i2c = 0; i2c < 2; ++i2c) {
-          const float c = at_coef(i2r, q2r) * at_coef(i2c, q2c);
-          if (c != 0.0f) {
-#pragma unroll
-            for (int i1r = 0; i1r < 2; ++i1r)
-#pragma unroll
-              for (int i1c = 0; i1c < 2; ++i1c)
-                po[i1r + 2 * i2r][i1c + 2 * i2c] += c * e[i1r][i1c];
-          }
-        }
-    }
+  for (int i2c = 0; i2c < 2; ++i2c) {
+    const float4 e0 = h[0][i2c] + h[1][i2c] + h[2][i2c];   // i2r = 0
+    const float4 e1 = h[1][i2c] - h[2][i2c] - h[3][i2c];   // i2r = 1
+    po[0][2 * i2c + 0] = e0.x;  po[0][2 * i2c + 1] = e0.y;
+    po[1][2 * i2c + 0] = e0.z;  po[1][2 * i2c + 1] = e0.w;
+    po[2][2 * i2c + 0] = e1.x;  po[2][2 * i2c + 1] = e1.y;
+    po[3][2 * i2c + 0] = e1.z;  po[3][2 * i2c + 1] = e1.w;
   }
 }
 
 // ---- depth 1 and 2: one thread per tile -----------------------------------
 template <int NLEV>
 __global__ __launch_bounds__(256) void output_xform_tile(
-    const float* __restrict__ Yh, float* __restrict__ y, int N, int Ho, int Wo, int th, int tw,
-    int T, long long NT) {
+    const float4* __restrict__ Z, float* __restrict__ y, int N, int Ho, int Wo, int th, int tw,
+    int T, long long gstride) {
   constexpr int Mn = 1 << NLEV;
   const int t = blockIdx.x * 256 + threadIdx.x;
   const int n = blockIdx.y;
   if (t >= T) return;
-  const float* yb = Yh + (size_t)n * T + t;
+  const float4* zb = Z + (size_t)n * T + t;
   float po[4][4];
   if constexpr (NLEV == 2) {
-    inner2_reduce(yb, (size_t)NT, po);
+    level2_reduce(zb, (size_t)gstride, po);
   } else {
-    float v[4][4];
-#pragma unroll
-    for (int q1r = 0; q1r < 4; ++q1r)
-#pragma unroll
-      for (int q1c = 0; q1c < 4; ++q1c) v[q1r][q1c] = yb[(size_t)(q1r * 4 + q1c) * NT];
-    float h[4][2];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      h[q][0] = v[q][0] + v[q][1] + v[q][2];
-      h[q][1] = v[q][1] - v[q][2] - v[q][3];
-    }
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      po[0][c] = h[0][c] + h[1][c] + h[2][c];
-      po[1][c] = h[1][c] - h[2][c] - h[3][c];
-    }
+    const float4 v = zb[0];
+    po[0][0] = v.x;  po[0][1] = v.y;
+    po[1][0] = v.z;  po[1][1] = v.w;
   }
   const int tpi = th * tw;
   const int b = t / tpi;
@@ -119,8 +87,8 @@ __global__ __launch_bounds__(256) void output_xform_tile(
 // ---- depth 3 and 4: 16 tiles x 16 level-3 branches per work-group ---------
 template <int NLEV>
 __global__ __launch_bounds__(256) void output_xform_branches(
-    const float* __restrict__ Yh, float* __restrict__ y, int N, int Ho, int Wo, int th, int tw,
-    int T, long long NT) {
+    const float4* __restrict__ Z, float* __restrict__ y, int N, int Ho, int Wo, int th, int tw,
+    int T, long long gstride) {
   constexpr int Mn = 1 << NLEV;
   constexpr int PASSES = NLEV == 4 ? 16 : 1;
   __shared__ float part[16][16][17];        // [tile][level-3 branch][partial output]
@@ -141,11 +109,11 @@ __global__ __launch_bounds__(256) void output_xform_branches(
 #pragma unroll
         for (int d = 0; d < 2; ++d) acc[a][b][c][d] = 0.0f;
 
-  const float* yslot = Yh + (size_t)slot * 256 * NT + (size_t)n * T + t;
+  const float4* zslot = Z + (size_t)slot * 16 * gstride + (size_t)n * T + t;
   for (int pass = 0; pass < PASSES; ++pass) {
     float po[4][4];
     if (valid) {
-      inner2_reduce(yslot + (size_t)pass * 4096 * NT, (size_t)NT, po);
+      level2_reduce(zslot + (size_t)pass * 256 * gstride, (size_t)gstride, po);
     } else {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -213,25 +181,27 @@ __global__ __launch_bounds__(256) void output_xform_branches(
 
 }  // namespace
 
-hipError_t launch_output_xform(const nwg_plan_info& g, const float* Yh, float* y, hipStream_t s) {
-  const long long NT = (long long)g.N * g.T;
+hipError_t launch_output_xform(const nwg_plan_info& g, const float* Zf, float* y, hipStream_t s) {
+  if ((uintptr_t)Zf & 15) return hipErrorInvalidValue;
+  const float4* Z = reinterpret_cast<const float4*>(Zf);
+  const long long gstride = (long long)g.N * g.T;    // float4 quads between groups
   const int T = (int)g.T;
   if (g.n >= 3) {
     dim3 grid((unsigned)((g.T + 15) / 16), (unsigned)g.N);
     if (g.n == 3)
-      hipLaunchKernelGGL(output_xform_branches<3>, grid, dim3(256), 0, s, Yh, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, NT);
+      hipLaunchKernelGGL(output_xform_branches<3>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo,
+                         g.th, g.tw, T, gstride);
     else
-      hipLaunchKernelGGL(output_xform_branches<4>, grid, dim3(256), 0, s, Yh, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, NT);
+      hipLaunchKernelGGL(output_xform_branches<4>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo,
+                         g.th, g.tw, T, gstride);
   } else {
     dim3 grid((unsigned)((g.T + 255) / 256), (unsigned)g.N);
     if (g.n == 2)
-      hipLaunchKernelGGL(output_xform_tile<2>, grid, dim3(256), 0, s, Yh, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, NT);
+      hipLaunchKernelGGL(output_xform_tile<2>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo,
+                         g.th, g.tw, T, gstride);
     else
-      hipLaunchKernelGGL(output_xform_tile<1>, grid, dim3(256), 0, s, Yh, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, NT);
+      hipLaunchKernelGGL(output_xform_tile<1>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo,
+                         g.th, g.tw, T, gstride);
   }
   return hipGetLastError();
 }

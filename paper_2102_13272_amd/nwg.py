@@ -146,21 +146,21 @@ class Plan:
     def __exit__(self, *exc):
         self.close()
 
-    # shapes of the Winograd-domain buffers (elements)
+    # shapes of the Winograd-domain buffers (quad-interleaved, see include/nwg.h)
     @property
     def u_shape(self):
         i = self.info
-        return (i["P"] if i["n"] else 1, i["M"], i["N"])
+        return (i["P"] // 4, i["M"], i["N"], 4) if i["n"] else (i["M"], i["N"])
 
     @property
     def v_shape(self):
         i = self.info
-        return (i["P"], i["M"], i["T"])
+        return (i["P"] // 4, i["M"], i["T"], 4)
 
     @property
-    def yhat_shape(self):
+    def z_shape(self):
         i = self.info
-        return (i["P"], i["N"], i["T"])
+        return (i["P"] // 16, i["N"], i["T"], 4)
 
     @property
     def y_shape(self):
@@ -183,12 +183,12 @@ class Plan:
         _check(self._lib.nwg_input_transform(self.handle, _ptr(x), _ptr(V), _stream(stream)),
                "nwg_input_transform")
 
-    def contract(self, U, V, Yh, stream=None):
-        _check(self._lib.nwg_contract(self.handle, _ptr(U), _ptr(V), _ptr(Yh), _stream(stream)),
+    def contract(self, U, V, Z, stream=None):
+        _check(self._lib.nwg_contract(self.handle, _ptr(U), _ptr(V), _ptr(Z), _stream(stream)),
                "nwg_contract")
 
-    def output_transform(self, Yh, y, stream=None):
-        _check(self._lib.nwg_output_transform(self.handle, _ptr(Yh), _ptr(y), _stream(stream)),
+    def output_transform(self, Z, y, stream=None):
+        _check(self._lib.nwg_output_transform(self.handle, _ptr(Z), _ptr(y), _stream(stream)),
                "nwg_output_transform")
 
     def set_timing(self, enable: bool):

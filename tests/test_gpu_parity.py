@@ -10,8 +10,8 @@ import pytest
 import torch
 
 from oracle.direct import direct_conv2d
-from oracle.nested import (ewmm, geometry, input_transform, kernel_transform, output_transform,
-                           point_permutation)
+from oracle.nested import (base_f23, ewmm, geometry, input_transform, kernel_transform,
+                           output_transform, point_permutation)
 from paper_2102_13272_amd import nwg
 from paper_2102_13272_amd.workloads import make_case
 from tests.gpu_util import assert_close, dev, run_conv
@@ -58,8 +58,23 @@ def _to_lib_points(a, n):
     return a[..., perm[:, 0], perm[:, 1]]
 
 
+def _quads(a_pxy):
+    """[P][X][Y] -> quad-interleaved [P/4][X][Y][4]."""
+    P, X, Y = a_pxy.shape
+    return np.ascontiguousarray(a_pxy.reshape(P // 4, 4, X, Y).transpose(0, 2, 3, 1))
+
+
+def _level1(yh_pnt):
+    """[P][N][T] -> Z [P/16][N][T][4]: the oracle's A^T along both level-1 digits."""
+    AT = base_f23().AT.astype(np.float64)
+    P, N, T = yh_pnt.shape
+    g = yh_pnt.reshape(P // 16, 4, 4, N, T)
+    z = np.einsum("iq,jr,gqrnt->gntij", AT, AT, g)
+    return np.ascontiguousarray(z.reshape(P // 16, N, T, 4))
+
+
 STAGES = [(1, 3, 4, 12, 10, 3, 1), (2, 4, 3, 13, 11, 6, 2), (1, 3, 5, 20, 19, 11, 5),
-          (1, 2, 3, 24, 20, 31, 15)]
+          (1, 2, 3, 24, 20, 31, 15), (2, 5, 2, 9, 9, 2, 0)]
 
 
 @pytest.mark.parametrize("case", STAGES, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
@@ -73,27 +88,29 @@ def test_stages_match_cpu_nested_reference(case):
     V_ref = input_transform(x, g)                       # (B, th, tw, M, P1, P1)
     Yh_ref = ewmm(U_ref, V_ref)                         # (B, th, tw, N, P1, P1)
     T = B * g.th * g.tw
-    U_lib = _to_lib_points(U_ref, n).transpose(2, 1, 0)                    # (P, M, N)
-    V_lib = _to_lib_points(V_ref.reshape(T, M, g.lv.P1, g.lv.P1), n).transpose(2, 1, 0)
-    Yh_lib = _to_lib_points(Yh_ref.reshape(T, N, g.lv.P1, g.lv.P1), n).transpose(2, 1, 0)
+    U_std = _to_lib_points(U_ref, n).transpose(2, 1, 0)                     # (P, M, N)
+    V_std = _to_lib_points(V_ref.reshape(T, M, g.lv.P1, g.lv.P1), n).transpose(2, 1, 0)
+    Yh_std = _to_lib_points(Yh_ref.reshape(T, N, g.lv.P1, g.lv.P1), n).transpose(2, 1, 0)
+    U_lib, V_lib, Z_lib = _quads(U_std), _quads(V_std), _level1(Yh_std)
 
     with nwg.Plan(B, M, N, H, W, r, pad) as plan:
-        assert plan.info["P"] == U_lib.shape[0] and plan.info["T"] == T
+        assert plan.info["P"] == U_std.shape[0] and plan.info["T"] == T
+        assert plan.info["yhat_bytes"] == 4 * Z_lib.size
         U = torch.empty(plan.u_shape, device="cuda")
         V = torch.empty(plan.v_shape, device="cuda")
-        Yh = torch.empty(plan.yhat_shape, device="cuda")
+        Z = torch.empty(plan.z_shape, device="cuda")
         y = torch.empty(plan.y_shape, device="cuda")
         plan.kernel_transform(dev(w), U)
         plan.input_transform(dev(x), V)
         torch.cuda.synchronize()
         assert_close(U.cpu().numpy(), U_lib, rel_tol=1e-6, abs_frac=1e-6, what="U")
         assert_close(V.cpu().numpy(), V_lib, rel_tol=1e-6, abs_frac=1e-6, what="V")
-        # contraction alone, on the oracle's transformed operands
-        plan.contract(dev(U_lib), dev(V_lib), Yh)
+        # contraction + level-1 output transform, on the oracle's transformed operands
+        plan.contract(dev(U_lib), dev(V_lib), Z)
         torch.cuda.synchronize()
-        assert_close(Yh.cpu().numpy(), Yh_lib, rel_tol=1e-5, abs_frac=1e-5, what="Yhat")
-        # output transform alone, on the oracle's Yhat
-        plan.output_transform(dev(Yh_lib), y)
+        assert_close(Z.cpu().numpy(), Z_lib, rel_tol=1e-5, abs_frac=1e-5, what="Z")
+        # output transform levels 2..n alone, on the oracle's Z
+        plan.output_transform(dev(Z_lib), y)
         torch.cuda.synchronize()
         assert_close(y.cpu().numpy(), output_transform(Yh_ref, g), rel_tol=1e-6, abs_frac=1e-6,
                      what="y")
@@ -102,24 +119,34 @@ def test_stages_match_cpu_nested_reference(case):
 @pytest.mark.parametrize("N,M,T,depth", [(1, 32, 4096, 1), (5, 5, 100, 1), (128, 128, 256, 1),
                                          (64, 64, 392, 1), (3, 7, 33, 1), (32, 1, 300, 1),
                                          (17, 33, 129, 1), (128, 20, 64, 0), (5, 32, 1000, 0),
-                                         (32, 5, 4096, 0)])
+                                         (32, 5, 4096, 0), (96, 40, 70, 2)])
 def test_contraction_matches_numpy(N, M, T, depth):
-    """Yhat[p] = U[p]^T V[p] for ragged shapes, through nwg_contract.
+    """Z = level-1 A^T of (U[p]^T V[p]) for ragged shapes, through nwg_contract.
 
-    Depth 1 (P = 16 points) uses B = T images of 2x2 with r = 2 (one tile
-    each); depth 0 (r = 1) uses one image of 1 x T, where V is x and Yhat is y.
+    Depth 1 (P = 16) uses B = T images of 2x2 with r = 2 (one tile each);
+    depth 2 (P = 256) uses B = T images of 4x4 with r = 4; depth 0 (r = 1)
+    uses one image of 1 x T, where V is x and the result is y.
     """
     rng = np.random.default_rng(N * 1000 + M * 10 + T)
-    plan = nwg.Plan(1, M, N, 1, T, 1, 0) if depth == 0 else nwg.Plan(T, M, N, 2, 2, 2, 0)
-    P = plan.info["P"]
-    assert P == (1 if depth == 0 else 16) and (depth == 0 or plan.info["T"] == T)
-    U = rng.standard_normal((P, M, N))
-    V = rng.standard_normal((P, M, T))
-    ref = np.einsum("pmn,pmt->pnt", U, V)
-    Yh = torch.empty((P, N, T), device="cuda")
-    plan.contract(dev(U), dev(V), Yh)
+    if depth == 0:
+        plan = nwg.Plan(1, M, N, 1, T, 1, 0)
+        U = rng.standard_normal((M, N))
+        V = rng.standard_normal((M, T))
+        ref = U.T @ V
+        out = torch.empty((N, T), device="cuda")
+        plan.contract(dev(U), dev(V), out)
+    else:
+        side = 2 if depth == 1 else 4
+        plan = nwg.Plan(T, M, N, side, side, side, 0)
+        P = plan.info["P"]
+        assert plan.info["n"] == depth and plan.info["T"] == T
+        U = rng.standard_normal((P, M, N))
+        V = rng.standard_normal((P, M, T))
+        ref = _level1(np.einsum("pmn,pmt->pnt", U, V))
+        out = torch.empty(plan.z_shape, device="cuda")
+        plan.contract(dev(_quads(U)), dev(_quads(V)), out)
     torch.cuda.synchronize()
-    assert_close(Yh.cpu().numpy(), ref, rel_tol=1e-5, abs_frac=1e-5, what="contract")
+    assert_close(out.cpu().numpy(), ref, rel_tol=1e-5, abs_frac=1e-5, what="contract")
     plan.close()
 
 
