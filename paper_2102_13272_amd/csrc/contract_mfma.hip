@@ -53,120 +53,134 @@ __device__ __forceinline__ long long xcd_remap(long long i, long long G) {
 // ---------------------------------------------------------------------------
 
 // BK x COLS tile of float4 quads from a [K][ncols] quad matrix into LDS.
-template <int COLS>
+// Each thread owns fixed (k, col) slots; the per-chunk part of the address
+// (quad and K offset) is uniform.  FULL: every tile is in bounds (no checks).
+template <int COLS, bool FULL>
 struct QuadLoader {
+  static_assert(256 % COLS == 0, "a tile row must split evenly over the threads");
   static constexpr int ELEMS = kBK * COLS;
-  static constexpr int PER = (ELEMS + 255) / 256;
+  static constexpr int PER = ELEMS / 256;     // slots per thread, rows RSTEP apart
+  static constexpr int RSTEP = 256 / COLS;
   float4 reg[PER];
+  int off0;     // (tid / COLS) * ld + c0 + tid % COLS
+  int k0row;    // tid / COLS
+  bool colok;   // c0 + tid % COLS < ncols
 
-  __device__ __forceinline__ void load(const float4* __restrict__ src, int ld, int k0, int c0,
-                                       int K, int ncols) {
+  __device__ __forceinline__ void init(int ld, int c0, int ncols) {
+    const int k = threadIdx.x / COLS, col = threadIdx.x % COLS;
+    off0 = k * ld + c0 + col;
+    k0row = k;
+    colok = c0 + col < ncols;
+  }
+
+  // base: uniform pointer of the quad matrix, k0 = first K row of the chunk
+  __device__ __forceinline__ void load(const float4* __restrict__ base, int ld, int k0, int K) {
+    const float4* __restrict__ p = base + (size_t)k0 * ld + off0;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int e = threadIdx.x + i * 256;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (e < ELEMS) {
-        const int k = e / COLS, col = e % COLS;
-        const int gk = k0 + k, gc = c0 + col;
-        if (gk < K && gc < ncols) v = src[(size_t)gk * ld + gc];
+      if (FULL) {
+        reg[i] = p[(size_t)i * RSTEP * ld];
+      } else {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (colok && k0row + i * RSTEP < K - k0) v = p[(size_t)i * RSTEP * ld];
+        reg[i] = v;
       }
-      reg[i] = v;
     }
   }
 
   __device__ __forceinline__ void store(float4 (*dst)[COLS]) const {
+    const int k = threadIdx.x / COLS, col = threadIdx.x % COLS;
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int e = threadIdx.x + i * 256;
-      if (e < ELEMS) dst[e / COLS][e % COLS] = reg[i];
-    }
+    for (int i = 0; i < PER; ++i) dst[k + i * RSTEP][col] = reg[i];
   }
 };
 
-template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(256) void contract_fused(const float4* __restrict__ U,
-                                                      const float4* __restrict__ V,
-                                                      float4* __restrict__ Z, int M, int N, int T,
-                                                      int ntb, int nnb) {
-  constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int FM = WTM / 16, FN = WTN / 16;
-  static_assert(WM * WN == 4, "four waves");
-  static_assert(FM >= 1 && FN >= 1, "wave tile at least 16x16");
-  __shared__ float4 As[2][kBK][BM];
-  __shared__ float4 Bs[2][kBK][BN];
+// Full-tile variant: gfx950 direct global->LDS loads (global_load_lds_dwordx4).
+// Wave w's j-th load covers flat tile elements [(4j + w) * 64, +64); the
+// hardware writes lane l's 16 bytes at the wave's LDS base + 16 l, so the
+// data lands in LDS without passing through registers.  The loads are
+// asynchronous; the barrier at the end of each step waits for them.
+template <int COLS>
+struct DirectLoader {
+  static_assert(256 % COLS == 0, "a tile row must split evenly over the threads");
+  static constexpr int PER = kBK * COLS / 256;
+  static constexpr int RSTEP = 256 / COLS;
+  int off0;
 
-  long long bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int tb = (int)(bid % ntb);
-  bid /= ntb;
-  const int nb = (int)(bid % nnb);
-  const long long g = bid / nnb;
-  const int n0 = nb * BM, c0 = tb * BN;
-  const size_t quadU = (size_t)M * N, quadV = (size_t)M * T;
+  __device__ __forceinline__ void init(int ld, int c0) {
+    off0 = (threadIdx.x / COLS) * ld + c0 + threadIdx.x % COLS;
+  }
 
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int lr = lane & 15, lk = lane >> 4;
+  __device__ __forceinline__ void load(const float4* __restrict__ base, int ld, int k0,
+                                       float4 (*dst)[COLS]) {
+    const float4* p = base + (size_t)k0 * ld + off0;
+    float4* flat = &dst[0][0];
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(p + (size_t)j * RSTEP * ld),
+          (__attribute__((address_space(3))) void*)(flat + j * 256 + wave * 64), 16, 0, 0);
+  }
+};
 
+// One pipeline step: MFMAs on (Ac, Bc) while the next chunk streams into
+// (An, Bn); at the end of a q1r sweep the four products are folded into the
+// level-1 outputs.  The buffers are distinct LDS objects so that the
+// compiler can see that the asynchronous loads into (An, Bn) never alias
+// the reads of (Ac, Bc) and need not be waited for before them.
+template <int BM, int BN, int WM, int WN, bool FULL>
+struct FusedTile {
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int FM = WTM / 16, FN = WTN / 16;
   floatx4 out[4][FM][FN];   // [2*i1r + i1c]
-#pragma unroll
-  for (int o = 0; o < 4; ++o)
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) out[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  floatx4 acc[4][FM][FN];   // [q1c]
+  QuadLoader<BM, FULL> la;
+  QuadLoader<BN, FULL> lb;
+  DirectLoader<BM> da;
+  DirectLoader<BN> db;
 
-  QuadLoader<BM> la;
-  QuadLoader<BN> lb;
-  const int nk = (M + kBK - 1) / kBK;
+  __device__ __forceinline__ void prefetch(const float4* Ub, const float4* Vb, int N, int T,
+                                           int k0, int M, float4 (*An)[BM], float4 (*Bn)[BN]) {
+    if (FULL) {
+      da.load(Ub, N, k0, An);
+      db.load(Vb, T, k0, Bn);
+    } else {
+      la.load(Ub, N, k0, M);
+      lb.load(Vb, T, k0, M);
+    }
+  }
 
-  for (int q1r = 0; q1r < 4; ++q1r) {
-    const float4* __restrict__ Uq = U + (size_t)(4 * g + q1r) * quadU;
-    const float4* __restrict__ Vq = V + (size_t)(4 * g + q1r) * quadV;
-    floatx4 acc[4][FM][FN];   // [q1c]
+  __device__ __forceinline__ void commit(float4 (*An)[BM], float4 (*Bn)[BN]) {
+    if (!FULL) {
+      la.store(An);
+      lb.store(Bn);
+    }
+  }
+
+  __device__ __forceinline__ void compute(const float4 (*Ac)[BM], const float4 (*Bc)[BN], int wm,
+                                          int wn, int lr, int lk) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
+    for (int kk = 0; kk < kBK / 4; ++kk) {
+      float4 af[FM], bf[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[i] = Ac[kk * 4 + lk][wm * WTM + i * 16 + lr];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bf[j] = Bc[kk * 4 + lk][wn * WTN + j * 16 + lr];
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[c][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    la.load(Uq, N, 0, n0, M, N);
-    lb.load(Vq, T, 0, c0, M, T);
-    la.store(As[0]);
-    lb.store(Bs[0]);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int cur = kt & 1;
-      const bool more = kt + 1 < nk;
-      if (more) {
-        la.load(Uq, N, (kt + 1) * kBK, n0, M, N);
-        lb.load(Vq, T, (kt + 1) * kBK, c0, M, T);
-      }
-#pragma unroll
-      for (int kk = 0; kk < kBK / 4; ++kk) {
-        float4 af[FM], bf[FN];
-#pragma unroll
-        for (int i = 0; i < FM; ++i) af[i] = As[cur][kk * 4 + lk][wm * WTM + i * 16 + lr];
-#pragma unroll
-        for (int j = 0; j < FN; ++j) bf[j] = Bs[cur][kk * 4 + lk][wn * WTN + j * 16 + lr];
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j) {
-            acc[0][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].x, bf[j].x, acc[0][i][j], 0, 0, 0);
-            acc[1][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].y, bf[j].y, acc[1][i][j], 0, 0, 0);
-            acc[2][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].z, bf[j].z, acc[2][i][j], 0, 0, 0);
-            acc[3][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].w, bf[j].w, acc[3][i][j], 0, 0, 0);
-          }
-      }
-      if (more) {
-        la.store(As[cur ^ 1]);
-        lb.store(Bs[cur ^ 1]);
-      }
-      __syncthreads();
+        for (int j = 0; j < FN; ++j) {
+          acc[0][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].x, bf[j].x, acc[0][i][j], 0, 0, 0);
+          acc[1][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].y, bf[j].y, acc[1][i][j], 0, 0, 0);
+          acc[2][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].z, bf[j].z, acc[2][i][j], 0, 0, 0);
+          acc[3][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].w, bf[j].w, acc[3][i][j], 0, 0, 0);
+        }
     }
-    // level 1 along columns (q1c -> i1c), then along rows with A^T[i1r][q1r]
+  }
+
+  // level 1 along columns (q1c -> i1c), then along rows with A^T[i1r][q1r]
+  __device__ __forceinline__ void fold(int q1r) {
     const float r0 = at_coef(0, q1r), r1 = at_coef(1, q1r);
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -178,7 +192,86 @@ __global__ __launch_bounds__(256) void contract_fused(const float4* __restrict__
         out[1][i][j] += r0 * z1;
         out[2][i][j] += r1 * z0;
         out[3][i][j] += r1 * z1;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
+  }
+};
+
+template <int BM, int BN, int WM, int WN, bool FULL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void contract_fused(
+    const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
+    int N, int T, int ntb, int nnb) {
+  using Tile = FusedTile<BM, BN, WM, WN, FULL>;
+  constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
+  static_assert(WM * WN == 4, "four waves");
+  static_assert(FM >= 1 && FN >= 1, "wave tile at least 16x16");
+  __shared__ float4 A0[kBK][BM], A1[kBK][BM];
+  __shared__ float4 B0[kBK][BN], B1[kBK][BN];
+
+  long long bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int tb = (int)(bid % ntb);
+  bid /= ntb;
+  const int nb = (int)(bid % nnb);
+  const long long g = bid / nnb;
+  const int n0 = nb * BM, c0 = tb * BN;
+  const size_t quadU = (size_t)M * N, quadV = (size_t)M * T;
+  const float4* __restrict__ Ug = U + (size_t)(4 * g) * quadU;
+  const float4* __restrict__ Vg = V + (size_t)(4 * g) * quadV;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int lr = lane & 15, lk = lane >> 4;
+
+  Tile tile;
+#pragma unroll
+  for (int o = 0; o < 4; ++o)
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        tile.out[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        tile.acc[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+  if (FULL) {
+    tile.da.init(N, n0);
+    tile.db.init(T, c0);
+  } else {
+    tile.la.init(N, n0, N);
+    tile.lb.init(T, c0, T);
+  }
+
+  const int nk = (M + kBK - 1) / kBK;
+  const int total = 4 * nk;                 // (q1r, K chunk) pairs, one pipeline
+  tile.prefetch(Ug, Vg, N, T, 0, M, A0, B0);
+  tile.commit(A0, B0);
+  __syncthreads();
+  // chunk it -> (q1r, kt); even chunks live in (A0, B0), odd ones in (A1, B1)
+  for (int it = 0; it < total; it += 2) {
+    {
+      const int q1r = it / nk, kt = it % nk;
+      const int nx = it + 1;
+      if (nx < total)
+        tile.prefetch(Ug + (size_t)(nx / nk) * quadU, Vg + (size_t)(nx / nk) * quadV, N, T,
+                      (nx % nk) * kBK, M, A1, B1);
+      tile.compute(A0, B0, wm, wn, lr, lk);
+      if (kt + 1 == nk) tile.fold(q1r);
+      if (nx < total) tile.commit(A1, B1);
+      __syncthreads();
+    }
+    if (it + 1 < total) {
+      const int c = it + 1;
+      const int q1r = c / nk, kt = c % nk;
+      const int nx = c + 1;
+      if (nx < total)
+        tile.prefetch(Ug + (size_t)(nx / nk) * quadU, Vg + (size_t)(nx / nk) * quadV, N, T,
+                      (nx % nk) * kBK, M, A0, B0);
+      tile.compute(A1, B1, wm, wn, lr, lk);
+      if (kt + 1 == nk) tile.fold(q1r);
+      if (nx < total) tile.commit(A0, B0);
+      __syncthreads();
+    }
   }
 
   float4* __restrict__ Zg = Z + (size_t)g * N * T;
@@ -187,13 +280,13 @@ __global__ __launch_bounds__(256) void contract_fused(const float4* __restrict__
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const int row = n0 + wm * WTM + i * 16 + lk * 4 + v;
-      if (row >= N) continue;
+      if (!FULL && row >= N) continue;
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = c0 + wn * WTN + j * 16 + lr;
-        if (col < T)
-          Zg[(size_t)row * T + col] =
-              make_float4(out[0][i][j][v], out[1][i][j][v], out[2][i][j][v], out[3][i][j][v]);
+        if (FULL || col < T)
+          Zg[(size_t)row * T + col] = make_float4(tile.out[0][i][j][v], tile.out[1][i][j][v],
+                                                  tile.out[2][i][j][v], tile.out[3][i][j][v]);
       }
     }
   }
@@ -207,8 +300,14 @@ hipError_t launch_fused(const float* U, const float* V, float* Z, int M, int N, 
   const long long blocks = (long long)ntb * nnb * G;
   if (blocks <= 0 || blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN>), dim3((unsigned)blocks), dim3(256), 0, s,
-                     (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
+  if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
+  const bool full = N % BM == 0 && T % BN == 0 && M % kBK == 0;
+  if (full)
+    hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN, true>), dim3((unsigned)blocks), dim3(256),
+                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
+  else
+    hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN, false>), dim3((unsigned)blocks), dim3(256),
+                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
   return hipGetLastError();
 }
 

@@ -119,7 +119,10 @@ def test_stages_match_cpu_nested_reference(case):
 @pytest.mark.parametrize("N,M,T,depth", [(1, 32, 4096, 1), (5, 5, 100, 1), (128, 128, 256, 1),
                                          (64, 64, 392, 1), (3, 7, 33, 1), (32, 1, 300, 1),
                                          (17, 33, 129, 1), (128, 20, 64, 0), (5, 32, 1000, 0),
-                                         (32, 5, 4096, 0), (96, 40, 70, 2)])
+                                         (32, 5, 4096, 0), (96, 40, 70, 2),
+                                         # full tiles (direct global->LDS path) per tile shape
+                                         (64, 32, 128, 1), (16, 16, 128, 2), (32, 48, 256, 1),
+                                         (128, 64, 192, 1)])
 def test_contraction_matches_numpy(N, M, T, depth):
     """Z = level-1 A^T of (U[p]^T V[p]) for ragged shapes, through nwg_contract.
 
