@@ -17,12 +17,11 @@
 //                  stages each of its 16 tiles' windows separately in LDS
 //                  (odd window stride, so that the 16 tiles of a
 //                  quarter-wave read 16 different banks).  At depth 4 the
-//                  work-group also owns one level-4 row branch q4r: the
-//                  fill already applies that B^T row along the window's
-//                  rows (46 -> 22 rows), and the threads loop over the four
-//                  level-4 column branches.  A branch's 10 x 10 sub-window
-//                  is then a signed sum of 2 x 2 (depth 3) or 2 x 4 (depth
-//                  4) shifted window reads at compile-time offsets.
+//                  work-group also owns one level-4 branch (q4r, q4c): the
+//                  fill already applies those B^T rows along both axes of
+//                  the 46 x 46 window (-> 22 x 22).  A branch's 10 x 10
+//                  sub-window is then a signed sum of 2 x 2 level-3 shifted
+//                  window reads at compile-time offsets.
 //
 // V is quad-interleaved, V[p/4][m][t][p%4] (p%4 is the level-1 column digit
 // q1c): every thread stores float4 quads, and the consecutive tiles of a
@@ -142,44 +141,94 @@ __global__ __launch_bounds__(256) void input_xform_tiles(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
     int tw, int T, long long qstride) {
   constexpr int Mn = 1 << NLEV;
-  constexpr int Ln = 3 * Mn - 2;
-  constexpr int ROWS = 22;                   // L_3: rows left after the level-4 row branch
-  constexpr int COLS = Ln;
-  constexpr int WS = ROWS * COLS + 1;        // odd window stride: 16 tiles -> 16 banks
-  constexpr int NCT = NLEV == 4 ? 4 : 2;     // column taps of the outer levels
+  constexpr int L3 = 22;                     // window side left for levels 1..3
+  constexpr int WS = L3 * L3 + 1;            // odd window stride: 16 tiles -> 16 banks
   extern __shared__ float lds[];
-  const int m = blockIdx.y;
-  const int q4r = blockIdx.z;                // level-4 row branch (depth 4), else 0
-  const int t0 = blockIdx.x * 16;
+  // Work-group -> (level-4 branch q4, 16-tile chunk, channel m), q4 fastest.
+  // The dispatcher deals work-groups round-robin over the 8 XCDs; this
+  // numbering gives each XCD a contiguous range, so the 16 branches that
+  // re-read the same input windows run back to back on one XCD and find
+  // them in its L2.
+  long long lid;
+  {
+    const long long G = (long long)gridDim.x, i = blockIdx.x;
+    const long long q = G / 8, rem = G % 8, xcd = i % 8, sl = i / 8;
+    lid = xcd < rem ? xcd * (q + 1) + sl : rem * (q + 1) + (xcd - rem) * q + sl;
+  }
+  const int q4 = NLEV == 4 ? (int)(lid % 16) : 0;   // level-4 branch (q4r, q4c), else 0
+  const long long rest = NLEV == 4 ? lid / 16 : lid;
+  const int nchunk = (T + 15) / 16;
+  const int t0 = (int)(rest % nchunk) * 16;
+  const int m = (int)(rest / nchunk);
+  const int q4r = q4 >> 2, q4c = q4 & 3;
   const int tpi = th * tw;
-  // fill: per tile, rows u in [0,22) of the window after the level-4 row
-  // transform (depth 4) or the window itself (depth 3)
-  const int a4a = 8 * bt_tap0(q4r), a4b = 8 * bt_tap1(q4r);
-  const float s4a = bt_sign0(q4r), s4b = bt_sign1(q4r);
-  for (int e = threadIdx.x; e < 16 * ROWS * COLS; e += 256) {
-    const int tl = e / (ROWS * COLS);
-    const int rem = e - tl * (ROWS * COLS);
-    const int row = rem / COLS, col = rem - row * COLS;
-    const int t = t0 + tl;
-    float v = 0.0f;
+  // fill: per tile, the 22 x 22 window after the level-4 B^T rows q4r (along
+  // the rows) and q4c (along the columns) at depth 4, the window itself at 3
+  const int a4r0 = 8 * bt_tap0(q4r), a4r1 = 8 * bt_tap1(q4r);
+  const int a4c0 = 8 * bt_tap0(q4c), a4c1 = 8 * bt_tap1(q4c);
+  const float s4r0 = bt_sign0(q4r), s4r1 = bt_sign1(q4r);
+  const float s4c0 = bt_sign0(q4c), s4c1 = bt_sign1(q4c);
+  // 16 threads per tile: thread (ftl, fj) fills columns fj and fj + 16 of
+  // tile ftl's window, walking its 22 rows with independent loads
+  {
+    const int ftl = threadIdx.x >> 4, fj = threadIdx.x & 15;
+    const int t = t0 + ftl;
     if (t < T) {
       const int b = t / tpi;
       const int r2 = t - b * tpi;
       const int ty = r2 / tw, tx = r2 - ty * tw;
-      const int gc = tx * Mn - pad + col;
-      const float* xp = x + ((size_t)b * M + m) * H * W;
-      if (gc >= 0 && gc < W) {
-        const int gr0 = ty * Mn - pad + row;
+      const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
+      const int gr0 = ty * Mn - pad, gc0 = tx * Mn - pad;
+      float* dst = lds + ftl * WS;
+      // Loads are unconditional, from addresses clamped into the image, and
+      // masked afterwards: no branches, so a whole column of loads can be in
+      // flight at once.
+      auto clampi = [](int v, int hi) { return v < 0 ? 0 : (v > hi ? hi : v); };
+#pragma unroll
+      for (int c = fj; c < L3; c += 16) {
+        const int gc = gc0 + c;
         if (NLEV == 4) {
-          const int ga = gr0 + a4a, gb = gr0 + a4b;
-          if (ga >= 0 && ga < H) v += s4a * xp[(size_t)ga * W + gc];
-          if (gb >= 0 && gb < H) v += s4b * xp[(size_t)gb * W + gc];
+          const int ca = gc + a4c0, cb = gc + a4c1;
+          const float mca = (ca >= 0 && ca < W) ? s4c0 : 0.0f;
+          const float mcb = (cb >= 0 && cb < W) ? s4c1 : 0.0f;
+          const int cac = clampi(ca, W - 1), cbc = clampi(cb, W - 1);
+          constexpr int RB = 11;   // rows per batch: 4*RB loads in flight
+#pragma unroll
+          for (int r0 = 0; r0 < L3; r0 += RB) {
+            float va[RB], vb[RB], vc[RB], vd[RB];
+#pragma unroll
+            for (int k = 0; k < RB; ++k) {
+              const int row = r0 + k;
+              const int rac = clampi(gr0 + row + a4r0, H - 1), rbc = clampi(gr0 + row + a4r1, H - 1);
+              va[k] = xp[(size_t)rac * W + cac];
+              vb[k] = xp[(size_t)rac * W + cbc];
+              vc[k] = xp[(size_t)rbc * W + cac];
+              vd[k] = xp[(size_t)rbc * W + cbc];
+            }
+#pragma unroll
+            for (int k = 0; k < RB; ++k) {
+              const int row = r0 + k;
+              const int ra = gr0 + row + a4r0, rb = gr0 + row + a4r1;
+              const float mra = (ra >= 0 && ra < H) ? s4r0 : 0.0f;
+              const float mrb = (rb >= 0 && rb < H) ? s4r1 : 0.0f;
+              dst[row * L3 + c] = mra * (mca * va[k] + mcb * vb[k]) +
+                                  mrb * (mca * vc[k] + mcb * vd[k]);
+            }
+          }
         } else {
-          if (gr0 >= 0 && gr0 < H) v = xp[(size_t)gr0 * W + gc];
+          const float mc = (gc >= 0 && gc < W) ? 1.0f : 0.0f;
+          const int gcc = clampi(gc, W - 1);
+          float va[L3];
+#pragma unroll
+          for (int row = 0; row < L3; ++row) va[row] = xp[(size_t)clampi(gr0 + row, H - 1) * W + gcc];
+#pragma unroll
+          for (int row = 0; row < L3; ++row) {
+            const int gr = gr0 + row;
+            dst[row * L3 + c] = (gr >= 0 && gr < H) ? mc * va[row] : 0.0f;
+          }
         }
       }
     }
-    lds[tl * WS + rem] = v;
   }
   __syncthreads();
   const int tl = threadIdx.x & 15;
@@ -188,43 +237,27 @@ __global__ __launch_bounds__(256) void input_xform_tiles(
   if (t >= T) return;                       // no barrier below
   const int q3r = slot >> 2, q3c = slot & 3;
   const float* win = lds + tl * WS;
+  // level 3 (stride 4): two row taps and two column taps
   const int ro0 = 4 * bt_tap0(q3r), ro1 = 4 * bt_tap1(q3r);
+  const int co0 = 4 * bt_tap0(q3c), co1 = 4 * bt_tap1(q3c);
   const float rs0 = bt_sign0(q3r), rs1 = bt_sign1(q3r);
-  constexpr int PASSES = NLEV == 4 ? 4 : 1;
-
-  for (int pass = 0; pass < PASSES; ++pass) {
-    const int q4c = pass;
-    // column taps: level 3 (stride 4) and, at depth 4, level 4 (stride 8)
-    int co[NCT];
-    float cs[NCT];
+  const float cs0 = bt_sign0(q3c), cs1 = bt_sign1(q3c);
+  const float* w00 = win + ro0 * L3 + co0;
+  const float* w01 = win + ro0 * L3 + co1;
+  const float* w10 = win + ro1 * L3 + co0;
+  const float* w11 = win + ro1 * L3 + co1;
+  float S[10][10];
 #pragma unroll
-    for (int k = 0; k < NCT; ++k) {
-      const int k3 = k & 1, k4 = k >> 1;
-      co[k] = 4 * (k3 ? bt_tap1(q3c) : bt_tap0(q3c));
-      cs[k] = k3 ? bt_sign1(q3c) : bt_sign0(q3c);
-      if (NLEV == 4) {
-        co[k] += 8 * (k4 ? bt_tap1(q4c) : bt_tap0(q4c));
-        cs[k] *= k4 ? bt_sign1(q4c) : bt_sign0(q4c);
-      }
+  for (int i = 0; i < 10; ++i)
+#pragma unroll
+    for (int j = 0; j < 10; ++j) {
+      const float a = cs0 * w00[i * L3 + j] + cs1 * w01[i * L3 + j];
+      const float c = cs0 * w10[i * L3 + j] + cs1 * w11[i * L3 + j];
+      S[i][j] = rs0 * a + rs1 * c;
     }
-    float S[10][10];
-#pragma unroll
-    for (int i = 0; i < 10; ++i) {
-#pragma unroll
-      for (int j = 0; j < 10; ++j) {
-        float a = 0.0f, c = 0.0f;
-#pragma unroll
-        for (int k = 0; k < NCT; ++k) {
-          a += cs[k] * win[(ro0 + i) * COLS + co[k] + j];
-          c += cs[k] * win[(ro1 + i) * COLS + co[k] + j];
-        }
-        S[i][j] = rs0 * a + rs1 * c;
-      }
-    }
-    // 256-point block of this branch: (q4r, q4c, q3r, q3c) at depth 4, (q3r, q3c) at depth 3
-    const int branch = NLEV == 4 ? (q4r * 64 + q4c * 16 + slot) : slot;
-    inner2_store(S, V + (size_t)branch * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
-  }
+  // 256-point block of this branch: (q4r, q4c, q3r, q3c) at depth 4, (q3r, q3c) at depth 3
+  const int branch = q4 * 16 + slot;
+  inner2_store(S, V + (size_t)branch * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
 }
 
 }  // namespace
@@ -235,28 +268,16 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
   const long long qstride = (long long)g.M * g.T;   // float4 quads between consecutive quads
   const int T = (int)g.T;
   if (g.n >= 3) {
-    const int Ln = 3 * (1 << g.n) - 2;
-    const size_t lds = (size_t)16 * (22 * Ln + 1) * sizeof(float);
-    int dev = 0, max_lds = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess)
-      e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-    if (e != hipSuccess) return e;
-    if ((size_t)max_lds < lds) return hipErrorInvalidConfiguration;
-    dim3 grid((unsigned)((g.T + 15) / 16), (unsigned)g.M, g.n == 4 ? 4u : 1u);
-    if (g.n == 3) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_tiles<3>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      if (e != hipSuccess) return e;
+    const size_t lds = (size_t)16 * (22 * 22 + 1) * sizeof(float);
+    const long long nwg = (g.T + 15) / 16 * g.M * (g.n == 4 ? 16 : 1);
+    if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
+    dim3 grid((unsigned)nwg);
+    if (g.n == 3)
       hipLaunchKernelGGL(input_xform_tiles<3>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
                          g.pad, g.th, g.tw, T, qstride);
-    } else {
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_tiles<4>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      if (e != hipSuccess) return e;
+    else
       hipLaunchKernelGGL(input_xform_tiles<4>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
                          g.pad, g.th, g.tw, T, qstride);
-    }
   } else {
     const int Mn = 1 << g.n, Ln = 3 * Mn - 2;
     // tiles per work-group: 256, or 64 when that leaves too few work-groups

@@ -91,7 +91,10 @@ __global__ __launch_bounds__(256) void output_xform_branches(
     int T, long long gstride) {
   constexpr int Mn = 1 << NLEV;
   constexpr int PASSES = NLEV == 4 ? 16 : 1;
-  __shared__ float part[16][16][17];        // [tile][level-3 branch][partial output]
+  // [tile][level-3 branch][partial output]; odd tile stride (16*17+1): the
+  // 16 tiles of a quarter-wave hit 16 different banks
+  constexpr int TS = 16 * 17 + 1;
+  __shared__ float part[16 * TS];
   const int n = blockIdx.y;
   const int tl = threadIdx.x & 15;
   const int slot = threadIdx.x >> 4;
@@ -123,14 +126,14 @@ __global__ __launch_bounds__(256) void output_xform_branches(
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int k = 0; k < 4; ++k) part[tl][slot][i * 4 + k] = po[i][k];
+      for (int k = 0; k < 4; ++k) part[tl * TS + slot * 17 + i * 4 + k] = po[i][k];
     __syncthreads();
     // level 3 across the 16 branches of tile tl, for partial output e
     float pv[4][4];
 #pragma unroll
     for (int q3r = 0; q3r < 4; ++q3r)
 #pragma unroll
-      for (int q3c = 0; q3c < 4; ++q3c) pv[q3r][q3c] = part[tl][q3r * 4 + q3c][e];
+      for (int q3c = 0; q3c < 4; ++q3c) pv[q3r][q3c] = part[tl * TS + (q3r * 4 + q3c) * 17 + e];
     const int q4r = pass >> 2, q4c = pass & 3;
 #pragma unroll
     for (int i3r = 0; i3r < 2; ++i3r)
