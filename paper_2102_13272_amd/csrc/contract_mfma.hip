@@ -21,8 +21,9 @@
 // operand of all four points, and four accumulator sets take the four GEMMs.
 // After the K loop the four products are folded into the 2x2 level-1
 // outputs.  Two pipelines:
-//   * deep (full 64x64 tiles, M a multiple of 32): four LDS stages of 8
-//     channels filled by direct global->LDS loads, three chunks in flight;
+//   * deep (full 64x128 or 64x64 tiles, M a multiple of 32; 8 or 4 waves):
+//     four LDS stages of 8 channels filled by direct global->LDS loads,
+//     three chunks in flight;
 //   * general (any shape): two LDS stages of 16 channels, direct loads for
 //     full tiles, bounds-checked register loads for ragged ones.
 // Without global loads the deep kernel reaches 93 % of the fp32 MFMA peak;
@@ -315,11 +316,12 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int BKD, int COLS>
+template <int BKD, int COLS, int NT>
 struct DeepLoader {
-  static_assert(256 % COLS == 0, "a tile row must split evenly over the threads");
-  static constexpr int PER = BKD * COLS / 256;   // loads per thread per chunk
-  static constexpr int RSTEP = 256 / COLS;
+  static_assert(NT % COLS == 0, "a tile row must split evenly over the threads");
+  static_assert((BKD * COLS) % NT == 0, "a tile must split evenly over the threads");
+  static constexpr int PER = BKD * COLS / NT;   // loads per thread per chunk
+  static constexpr int RSTEP = NT / COLS;
   int off0;
   __device__ __forceinline__ void init(int ld, int c0) {
     off0 = (threadIdx.x / COLS) * ld + c0 + threadIdx.x % COLS;
@@ -333,19 +335,20 @@ struct DeepLoader {
     for (int j = 0; j < PER; ++j)
       __builtin_amdgcn_global_load_lds(
           (const void*)(p + (size_t)j * RSTEP * ld),
-          (__attribute__((address_space(3))) void*)(flat + j * 256 + wave * 64), 16, 0, 0);
+          (__attribute__((address_space(3))) void*)(flat + j * NT + wave * 64), 16, 0, 0);
   }
 };
 
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES>
 struct DeepTile {
+  static constexpr int NT = 64 * WM * WN;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
   static constexpr int FM = WTM / 16, FN = WTN / 16;
-  static constexpr int LPC = DeepLoader<BKD, BM>::PER + DeepLoader<BKD, BN>::PER;
+  static constexpr int LPC = DeepLoader<BKD, BM, NT>::PER + DeepLoader<BKD, BN, NT>::PER;
   floatx4 out[4][FM][FN];
   floatx4 acc[4][FM][FN];
-  DeepLoader<BKD, BM> da;
-  DeepLoader<BKD, BN> db;
+  DeepLoader<BKD, BM, NT> da;
+  DeepLoader<BKD, BN, NT> db;
   const float4* Ug;
   const float4* Vg;
   size_t quadU, quadV;
@@ -409,13 +412,12 @@ struct DeepTile {
 };
 
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void contract_deep(const float4* __restrict__ U,
-                                                     const float4* __restrict__ V,
-                                                     float4* __restrict__ Z, int M, int N, int T,
-                                                     int ntb, int nnb) {
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2))) void contract_deep(
+    const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
+    int N, int T, int ntb, int nnb) {
   using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
-  static_assert(WM * WN == 4, "four waves");
+  static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
   static_assert(STAGES >= 2 && STAGES <= 4, "2 to 4 stages");
   __shared__ float4 A0[BKD][BM], A1[BKD][BM], A2[STAGES > 2 ? BKD : 1][BM],
       A3[STAGES > 3 ? BKD : 1][BM];
@@ -506,8 +508,8 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
   hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES>), dim3((unsigned)blocks),
-                     dim3(256), 0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T,
-                     ntb, nnb);
+                     dim3(64 * WM * WN), 0, s, (const float4*)U, (const float4*)V, (float4*)Z,
+                     M, N, T, ntb, nnb);
   return hipGetLastError();
 }
 
@@ -693,7 +695,10 @@ hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s) {
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
                                  long long G, hipStream_t s) {
   // full 64x64 tiles and whole 4-stage K sweeps: the deep pipeline
-  if (M % 32 == 0 && N % 64 == 0 && T % 64 == 0) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
+  if (M % 32 == 0 && N % 64 == 0) {
+    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s);
+    if (T % 64 == 0) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
+  }
   if (N <= 16) return launch_fused<16, 128, 1, 4>(U, V, Z, M, N, T, G, s);
   if (N <= 32) return launch_fused<32, 128, 1, 4>(U, V, Z, M, N, T, G, s);
   return launch_fused<64, 64, 2, 2>(U, V, Z, M, N, T, G, s);

@@ -139,7 +139,7 @@ __global__ __launch_bounds__(256) void input_xform_box(
 template <int NLEV>
 __global__ __launch_bounds__(256) void input_xform_tiles(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
-    int tw, int T, long long qstride) {
+    int tw, int T, long long qstride, int q4_0, int nq4) {
   constexpr int Mn = 1 << NLEV;
   constexpr int L3 = 22;                     // window side left for levels 1..3
   constexpr int WS = L3 * L3 + 1;            // odd window stride: 16 tiles -> 16 banks
@@ -155,8 +155,9 @@ __global__ __launch_bounds__(256) void input_xform_tiles(
     const long long q = G / 8, rem = G % 8, xcd = i % 8, sl = i / 8;
     lid = xcd < rem ? xcd * (q + 1) + sl : rem * (q + 1) + (xcd - rem) * q + sl;
   }
-  const int q4 = NLEV == 4 ? (int)(lid % 16) : 0;   // level-4 branch (q4r, q4c), else 0
-  const long long rest = NLEV == 4 ? lid / 16 : lid;
+  // level-4 branch (q4r, q4c) in [q4_0, q4_0 + nq4), else 0
+  const int q4 = NLEV == 4 ? q4_0 + (int)(lid % nq4) : 0;
+  const long long rest = NLEV == 4 ? lid / nq4 : lid;
   const int nchunk = (T + 15) / 16;
   const int t0 = (int)(rest % nchunk) * 16;
   const int m = (int)(rest / nchunk);
@@ -262,23 +263,34 @@ __global__ __launch_bounds__(256) void input_xform_tiles(
 
 }  // namespace
 
-hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf, hipStream_t s) {
+hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf, hipStream_t s,
+                              int part, int nparts) {
   float4* V = reinterpret_cast<float4*>(Vf);
   if ((uintptr_t)Vf & 15) return hipErrorInvalidValue;
   const long long qstride = (long long)g.M * g.T;   // float4 quads between consecutive quads
   const int T = (int)g.T;
   if (g.n >= 3) {
     const size_t lds = (size_t)16 * (22 * 22 + 1) * sizeof(float);
-    const long long nwg = (g.T + 15) / 16 * g.M * (g.n == 4 ? 16 : 1);
+    // depth 4: part k of nparts covers level-4 branches [16k/nparts, 16(k+1)/nparts)
+    int q4_0 = 0, nq4 = 1;
+    if (g.n == 4) {
+      if (nparts < 1 || 16 % nparts || part < 0 || part >= nparts) return hipErrorInvalidValue;
+      nq4 = 16 / nparts;
+      q4_0 = part * nq4;
+    } else if (nparts != 1) {
+      return hipErrorInvalidValue;
+    }
+    const long long nwg = (g.T + 15) / 16 * g.M * nq4;
     if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
     dim3 grid((unsigned)nwg);
     if (g.n == 3)
       hipLaunchKernelGGL(input_xform_tiles<3>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
-                         g.pad, g.th, g.tw, T, qstride);
+                         g.pad, g.th, g.tw, T, qstride, q4_0, nq4);
     else
       hipLaunchKernelGGL(input_xform_tiles<4>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
-                         g.pad, g.th, g.tw, T, qstride);
+                         g.pad, g.th, g.tw, T, qstride, q4_0, nq4);
   } else {
+    if (nparts != 1) return hipErrorInvalidValue;
     const int Mn = 1 << g.n, Ln = 3 * Mn - 2;
     // tiles per work-group: 256, or 64 when that leaves too few work-groups
     int tpb = 256;

@@ -97,7 +97,10 @@ struct ContractArgs {
 };
 
 hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s);
-hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s);
+// part/nparts: at depth 4, the level-4 branches [16 part/nparts, 16 (part+1)/nparts)
+// (V quads [4096 part/nparts, ...)); other depths take nparts = 1
+hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s,
+                              int part = 0, int nparts = 1);
 // depth 0: y[b] = U^T x[b]
 hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s);
 // depth >= 1: Z = level-1 A^T of (U^T V per point); G = P / 16 groups

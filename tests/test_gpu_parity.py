@@ -122,7 +122,7 @@ def test_stages_match_cpu_nested_reference(case):
                                          (32, 5, 4096, 0), (96, 40, 70, 2),
                                          # full tiles (direct global->LDS path) per tile shape
                                          (64, 32, 128, 1), (16, 16, 128, 2), (32, 48, 256, 1),
-                                         (128, 64, 192, 1)])
+                                         (128, 64, 192, 1), (64, 96, 256, 1), (128, 32, 128, 2)])
 def test_contraction_matches_numpy(N, M, T, depth):
     """Z = level-1 A^T of (U[p]^T V[p]) for ragged shapes, through nwg_contract.
 
