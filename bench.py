@@ -80,6 +80,58 @@ def measured_traffic(workload: str, stage: str):
     return ent.get("hbm_bytes_per_launch")
 
 
+STAGE_OF_KERNEL = [("contract", "contraction"), ("gemm_mfma", "contraction"),
+                   ("input_xform", "input_transform"), ("output_xform", "output_transform"),
+                   ("kernel_xform", "kernel_transform")]
+
+
+def traffic_from_counters(workload: str, fetch_csv: str, write_csv: str, copy_mib: int):
+    """HBM bytes per launch of each stage from two rocprofv3 --pmc runs.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by what the same
+    counters read for the plain device-to-device copy of `copy_mib` MiB that
+    `--calibrate-copy-mib` performs at the start of the profiled run.
+    Writes profiles/traffic_<workload>.json and returns its content.
+    """
+    import csv
+    from collections import defaultdict
+
+    def per_kernel(path, counter):
+        vals = defaultdict(list)
+        with open(path) as fh:
+            for row in csv.DictReader(fh):
+                if row["Counter_Name"] == counter:
+                    vals[row["Kernel_Name"]].append(float(row["Counter_Value"]))
+        return vals
+
+    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    copy_bytes = copy_mib * (1 << 20)
+    cf = [v for k, v in fetch.items() if "copyBuffer" in k]
+    cw = [v for k, v in write.items() if "copyBuffer" in k]
+    if not cf or not cw:
+        raise SystemExit("no copy-kernel dispatch in the counter files (run with --calibrate-copy-mib)")
+    fscale = copy_bytes / (cf[0][0] * 1024.0)
+    wscale = copy_bytes / (cw[0][0] * 1024.0)
+    out = {"workload": workload, "copy_calibration_bytes": copy_bytes,
+           "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4), "kernels": {}}
+    for name in fetch:
+        stage = next((st for key, st in STAGE_OF_KERNEL if key in name), None)
+        if stage is None or name not in write:
+            continue
+        f = sum(fetch[name]) / len(fetch[name]) * 1024.0 * fscale
+        w = sum(write[name]) / len(write[name]) * 1024.0 * wscale
+        short = name.split("::")[-1].split("(")[0] if "(anonymous namespace)::" in name else name
+        short = name.split("(anonymous namespace)::")[-1].split("(")[0] if "(anonymous namespace)::" in name else short
+        out["kernels"][stage] = {"kernel": short[:120], "dispatches": len(fetch[name]),
+                                 "fetch_bytes": round(f), "write_bytes": round(w),
+                                 "hbm_bytes_per_launch": round(f + w),
+                                 "source_hash": source_hash(KERNEL_SOURCES[stage])}
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    return out
+
+
 def cpu_baseline(workload: str, target_s: float):
     """The fp64 oracle timed on this host's cores over a bounded sample."""
     from oracle.direct import direct_conv2d
@@ -128,7 +180,18 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="first copy a float32 buffer of this many MiB (a plain copy kernel of "
+                         "known size, to scale hardware byte counters)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU work: turn two rocprofv3 --pmc counter files (FETCH_SIZE, "
+                         "WRITE_SIZE) of a --calibrate-copy-mib run into profiles/traffic_*.json")
     args = ap.parse_args()
+    if args.traffic_from:
+        res = traffic_from_counters(args.workload, args.traffic_from[0], args.traffic_from[1],
+                                    args.calibrate_copy_mib or 1024)
+        print(json.dumps(res, indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); the path "
               f"shards over output tiles or Winograd points, which is not built here.",
@@ -144,6 +207,14 @@ def main():
         sys.exit(1)
     nwg.load_library()
     torch.cuda.set_device(0)
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     wl = WORKLOADS[args.workload]
     x, ws = make_workload(args.workload)
     xd = torch.from_numpy(x).to("cuda")
