@@ -11,8 +11,10 @@
 // independent sub-windows ("branches"), and the two innermost levels
 // (10 -> 16 per axis) run in registers.
 //
-//   depth n <= 2 : one thread per tile; the work-group stages the union of
+//   depth 1      : one thread per tile; the work-group stages the union of
 //                  its tiles' windows (a box of whole-row tile runs) in LDS.
+//   depth 2      : the same box staging for 16 tiles, with 16 threads per
+//                  tile (one per row of the two-level transform).
 //   depth n >= 3 : one thread per (tile, level-3 branch); the work-group
 //                  stages each of its 16 tiles' windows separately in LDS
 //                  (odd window stride, so that the 16 tiles of a
@@ -67,7 +69,7 @@ __device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* _
   }
 }
 
-// ---- depth 1 and 2: union box of tiles in LDS ------------------------------
+// ---- depth 1: union box of tiles in LDS, one thread per tile ----------------
 template <int NLEV>
 __global__ __launch_bounds__(256) void input_xform_box(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
@@ -102,14 +104,8 @@ __global__ __launch_bounds__(256) void input_xform_box(
   const int t = (b * th + ty) * tw + tx;
   const float* win = lds + ly * Mn * BW + lx * Mn;
   float4* vb = V + (size_t)m * T + t;
-  if constexpr (NLEV == 2) {
-    float S[10][10];
-#pragma unroll
-    for (int i = 0; i < 10; ++i)
-#pragma unroll
-      for (int j = 0; j < 10; ++j) S[i][j] = win[i * BW + j];
-    inner2_store(S, vb, (size_t)qstride);
-  } else {
+  static_assert(NLEV == 1, "the box kernel serves depth 1");
+  {
     float X[4][4], Rw[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -132,6 +128,62 @@ __global__ __launch_bounds__(256) void input_xform_box(
 #pragma unroll
     for (int q1r = 0; q1r < 4; ++q1r)
       vb[(size_t)q1r * qstride] = make_float4(Rw[q1r][0], Rw[q1r][1], Rw[q1r][2], Rw[q1r][3]);
+  }
+}
+
+// ---- depth 2: 16 tiles per work-group, 16 threads per tile -----------------
+// Thread (tile, rho = (q2r, q1r)) applies that row of the two-level B^T to
+// the tile's 10 x 10 window (4 window rows per output row) and the two
+// levels along the columns to the result, storing 4 quads.  The work-group's
+// 16 tiles form a box of RX x RY tiles whose windows are staged in LDS.
+__global__ __launch_bounds__(256) void input_xform_d2(
+    const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
+    int tw, int T, long long qstride, int RX, int RY, int nbx, int nby) {
+  constexpr int Mn = 4, Ln = 10;
+  extern __shared__ float lds[];
+  const int m = blockIdx.y;
+  int bid = blockIdx.x;
+  const int bx = bid % nbx;
+  bid /= nbx;
+  const int by = bid % nby;
+  const int b = bid / nby;
+  const int ty0 = by * RY, tx0 = bx * RX;
+  const int BH = (RY - 1) * Mn + Ln, BW = (RX - 1) * Mn + Ln;
+  const int r0 = ty0 * Mn - pad, c0 = tx0 * Mn - pad;
+  const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
+  for (int e = threadIdx.x; e < BH * BW; e += 256) {
+    const int row = e / BW, col = e - row * BW;
+    const int gr = r0 + row, gc = c0 + col;
+    float v = 0.0f;
+    if (gr >= 0 && gr < H && gc >= 0 && gc < W) v = xp[(size_t)gr * W + gc];
+    lds[e] = v;
+  }
+  __syncthreads();
+  const int s = threadIdx.x & 15, rho = threadIdx.x >> 4;
+  if (s >= RX * RY) return;
+  const int ly = s / RX, lx = s - ly * RX;
+  const int ty = ty0 + ly, tx = tx0 + lx;
+  if (ty >= th || tx >= tw) return;
+  const int t = (b * th + ty) * tw + tx;
+  const float* win = lds + ly * Mn * BW + lx * Mn;
+  const int q2r = rho >> 2, q1r = rho & 3;
+  // row rho of the two-level B^T: taps 2 a2 + a1 with sign s2 * s1
+  const int a20 = 2 * bt_tap0(q2r), a21 = 2 * bt_tap1(q2r);
+  const int a10 = bt_tap0(q1r), a11 = bt_tap1(q1r);
+  const float s20 = bt_sign0(q2r), s21 = bt_sign1(q2r), s10 = bt_sign0(q1r), s11 = bt_sign1(q1r);
+  float R[10];
+#pragma unroll
+  for (int j = 0; j < 10; ++j)
+    R[j] = s20 * (s10 * win[(a20 + a10) * BW + j] + s11 * win[(a20 + a11) * BW + j]) +
+           s21 * (s10 * win[(a21 + a10) * BW + j] + s11 * win[(a21 + a11) * BW + j]);
+  float o[16];
+  bt_inner2(R, o);  // columns: index q2c*4 + q1c
+  float4* vb = V + (size_t)m * T + t;
+#pragma unroll
+  for (int q2c = 0; q2c < 4; ++q2c) {
+    const int quad = q2r * 16 + q2c * 4 + q1r;
+    vb[(size_t)quad * qstride] =
+        make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
   }
 }
 
@@ -289,6 +341,17 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
     else
       hipLaunchKernelGGL(input_xform_tiles<4>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
                          g.pad, g.th, g.tw, T, qstride, q4_0, nq4);
+  } else if (g.n == 2) {
+    if (nparts != 1) return hipErrorInvalidValue;
+    const int Mn = 4, Ln = 10;
+    const int RX = g.tw < 16 ? g.tw : 16;
+    int RY = 16 / RX;
+    if (RY > g.th) RY = g.th;
+    const int nbx = (g.tw + RX - 1) / RX, nby = (g.th + RY - 1) / RY;
+    const size_t lds = (size_t)((RY - 1) * Mn + Ln) * ((RX - 1) * Mn + Ln) * sizeof(float);
+    dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)g.M);
+    hipLaunchKernelGGL(input_xform_d2, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W, g.pad, g.th,
+                       g.tw, T, qstride, RX, RY, nbx, nby);
   } else {
     if (nparts != 1) return hipErrorInvalidValue;
     const int Mn = 1 << g.n, Ln = 3 * Mn - 2;
@@ -308,12 +371,8 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
     const int nbx = (g.tw + RX - 1) / RX, nby = (g.th + RY - 1) / RY;
     const size_t lds = (size_t)((RY - 1) * Mn + Ln) * ((RX - 1) * Mn + Ln) * sizeof(float);
     dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)g.M);
-    if (g.n == 2)
-      hipLaunchKernelGGL(input_xform_box<2>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
-                         g.th, g.tw, T, qstride, RX, RY, nbx, nby);
-    else
-      hipLaunchKernelGGL(input_xform_box<1>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
-                         g.th, g.tw, T, qstride, RX, RY, nbx, nby);
+    hipLaunchKernelGGL(input_xform_box<1>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
+                       g.th, g.tw, T, qstride, RX, RY, nbx, nby);
   }
   return hipGetLastError();
 }

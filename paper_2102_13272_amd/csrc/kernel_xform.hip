@@ -7,10 +7,11 @@
 // digit as large as allowed.  Every other entry of the 3^n x 3^n reordered
 // kernel is zero.  G of F(2,3) along every axis gives U[p][m][n].
 //
-// One thread per (output channel, input channel, outer branch): the outer
-// levels (3 and 4) fold the reordered kernel into a 9 x 9 sub-kernel over
-// the digits (k2, k1) of each axis, and the two inner levels (9 -> 16 per
-// axis) run in registers.  U is quad-interleaved, U[p/4][m][n][p%4] (p%4 is
+// Depth <= 2: one thread per (output channel, input channel).  Depth 3 and
+// 4: see kernel_xform_lds below.  Per outer branch the outer levels (3 and
+// 4) fold the reordered kernel into a 9 x 9 sub-kernel over the digits
+// (k2, k1) of each axis, and the two inner levels (9 -> 16 per axis) run in
+// registers.  U is quad-interleaved, U[p/4][m][n][p%4] (p%4 is
 // the level-1 column digit), written as float4; consecutive threads take
 // consecutive output channels, then input channels, so the writes are
 // contiguous.  Depth 0 (r = 1) stores U[m][n] = w[n][m][0][0].
@@ -168,18 +169,126 @@ __global__ __launch_bounds__(256) void kernel_xform(const float* __restrict__ w,
   }
 }
 
+// Depth 3 and 4: a work-group takes 16 consecutive output channels of one
+// input channel; their r x r kernels sit in LDS (odd stride per kernel, so
+// the 16 channels of a quarter-wave read 16 different banks).  Thread
+// (channel, slot) handles the outer branches slot, slot + 16, ...; the
+// quarter-wave's 16 channels store 256 contiguous bytes per quad.
+template <int NLEV>
+__global__ __launch_bounds__(256) void kernel_xform_lds(const float* __restrict__ w,
+                                                        float* __restrict__ U, int M, int N,
+                                                        int r) {
+  extern __shared__ float wl[];
+  const int m = blockIdx.y;
+  const int n0 = blockIdx.x * 16;
+  const int rr = r * r;
+  const int kstride = (rr & 1) ? rr : rr + 1;   // odd stride >= r*r
+  for (int e = threadIdx.x; e < 16 * rr; e += 256) {
+    const int c = e / rr, k = e - c * rr;
+    const int nn = n0 + c;
+    wl[c * kstride + k] = nn < N ? w[((size_t)nn * M + m) * rr + k] : 0.0f;
+  }
+  __syncthreads();
+  const int cl = threadIdx.x & 15, slot = threadIdx.x >> 4;
+  const int nn = n0 + cl;
+  if (nn >= N) return;                      // no barrier below
+  const float* wk = wl + cl * kstride;
+  const size_t MN = (size_t)M * N;
+  constexpr int NB = NLEV == 4 ? 256 : 16;  // outer branches
+  for (int branch = slot; branch < NB; branch += 16) {
+    int qr3, qc3, qr4 = 0, qc4 = 0;
+    if (NLEV == 3) {
+      qr3 = branch >> 2;
+      qc3 = branch & 3;
+    } else {
+      qr4 = branch >> 6;
+      qc4 = (branch >> 4) & 3;
+      qr3 = (branch >> 2) & 3;
+      qc3 = branch & 3;
+    }
+    float S[9][9];
+#pragma unroll
+    for (int i = 0; i < 9; ++i)
+#pragma unroll
+      for (int j = 0; j < 9; ++j) S[i][j] = 0.0f;
+    const int n4 = NLEV == 4 ? 3 : 1;
+    for (int a4 = 0; a4 < n4; ++a4)
+      for (int a3 = 0; a3 < 3; ++a3) {
+        float gr = g_coef(qr3, a3);
+        if (NLEV == 4) gr *= g_coef(qr4, a4);
+        if (gr == 0.0f) continue;
+        for (int b4 = 0; b4 < n4; ++b4)
+          for (int b3 = 0; b3 < 3; ++b3) {
+            float gc = gr * g_coef(qc3, b3);
+            if (NLEV == 4) gc *= g_coef(qc4, b4);
+            if (gc == 0.0f) continue;
+#pragma unroll
+            for (int ir = 0; ir < 9; ++ir) {
+              const int tr = canonical_tap<NLEV>(a4, a3, ir / 3, ir % 3);
+              if (tr < 0 || tr >= r) continue;
+#pragma unroll
+              for (int ic = 0; ic < 9; ++ic) {
+                const int tc = canonical_tap<NLEV>(b4, b3, ic / 3, ic % 3);
+                if (tc < 0 || tc >= r) continue;
+                S[ir][ic] += gc * wk[tr * r + tc];
+              }
+            }
+          }
+      }
+    float4* ub = reinterpret_cast<float4*>(U) + (size_t)branch * 64 * MN + (size_t)m * N + nn;
+#pragma unroll
+    for (int rho = 0; rho < 16; ++rho) {
+      const int q2r = rho >> 2, q1r = rho & 3;
+      float rowv[9];
+#pragma unroll
+      for (int ic = 0; ic < 9; ++ic) {
+        float sacc = 0.0f;
+#pragma unroll
+        for (int ir = 0; ir < 9; ++ir) {
+          const float c = g_coef(q2r, ir / 3) * g_coef(q1r, ir % 3);
+          if (c != 0.0f) sacc += c * S[ir][ic];
+        }
+        rowv[ic] = sacc;
+      }
+      float o[16];
+      g_inner2(rowv, o);
+#pragma unroll
+      for (int q2c = 0; q2c < 4; ++q2c) {
+        const int quad = q2r * 16 + q2c * 4 + q1r;
+        ub[(size_t)quad * MN] =
+            make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
-  const int nb = g.n >= 3 ? (g.n == 3 ? 16 : 256) : 1;
-  const long long nthreads = (long long)g.N * g.M * nb;
+  if (g.n >= 3) {
+    const int rr = g.r * g.r;
+    const size_t lds = (size_t)16 * ((rr & 1) ? rr : rr + 1) * sizeof(float);
+    dim3 grid((unsigned)((g.N + 15) / 16), (unsigned)g.M);
+    hipError_t e;
+    if (g.n == 3) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&kernel_xform_lds<3>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(kernel_xform_lds<3>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
+    } else {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&kernel_xform_lds<4>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(kernel_xform_lds<4>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
+    }
+    return hipGetLastError();
+  }
+  const long long nthreads = (long long)g.N * g.M;
   dim3 grid((unsigned)((nthreads + 255) / 256));
   switch (g.n) {
     case 0: hipLaunchKernelGGL(kernel_xform<0>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
     case 1: hipLaunchKernelGGL(kernel_xform<1>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
     case 2: hipLaunchKernelGGL(kernel_xform<2>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
-    case 3: hipLaunchKernelGGL(kernel_xform<3>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
-    case 4: hipLaunchKernelGGL(kernel_xform<4>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
