@@ -46,6 +46,11 @@ def stage_bytes_flops(info: dict):
                 "contraction": (x + y + 4 * M * N, 2.0 * B * N * M * Ho * Wo)}
     # Z: the contraction's output after the first output level, P/4 values per (n, t)
     U, V, Yh = 4 * P * M * N, 4 * P * M * T, 4 * (P // 4) * N * T
+    if info.get("fused_input"):
+        # one kernel reads x and U and writes Z; V never reaches memory
+        return {"kernel_transform": (w + U, 0.0),
+                "contraction": (x + U + Yh, 2.0 * P * M * N * T),
+                "output_transform": (Yh + y, 0.0)}
     return {"kernel_transform": (w + U, 0.0),
             "input_transform": (x + V, 0.0),
             "contraction": (U + V + Yh, 2.0 * P * M * N * T),
@@ -267,7 +272,9 @@ def main():
             s["bytes"] += b * cnt[si]
             s["flop"] += f * cnt[si]
             s["per_layer"].append({"r": p.info["r"], "n": p.info["n"],
-                                   "avg_us": round(1e3 * ms[si] / cnt[si], 2)})
+                                   "avg_us": round(1e3 * ms[si] / cnt[si], 2),
+                                   **({"fused_input": True} if p.info["fused_input"]
+                                      and name == "contraction" else {})})
     detail = {}
     for name, s in stages.items():
         sec = s["ms_total"] * 1e-3

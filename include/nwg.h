@@ -37,7 +37,8 @@
  *
  * Ownership: the caller owns x, w, y, U/V/Z passed to stage calls, and
  * the stream; they must stay valid until the work queued on the stream has
- * finished.  A plan owns its workspace (U, V, Z), allocated at creation.
+ * finished.  A plan owns its workspace (U, V, Z; workspace_bytes),
+ * allocated at creation; V is left out when info.fused_input is set.
  * Every call that takes a stream only queues work on it (`stream` is a
  * hipStream_t; NULL is the default stream) and never synchronises, except
  * nwg_plan_get_timing.  A plan is not thread-safe; one call in flight per
@@ -86,6 +87,8 @@ typedef struct nwg_plan_info {
   long long ewmm_mults;         /* general multiplications per call: P*T*M*N */
   double direct_flop;           /* 2*B*N*M*Ho*Wo*r*r */
   double contract_flop;         /* 2*P*M*N*T (n = 0: 2*B*N*M*Ho*Wo) */
+  int fused_input;              /* 1: nwg_conv2d runs nwg_input_contract (depth 3-4,
+                                   N <= 2) and the plan holds no V */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).
@@ -136,6 +139,15 @@ int nwg_input_transform(const nwg_plan* plan, const float* x, float* V, void* st
 int nwg_contract(const nwg_plan* plan, const float* U, const float* V, float* Z,
                  void* stream);
 
+/* Input transformation, contraction and first output level in one kernel,
+ * x, U -> Z (yhat_bytes), with the same result as nwg_input_transform
+ * followed by nwg_contract but without forming V.  For layers with one or
+ * two output channels, whose contraction is too small to pay for writing
+ * and re-reading V.  Depth 3 or 4 (8 <= r <= 31) and N <= 2 only;
+ * NWG_EUNSUPPORTED otherwise. */
+int nwg_input_contract(const nwg_plan* plan, const float* x, const float* U, float* Z,
+                       void* stream);
+
 /* Nested output transformation (Sec. III.B, final step), levels 2..n:
  * Z -> y, cropped to Ho x Wo.  NWG_EINVAL at depth 0. */
 int nwg_output_transform(const nwg_plan* plan, const float* Z, float* y, void* stream);
@@ -145,7 +157,8 @@ int nwg_output_transform(const nwg_plan* plan, const float* Z, float* y, void* s
  * the caller's stream.  nwg_plan_get_timing waits for the recorded events,
  * adds their durations to ms[4] and launch counts to count[4] (index 0 kernel
  * transform, 1 input transform, 2 contraction, 3 output transform), then
- * forgets them. */
+ * forgets them.  A fused nwg_input_contract launch counts as a contraction
+ * (index 2) and leaves index 1 untouched. */
 int nwg_plan_set_timing(nwg_plan* plan, int enable);
 int nwg_plan_get_timing(nwg_plan* plan, double ms[4], long long count[4]);
 

@@ -131,7 +131,9 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     g->ewmm_mults = P * g->T * M * (long long)N;
     g->contract_flop = 2.0 * P * (double)M * N * g->T;
   }
-  g->workspace_bytes = g->u_bytes + g->v_bytes + g->yhat_bytes;
+  // one or two output channels at depth 3-4: the fused kernel never forms V
+  g->fused_input = nwg::input_contract_applies(*g) ? 1 : 0;
+  g->workspace_bytes = g->u_bytes + (g->fused_input ? 0 : g->v_bytes) + g->yhat_bytes;
   return NWG_OK;
 }
 
@@ -159,11 +161,12 @@ int timed(nwg_plan* p, int stage, hipStream_t s, const char* what, F&& launch) {
   if (p && p->timing) {
     e0 = take_event(p);
     e1 = take_event(p);
-    if (e0 && e1) hipEventRecord(e0, s);
   }
+  // a launch whose events cannot be recorded runs untimed
+  bool timed_ok = e0 && e1 && hipEventRecord(e0, s) == hipSuccess;
   const int rc = check_hip(launch(), what);
-  if (e0 && e1) {
-    hipEventRecord(e1, s);
+  timed_ok = timed_ok && hipEventRecord(e1, s) == hipSuccess;
+  if (timed_ok) {
     p->pending.push_back({stage, e0, e1});
   } else {
     if (e0) p->event_pool.push_back(e0);
@@ -245,7 +248,7 @@ nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad,
     }
     return true;
   };
-  if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, g.v_bytes, "V") ||
+  if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, g.fused_input ? 0 : g.v_bytes, "V") ||
       !alloc(&p->Yh, g.yhat_bytes, "Yhat")) {
     nwg_plan_destroy(p);
     // keep the allocation message
@@ -311,6 +314,21 @@ int nwg_contract(const nwg_plan* p, const float* U, const float* V, float* Yh, v
                    "contraction launch");
 }
 
+int nwg_input_contract(const nwg_plan* p, const float* x, const float* U, float* Yh,
+                       void* stream) {
+  if (!p || !x || !U || !Yh) {
+    set_error("NULL argument to nwg_input_contract");
+    return NWG_EINVAL;
+  }
+  if (!nwg::input_contract_applies(p->info)) {
+    set_error("fused input transform + contraction needs depth 3 or 4 and N <= 2 "
+              "(depth %d, N = %d)", p->info.n, p->info.N);
+    return NWG_EUNSUPPORTED;
+  }
+  return check_hip(nwg::launch_input_contract(p->info, x, U, Yh, (hipStream_t)stream),
+                   "fused input transform + contraction launch");
+}
+
 int nwg_output_transform(const nwg_plan* p, const float* Yh, float* y, void* stream) {
   if (!p || !Yh || !y) {
     set_error("NULL argument to nwg_output_transform");
@@ -354,11 +372,17 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
     return timed(p, 2, s, "contraction launch",
                  [&] { return launch_contract(g, p->U, x, y, s); });
   }
-  int rc = timed(p, 1, s, "input transform launch",
-                 [&] { return nwg::launch_input_xform(g, x, p->V, s); });
-  if (rc != NWG_OK) return rc;
-  rc = timed(p, 2, s, "contraction launch",
-             [&] { return launch_contract(g, p->U, p->V, p->Yh, s); });
+  int rc;
+  if (g.fused_input) {
+    rc = timed(p, 2, s, "fused input transform + contraction launch",
+               [&] { return nwg::launch_input_contract(g, x, p->U, p->Yh, s); });
+  } else {
+    rc = timed(p, 1, s, "input transform launch",
+               [&] { return nwg::launch_input_xform(g, x, p->V, s); });
+    if (rc != NWG_OK) return rc;
+    rc = timed(p, 2, s, "contraction launch",
+               [&] { return launch_contract(g, p->U, p->V, p->Yh, s); });
+  }
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",
                [&] { return nwg::launch_output_xform(g, p->Yh, y, s); });

@@ -106,6 +106,10 @@ hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s);
 // depth >= 1: Z = level-1 A^T of (U^T V per point); G = P / 16 groups
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
                                  long long G, hipStream_t s);
+// depth 3-4 and N <= 2: x, U -> Z without forming V
+bool input_contract_applies(const nwg_plan_info& g);
+hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* U, float* Z,
+                                 hipStream_t s);
 hipError_t launch_output_xform(const nwg_plan_info& g, const float* Yh, float* y, hipStream_t s);
 
 }  // namespace nwg

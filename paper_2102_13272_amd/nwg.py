@@ -33,7 +33,7 @@ class nwg_plan_info(ctypes.Structure):
         ("u_bytes", ctypes.c_size_t), ("v_bytes", ctypes.c_size_t),
         ("yhat_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
         ("ewmm_mults", ctypes.c_longlong), ("direct_flop", ctypes.c_double),
-        ("contract_flop", ctypes.c_double),
+        ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -56,6 +56,7 @@ SIGNATURES = [
     ("nwg_kernel_transform", _I, [_P, _P, _P, _P]),
     ("nwg_input_transform", _I, [_P, _P, _P, _P]),
     ("nwg_contract", _I, [_P, _P, _P, _P, _P]),
+    ("nwg_input_contract", _I, [_P, _P, _P, _P, _P]),
     ("nwg_output_transform", _I, [_P, _P, _P, _P]),
     ("nwg_plan_set_timing", _I, [_P, _I]),
     ("nwg_plan_get_timing", _I, [_P, ctypes.POINTER(ctypes.c_double),
@@ -186,6 +187,10 @@ class Plan:
     def contract(self, U, V, Z, stream=None):
         _check(self._lib.nwg_contract(self.handle, _ptr(U), _ptr(V), _ptr(Z), _stream(stream)),
                "nwg_contract")
+
+    def input_contract(self, x, U, Z, stream=None):
+        _check(self._lib.nwg_input_contract(self.handle, _ptr(x), _ptr(U), _ptr(Z),
+                                            _stream(stream)), "nwg_input_contract")
 
     def output_transform(self, Z, y, stream=None):
         _check(self._lib.nwg_output_transform(self.handle, _ptr(Z), _ptr(y), _stream(stream)),

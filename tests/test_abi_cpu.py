@@ -119,3 +119,15 @@ def test_no_silent_fallback_without_device():
         pytest.skip("a GPU is present")
     with pytest.raises(nwg.NwgError):
         nwg.Plan(1, 1, 1, 8, 8, 3)
+
+
+@pytest.mark.parametrize("N", [1, 2, 3])
+def test_fused_input_flag_and_workspace(N):
+    # depth 3-4 with one or two output channels: nwg_conv2d fuses the input
+    # transform into the contraction and the plan allocates no V
+    for r in range(1, 32):
+        g = nwg.plan_geometry(2, 4, N, 70, 66, r, (r - 1) // 2)
+        fused = g["n"] in (3, 4) and N <= 2
+        assert g["fused_input"] == int(fused), r
+        v = 0 if fused else g["v_bytes"]
+        assert g["workspace_bytes"] == g["u_bytes"] + v + g["yhat_bytes"]

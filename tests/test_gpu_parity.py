@@ -116,6 +116,67 @@ def test_stages_match_cpu_nested_reference(case):
                      what="y")
 
 
+# depth 3-4 with N <= 2: the fused kernel.  Tile counts not a multiple of 4
+# (a ragged last wavefront), M = 1, 3, 5, 9 (1, 2 and 4 channel groups, some
+# of them uneven), padding that reaches past whole windows.
+FUSED = [(1, 3, 1, 20, 19, 11, 5), (2, 5, 2, 17, 21, 9, 4), (1, 1, 1, 23, 18, 15, 7),
+         (1, 9, 2, 12, 13, 8, 0), (1, 2, 1, 21, 26, 31, 15), (2, 3, 2, 18, 17, 17, 8),
+         (1, 5, 1, 33, 16, 16, 0), (2, 4, 1, 70, 45, 9, 4)]
+
+
+def _stage_refs(case, seed):
+    B, M, N, H, W, r, pad = case
+    L, x, w = make_case(B, M, N, H, W, r, pad, seed=seed)
+    g = geometry(x.shape, w.shape, pad)
+    n = g.lv.n
+    U_ref = kernel_transform(w, g)
+    V_ref = input_transform(x, g)
+    Yh_ref = ewmm(U_ref, V_ref)
+    T = B * g.th * g.tw
+    U_std = _to_lib_points(U_ref, n).transpose(2, 1, 0)
+    Yh_std = _to_lib_points(Yh_ref.reshape(T, N, g.lv.P1, g.lv.P1), n).transpose(2, 1, 0)
+    return x, w, g, _quads(U_std), _level1(Yh_std), Yh_ref
+
+
+@pytest.mark.parametrize("case", FUSED, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
+def test_fused_input_contract_matches_cpu_nested_reference(case):
+    B, M, N, H, W, r, pad = case
+    print(f"fused {case}", flush=True)
+    x, w, g, U_lib, Z_lib, Yh_ref = _stage_refs(case, seed=11 + r)
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        assert plan.info["fused_input"] == 1 and plan.info["n"] in (3, 4)
+        assert plan.info["workspace_bytes"] == plan.info["u_bytes"] + plan.info["yhat_bytes"]
+        Z = torch.full(plan.z_shape, float("nan"), device="cuda")
+        plan.input_contract(dev(x), dev(U_lib), Z)
+        torch.cuda.synchronize()
+        assert_close(Z.cpu().numpy(), Z_lib, rel_tol=1e-5, abs_frac=1e-5, what="Z fused")
+        # the unfused stages on the same operands agree
+        V = torch.empty(plan.v_shape, device="cuda")
+        Z2 = torch.empty(plan.z_shape, device="cuda")
+        plan.input_transform(dev(x), V)
+        plan.contract(dev(U_lib), V, Z2)
+        torch.cuda.synchronize()
+        assert_close(Z.cpu().numpy(), Z2.cpu().numpy(), rel_tol=1e-5, abs_frac=1e-5,
+                     what="fused vs staged")
+        y = torch.empty(plan.y_shape, device="cuda")
+        plan.conv2d(dev(x), dev(w), y)
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w, pad), what=f"y {case}")
+
+
+def test_fused_input_contract_rejects_other_shapes():
+    with nwg.Plan(1, 2, 3, 20, 20, 9, 4) as plan:           # N = 3
+        assert plan.info["fused_input"] == 0
+        x = torch.zeros((1, 2, 20, 20), device="cuda")
+        with pytest.raises(nwg.NwgError, match="N <= 2"):
+            plan.input_contract(x, x, x)
+    with nwg.Plan(1, 2, 1, 20, 20, 7, 3) as plan:           # depth 2
+        assert plan.info["fused_input"] == 0
+        x = torch.zeros((1, 2, 20, 20), device="cuda")
+        with pytest.raises(nwg.NwgError):
+            plan.input_contract(x, x, x)
+
+
 @pytest.mark.parametrize("N,M,T,depth", [(1, 32, 4096, 1), (5, 5, 100, 1), (128, 128, 256, 1),
                                          (64, 64, 392, 1), (3, 7, 33, 1), (32, 1, 300, 1),
                                          (17, 33, 129, 1), (128, 20, 64, 0), (5, 32, 1000, 0),
@@ -197,3 +258,18 @@ def test_timing_records_each_stage():
         assert all(t > 0 for t in ms)
         ms2, cnt2 = plan.get_timing()
         assert cnt2 == [0, 0, 0, 0]
+
+
+def test_timing_of_the_fused_path_counts_one_launch_as_contraction():
+    B, M, N, H, W, r, pad = 1, 4, 1, 32, 32, 9, 4
+    _, x, w = make_case(B, M, N, H, W, r, pad, seed=4)
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        assert plan.info["fused_input"] == 1
+        xd, wd = dev(x), dev(w)
+        y = torch.empty(plan.y_shape, device="cuda")
+        plan.set_timing(True)
+        for _ in range(2):
+            plan.conv2d(xd, wd, y)
+        ms, cnt = plan.get_timing()
+        assert cnt == [1, 0, 2, 2]
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w, pad), what="fused timing")
