@@ -12,10 +12,10 @@
 // Reads are float4 quads Z[g][n][t] with consecutive lanes on consecutive
 // tiles: 256 contiguous bytes per quarter-wave.  Each thread reduces the
 // 16 level-2 groups of one branch in registers (4x4 partial tile).  At depth
-// >= 3 the 16 level-3 branches of a tile sit in 16 different threads; their
-// partial tiles go through LDS, where the level-3 A^T combines them, and at
-// depth 4 the level-4 A^T accumulates the 16 level-4 branches in registers
-// over 16 passes.
+// >= 3 a lane sums the 4 branches of one level-3 row digit, and the 4 rows
+// of a tile, held by the 4 quarter-waves of one wavefront, are combined by
+// lane shuffles (no LDS); at depth 4 the level-4 A^T accumulates the 16
+// level-4 branches in registers.
 #include "nwg_internal.h"
 
 namespace nwg {
@@ -84,79 +84,99 @@ __global__ __launch_bounds__(256) void output_xform_tile(
   }
 }
 
-// ---- depth 3 and 4: 16 tiles x 16 level-3 branches per work-group ---------
+// ---- depth 3 and 4: one wavefront per 16 tiles, level 3 by shuffles -------
+// Lane (tl, q3r): tile tl of the wavefront's 16, level-3 row digit q3r.
+// Per level-4 branch the lane reduces the 4 branches q3c of its row (levels
+// 2 and the column half of level 3) in registers, giving C[i3c][rr][cc].
+// The row half of level 3, y3[i3r] = sum_q3r A^T[i3r][q3r] C_q3r, combines
+// the 4 quarter-waves holding q3r = 0..3 in two shuffle steps (lane xor 16,
+// then xor 32), each moving 16 values, after which the lane owns the 4x4
+// block (i3r, i3c) = (q3r >> 1, q3r & 1) of the tile.  Level 4 accumulates
+// over the 16 level-4 branches in registers.  Z reads are float4 with 16
+// consecutive tiles per quarter-wave; y is written as float4 row segments.
+//
+// Shuffle step 1 (partner q3r ^ 1) keeps half k = q3r & 1 (i3c = k):
+//   q3r = 0: u = a0 + a1, w = a1      q3r = 1: u = a0 + a1, w = a1
+//   q3r = 2: u = a2,      w = a2 + a3 q3r = 3: u = a2,      w = a2 + a3
+// (a_q = C of row q, for column half k).  Step 2 (partner q3r ^ 2):
+//   q3r < 2: y3[0] = u + u(partner)   q3r >= 2: y3[1] = w(partner) - w
+// which are the two A^T rows (1, 1, 1, 0) and (0, 1, -1, -1).
 template <int NLEV>
-__global__ __launch_bounds__(256) void output_xform_branches(
+__global__ __launch_bounds__(64) void output_xform_shfl(
     const float4* __restrict__ Z, float* __restrict__ y, int N, int Ho, int Wo, int th, int tw,
-    int T, long long gstride) {
+    int T, long long gstride, int vec) {
   constexpr int Mn = 1 << NLEV;
   constexpr int PASSES = NLEV == 4 ? 16 : 1;
-  // [tile][level-3 branch][partial output]; odd tile stride (16*17+1): the
-  // 16 tiles of a quarter-wave hit 16 different banks
-  constexpr int TS = 16 * 17 + 1;
-  __shared__ float part[16 * TS];
+  constexpr int NI4 = NLEV == 4 ? 2 : 1;
   const int n = blockIdx.y;
-  const int tl = threadIdx.x & 15;
-  const int slot = threadIdx.x >> 4;
+  const int lane = threadIdx.x;
+  const int tl = lane & 15, q3r = lane >> 4;
   const int t = blockIdx.x * 16 + tl;
   const bool valid = t < T;
-  // phase-2 role: this thread finalises partial output e = slot of tile tl
-  const int e = slot;
-  float acc[2][2][2][2];                    // [i4r][i4c][i3r][i3c]
+  const int k = q3r & 1;
+  // step-1 and step-2 coefficients of this lane (see above)
+  const float cu0 = q3r == 3 ? 0.0f : 1.0f, cu1 = q3r == 2 ? 0.0f : 1.0f;
+  const float cw0 = q3r == 0 ? 0.0f : 1.0f, cw1 = q3r == 1 ? 0.0f : 1.0f;
+  const bool low = q3r < 2;
+  float acc[NI4][NI4][16];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < NI4; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NI4; ++b)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int d = 0; d < 2; ++d) acc[a][b][c][d] = 0.0f;
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
 
-  const float4* zslot = Z + (size_t)slot * 16 * gstride + (size_t)n * T + t;
+  const float4* zt = Z + (size_t)n * T + (valid ? t : 0);
   for (int pass = 0; pass < PASSES; ++pass) {
-    float po[4][4];
+    // levels 2 and the column half of level 3 over this row's 4 branches
+    float C[2][16];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) C[h][e] = 0.0f;
     if (valid) {
-      level2_reduce(zslot + (size_t)pass * 256 * gstride, (size_t)gstride, po);
-    } else {
+      // depth 4: two branches' 32 quad loads in flight at a time (240
+      // registers, two wavefronts per SIMD); depth 3 has one pass and keeps
+      // all four branches in flight
+#pragma unroll (NLEV == 3 ? 4 : 2)
+      for (int q3c = 0; q3c < 4; ++q3c) {
+        const int branch = pass * 16 + q3r * 4 + q3c;
+        float po[4][4];
+        level2_reduce(zt + (size_t)branch * 16 * gstride, (size_t)gstride, po);
+        const float c0 = at_coef(0, q3c), c1 = at_coef(1, q3c);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) po[i][k] = 0.0f;
+        for (int e = 0; e < 16; ++e) {
+          C[0][e] += c0 * po[e >> 2][e & 3];
+          C[1][e] += c1 * po[e >> 2][e & 3];
+        }
+      }
     }
+    // row half of level 3 across the four quarter-waves
+    float out[16];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int k = 0; k < 4; ++k) part[tl * TS + slot * 17 + i * 4 + k] = po[i][k];
-    __syncthreads();
-    // level 3 across the 16 branches of tile tl, for partial output e
-    float pv[4][4];
-#pragma unroll
-    for (int q3r = 0; q3r < 4; ++q3r)
-#pragma unroll
-      for (int q3c = 0; q3c < 4; ++q3c) pv[q3r][q3c] = part[tl * TS + (q3r * 4 + q3c) * 17 + e];
+    for (int e = 0; e < 16; ++e) {
+      const float keep = k ? C[1][e] : C[0][e];
+      const float give = k ? C[0][e] : C[1][e];
+      const float r = __shfl_xor(give, 16);
+      const float u = cu0 * keep + cu1 * r;
+      const float w = cw0 * keep + cw1 * r;
+      const float r2 = __shfl_xor(low ? w : u, 32);
+      out[e] = low ? u + r2 : r2 - w;
+    }
     const int q4r = pass >> 2, q4c = pass & 3;
 #pragma unroll
-    for (int i3r = 0; i3r < 2; ++i3r)
+    for (int a = 0; a < NI4; ++a)
 #pragma unroll
-      for (int i3c = 0; i3c < 2; ++i3c) {
-        float s = 0.0f;
+      for (int b = 0; b < NI4; ++b) {
+        const float c4 = NLEV == 4 ? at_coef(a, q4r) * at_coef(b, q4c) : 1.0f;
+        if (NLEV == 4) {
 #pragma unroll
-        for (int q3r = 0; q3r < 4; ++q3r)
+          for (int e = 0; e < 16; ++e) acc[a][b][e] += c4 * out[e];
+        } else {
 #pragma unroll
-          for (int q3c = 0; q3c < 4; ++q3c) {
-            const float c = at_coef(i3r, q3r) * at_coef(i3c, q3c);
-            if (c != 0.0f) s += c * pv[q3r][q3c];
-          }
-#pragma unroll
-        for (int i4r = 0; i4r < 2; ++i4r)
-#pragma unroll
-          for (int i4c = 0; i4c < 2; ++i4c) {
-            const float c4 = NLEV == 4 ? at_coef(i4r, q4r) * at_coef(i4c, q4c)
-                                       : (i4r == 0 && i4c == 0 ? 1.0f : 0.0f);
-            acc[i4r][i4c][i3r][i3c] += c4 * s;
-          }
+          for (int e = 0; e < 16; ++e) acc[a][b][e] = out[e];
+        }
       }
-    __syncthreads();
   }
   if (!valid) return;
   const int tpi = th * tw;
@@ -164,21 +184,26 @@ __global__ __launch_bounds__(256) void output_xform_branches(
   const int r2 = t - b * tpi;
   const int ty = r2 / tw, tx = r2 - ty * tw;
   float* yo = y + ((size_t)b * N + n) * Ho * Wo;
-  const int rr = e >> 2, cc = e & 3;
-  constexpr int NI4 = NLEV == 4 ? 2 : 1;
+  const int i3r = q3r >> 1, i3c = q3r & 1;
 #pragma unroll
-  for (int i4r = 0; i4r < NI4; ++i4r)
+  for (int a = 0; a < NI4; ++a)
 #pragma unroll
-    for (int i3r = 0; i3r < 2; ++i3r) {
-      const int row = ty * Mn + 8 * i4r + 4 * i3r + rr;
+    for (int rr = 0; rr < 4; ++rr) {
+      const int row = ty * Mn + 8 * a + 4 * i3r + rr;
       if (row >= Ho) continue;
+      float* yr = yo + (size_t)row * Wo;
 #pragma unroll
-      for (int i4c = 0; i4c < NI4; ++i4c)
+      for (int c = 0; c < NI4; ++c) {
+        const int col = tx * Mn + 8 * c + 4 * i3c;
+        const float* v = &acc[a][c][rr * 4];
+        if (vec && col + 3 < Wo) {
+          *reinterpret_cast<float4*>(yr + col) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
 #pragma unroll
-        for (int i3c = 0; i3c < 2; ++i3c) {
-          const int col = tx * Mn + 8 * i4c + 4 * i3c + cc;
-          if (col < Wo) yo[(size_t)row * Wo + col] = acc[i4r][i4c][i3r][i3c];
+          for (int cc = 0; cc < 4; ++cc)
+            if (col + cc < Wo) yr[col + cc] = v[cc];
         }
+      }
     }
 }
 
@@ -190,13 +215,15 @@ hipError_t launch_output_xform(const nwg_plan_info& g, const float* Zf, float* y
   const long long gstride = (long long)g.N * g.T;    // float4 quads between groups
   const int T = (int)g.T;
   if (g.n >= 3) {
+    // float4 stores of y rows need 16-byte aligned rows
+    const int vec = (g.Wo % 4 == 0 && ((uintptr_t)y & 15) == 0) ? 1 : 0;
     dim3 grid((unsigned)((g.T + 15) / 16), (unsigned)g.N);
     if (g.n == 3)
-      hipLaunchKernelGGL(output_xform_branches<3>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, gstride);
+      hipLaunchKernelGGL(output_xform_shfl<3>, grid, dim3(64), 0, s, Z, y, g.N, g.Ho, g.Wo,
+                         g.th, g.tw, T, gstride, vec);
     else
-      hipLaunchKernelGGL(output_xform_branches<4>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, gstride);
+      hipLaunchKernelGGL(output_xform_shfl<4>, grid, dim3(64), 0, s, Z, y, g.N, g.Ho, g.Wo,
+                         g.th, g.tw, T, gstride, vec);
   } else {
     dim3 grid((unsigned)((g.T + 255) / 256), (unsigned)g.N);
     if (g.n == 2)
