@@ -74,6 +74,33 @@ def brute_force_conv2d(x, w, pad: int = 0) -> np.ndarray:
     return y
 
 
+def direct_depthwise_conv2d(x, w, pad: int = 0) -> np.ndarray:
+    """fp64 depthwise correlation: one r x r kernel per channel, no channel sum.
+
+    Table I's depth-wise row: x [B][C][H][W], w [C][1][r][r],
+
+        y[b,c,i,j] = sum_{u<r} sum_{v<r} xp[b,c,i+u,j+v] * w[c,0,u,v],
+
+    computed as r*r shifted windows, each scaled per channel.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    if x.ndim != 4 or w.ndim != 4 or w.shape[1] != 1 or w.shape[0] != x.shape[1] \
+            or w.shape[2] != w.shape[3]:
+        raise ValueError("x must be [B][C][H][W] and w [C][1][r][r]")
+    B, C, H, W = x.shape
+    r = w.shape[2]
+    Ho, Wo = H + 2 * pad - r + 1, W + 2 * pad - r + 1
+    if Ho <= 0 or Wo <= 0:
+        raise ValueError("kernel larger than the padded input")
+    xp = np.pad(x, ((0, 0), (0, 0), (pad, pad), (pad, pad)))
+    y = np.zeros((B, C, Ho, Wo), dtype=np.float64)
+    for u in range(r):
+        for v in range(r):
+            y += w[None, :, 0, u, v, None, None] * xp[:, :, u:u + Ho, v:v + Wo]
+    return y
+
+
 def direct_conv2d_points(x, w, pad: int, points) -> np.ndarray:
     """Selected outputs y[b,n,i,j] of the same definition, one at a time.
 

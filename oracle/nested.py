@@ -373,6 +373,25 @@ def ewmm(U, V, counter: Optional[MultCounter] = None) -> np.ndarray:
     return Yh
 
 
+def ewmm_depthwise(U, V, counter: Optional[MultCounter] = None) -> np.ndarray:
+    """Depthwise EWMM: Yhat[b,ty,tx,c] = U[c,0] (.) V[b,ty,tx,c], no channel sum.
+
+    U has shape (C, 1, P1, P1) (the kernel transform of w [C][1][r][r]).
+    """
+    B, th, tw, C, P1, _ = V.shape
+    if U.shape[:2] != (C, 1):
+        raise ValueError("depthwise U must be (C, 1, P1, P1)")
+    Yh = np.empty_like(V)
+    for b in range(B):
+        for ty in range(th):
+            for tx in range(tw):
+                for c in range(C):
+                    Yh[b, ty, tx, c] = U[c, 0] * V[b, ty, tx, c]
+                    if counter is not None:
+                        counter.count += P1 * P1
+    return Yh
+
+
 def output_transform(Yh, g: Geometry, exact: bool = False) -> np.ndarray:
     """y tile = OA . Yhat . OA^T (M_n x M_n), placed at (ty*M_n, tx*M_n), cropped to Ho x Wo."""
     OA = _as(nested_output_matrix(g.base, g.lv), exact)
@@ -424,6 +443,42 @@ def nested_conv2d(x, w, pad: int = 0, base: Optional[Base] = None, exact: bool =
     V = input_transform(x, g, exact)
     Yh = ewmm(U, V, counter)
     return output_transform(Yh, g, exact)
+
+
+def depthwise_geometries(x_shape, w_shape, pad: int, base: Optional[Base] = None):
+    """(kernel geometry, data geometry) of a depthwise layer x [B][C][H][W], w [C][1][r][r].
+
+    The kernel transform sees C kernels of one input channel (N = C, M = 1);
+    the input and output transforms see C channels (M = N = C).
+    """
+    B, C, H, W = x_shape
+    Cw, one, r, r2 = w_shape
+    if Cw != C or one != 1 or r != r2:
+        raise ValueError("x must be [B][C][H][W] and w [C][1][r][r]")
+    return (geometry((B, 1, H, W), w_shape, pad, base),
+            geometry(x_shape, (C, C, r, r), pad, base))
+
+
+def nested_depthwise_conv2d(x, w, pad: int = 0, base: Optional[Base] = None,
+                            exact: bool = False,
+                            counter: Optional[MultCounter] = None) -> np.ndarray:
+    """Depthwise correlation by nested Winograd: the same transforms as
+    nested_conv2d, with the element-wise product of each channel's own
+    transformed kernel and no sum over channels."""
+    gk, gx = depthwise_geometries(np.shape(x), np.shape(w), pad, base)
+    if exact:
+        x, w = _to_fractions(x), _to_fractions(w)
+    if gx.lv.n == 0:
+        # 1x1 kernel: each channel scaled by its single weight
+        ws = w if exact else np.asarray(w, np.float64)
+        xp = padded_input(x, gx, exact)
+        if counter is not None:
+            counter.count += gx.B * gx.N * gx.Ho * gx.Wo
+        return ws[None, :, 0, 0:1, 0:1] * xp[:, :, :gx.Ho, :gx.Wo]
+    U = kernel_transform(w, gk, exact)
+    V = input_transform(x, gx, exact)
+    Yh = ewmm_depthwise(U, V, counter)
+    return output_transform(Yh, gx, exact)
 
 
 # ---------------------------------------------------------------------------
