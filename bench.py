@@ -38,22 +38,28 @@ def stage_bytes_flops(info: dict):
     """Algorithmic bytes (fp32) and FLOPs per launch of each stage of one layer."""
     P, M, N, T = info["P"], info["M"], info["N"], info["T"]
     B, H, W, Ho, Wo, r = info["B"], info["H"], info["W"], info["Ho"], info["Wo"], info["r"]
+    dw = bool(info.get("depthwise"))
+    mk = 1 if dw else M                      # input channels per kernel
     x = 4 * B * M * H * W
     y = 4 * B * N * Ho * Wo
-    w = 4 * N * M * r * r
+    w = 4 * N * mk * r * r
+    flop = info["contract_flop"]
     if info["n"] == 0:
-        return {"kernel_transform": (w + 4 * M * N, 0.0),
-                "contraction": (x + y + 4 * M * N, 2.0 * B * N * M * Ho * Wo)}
+        return {"kernel_transform": (w + 4 * mk * N, 0.0),
+                "contraction": (x + y + 4 * mk * N, flop)}
     # Z: the contraction's output after the first output level, P/4 values per (n, t)
-    U, V, Yh = 4 * P * M * N, 4 * P * M * T, 4 * (P // 4) * N * T
+    U, V, Yh = 4 * P * mk * N, 4 * P * M * T, 4 * (P // 4) * N * T
+    if dw and info["n"] <= 2:
+        # one kernel: x and U in, y out
+        return {"kernel_transform": (w + U, 0.0), "contraction": (x + U + y, flop)}
     if info.get("fused_input"):
         # one kernel reads x and U and writes Z; V never reaches memory
         return {"kernel_transform": (w + U, 0.0),
-                "contraction": (x + U + Yh, 2.0 * P * M * N * T),
+                "contraction": (x + U + Yh, flop),
                 "output_transform": (Yh + y, 0.0)}
     return {"kernel_transform": (w + U, 0.0),
             "input_transform": (x + V, 0.0),
-            "contraction": (U + V + Yh, 2.0 * P * M * N * T),
+            "contraction": (U + V + Yh, flop),
             "output_transform": (Yh + y, 0.0)}
 
 
@@ -139,8 +145,11 @@ def traffic_from_counters(workload: str, fetch_csv: str, write_csv: str, copy_mi
 
 def cpu_baseline(workload: str, target_s: float):
     """The fp64 oracle timed on this host's cores over a bounded sample."""
-    from oracle.direct import direct_conv2d
+    from oracle.direct import direct_conv2d, direct_depthwise_conv2d
     from paper_2102_13272_amd.workloads import WORKLOADS, make_workload
+
+    def conv(L, xs, w):
+        return (direct_depthwise_conv2d if L.depthwise else direct_conv2d)(xs, w, L.pad)
     try:
         from threadpoolctl import threadpool_info
         threads = max([d.get("num_threads", 1) for d in threadpool_info()
@@ -155,7 +164,7 @@ def cpu_baseline(workload: str, target_s: float):
     if len(wl.layers) == 1:
         L = wl.layers[0]
         for b in range(L.B):
-            direct_conv2d(x[b:b + 1], ws[0], L.pad)
+            conv(L, x[b:b + 1], ws[0])
             flop += L.direct_flop / L.B
             images += 1
             if time.perf_counter() - t0 >= target_s:
@@ -165,7 +174,7 @@ def cpu_baseline(workload: str, target_s: float):
         for b in range(wl.layers[0].B):
             cur = x[b:b + 1].astype(np.float64)
             for L, w in zip(wl.layers, ws):
-                cur = direct_conv2d(cur, w, L.pad)
+                cur = conv(L, cur, w)
                 flop += L.direct_flop / L.B
             images += 1
             if time.perf_counter() - t0 >= target_s:
@@ -224,7 +233,8 @@ def main():
     x, ws = make_workload(args.workload)
     xd = torch.from_numpy(x).to("cuda")
     wds = [torch.from_numpy(w).to("cuda") for w in ws]
-    plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad) for L in wl.layers]
+    plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, depthwise=L.depthwise)
+             for L in wl.layers]
     outs = [torch.empty(p.y_shape, dtype=torch.float32, device="cuda") for p in plans]
     stream = torch.cuda.current_stream()
 

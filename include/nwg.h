@@ -88,7 +88,8 @@ typedef struct nwg_plan_info {
   double direct_flop;           /* 2*B*N*M*Ho*Wo*r*r */
   double contract_flop;         /* 2*P*M*N*T (n = 0: 2*B*N*M*Ho*Wo) */
   int fused_input;              /* 1: nwg_conv2d runs nwg_input_contract (depth 3-4,
-                                   N <= 2) and the plan holds no V */
+                                   N <= 2, or depthwise) and the plan holds no V */
+  int depthwise;                /* 1: depthwise plan (see nwg_plan_create_depthwise) */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).
@@ -104,6 +105,24 @@ nwg_plan* nwg_plan_create(int B, int M, int N, int H, int W, int r, int tile);
 
 /* Same with explicit zero padding on all four sides ("same": pad = (r-1)/2). */
 nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad, int tile);
+
+/* --- Depthwise convolution (Table I's depth-wise row) --------------------
+ * Each of C channels is correlated with its own r x r kernel and there is
+ * no sum over channels:
+ *   y[b][c][i][j] = sum_{u,v} xpad[b][c][i+u][j+v] * w[c][0][u][v],
+ * x [B][C][H][W], w [C][1][r][r], y [B][C][Ho][Wo].  The plan's info has
+ * M = N = C and depthwise = 1; the Winograd-domain step is the element-wise
+ * product Yhat[p][c][t] = U[p][c] V[p][c][t].  U is [P/4][1][C][4] (depth 0:
+ * [1][C]); V and Z have the dense layouts with M = N = C.  nwg_conv2d runs,
+ * by depth: 0, y = w[c] x (pad must be 0); 1-2, one kernel x -> y (timed as
+ * the contraction, index 2); 3-4, nwg_input_contract then
+ * nwg_output_transform.  The stage calls take the same buffers as for dense
+ * plans; nwg_contract computes the element-wise product (with the level-1
+ * output transform) instead of a channel sum.  Errors as for the dense
+ * calls. */
+int nwg_plan_geometry_depthwise(int B, int C, int H, int W, int r, int pad, int tile,
+                                nwg_plan_info* out);
+nwg_plan* nwg_plan_create_depthwise(int B, int C, int H, int W, int r, int pad, int tile);
 
 /* Release a plan and its workspace.  NULL is a no-op.  The caller must make
  * sure no work using the plan is still queued. */
@@ -143,8 +162,9 @@ int nwg_contract(const nwg_plan* plan, const float* U, const float* V, float* Z,
  * x, U -> Z (yhat_bytes), with the same result as nwg_input_transform
  * followed by nwg_contract but without forming V.  For layers with one or
  * two output channels, whose contraction is too small to pay for writing
- * and re-reading V.  Depth 3 or 4 (8 <= r <= 31) and N <= 2 only;
- * NWG_EUNSUPPORTED otherwise. */
+ * and re-reading V, and for depthwise layers.  Depth 3 or 4
+ * (8 <= r <= 31) and N <= 2 or a depthwise plan only; NWG_EUNSUPPORTED
+ * otherwise. */
 int nwg_input_contract(const nwg_plan* plan, const float* x, const float* U, float* Z,
                        void* stream);
 

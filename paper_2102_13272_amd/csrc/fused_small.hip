@@ -1,5 +1,6 @@
 // Fused nested input transformation + channel contraction + level-1 output
-// transformation for layers with one or two output channels at depth 3 or 4
+// transformation for layers with one or two output channels at depth 3 or 4,
+// and for depthwise layers at depth 3 or 4
 // (Sec. III.B: the input-transform and element-wise steps, and the first
 // level of the output transform).
 //
@@ -42,10 +43,14 @@ constexpr int kTilesPerWave = 4;
 constexpr int kWin = 22;                    // window side left for levels 1..3
 constexpr int kWinStride = kWin * kWin + 1; // odd: the 4 tiles' windows start in different banks
 
-template <int NLEV, int NC, int CS>
+// DW: depthwise, one channel per launch row (blockIdx.y): x channel ch is
+// multiplied by U quad (p/4, 0, ch) of U[P/4][1][C][4] and written to Z
+// channel ch; no sum over channels (M = N = C, NC = 1, CS = 1).
+template <int NLEV, int NC, int CS, bool DW>
 __global__ __launch_bounds__(64 * CS) void input_contract_small(
     const float* __restrict__ x, const float4* __restrict__ U, float4* __restrict__ Z, int M,
     int N, int H, int W, int pad, int th, int tw, int T) {
+  static_assert(!DW || (NC == 1 && CS == 1), "depthwise: one channel, one wavefront");
   constexpr int Mn = 1 << NLEV;
   constexpr int L3 = kWin, WS = kWinStride, TW = kTilesPerWave;
   constexpr int NTASK = (TW * L3 + 63) / 64;   // window columns filled per lane
@@ -123,8 +128,9 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
   // U quad (p/4, m, n) sits at float4 index (p/4) M N + m N + n; the
   // branch's 64 quads start at branch * 64 M N (a per-lane offset, < 2^31
   // by the launch check), the rest is uniform
-  const unsigned qsU = (unsigned)(M * N);          // float4 quads between U quads
+  const unsigned qsU = (unsigned)(DW ? N : M * N); // float4 quads between U quads
   const unsigned ulane = (unsigned)branch * 64u * qsU;
+  const int ch = DW ? (int)blockIdx.y : 0;
 
   float acc[NC][4][4][4];                         // [n][q2r][q2c][2 i1r + i1c]
 #pragma unroll
@@ -136,7 +142,8 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
 #pragma unroll
         for (int d = 0; d < 4; ++d) acc[c][a][b][d] = 0.0f;
 
-  for (int m = wave; m < M; m += CS) {
+  const int m_begin = DW ? ch : wave, m_end = DW ? ch + 1 : M;
+  for (int m = m_begin; m < m_end; m += CS) {
     // fill: this wavefront's 4 windows of channel m (after the level-4 rows)
     const float* __restrict__ xm = x + (size_t)m * H * W;
 #pragma unroll
@@ -192,7 +199,7 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
       // (scalar ALU) instead of being held across the loop
       unsigned qs = qsU;
       asm volatile("" : "+s"(qs));
-      const float4* __restrict__ Um = U + (size_t)m * N;
+      const float4* __restrict__ Um = U + (DW ? (size_t)ch : (size_t)m * N);
       // Two passes over column halves: pass hc produces the level-2 column
       // digits q2c = 2 hc, 2 hc + 1, which read sub-window columns
       // [2 hc, 2 hc + 8) only; the halves share rows 2..9, recomputed.
@@ -303,7 +310,7 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
       for (int q2c = 0; q2c < 4; ++q2c) {
         const size_t g = (size_t)branch * 16 + q2r * 4 + q2c;
         const float* a = acc[c][q2r][q2c];
-        Z[g * gstride + (size_t)c * T + t] =
+        Z[g * gstride + (size_t)(DW ? ch : c) * T + t] =
             make_float4(ksign * a[0], ksign * a[1], ksign * a[2], ksign * a[3]);
       }
 }
@@ -313,20 +320,22 @@ hipError_t launch_ics(const nwg_plan_info& g, const float* x, const float4* U, f
                       unsigned nwg, int cs, hipStream_t s) {
   const int T = (int)g.T;
   if (cs == 4)
-    hipLaunchKernelGGL((input_contract_small<NLEV, NC, 4>), dim3(nwg), dim3(256), 0, s, x, U, Z,
-                       g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
+    hipLaunchKernelGGL((input_contract_small<NLEV, NC, 4, false>), dim3(nwg), dim3(256), 0, s, x,
+                       U, Z, g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
   else if (cs == 2)
-    hipLaunchKernelGGL((input_contract_small<NLEV, NC, 2>), dim3(nwg), dim3(128), 0, s, x, U, Z,
-                       g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
+    hipLaunchKernelGGL((input_contract_small<NLEV, NC, 2, false>), dim3(nwg), dim3(128), 0, s, x,
+                       U, Z, g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
   else
-    hipLaunchKernelGGL((input_contract_small<NLEV, NC, 1>), dim3(nwg), dim3(64), 0, s, x, U, Z,
-                       g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
+    hipLaunchKernelGGL((input_contract_small<NLEV, NC, 1, false>), dim3(nwg), dim3(64), 0, s, x,
+                       U, Z, g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
   return hipGetLastError();
 }
 
 }  // namespace
 
-bool input_contract_applies(const nwg_plan_info& g) { return g.n >= 3 && g.n <= 4 && g.N <= 2; }
+bool input_contract_applies(const nwg_plan_info& g) {
+  return g.n >= 3 && g.n <= 4 && (g.depthwise || g.N <= 2);
+}
 
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* Uf,
                                  float* Zf, hipStream_t s) {
@@ -335,13 +344,26 @@ hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const f
   const long long chunks = (g.T + kTilesPerWave - 1) / kTilesPerWave;
   const long long nwg = chunks * (g.n == 4 ? 16 : 1);
   if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
-  if ((long long)g.P / 4 * g.M * g.N > 0x7fffffffLL) return hipErrorInvalidValue;  // U quads
+  const long long uquads = (long long)g.P / 4 * (g.depthwise ? 1 : g.M) * g.N;
+  if (uquads > 0x7fffffffLL) return hipErrorInvalidValue;
+  const float4* U = reinterpret_cast<const float4*>(Uf);
+  float4* Z = reinterpret_cast<float4*>(Zf);
+  const int T = (int)g.T;
+  if (g.depthwise) {
+    if (g.N > 65535) return hipErrorInvalidValue;
+    dim3 grid((unsigned)nwg, (unsigned)g.N);
+    if (g.n == 3)
+      hipLaunchKernelGGL((input_contract_small<3, 1, 1, true>), grid, dim3(64), 0, s, x, U, Z,
+                         g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
+    else
+      hipLaunchKernelGGL((input_contract_small<4, 1, 1, true>), grid, dim3(64), 0, s, x, U, Z,
+                         g.M, g.N, g.H, g.W, g.pad, g.th, g.tw, T);
+    return hipGetLastError();
+  }
   // channel split: enough wavefronts for two per SIMD (1024 SIMDs), at
   // least one channel per wavefront
   int cs = 1;
   while (cs < 4 && nwg * cs < 2048 && 2 * cs <= g.M) cs *= 2;
-  const float4* U = reinterpret_cast<const float4*>(Uf);
-  float4* Z = reinterpret_cast<float4*>(Zf);
   if (g.n == 3)
     return g.N == 1 ? launch_ics<3, 1>(g, x, U, Z, (unsigned)nwg, cs, s)
                     : launch_ics<3, 2>(g, x, U, Z, (unsigned)nwg, cs, s);

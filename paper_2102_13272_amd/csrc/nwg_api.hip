@@ -54,7 +54,8 @@ namespace {
 // Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,
 // s_j = min(M_j, K_j), M_{j+1} = M_j + s_j (m-1), K_{j+1} = K_j + s_j (rb-1);
 // n is the smallest depth with K_n >= r, and r = 1 needs no level.
-int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
+// depthwise: M = N = C channels, one r x r kernel each, no channel sum.
+int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile, int depthwise,
                      nwg_plan_info* g) {
   if (!g) {
     set_error("output pointer is NULL");
@@ -96,6 +97,9 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     }
   }
   g->B = B; g->M = M; g->N = N; g->H = H; g->W = W; g->r = r; g->pad = pad; g->tile = tile;
+  g->depthwise = depthwise ? 1 : 0;
+  // the kernel transform sees M_k input channels: 1 for a depthwise layer
+  const int Mk = depthwise ? 1 : M;
   g->Ho = (int)Ho;
   g->Wo = (int)Wo;
   g->n = n;
@@ -111,16 +115,16 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
   for (int j = 0; j < 2 * n; ++j) P *= l;
   g->P = P;
   const double f = (double)sizeof(float);
-  g->direct_flop = 2.0 * B * N * (double)M * Ho * Wo * r * r;
+  g->direct_flop = 2.0 * B * N * (double)Mk * Ho * Wo * r * r;
   if (n == 0) {
-    g->u_bytes = (size_t)M * N * sizeof(float);
+    g->u_bytes = (size_t)Mk * N * sizeof(float);
     g->v_bytes = 0;
     g->yhat_bytes = 0;
-    g->ewmm_mults = (long long)B * N * M * Ho * Wo;
-    g->contract_flop = 2.0 * B * N * (double)M * Ho * Wo;
+    g->ewmm_mults = (long long)B * N * Mk * Ho * Wo;
+    g->contract_flop = 2.0 * B * N * (double)Mk * Ho * Wo;
   } else {
     // the contraction writes the level-1 output transform of Yhat: P/4 values per (n, t)
-    const double u = f * P * M * N, v = f * P * M * g->T, yh = f * (P / 4) * N * g->T;
+    const double u = f * P * Mk * N, v = f * P * M * g->T, yh = f * (P / 4) * N * g->T;
     if (u > 1e13 || v > 1e13 || yh > 1e13 || g->T > 0x7fffffffLL / 64) {
       set_error("workspace too large");
       return NWG_EUNSUPPORTED;
@@ -128,12 +132,15 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     g->u_bytes = (size_t)u;
     g->v_bytes = (size_t)v;
     g->yhat_bytes = (size_t)yh;
-    g->ewmm_mults = P * g->T * M * (long long)N;
-    g->contract_flop = 2.0 * P * (double)M * N * g->T;
+    g->ewmm_mults = P * g->T * Mk * (long long)N;
+    g->contract_flop = 2.0 * P * (double)Mk * N * g->T;
   }
-  // one or two output channels at depth 3-4: the fused kernel never forms V
+  // one or two output channels (or depthwise) at depth 3-4: the fused kernel
+  // never forms V.  Depthwise at depth 1-2 runs x -> y in one kernel.
   g->fused_input = nwg::input_contract_applies(*g) ? 1 : 0;
-  g->workspace_bytes = g->u_bytes + (g->fused_input ? 0 : g->v_bytes) + g->yhat_bytes;
+  const bool no_v = g->fused_input || depthwise;
+  const bool no_z = depthwise && n <= 2;
+  g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : g->yhat_bytes);
   return NWG_OK;
 }
 
@@ -195,8 +202,17 @@ nwg::ContractArgs depth0_args(const nwg_plan_info& g, const float* U, const floa
   return a;
 }
 
+// geometry seen by the kernel transform: one input channel when depthwise
+nwg_plan_info kernel_geometry(const nwg_plan_info& g) {
+  nwg_plan_info k = g;
+  if (g.depthwise) k.M = 1;
+  return k;
+}
+
 hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* V, float* Z,
                            hipStream_t s) {
+  if (g.depthwise)
+    return g.n == 0 ? nwg::launch_dw_scale(g, V, U, Z, s) : nwg::launch_dw_contract(g, U, V, Z, s);
   if (g.n == 0) return nwg::launch_gemm_depth0(depth0_args(g, U, V, Z), s);
   return nwg::launch_contract_fused(U, V, Z, g.M, g.N, (int)g.T, g.P / 16, s);
 }
@@ -204,7 +220,7 @@ hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* 
 int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, float* U,
                          hipStream_t s) {
   return timed(p, 0, s, "kernel transform launch",
-               [&] { return nwg::launch_kernel_xform(g, w, U, s); });
+               [&] { return nwg::launch_kernel_xform(kernel_geometry(g), w, U, s); });
 }
 
 }  // namespace
@@ -217,13 +233,20 @@ const char* nwg_last_error(void) { return g_last_error.c_str(); }
 
 int nwg_plan_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
                       nwg_plan_info* out) {
-  return compute_geometry(B, M, N, H, W, r, pad, tile, out);
+  return compute_geometry(B, M, N, H, W, r, pad, tile, 0, out);
 }
 
-nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad, int tile) {
-  nwg_plan_info g;
-  if (compute_geometry(B, M, N, H, W, r, pad, tile, &g) != NWG_OK) return nullptr;
-  if (g.n == 0 && pad != 0) {
+int nwg_plan_geometry_depthwise(int B, int C, int H, int W, int r, int pad, int tile,
+                                nwg_plan_info* out) {
+  return compute_geometry(B, C, C, H, W, r, pad, tile, 1, out);
+}
+
+}  // extern "C"
+
+namespace {
+
+nwg_plan* create_plan(const nwg_plan_info& g) {
+  if (g.n == 0 && g.pad != 0) {
     set_error("1x1 kernels with padding are not supported (pad must be 0 for r = 1)");
     return nullptr;
   }
@@ -248,13 +271,31 @@ nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad,
     }
     return true;
   };
-  if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, g.fused_input ? 0 : g.v_bytes, "V") ||
-      !alloc(&p->Yh, g.yhat_bytes, "Yhat")) {
+  const bool no_v = g.fused_input || g.depthwise;
+  const bool no_z = g.depthwise && g.n <= 2;
+  if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, no_v ? 0 : g.v_bytes, "V") ||
+      !alloc(&p->Yh, no_z ? 0 : g.yhat_bytes, "Yhat")) {
     nwg_plan_destroy(p);
     // keep the allocation message
     return nullptr;
   }
   return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad, int tile) {
+  nwg_plan_info g;
+  if (compute_geometry(B, M, N, H, W, r, pad, tile, 0, &g) != NWG_OK) return nullptr;
+  return create_plan(g);
+}
+
+nwg_plan* nwg_plan_create_depthwise(int B, int C, int H, int W, int r, int pad, int tile) {
+  nwg_plan_info g;
+  if (compute_geometry(B, C, C, H, W, r, pad, tile, 1, &g) != NWG_OK) return nullptr;
+  return create_plan(g);
 }
 
 nwg_plan* nwg_plan_create(int B, int M, int N, int H, int W, int r, int tile) {
@@ -288,7 +329,7 @@ int nwg_kernel_transform(const nwg_plan* p, const float* w, float* U, void* stre
     set_error("NULL argument to nwg_kernel_transform");
     return NWG_EINVAL;
   }
-  return check_hip(nwg::launch_kernel_xform(p->info, w, U, (hipStream_t)stream),
+  return check_hip(nwg::launch_kernel_xform(kernel_geometry(p->info), w, U, (hipStream_t)stream),
                    "kernel transform launch");
 }
 
@@ -321,8 +362,8 @@ int nwg_input_contract(const nwg_plan* p, const float* x, const float* U, float*
     return NWG_EINVAL;
   }
   if (!nwg::input_contract_applies(p->info)) {
-    set_error("fused input transform + contraction needs depth 3 or 4 and N <= 2 "
-              "(depth %d, N = %d)", p->info.n, p->info.N);
+    set_error("fused input transform + contraction needs depth 3 or 4 and N <= 2 or a "
+              "depthwise plan (depth %d, N = %d)", p->info.n, p->info.N);
     return NWG_EUNSUPPORTED;
   }
   return check_hip(nwg::launch_input_contract(p->info, x, U, Yh, (hipStream_t)stream),
@@ -371,6 +412,11 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
   if (g.n == 0) {
     return timed(p, 2, s, "contraction launch",
                  [&] { return launch_contract(g, p->U, x, y, s); });
+  }
+  if (g.depthwise && g.n <= 2) {
+    // input transform, product and output transform in one kernel
+    return timed(p, 2, s, "depthwise launch",
+                 [&] { return nwg::launch_dw_small(g, x, p->U, y, s); });
   }
   int rc;
   if (g.fused_input) {

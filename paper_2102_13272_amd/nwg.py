@@ -34,6 +34,7 @@ class nwg_plan_info(ctypes.Structure):
         ("yhat_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
         ("ewmm_mults", ctypes.c_longlong), ("direct_flop", ctypes.c_double),
         ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
+        ("depthwise", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -49,6 +50,8 @@ SIGNATURES = [
     ("nwg_plan_geometry", _I, [_I] * 8 + [ctypes.POINTER(nwg_plan_info)]),
     ("nwg_plan_create", _P, [_I] * 7),
     ("nwg_plan_create_pad", _P, [_I] * 8),
+    ("nwg_plan_geometry_depthwise", _I, [_I] * 7 + [ctypes.POINTER(nwg_plan_info)]),
+    ("nwg_plan_create_depthwise", _P, [_I] * 7),
     ("nwg_plan_destroy", None, [_P]),
     ("nwg_plan_query", _I, [_P, ctypes.POINTER(nwg_plan_info)]),
     ("nwg_conv2d", _I, [_P, _P, _P, _P, _P]),
@@ -106,6 +109,15 @@ def plan_geometry(B, M, N, H, W, r, pad=0, tile=NWG_TILE_F2X2_3X3) -> dict:
     return info.as_dict()
 
 
+def plan_geometry_depthwise(B, C, H, W, r, pad=0, tile=NWG_TILE_F2X2_3X3) -> dict:
+    """Host-only geometry of a depthwise convolution (no device is touched)."""
+    info = nwg_plan_info()
+    _check(load_library().nwg_plan_geometry_depthwise(B, C, H, W, r, pad, tile,
+                                                      ctypes.byref(info)),
+           "nwg_plan_geometry_depthwise")
+    return info.as_dict()
+
+
 def _ptr(t) -> int:
     return int(t.data_ptr())
 
@@ -120,12 +132,19 @@ def _stream(stream) -> int:
 class Plan:
     """A plan handle; tensors are torch float32 CUDA (HIP) tensors, contiguous."""
 
-    def __init__(self, B, M, N, H, W, r, pad=0, tile=NWG_TILE_F2X2_3X3):
+    def __init__(self, B, M, N, H, W, r, pad=0, tile=NWG_TILE_F2X2_3X3, depthwise=False):
+        """Dense plan (M -> N channels), or with depthwise=True a depthwise plan
+        over M = N channels (nwg_plan_create_depthwise)."""
         lib = load_library()
         self._lib = lib
-        self.handle = lib.nwg_plan_create_pad(B, M, N, H, W, r, pad, tile)
+        if depthwise:
+            if M != N:
+                raise ValueError("a depthwise plan has M == N channels")
+            self.handle = lib.nwg_plan_create_depthwise(B, M, H, W, r, pad, tile)
+        else:
+            self.handle = lib.nwg_plan_create_pad(B, M, N, H, W, r, pad, tile)
         if not self.handle:
-            raise NwgError(f"nwg_plan_create_pad failed: {last_error()}")
+            raise NwgError(f"plan creation failed: {last_error()}")
         info = nwg_plan_info()
         _check(lib.nwg_plan_query(self.handle, ctypes.byref(info)), "nwg_plan_query")
         self.info = info.as_dict()
@@ -151,7 +170,8 @@ class Plan:
     @property
     def u_shape(self):
         i = self.info
-        return (i["P"] // 4, i["M"], i["N"], 4) if i["n"] else (i["M"], i["N"])
+        mk = 1 if i["depthwise"] else i["M"]
+        return (i["P"] // 4, mk, i["N"], 4) if i["n"] else (mk, i["N"])
 
     @property
     def v_shape(self):

@@ -27,7 +27,10 @@ import numpy as np
 
 @dataclass(frozen=True)
 class Layer:
-    """One stride-1 convolution: x[B][M][H][W] * w[N][M][r][r] -> y[B][N][Ho][Wo]."""
+    """One stride-1 convolution: x[B][M][H][W] * w[N][M][r][r] -> y[B][N][Ho][Wo].
+
+    depthwise: M == N channels, w[N][1][r][r], no sum over channels.
+    """
     B: int
     M: int
     N: int
@@ -35,6 +38,7 @@ class Layer:
     W: int
     r: int
     pad: int
+    depthwise: bool = False
 
     @property
     def Ho(self) -> int:
@@ -47,7 +51,12 @@ class Layer:
     @property
     def direct_flop(self) -> int:
         """FLOP of the direct convolution (one multiply + one add per tap)."""
-        return 2 * self.B * self.N * self.M * self.Ho * self.Wo * self.r * self.r
+        mk = 1 if self.depthwise else self.M
+        return 2 * self.B * self.N * mk * self.Ho * self.Wo * self.r * self.r
+
+    @property
+    def w_shape(self):
+        return (self.N, 1 if self.depthwise else self.M, self.r, self.r)
 
 
 @dataclass(frozen=True)
@@ -93,10 +102,15 @@ WORKLOADS = {
     "c5_r31": Workload(
         "c5_r31", [Layer(16, 128, 128, 56, 56, 31, 15)], "normal", "fanin_normal", 5000,
         note="31x31 large-kernel backbone layer, B=16, 128->128 channels, 56x56, same padding"),
+    "dw7_pnasnet": Workload(
+        "dw7_pnasnet", [Layer(8, 54, 54, 83, 83, 7, 3, depthwise=True)], "normal",
+        "fanin_normal", 6000,
+        note="depthwise 7x7 on 54 channels of 83x83 (the shape of Table I's depth-wise row), "
+             "B=8, same padding"),
 }
 
 # Order in which the workloads are listed (1-based index k matches seed 1000*k).
-ORDER = ["c1_r4_valid", "c2_r7", "c3_r13", "c4_sr_stack", "c5_r31"]
+ORDER = ["c1_r4_valid", "c2_r7", "c3_r13", "c4_sr_stack", "c5_r31", "dw7_pnasnet"]
 
 
 def _draw(rng: np.random.Generator, shape, dist: str, fan_in: int = 1) -> np.ndarray:
@@ -122,8 +136,7 @@ def make_input(layer: Layer, dist: str, seed: int) -> np.ndarray:
 
 
 def make_weight(layer: Layer, dist: str, rng: np.random.Generator) -> np.ndarray:
-    return _draw(rng, (layer.N, layer.M, layer.r, layer.r), dist,
-                 fan_in=layer.M * layer.r * layer.r)
+    return _draw(rng, layer.w_shape, dist, fan_in=layer.w_shape[1] * layer.r * layer.r)
 
 
 def make_workload(name: str):
@@ -141,10 +154,11 @@ def make_workload(name: str):
     return x, ws
 
 
-def make_case(B, M, N, H, W, r, pad, seed, x_dist="uniform_pm1", w_dist="uniform_pm1"):
+def make_case(B, M, N, H, W, r, pad, seed, x_dist="uniform_pm1", w_dist="uniform_pm1",
+              depthwise=False):
     """A single ad-hoc layer for tests: returns (Layer, x, w)."""
-    L = Layer(B, M, N, H, W, r, pad)
+    L = Layer(B, M, N, H, W, r, pad, depthwise)
     rng = np.random.Generator(np.random.PCG64(seed))
     x = _draw(rng, (B, M, H, W), x_dist)
-    w = _draw(rng, (N, M, r, r), w_dist, fan_in=M * r * r)
+    w = _draw(rng, L.w_shape, w_dist, fan_in=L.w_shape[1] * r * r)
     return L, x, w

@@ -75,11 +75,15 @@ def test_geometry_of_the_five_workloads():
     expect = {"c1_r4_valid": [(2, 16, 256)], "c2_r7": [(2, 256, 256)], "c3_r13": [(3, 392, 4096)],
               "c5_r31": [(4, 256, 65536)],
               "c4_sr_stack": [(2, 16384, 256), (0, 65536, 1)] + [(1, 65536, 16)] * 4
-              + [(0, 65536, 1), (3, 4096, 4096)]}
+              + [(0, 65536, 1), (3, 4096, 4096)],
+              "dw7_pnasnet": [(2, 8 * 21 * 21, 256)]}
     for name, wl in WORKLOADS.items():
         got = []
         for L in wl.layers:
-            g = nwg.plan_geometry(L.B, L.M, L.N, L.H, L.W, L.r, L.pad)
+            if L.depthwise:
+                g = nwg.plan_geometry_depthwise(L.B, L.M, L.H, L.W, L.r, L.pad)
+            else:
+                g = nwg.plan_geometry(L.B, L.M, L.N, L.H, L.W, L.r, L.pad)
             got.append((g["n"], g["T"] if g["n"] else g["Ho"] * g["Wo"], g["P"]))
         assert got == expect[name], name
     g = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15)
@@ -131,3 +135,23 @@ def test_fused_input_flag_and_workspace(N):
         assert g["fused_input"] == int(fused), r
         v = 0 if fused else g["v_bytes"]
         assert g["workspace_bytes"] == g["u_bytes"] + v + g["yhat_bytes"]
+
+
+@pytest.mark.parametrize("r", [1, 3, 7, 13, 31])
+def test_depthwise_geometry(r):
+    B, C, H, W, pad = 2, 6, 40, 33, (r - 1) // 2
+    g = nwg.plan_geometry_depthwise(B, C, H, W, r, pad)
+    d = nwg.plan_geometry(B, C, C, H, W, r, pad)
+    assert g["depthwise"] == 1 and d["depthwise"] == 0
+    for k in ("n", "Mn", "Ln", "th", "tw", "T", "P", "Ho", "Wo", "v_bytes", "yhat_bytes"):
+        assert g[k] == d[k], k
+    assert (g["M"], g["N"]) == (C, C)
+    assert g["direct_flop"] == 2 * B * C * g["Ho"] * g["Wo"] * r * r
+    if g["n"]:
+        assert g["u_bytes"] == 4 * g["P"] * C
+        assert g["ewmm_mults"] == g["P"] * g["T"] * C
+        assert g["fused_input"] == int(g["n"] >= 3)
+        z = g["yhat_bytes"] if g["n"] >= 3 else 0
+        assert g["workspace_bytes"] == g["u_bytes"] + z
+    else:
+        assert g["u_bytes"] == 4 * C

@@ -10,11 +10,11 @@ import pytest
 import torch
 
 from oracle.direct import direct_conv2d
-from oracle.nested import (base_f23, ewmm, geometry, input_transform, kernel_transform,
-                           output_transform, point_permutation)
+from oracle.nested import ewmm, geometry, input_transform, kernel_transform, output_transform
 from paper_2102_13272_amd import nwg
 from paper_2102_13272_amd.workloads import make_case
 from tests.gpu_util import assert_close, dev, run_conv
+from tests.layout import level1 as _level1, quads as _quads, to_lib_points as _to_lib_points
 
 pytestmark = pytest.mark.gpu
 
@@ -50,27 +50,6 @@ def test_conv2d_matches_direct_oracle(case):
     print(f"case {case}", flush=True)
     y = run_conv(x, w, pad)
     assert_close(y, direct_conv2d(x, w, pad), what=str(case))
-
-
-def _to_lib_points(a, n):
-    """oracle [..., P1, P1] -> [..., P] in the library's point order."""
-    perm = point_permutation(n)
-    return a[..., perm[:, 0], perm[:, 1]]
-
-
-def _quads(a_pxy):
-    """[P][X][Y] -> quad-interleaved [P/4][X][Y][4]."""
-    P, X, Y = a_pxy.shape
-    return np.ascontiguousarray(a_pxy.reshape(P // 4, 4, X, Y).transpose(0, 2, 3, 1))
-
-
-def _level1(yh_pnt):
-    """[P][N][T] -> Z [P/16][N][T][4]: the oracle's A^T along both level-1 digits."""
-    AT = base_f23().AT.astype(np.float64)
-    P, N, T = yh_pnt.shape
-    g = yh_pnt.reshape(P // 16, 4, 4, N, T)
-    z = np.einsum("iq,jr,gqrnt->gntij", AT, AT, g)
-    return np.ascontiguousarray(z.reshape(P // 16, N, T, 4))
 
 
 STAGES = [(1, 3, 4, 12, 10, 3, 1), (2, 4, 3, 13, 11, 6, 2), (1, 3, 5, 20, 19, 11, 5),
