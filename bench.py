@@ -191,6 +191,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5_r31")
+    ap.add_argument("--pipeline-parts", type=int, default=0,
+                    help="input-transform/contraction pieces on two streams (0: the library's "
+                         "default for each plan, 1: off)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -235,6 +238,10 @@ def main():
     wds = [torch.from_numpy(w).to("cuda") for w in ws]
     plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, depthwise=L.depthwise)
              for L in wl.layers]
+    if args.pipeline_parts:
+        for p in plans:
+            if p.info["pipeline_parts"] > 1 or args.pipeline_parts == 1:
+                p.set_pipeline(args.pipeline_parts)
     outs = [torch.empty(p.y_shape, dtype=torch.float32, device="cuda") for p in plans]
     stream = torch.cuda.current_stream()
 
@@ -271,10 +278,14 @@ def main():
     stages = {}
     for p, (ms, cnt) in zip(plans, timing):
         bf = stage_bytes_flops(p.info)
+        parts = p.info["pipeline_parts"]
         for si, name in enumerate(STAGES):
             if name == "kernel_transform" or cnt[si] == 0:
                 continue
             b, f = bf[name]
+            if name in ("input_transform", "contraction") and parts > 1:
+                # the two-stream pipeline launches these in `parts` pieces
+                b, f = b / parts, f / parts
             s = stages.setdefault(name, {"ms_total": 0.0, "launches": 0, "bytes": 0.0,
                                          "flop": 0.0, "per_layer": []})
             s["ms_total"] += ms[si]
@@ -283,6 +294,8 @@ def main():
             s["flop"] += f * cnt[si]
             s["per_layer"].append({"r": p.info["r"], "n": p.info["n"],
                                    "avg_us": round(1e3 * ms[si] / cnt[si], 2),
+                                   **({"pieces": parts} if parts > 1 and name in (
+                                       "input_transform", "contraction") else {}),
                                    **({"fused_input": True} if p.info["fused_input"]
                                       and name == "contraction" else {})})
     detail = {}
@@ -320,7 +333,8 @@ def main():
            "M": L0.M, "N": wl.layers[-1].N, "H": L0.H, "W": L0.W,
            "r": [L.r for L in wl.layers] if len(wl.layers) > 1 else L0.r,
            "pad": [L.pad for L in wl.layers] if len(wl.layers) > 1 else L0.pad,
-           "base": "F(2x2,3x3)", "nesting_depth": [p.info["n"] for p in plans]}
+           "base": "F(2x2,3x3)", "nesting_depth": [p.info["n"] for p in plans],
+           "pipeline_parts": [p.info["pipeline_parts"] for p in plans]}
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),

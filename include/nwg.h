@@ -90,6 +90,8 @@ typedef struct nwg_plan_info {
   int fused_input;              /* 1: nwg_conv2d runs nwg_input_contract (depth 3-4,
                                    N <= 2, or depthwise) and the plan holds no V */
   int depthwise;                /* 1: depthwise plan (see nwg_plan_create_depthwise) */
+  int pipeline_parts;           /* 1, or the parts nwg_conv2d splits the input transform
+                                   and contraction into (nwg_plan_set_pipeline) */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).
@@ -171,6 +173,20 @@ int nwg_input_contract(const nwg_plan* plan, const float* x, const float* U, flo
 /* Nested output transformation (Sec. III.B, final step), levels 2..n:
  * Z -> y, cropped to Ho x Wo.  NWG_EINVAL at depth 0. */
 int nwg_output_transform(const nwg_plan* plan, const float* Z, float* y, void* stream);
+
+/* Two-stream pipeline (depth-4 dense plans whose contraction takes full
+ * 64-wide tiles: M % 32 == 0, N % 64 == 0, T % 64 == 0; off by default).
+ * With parts > 1, nwg_conv2d splits the input
+ * transform and the contraction into `parts` pieces over the level-4 branches
+ * (contiguous point ranges of V, U and Z) and queues each contraction piece on
+ * a stream of the plan's own, after its input piece, so that the next input
+ * piece (HBM-bound) overlaps it (MFMA-bound).  The plan's stream waits for
+ * the work already queued on the caller's stream first, and the caller's
+ * stream waits for the last piece before the output transform: the call
+ * stays ordered on the caller's stream.  parts: 1 (off), 2, 4, 8 or 16;
+ * NWG_EINVAL for other values, NWG_EUNSUPPORTED for a plan that cannot
+ * split.  Timing records each piece (counts then grow by `parts`). */
+int nwg_plan_set_pipeline(nwg_plan* plan, int parts);
 
 /* --- Per-stage timing ------------------------------------------------------
  * When enabled, nwg_conv2d records HIP events around each of its launches on

@@ -47,6 +47,12 @@ struct nwg_plan {
   bool timing = false;
   std::vector<TimingRecord> pending;
   std::vector<hipEvent_t> event_pool;
+  // two-stream pipeline (depth 4, dense): the input transform of part k+1
+  // runs on the caller's stream while the contraction of part k runs on
+  // `side`; created on first use, default priority
+  hipStream_t side = nullptr;
+  hipEvent_t ev_start = nullptr, ev_join = nullptr;
+  std::vector<hipEvent_t> ev_part;
 };
 
 namespace {
@@ -54,6 +60,17 @@ namespace {
 // Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,
 // s_j = min(M_j, K_j), M_{j+1} = M_j + s_j (m-1), K_{j+1} = K_j + s_j (rb-1);
 // n is the smallest depth with K_n >= r, and r = 1 needs no level.
+// Depth-4 dense plans whose contraction takes the full-tile path can split
+// the input transform and the contraction into parts over the level-4
+// branches (contiguous ranges of points) and overlap them on two streams.
+// Off by default: on the 31x31 layer (B = 16, 128 -> 128) the overlapped
+// contraction lost more (4.73 -> 5.6-6.6 ms over its parts) than the hidden
+// input transform saved; every part count from 2 to 16 made the step slower.
+bool pipeline_allowed(const nwg_plan_info& g) {
+  return g.n == 4 && !g.depthwise && !g.fused_input && g.M % 32 == 0 && g.N % 64 == 0 &&
+         g.T % 64 == 0;
+}
+
 // depthwise: M = N = C channels, one r x r kernel each, no channel sum.
 int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile, int depthwise,
                      nwg_plan_info* g) {
@@ -141,6 +158,7 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
   const bool no_v = g->fused_input || depthwise;
   const bool no_z = depthwise && n <= 2;
   g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : g->yhat_bytes);
+  g->pipeline_parts = 1;
   return NWG_OK;
 }
 
@@ -215,6 +233,51 @@ hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* 
     return g.n == 0 ? nwg::launch_dw_scale(g, V, U, Z, s) : nwg::launch_dw_contract(g, U, V, Z, s);
   if (g.n == 0) return nwg::launch_gemm_depth0(depth0_args(g, U, V, Z), s);
   return nwg::launch_contract_fused(U, V, Z, g.M, g.N, (int)g.T, g.P / 16, s);
+}
+
+// Input transform and contraction in `parts` pieces on two streams: part k's
+// contraction (on the plan's side stream) waits only for part k's input
+// transform, so part k+1's input transform (HBM-bound) overlaps it
+// (MFMA-bound).  The side stream starts after the work already queued on s
+// and s continues only after the last contraction.
+int run_pipelined(nwg_plan* p, const float* x, hipStream_t s) {
+  const nwg_plan_info& g = p->info;
+  const int np = g.pipeline_parts;
+  if (!p->side) {
+    int rc = check_hip(hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking), "side stream");
+    if (rc == NWG_OK)
+      rc = check_hip(hipEventCreateWithFlags(&p->ev_start, hipEventDisableTiming), "event");
+    if (rc == NWG_OK)
+      rc = check_hip(hipEventCreateWithFlags(&p->ev_join, hipEventDisableTiming), "event");
+    if (rc != NWG_OK) return rc;
+  }
+  while ((int)p->ev_part.size() < np) {
+    hipEvent_t e = nullptr;
+    const int rc = check_hip(hipEventCreateWithFlags(&e, hipEventDisableTiming), "event");
+    if (rc != NWG_OK) return rc;
+    p->ev_part.push_back(e);
+  }
+  int rc = check_hip(hipEventRecord(p->ev_start, s), "event record");
+  if (rc == NWG_OK) rc = check_hip(hipStreamWaitEvent(p->side, p->ev_start, 0), "stream wait");
+  if (rc != NWG_OK) return rc;
+  const long long G = g.P / 16, Gp = G / np;
+  const size_t M = g.M, N = g.N, T = g.T;
+  for (int k = 0; k < np && rc == NWG_OK; ++k) {
+    rc = timed(p, 1, s, "input transform launch",
+               [&] { return nwg::launch_input_xform(g, x, p->V, s, k, np); });
+    if (rc == NWG_OK) rc = check_hip(hipEventRecord(p->ev_part[k], s), "event record");
+    if (rc == NWG_OK) rc = check_hip(hipStreamWaitEvent(p->side, p->ev_part[k], 0), "stream wait");
+    if (rc != NWG_OK) break;
+    const size_t g0 = (size_t)k * Gp;
+    rc = timed(p, 2, p->side, "contraction launch", [&] {
+      return nwg::launch_contract_fused(p->U + 16 * g0 * M * N, p->V + 16 * g0 * M * T,
+                                        p->Yh + 4 * g0 * N * T, g.M, g.N, (int)g.T, Gp, p->side);
+    });
+  }
+  // join even after an error, so that s never runs ahead of the side stream
+  const int rj = check_hip(hipEventRecord(p->ev_join, p->side), "event record");
+  const int rw = rj == NWG_OK ? check_hip(hipStreamWaitEvent(s, p->ev_join, 0), "stream wait") : rj;
+  return rc != NWG_OK ? rc : rw;
 }
 
 int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, float* U,
@@ -312,6 +375,10 @@ void nwg_plan_destroy(nwg_plan* p) {
     hipEventDestroy(r.stop);
   }
   for (auto e : p->event_pool) hipEventDestroy(e);
+  for (auto e : p->ev_part) hipEventDestroy(e);
+  if (p->ev_start) hipEventDestroy(p->ev_start);
+  if (p->ev_join) hipEventDestroy(p->ev_join);
+  if (p->side) hipStreamDestroy(p->side);
   delete p;
 }
 
@@ -422,6 +489,8 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
   if (g.fused_input) {
     rc = timed(p, 2, s, "fused input transform + contraction launch",
                [&] { return nwg::launch_input_contract(g, x, p->U, p->Yh, s); });
+  } else if (g.pipeline_parts > 1) {
+    rc = run_pipelined(p, x, s);
   } else {
     rc = timed(p, 1, s, "input transform launch",
                [&] { return nwg::launch_input_xform(g, x, p->V, s); });
@@ -432,6 +501,28 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",
                [&] { return nwg::launch_output_xform(g, p->Yh, y, s); });
+}
+
+int nwg_plan_set_pipeline(nwg_plan* p, int parts) {
+  if (!p) {
+    set_error("NULL plan");
+    return NWG_EINVAL;
+  }
+  if (parts == 1) {
+    p->info.pipeline_parts = 1;
+    return NWG_OK;
+  }
+  if (parts != 2 && parts != 4 && parts != 8 && parts != 16) {
+    set_error("pipeline parts must be 1, 2, 4, 8 or 16 (got %d)", parts);
+    return NWG_EINVAL;
+  }
+  if (!pipeline_allowed(p->info)) {
+    set_error("the two-stream pipeline needs a dense depth-4 plan with M %% 32 == 0, "
+              "N %% 64 == 0 and T %% 64 == 0");
+    return NWG_EUNSUPPORTED;
+  }
+  p->info.pipeline_parts = parts;
+  return NWG_OK;
 }
 
 int nwg_plan_set_timing(nwg_plan* p, int enable) {

@@ -34,7 +34,7 @@ class nwg_plan_info(ctypes.Structure):
         ("yhat_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
         ("ewmm_mults", ctypes.c_longlong), ("direct_flop", ctypes.c_double),
         ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
-        ("depthwise", ctypes.c_int),
+        ("depthwise", ctypes.c_int), ("pipeline_parts", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -61,6 +61,7 @@ SIGNATURES = [
     ("nwg_contract", _I, [_P, _P, _P, _P, _P]),
     ("nwg_input_contract", _I, [_P, _P, _P, _P, _P]),
     ("nwg_output_transform", _I, [_P, _P, _P, _P]),
+    ("nwg_plan_set_pipeline", _I, [_P, _I]),
     ("nwg_plan_set_timing", _I, [_P, _I]),
     ("nwg_plan_get_timing", _I, [_P, ctypes.POINTER(ctypes.c_double),
                                  ctypes.POINTER(ctypes.c_longlong)]),
@@ -215,6 +216,12 @@ class Plan:
     def output_transform(self, Z, y, stream=None):
         _check(self._lib.nwg_output_transform(self.handle, _ptr(Z), _ptr(y), _stream(stream)),
                "nwg_output_transform")
+
+    def set_pipeline(self, parts: int):
+        _check(self._lib.nwg_plan_set_pipeline(self.handle, int(parts)), "nwg_plan_set_pipeline")
+        info = nwg_plan_info()
+        _check(self._lib.nwg_plan_query(self.handle, ctypes.byref(info)), "nwg_plan_query")
+        self.info = info.as_dict()
 
     def set_timing(self, enable: bool):
         _check(self._lib.nwg_plan_set_timing(self.handle, int(bool(enable))), "nwg_plan_set_timing")

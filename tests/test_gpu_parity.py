@@ -252,3 +252,39 @@ def test_timing_of_the_fused_path_counts_one_launch_as_contraction():
         ms, cnt = plan.get_timing()
         assert cnt == [1, 0, 2, 2]
         assert_close(y.cpu().numpy(), direct_conv2d(x, w, pad), what="fused timing")
+
+
+def test_two_stream_pipeline_matches_single_stream_bit_for_bit():
+    # depth 4, M % 32 == 0, N % 64 == 0, T % 64 == 0: the pipelined path
+    B, M, N, H, W, r, pad = 4, 32, 64, 56, 56, 31, 15
+    _, x, w = make_case(B, M, N, H, W, r, pad, seed=9, x_dist="normal", w_dist="fanin_normal")
+    print("pipeline", flush=True)
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        assert plan.info["pipeline_parts"] == 1 and plan.info["T"] == 64
+        xd, wd = dev(x), dev(w)
+        ys = {}
+        for parts in (1, 2, 4, 8, 16):
+            plan.set_pipeline(parts)
+            assert plan.info["pipeline_parts"] == parts
+            y = torch.full(plan.y_shape, float("nan"), device="cuda")
+            plan.conv2d(xd, wd, y)
+            torch.cuda.synchronize()
+            ys[parts] = y.cpu().numpy()
+        plan.set_timing(True)
+        plan.set_pipeline(4)
+        plan.conv2d(xd, wd, y)
+        ms, cnt = plan.get_timing()
+        assert cnt == [0, 4, 4, 1]
+        with pytest.raises(nwg.NwgError):
+            plan.set_pipeline(3)
+    for parts in (2, 4, 8, 16):
+        assert np.array_equal(ys[parts], ys[1]), parts
+    assert_close(ys[4], direct_conv2d(x, w, pad), what="pipelined y")
+
+
+def test_pipeline_is_refused_where_it_cannot_split():
+    with nwg.Plan(1, 3, 5, 20, 19, 11, 5) as plan:          # depth 3
+        assert plan.info["pipeline_parts"] == 1
+        with pytest.raises(nwg.NwgError):
+            plan.set_pipeline(4)
+        plan.set_pipeline(1)
