@@ -49,7 +49,7 @@ def stage_bytes_flops(info: dict):
                 "contraction": (x + y + 4 * mk * N, flop)}
     # Z: the contraction's output after the first output level, P/4 values per (n, t)
     U, V, Yh = 4 * P * mk * N, 4 * P * M * T, 4 * (P // 4) * N * T
-    if dw and info["n"] <= 2:
+    if info.get("fused_conv"):
         # one kernel: x and U in, y out
         return {"kernel_transform": (w + U, 0.0), "contraction": (x + U + y, flop)}
     if info.get("fused_input"):
@@ -297,6 +297,8 @@ def main():
                                    **({"pieces": parts} if parts > 1 and name in (
                                        "input_transform", "contraction") else {}),
                                    **({"fused_input": True} if p.info["fused_input"]
+                                      and name == "contraction" else {}),
+                                   **({"fused_conv": True} if p.info["fused_conv"]
                                       and name == "contraction" else {})})
     detail = {}
     for name, s in stages.items():

@@ -38,7 +38,9 @@
  * Ownership: the caller owns x, w, y, U/V/Z passed to stage calls, and
  * the stream; they must stay valid until the work queued on the stream has
  * finished.  A plan owns its workspace (U, V, Z; workspace_bytes),
- * allocated at creation; V is left out when info.fused_input is set.
+ * allocated at creation; V is left out when info.fused_input is set, V and
+ * Z when info.fused_conv is set (the stage calls still work on caller
+ * buffers).
  * Every call that takes a stream only queues work on it (`stream` is a
  * hipStream_t; NULL is the default stream) and never synchronises, except
  * nwg_plan_get_timing.  A plan is not thread-safe; one call in flight per
@@ -90,6 +92,9 @@ typedef struct nwg_plan_info {
   int fused_input;              /* 1: nwg_conv2d runs nwg_input_contract (depth 3-4,
                                    N <= 2, or depthwise) and the plan holds no V */
   int depthwise;                /* 1: depthwise plan (see nwg_plan_create_depthwise) */
+  int fused_conv;               /* 1: nwg_conv2d runs one kernel x -> y (depth 1 with
+                                   M <= 8, N <= 16; depth 2 with M <= 2, M N <= 64;
+                                   depthwise at depth 1-2); the plan holds only U */
   int pipeline_parts;           /* 1, or the parts nwg_conv2d splits the input transform
                                    and contraction into (nwg_plan_set_pipeline) */
 } nwg_plan_info;

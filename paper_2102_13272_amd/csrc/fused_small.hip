@@ -76,7 +76,7 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
   const int a4r0 = 8 * bt_tap0(q4r), a4r1 = 8 * bt_tap1(q4r);
   const float s4r0 = bt_sign0(q4r), s4r1 = bt_sign1(q4r);
   bool f_ok[NTASK];
-  size_t f_img[NTASK];
+  int f_img[NTASK];                                // b M H W (< 2^31, checked at launch)
   int f_dst[NTASK], f_gr0[NTASK], f_ca[NTASK], f_cb[NTASK];
   float f_ma[NTASK], f_mb[NTASK];
 #pragma unroll
@@ -94,7 +94,7 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
       const int b = ft / tpi;
       const int r2 = ft - b * tpi;
       const int ty = r2 / tw, tx = r2 - ty * tw;
-      f_img[k] = (size_t)b * M * H * W;
+      f_img[k] = b * M * H * W;
       f_dst[k] = ftl * WS + c;
       f_gr0[k] = ty * Mn - pad;
       const int gc = tx * Mn - pad + c;
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
 #pragma unroll
     for (int k = 0; k < NTASK; ++k) {
       if (!f_ok[k]) continue;
-      const float* __restrict__ xp = xm + f_img[k];
+      const int img = f_img[k];
       float* dst = wbuf + f_dst[k];
       // opaque per channel: keeps the 22 clamped row offsets and masks from
       // being hoisted out of the channel loop (they would hold ~90 registers)
@@ -165,10 +165,11 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
             const int ra = gr0 + r0 + i + a4r0, rb = gr0 + r0 + i + a4r1;
             const int rac = ra < 0 ? 0 : (ra > H - 1 ? H - 1 : ra);
             const int rbc = rb < 0 ? 0 : (rb > H - 1 ? H - 1 : rb);
-            va[i] = xp[(size_t)rac * W + f_ca[k]];
-            vb[i] = xp[(size_t)rac * W + f_cb[k]];
-            vc[i] = xp[(size_t)rbc * W + f_ca[k]];
-            vd[i] = xp[(size_t)rbc * W + f_cb[k]];
+            // uniform channel base plus a 32-bit per-lane offset
+            va[i] = xm[img + rac * W + f_ca[k]];
+            vb[i] = xm[img + rac * W + f_cb[k]];
+            vc[i] = xm[img + rbc * W + f_ca[k]];
+            vd[i] = xm[img + rbc * W + f_cb[k]];
           }
 #pragma unroll
           for (int i = 0; i < RB; ++i) {
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(64 * CS) void input_contract_small(
 #pragma unroll
         for (int i = 0; i < L3; ++i) {
           const int gr = gr0 + i;
-          va[i] = xp[(size_t)(gr < 0 ? 0 : (gr > H - 1 ? H - 1 : gr)) * W + f_ca[k]];
+          va[i] = xm[img + (gr < 0 ? 0 : (gr > H - 1 ? H - 1 : gr)) * W + f_ca[k]];
         }
 #pragma unroll
         for (int i = 0; i < L3; ++i) {
@@ -346,6 +347,7 @@ hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const f
   if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
   const long long uquads = (long long)g.P / 4 * (g.depthwise ? 1 : g.M) * g.N;
   if (uquads > 0x7fffffffLL) return hipErrorInvalidValue;
+  if ((long long)g.B * g.M * g.H * g.W > 0x7fffffffLL) return hipErrorInvalidValue;
   const float4* U = reinterpret_cast<const float4*>(Uf);
   float4* Z = reinterpret_cast<float4*>(Zf);
   const int T = (int)g.T;

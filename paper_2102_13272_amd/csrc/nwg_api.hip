@@ -153,10 +153,12 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     g->contract_flop = 2.0 * P * (double)Mk * N * g->T;
   }
   // one or two output channels (or depthwise) at depth 3-4: the fused kernel
-  // never forms V.  Depthwise at depth 1-2 runs x -> y in one kernel.
+  // never forms V.  Few channels (or depthwise) at depth 1-2: one kernel
+  // x -> y, neither V nor Z.
   g->fused_input = nwg::input_contract_applies(*g) ? 1 : 0;
-  const bool no_v = g->fused_input || depthwise;
-  const bool no_z = depthwise && n <= 2;
+  g->fused_conv = (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
+  const bool no_v = g->fused_input || depthwise || g->fused_conv;
+  const bool no_z = g->fused_conv;
   g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : g->yhat_bytes);
   g->pipeline_parts = 1;
   return NWG_OK;
@@ -334,8 +336,8 @@ nwg_plan* create_plan(const nwg_plan_info& g) {
     }
     return true;
   };
-  const bool no_v = g.fused_input || g.depthwise;
-  const bool no_z = g.depthwise && g.n <= 2;
+  const bool no_v = g.fused_input || g.depthwise || g.fused_conv;
+  const bool no_z = g.fused_conv;
   if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, no_v ? 0 : g.v_bytes, "V") ||
       !alloc(&p->Yh, no_z ? 0 : g.yhat_bytes, "Yhat")) {
     nwg_plan_destroy(p);
@@ -480,10 +482,12 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
     return timed(p, 2, s, "contraction launch",
                  [&] { return launch_contract(g, p->U, x, y, s); });
   }
-  if (g.depthwise && g.n <= 2) {
-    // input transform, product and output transform in one kernel
-    return timed(p, 2, s, "depthwise launch",
-                 [&] { return nwg::launch_dw_small(g, x, p->U, y, s); });
+  if (g.fused_conv) {
+    // input transform, channel sum (or product) and output transform in one kernel
+    return timed(p, 2, s, "single-kernel convolution launch", [&] {
+      return g.depthwise ? nwg::launch_dw_small(g, x, p->U, y, s)
+                         : nwg::launch_small_conv(g, x, p->U, y, s);
+    });
   }
   int rc;
   if (g.fused_input) {

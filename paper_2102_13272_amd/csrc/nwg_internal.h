@@ -110,6 +110,10 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
 bool input_contract_applies(const nwg_plan_info& g);
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* U, float* Z,
                                  hipStream_t s);
+// few channels at depth 1-2 (dense): x -> y in one kernel
+bool small_conv_applies(const nwg_plan_info& g);
+hipError_t launch_small_conv(const nwg_plan_info& g, const float* x, const float* U, float* y,
+                             hipStream_t s);
 // depthwise: y = U[c] x (depth 0); x -> y in one kernel (depth 1-2);
 // U, V -> Z element-wise with the level-1 output transform (depth >= 1)
 hipError_t launch_dw_scale(const nwg_plan_info& g, const float* x, const float* U, float* y,

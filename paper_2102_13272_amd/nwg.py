@@ -34,7 +34,8 @@ class nwg_plan_info(ctypes.Structure):
         ("yhat_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
         ("ewmm_mults", ctypes.c_longlong), ("direct_flop", ctypes.c_double),
         ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
-        ("depthwise", ctypes.c_int), ("pipeline_parts", ctypes.c_int),
+        ("depthwise", ctypes.c_int), ("fused_conv", ctypes.c_int),
+        ("pipeline_parts", ctypes.c_int),
     ]
 
     def as_dict(self):

@@ -133,6 +133,9 @@ def test_fused_input_flag_and_workspace(N):
         g = nwg.plan_geometry(2, 4, N, 70, 66, r, (r - 1) // 2)
         fused = g["n"] in (3, 4) and N <= 2
         assert g["fused_input"] == int(fused), r
+        if g["fused_conv"]:                     # one kernel x -> y: U only
+            assert g["workspace_bytes"] == g["u_bytes"]
+            continue
         v = 0 if fused else g["v_bytes"]
         assert g["workspace_bytes"] == g["u_bytes"] + v + g["yhat_bytes"]
 
@@ -155,3 +158,17 @@ def test_depthwise_geometry(r):
         assert g["workspace_bytes"] == g["u_bytes"] + z
     else:
         assert g["u_bytes"] == 4 * C
+
+
+def test_fused_conv_flag():
+    # depth 1: M <= 8 and N <= 16; depth 2: M <= 2 and M N <= 64; depthwise depth 1-2
+    for (M, N, r, want) in [(5, 5, 3, 1), (8, 16, 3, 1), (9, 4, 3, 0), (4, 17, 3, 0),
+                            (1, 32, 5, 1), (2, 32, 5, 1), (2, 33, 5, 0), (3, 4, 5, 0),
+                            (1, 1, 9, 0), (4, 4, 1, 0)]:
+        g = nwg.plan_geometry(2, M, N, 40, 40, r, (r - 1) // 2)
+        assert g["fused_conv"] == want, (M, N, r)
+        if want:
+            assert g["workspace_bytes"] == g["u_bytes"]
+    for r, want in [(3, 1), (7, 1), (9, 0), (1, 0)]:
+        g = nwg.plan_geometry_depthwise(2, 6, 40, 40, r, (r - 1) // 2)
+        assert g["fused_conv"] == want, r

@@ -288,3 +288,25 @@ def test_pipeline_is_refused_where_it_cannot_split():
         with pytest.raises(nwg.NwgError):
             plan.set_pipeline(4)
         plan.set_pipeline(1)
+
+
+# few channels at depth 1-2: one kernel x -> y (depth 1: M <= 8, N <= 16;
+# depth 2: M <= 2, M N <= 64), ragged tiles, B > 1, both paddings
+SMALL = [(2, 1, 1, 9, 7, 3, 1), (1, 3, 16, 17, 30, 3, 1), (3, 5, 5, 20, 21, 3, 1),
+         (1, 8, 2, 13, 15, 2, 0), (2, 7, 9, 16, 16, 3, 0), (1, 1, 32, 33, 29, 5, 2),
+         (2, 2, 7, 18, 19, 7, 3), (1, 1, 64, 16, 16, 4, 0), (2, 2, 32, 21, 22, 6, 0)]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
+def test_single_kernel_small_channel_layers(case):
+    B, M, N, H, W, r, pad = case
+    print(f"small {case}", flush=True)
+    L, x, w = make_case(B, M, N, H, W, r, pad, seed=sum(case) + 1)
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        assert plan.info["fused_conv"] == 1 and plan.info["n"] in (1, 2)
+        assert plan.info["workspace_bytes"] == plan.info["u_bytes"]
+        plan.set_timing(True)
+        y = run_conv(x, w, pad, plan)
+        ms, cnt = plan.get_timing()
+        assert cnt == [1, 0, 1, 0]
+    assert_close(y, direct_conv2d(x, w, pad), what=str(case))
