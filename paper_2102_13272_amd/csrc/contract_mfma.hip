@@ -21,7 +21,8 @@
 // operand of all four points, and four accumulator sets take the four GEMMs.
 // After the K loop the four products are folded into the 2x2 level-1
 // outputs.  Two pipelines:
-//   * deep (full 64x128 or 64x64 tiles, M a multiple of 32; 8 or 4 waves):
+//   * deep (64x128 tiles when T is a multiple of 128, else 64x64 with a
+//     ragged last column tile; N a multiple of 64, M of 32; 8 or 4 waves):
 //     four LDS stages of 8 channels filled by direct global->LDS loads,
 //     three chunks in flight;
 //   * general (any shape): two LDS stages of 16 channels, direct loads for
@@ -323,8 +324,11 @@ struct DeepLoader {
   static constexpr int PER = BKD * COLS / NT;   // loads per thread per chunk
   static constexpr int RSTEP = NT / COLS;
   int off0;
-  __device__ __forceinline__ void init(int ld, int c0) {
-    off0 = (threadIdx.x / COLS) * ld + c0 + threadIdx.x % COLS;
+  // columns past ncols (a ragged last tile) re-read column ncols - 1; their
+  // results are not stored
+  __device__ __forceinline__ void init(int ld, int c0, int ncols) {
+    const int c = c0 + threadIdx.x % COLS;
+    off0 = (threadIdx.x / COLS) * ld + (c < ncols ? c : ncols - 1);
   }
   __device__ __forceinline__ void load(const float4* __restrict__ base, int ld, int k0,
                                        float4 (*dst)[COLS]) {
@@ -455,8 +459,8 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
         tile.out[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
         tile.acc[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
-  tile.da.init(N, n0);
-  tile.db.init(T, c0);
+  tile.da.init(N, n0, N);
+  tile.db.init(T, c0, T);
 
   // prologue: chunks 0 .. STAGES-2 (the K loop has nk % STAGES == 0 chunks per q1r)
   tile.request(0, A0, B0);
@@ -491,8 +495,9 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = c0 + tile.wn * WTN + j * 16 + tile.lr;
-        Zg[(size_t)row * T + col] = make_float4(tile.out[0][i][j][v], tile.out[1][i][j][v],
-                                                tile.out[2][i][j][v], tile.out[3][i][j][v]);
+        if (col < T)
+          Zg[(size_t)row * T + col] = make_float4(tile.out[0][i][j][v], tile.out[1][i][j][v],
+                                                  tile.out[2][i][j][v], tile.out[3][i][j][v]);
       }
     }
   }
@@ -501,9 +506,10 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES>
 hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, int T,
                        long long G, hipStream_t s) {
-  const int ntb = T / BN, nnb = N / BM;
+  // T need not be a multiple of BN: the last column tile is ragged
+  const int ntb = (T + BN - 1) / BN, nnb = N / BM;
   const long long blocks = (long long)ntb * nnb * G;
-  if (T % BN || N % BM || M % (BKD * STAGES) || blocks <= 0 || blocks > 0x7fffffffLL)
+  if (N % BM || M % (BKD * STAGES) || blocks <= 0 || blocks > 0x7fffffffLL)
     return hipErrorInvalidValue;
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
@@ -694,10 +700,11 @@ hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s) {
 
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
                                  long long G, hipStream_t s) {
-  // full 64x64 tiles and whole 4-stage K sweeps: the deep pipeline
+  // full 64-row tiles and whole 4-stage K sweeps: the deep pipeline; a
+  // ragged T takes 64-column tiles (the last one partly recomputed)
   if (M % 32 == 0 && N % 64 == 0) {
     if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s);
-    if (T % 64 == 0) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
+    if (T >= 64) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
   }
   if (N <= 16) return launch_fused<16, 128, 1, 4>(U, V, Z, M, N, T, G, s);
   if (N <= 32) return launch_fused<32, 128, 1, 4>(U, V, Z, M, N, T, G, s);

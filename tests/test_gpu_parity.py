@@ -162,7 +162,9 @@ def test_fused_input_contract_rejects_other_shapes():
                                          (32, 5, 4096, 0), (96, 40, 70, 2),
                                          # full tiles (direct global->LDS path) per tile shape
                                          (64, 32, 128, 1), (16, 16, 128, 2), (32, 48, 256, 1),
-                                         (128, 64, 192, 1), (64, 96, 256, 1), (128, 32, 128, 2)])
+                                         (128, 64, 192, 1), (64, 96, 256, 1), (128, 32, 128, 2),
+                                         # deep path with a ragged last column tile
+                                         (64, 32, 100, 1), (128, 64, 200, 2), (64, 64, 65, 1)])
 def test_contraction_matches_numpy(N, M, T, depth):
     """Z = level-1 A^T of (U[p]^T V[p]) for ragged shapes, through nwg_contract.
 
