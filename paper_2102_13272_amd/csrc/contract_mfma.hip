@@ -706,6 +706,10 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
     if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s);
     if (T >= 64) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
   }
+  // small problems (fewer than 256 work-groups with the wide tiles, e.g.
+  // 32 channels on 256 tiles at depth 2: 32 work-groups): 16 x 64 tiles
+  const long long wide = (long long)((T + 127) / 128) * ((N + 31) / 32) * G;
+  if (N <= 32 && wide < 256) return launch_fused<16, 64, 1, 4>(U, V, Z, M, N, T, G, s);
   if (N <= 16) return launch_fused<16, 128, 1, 4>(U, V, Z, M, N, T, G, s);
   if (N <= 32) return launch_fused<32, 128, 1, 4>(U, V, Z, M, N, T, G, s);
   return launch_fused<64, 64, 2, 2>(U, V, Z, M, N, T, G, s);
