@@ -61,8 +61,21 @@ extern "C" {
 
 typedef struct nwg_plan nwg_plan;
 
-/* Winograd base of the nest.  Only F(2x2, 3x3) (eq. 2.3) is provided. */
-enum { NWG_TILE_F2X2_3X3 = 0 };
+/* Winograd base of the nest.
+ *   NWG_TILE_F2X2_3X3: F(2x2, 3x3) (eq. 2.3), depth 0-4 (r <= 31), the layouts
+ *     above.
+ *   NWG_TILE_F3X3_3X3: F(3x3, 3x3), dense plans at depth 1-2 only (r <= 9):
+ *     strides 1, 3, M_n = K_n = 3^n, L_n = 5 or 17, P = 5^(2n) points with
+ *     base-5 digits (q_n^row, q_n^col, ..., q_1^row, q_1^col); Toom-Cook
+ *     points 0, 1, -1, 2, infinity.  Plain layouts (no quads):
+ *       U [P][M][N], V [P][M][T],
+ *       Z [P/25][5][3][N][T], the level-1 output transform along the
+ *         columns only: Z[g][q1r][i1c][n][t] = sum over q1c of
+ *         A^T[i1c][q1c] Yhat[25g + 5 q1r + q1c][n][t]
+ *     (A^T rows [1,1,1,1,0], [0,1,-1,2,0], [0,1,1,4,1]).
+ *     Depth 0 (r = 1) is the plain contraction as for F(2x2, 3x3).  Never
+ *     fused (fused_input = fused_conv = 0, pipeline_parts = 1). */
+enum { NWG_TILE_F2X2_3X3 = 0, NWG_TILE_F3X3_3X3 = 1 };
 
 enum {
   NWG_OK = 0,
@@ -100,8 +113,8 @@ typedef struct nwg_plan_info {
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).
- * Returns NWG_EINVAL for a bad shape, NWG_EUNSUPPORTED for r > 31 or an
- * unknown tile. */
+ * Returns NWG_EINVAL for a bad shape, NWG_EUNSUPPORTED for r > 31 (r > 9 on
+ * NWG_TILE_F3X3_3X3) or an unknown tile. */
 int nwg_plan_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
                       nwg_plan_info* out);
 

@@ -50,12 +50,6 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBK = 16;
 
-__device__ __forceinline__ long long xcd_remap(long long i, long long G) {
-  const long long q = G / 8, rem = G % 8;
-  const long long xcd = i % 8, slot = i / 8;
-  return xcd < rem ? xcd * (q + 1) + slot : rem * (q + 1) + (xcd - rem) * q + slot;
-}
-
 // ---------------------------------------------------------------------------
 // Fused contraction + level-1 output transform (depth >= 1)
 // ---------------------------------------------------------------------------
@@ -309,13 +303,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 // them); the barrier then also guarantees that nobody still reads the
 // buffer the step's new loads overwrite (it was read in step it-1).
 // ---------------------------------------------------------------------------
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
 
 template <int BKD, int COLS, int NT>
 struct DeepLoader {

@@ -1,0 +1,629 @@
+// Nested Winograd on the base F(3,3) (Sec. III.B with m = r = 3, l = 5),
+// depth 1 or 2 (kernels up to 9 x 9): the level recurrence gives strides
+// 1, 3, M_n = K_n = 3^n, L_n = 5 at depth 1 and 17 at depth 2, and
+// P = 5^(2n) = 25 or 625 points per tile.  Sec. V.A names F(3,3) among the
+// bases of its comparison; at depth <= 2 its fp32 error stays near 1e-6.
+//
+// Base matrices from the Toom-Cook construction with interpolation points
+// 0, 1, -1, 2 and infinity (correlation form y = A^T[(G w) (.) (B^T x)]):
+//   G (5x3):  [1,0,0] [1,1,1] [1,-1,1] [1,2,4] [0,0,1]
+//   A^T (3x5): [1,1,1,1,0] [0,1,-1,2,0] [0,1,1,4,1]
+//   B^T (5x5) = (Vandermonde of the points)^-T:
+//     [1,-1/2,-1,1/2,0] [0,1,1/2,-1/2,0] [0,-1/3,1/2,-1/6,0] [0,-1/6,0,1/6,0] [0,2,-1,-2,1]
+// (the inverse of the Vandermonde map f = V c of a degree-4 polynomial
+// sampled at 0, 1, -1, 2 with its leading coefficient, solved by hand).
+//
+// Layouts (plain fp32; p has base-5 digits (q2r, q2c, q1r, q1c), most
+// significant first, the level-2 digits absent at depth 1):
+//   U [P][M][N], V [P][M][T],
+//   Z [P/25][5][3][N][T]: the contraction applies the level-1 A^T along the
+//       columns, Z[g][q1r][i1c][n][t] = sum_q1c A^T[i1c][q1c] Yhat[25 g + 5 q1r + q1c][n][t].
+// Consecutive lanes take consecutive tiles (or output channels), so every
+// store and load of a wavefront covers 256 contiguous bytes.
+#include "nwg_internal.h"
+
+namespace nwg {
+namespace {
+
+constexpr int L5 = 5;
+
+// B^T[q][a], G[q][k], A^T[i][q] of F(3,3)
+__device__ __forceinline__ float bt5(int q, int a) {
+  constexpr float T[5][5] = {{1.0f, -0.5f, -1.0f, 0.5f, 0.0f},
+                             {0.0f, 1.0f, 0.5f, -0.5f, 0.0f},
+                             {0.0f, -1.0f / 3.0f, 0.5f, -1.0f / 6.0f, 0.0f},
+                             {0.0f, -1.0f / 6.0f, 0.0f, 1.0f / 6.0f, 0.0f},
+                             {0.0f, 2.0f, -1.0f, -2.0f, 1.0f}};
+  return T[q][a];
+}
+__device__ __forceinline__ float g5(int q, int k) {
+  constexpr float G[5][3] = {{1.0f, 0.0f, 0.0f}, {1.0f, 1.0f, 1.0f}, {1.0f, -1.0f, 1.0f},
+                             {1.0f, 2.0f, 4.0f}, {0.0f, 0.0f, 1.0f}};
+  return G[q][k];
+}
+__host__ __device__ constexpr float at5(int i, int q) {
+  return i == 0 ? (q == 4 ? 0.0f : 1.0f)
+       : i == 1 ? (q == 0 ? 0.0f : q == 1 ? 1.0f : q == 2 ? -1.0f : q == 3 ? 2.0f : 0.0f)
+                : (q == 0 ? 0.0f : q == 3 ? 4.0f : 1.0f);
+}
+
+// B^T along a length-5 vector
+__device__ __forceinline__ void bt5_vec(const float (&v)[5], float (&o)[5]) {
+#pragma unroll
+  for (int q = 0; q < 5; ++q) {
+    float s = 0.0f;
+#pragma unroll
+    for (int a = 0; a < 5; ++a)
+      if (bt5(q, a) != 0.0f) s = fmaf(bt5(q, a), v[a], s);
+    o[q] = s;
+  }
+}
+
+// ---- kernel transform: one thread per (n, m) --------------------------------
+// w (r x r, zero-padded to K_n x K_n at its end) -> U[p][m][n].  Tap k splits
+// as k = k1 + 3 k2 (k1, k2 < 3).  For every pair of row digits (q2r, q1r)
+// the weighted rows give a length-K_n row wr, transformed along the columns.
+template <int NLEV>
+__global__ __launch_bounds__(256) void kernel_xform5(const float* __restrict__ w,
+                                                     float* __restrict__ U, int M, int N, int r,
+                                                     long long nthreads) {
+  constexpr int K = NLEV == 1 ? 3 : 9;
+  const long long id = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (id >= nthreads) return;
+  const int n = (int)(id % N), m = (int)(id / N);
+  const float* __restrict__ wp = w + ((size_t)n * M + m) * r * r;
+  float wk[K][K];
+#pragma unroll
+  for (int i = 0; i < K; ++i)
+#pragma unroll
+    for (int j = 0; j < K; ++j) wk[i][j] = (i < r && j < r) ? wp[i * r + j] : 0.0f;
+  const size_t pstride = (size_t)M * N;
+  float* __restrict__ up = U + (size_t)m * N + n;
+  constexpr int R1 = NLEV == 1 ? 1 : 5;     // level-2 digits per axis
+#pragma unroll
+  for (int q2r = 0; q2r < R1; ++q2r)
+#pragma unroll
+    for (int q1r = 0; q1r < 5; ++q1r) {
+      // row combination: coefficient of kernel row k1 + 3 k2
+      float wr[K];
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        float s = 0.0f;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const float c = NLEV == 1 ? g5(q1r, k) : g5(q2r, k / 3) * g5(q1r, k % 3);
+          s = fmaf(c, wk[k][j], s);
+        }
+        wr[j] = s;
+      }
+#pragma unroll
+      for (int q2c = 0; q2c < R1; ++q2c)
+#pragma unroll
+        for (int q1c = 0; q1c < 5; ++q1c) {
+          float s = 0.0f;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            const float c = NLEV == 1 ? g5(q1c, k) : g5(q2c, k / 3) * g5(q1c, k % 3);
+            s = fmaf(c, wr[k], s);
+          }
+          const int p = NLEV == 1 ? q1r * 5 + q1c : ((q2r * 5 + q2c) * 5 + q1r) * 5 + q1c;
+          up[(size_t)p * pstride] = s;
+        }
+    }
+}
+
+// ---- input transform --------------------------------------------------------
+// Work-group: a box of RX x RY tiles of one (image, channel) staged in LDS;
+// depth 1: one thread per tile; depth 2: wavefront q2r (5 wavefronts) of 64
+// tiles, each lane computing the 125 points of its level-2 row digit.
+template <int NLEV>
+__global__ __launch_bounds__(320) void input_xform5(const float* __restrict__ x,
+                                                    float* __restrict__ V, int M, int H, int W,
+                                                    int pad, int th, int tw, int T, int RX, int RY,
+                                                    int nbx, int nby) {
+  constexpr int Mn = NLEV == 1 ? 3 : 9;
+  constexpr int Ln = NLEV == 1 ? 5 : 17;
+  extern __shared__ float box[];
+  const int m = blockIdx.y;
+  int bid = blockIdx.x;
+  const int bx = bid % nbx;
+  bid /= nbx;
+  const int by = bid % nby;
+  const int b = bid / nby;
+  const int ty0 = by * RY, tx0 = bx * RX;
+  const int BH = (RY - 1) * Mn + Ln, BW = (RX - 1) * Mn + Ln;
+  const int r0 = ty0 * Mn - pad, c0 = tx0 * Mn - pad;
+  const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
+  const int nth = blockDim.x;
+  for (int e = threadIdx.x; e < BH * BW; e += nth) {
+    const int row = e / BW, col = e - row * BW;
+    const int gr = r0 + row, gc = c0 + col;
+    float v = 0.0f;
+    if (gr >= 0 && gr < H && gc >= 0 && gc < W) v = xp[(size_t)gr * W + gc];
+    box[e] = v;
+  }
+  __syncthreads();
+  const int s = threadIdx.x & 63;                      // tile within the box (<= 64)
+  const int q2r = NLEV == 1 ? 0 : (int)(threadIdx.x >> 6);
+  if (NLEV == 1 && threadIdx.x >= 64) return;
+  if (s >= RX * RY) return;
+  const int ly = s / RX, lx = s - ly * RX;
+  const int ty = ty0 + ly, tx = tx0 + lx;
+  if (ty >= th || tx >= tw) return;
+  const int t = (b * th + ty) * tw + tx;
+  const float* win = box + ly * Mn * BW + lx * Mn;
+  const size_t pstride = (size_t)M * T;
+  float* __restrict__ vp = V + (size_t)m * T + t;
+  if constexpr (NLEV == 1) {
+    float X[5][5];
+#pragma unroll
+    for (int i = 0; i < 5; ++i)
+#pragma unroll
+      for (int j = 0; j < 5; ++j) X[i][j] = win[i * BW + j];
+    float C[5][5];                                     // rows transformed: C[q1r][col]
+#pragma unroll
+    for (int j = 0; j < 5; ++j) {
+      const float col[5] = {X[0][j], X[1][j], X[2][j], X[3][j], X[4][j]};
+      float o[5];
+      bt5_vec(col, o);
+#pragma unroll
+      for (int q = 0; q < 5; ++q) C[q][j] = o[q];
+    }
+#pragma unroll
+    for (int q1r = 0; q1r < 5; ++q1r) {
+      float o[5];
+      bt5_vec(C[q1r], o);
+#pragma unroll
+      for (int q1c = 0; q1c < 5; ++q1c) vp[(size_t)(q1r * 5 + q1c) * pstride] = o[q1c];
+    }
+  } else {
+    // level 2 along the rows (stride 3) for this wavefront's digit q2r:
+    // Rw[a1][c] = sum_a2 B^T[q2r][a2] win[a1 + 3 a2][c]; the row of B^T is
+    // selected, since q2r is not a compile-time index
+    float c2v[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int q = 0; q < 5; ++q)
+#pragma unroll
+      for (int a2 = 0; a2 < 5; ++a2) c2v[a2] = q2r == q ? bt5(q, a2) : c2v[a2];
+    float Rw[5][17];
+#pragma unroll
+    for (int a1 = 0; a1 < 5; ++a1) {
+#pragma unroll
+      for (int c = 0; c < 17; ++c) Rw[a1][c] = 0.0f;
+#pragma unroll
+      for (int a2 = 0; a2 < 5; ++a2) {
+        const float* rowp = win + (a1 + 3 * a2) * BW;
+#pragma unroll
+        for (int c = 0; c < 17; ++c) Rw[a1][c] = fmaf(c2v[a2], rowp[c], Rw[a1][c]);
+      }
+    }
+#pragma unroll
+    for (int q1r = 0; q1r < 5; ++q1r) {
+      // level 1 along the rows
+      float R[17];
+#pragma unroll
+      for (int c = 0; c < 17; ++c) {
+        float sr = 0.0f;
+#pragma unroll
+        for (int a1 = 0; a1 < 5; ++a1)
+          if (bt5(q1r, a1) != 0.0f) sr = fmaf(bt5(q1r, a1), Rw[a1][c], sr);
+        R[c] = sr;
+      }
+      // columns: level 2 (stride 3), then level 1
+#pragma unroll
+      for (int q2c = 0; q2c < 5; ++q2c) {
+        float v5[5];
+#pragma unroll
+        for (int b1 = 0; b1 < 5; ++b1) {
+          float s2 = 0.0f;
+#pragma unroll
+          for (int b2 = 0; b2 < 5; ++b2)
+            if (bt5(q2c, b2) != 0.0f) s2 = fmaf(bt5(q2c, b2), R[b1 + 3 * b2], s2);
+          v5[b1] = s2;
+        }
+        float o[5];
+        bt5_vec(v5, o);
+#pragma unroll
+        for (int q1c = 0; q1c < 5; ++q1c) {
+          const int p = ((q2r * 5 + q2c) * 5 + q1r) * 5 + q1c;
+          vp[(size_t)p * pstride] = o[q1c];
+        }
+      }
+    }
+  }
+}
+
+// ---- contraction: per point U[p]^T V[p] on fp32 MFMA ----------------------
+// Work-group (256 threads, 2 x 2 wavefronts of 32 x 32): a 64 x 64 block of
+// (n, t) for the 5 points of one level-1 row digit (group g, digit q1r).
+// The 5 products are folded along the level-1 columns in registers,
+//   Z[g][q1r][i1c] = sum_q1c A^T[i1c][q1c] Yhat[25 g + 5 q1r + q1c],
+// and the output transform applies the level-1 rows.  Splitting the 25
+// points of a group over 5 work-groups keeps 48 accumulator registers per
+// lane instead of 144 and gives 5x the work-groups.
+//
+// The K loop runs over chunks of BK channels (5 points x M/BK chunks in a
+// row) through a ring of 4 LDS stages, each a distinct LDS object, filled by
+// direct global->LDS loads; three chunks are in flight while one is
+// multiplied.  Columns past N or T re-read the last valid column (those
+// results are not stored).  Two loaders:
+//   VEC (N, T multiples of 4, 16-byte aligned buffers): global_load_lds_dwordx4,
+//     lane l of a load writes LDS floats [4 l, 4 l + 4) of a 4-row slab of
+//     64-float rows; the lane fetches column quad (l % 16) ^ 4 (row % 4), so
+//     that the 4 rows one MFMA operand read touches fall in distinct
+//     16-bank groups (the reader undoes the XOR);
+//   otherwise global_load_lds_dword, lane l writing word l of one row,
+//     rows padded to 80 floats for the same bank spread.
+//   EVEN (M a multiple of 4 BK): every point takes a whole number of ring
+//     turns, so the loop body is four unconditional steps and the fold
+//     follows each point;
+//   otherwise every step is guarded, the fold is tested per step, and in a
+//     ragged last chunk the operand values of channels >= M are zeroed in
+//     registers before the MFMA.
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int C5_BM = 64, C5_BN = 64;
+
+template <int BK, bool VEC>
+using C5Buf = float[BK][VEC ? 64 : 80];
+
+// LDS word of (row, col) in a VEC buffer: column quad XOR 4 (row % 4)
+__device__ __forceinline__ int c5_swz(int row, int col) {
+  return row * 64 + ((((col >> 2) ^ ((row & 3) << 2))) << 2) + (col & 3);
+}
+
+template <int BK, bool EVEN, bool VEC>
+__global__ __launch_bounds__(256) void contract5(const float* __restrict__ U,
+                                                 const float* __restrict__ V,
+                                                 float* __restrict__ Z, int M, int N, int T,
+                                                 int ntb, int nnb) {
+  // loads per wavefront per chunk: VEC, 2 BK / 4 slabs of 4 rows over 4
+  // wavefronts (BK = 8: wavefronts 0-1 load U, 2-3 load V); else BK / 4
+  // rows of each operand
+  static_assert(!VEC || BK == 8 || BK == 16, "VEC chunks of 8 or 16 channels");
+  constexpr int RPW = BK / 4;
+  constexpr int LPC = VEC ? BK / 8 : 2 * RPW;
+  using Buf = C5Buf<BK, VEC>;
+  __shared__ Buf A0, A1, A2, A3, B0, B1, B2, B3;
+  long long bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int tb = (int)(bid % ntb);
+  bid /= ntb;
+  const int nb = (int)(bid % nnb);
+  const long long gq = bid / nnb;                      // 5 g + q1r
+  const int n0 = nb * C5_BM, c0 = tb * C5_BN;
+  const int lane = threadIdx.x & 63;
+  // the wavefront index is uniform: in a scalar register, the row addresses
+  // and LDS bases below are scalar too
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lr = lane & 15, lk = lane >> 4;
+  const size_t pU = (size_t)M * N, pV = (size_t)M * T;
+  const float* __restrict__ Ub = U + (size_t)(5 * gq) * pU;
+  const float* __restrict__ Vb = V + (size_t)(5 * gq) * pV;
+  int ulane, vlane;
+  if constexpr (VEC) {
+    // slab lane l -> row l / 16, column quad (l % 16) ^ 4 (l / 16), clamped
+    const int q = (lane & 15) ^ ((lane >> 4) << 2);
+    const int qu = (n0 >> 2) + q, qv = (c0 >> 2) + q;
+    ulane = 4 * (qu < (N >> 2) ? qu : (N >> 2) - 1);
+    vlane = 4 * (qv < (T >> 2) ? qv : (T >> 2) - 1);
+  } else {
+    ulane = n0 + lane < N ? n0 + lane : N - 1;
+    vlane = c0 + lane < T ? c0 + lane : T - 1;
+  }
+  const int nk = (M + BK - 1) / BK;
+  const int total = 5 * nk;
+
+  floatx4 acc[2][2], w[3][2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int o = 0; o < 3; ++o) w[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  // chunk c: point q1c = c / nk, channels [BK (c % nk), +BK)
+  auto request = [&](int c, Buf& An, Buf& Bn) {
+    const int q1c = c / nk;
+    const int kc0 = (c - q1c * nk) * BK;
+    if constexpr (VEC) {
+      // slabs of 4 rows: BK = 16, wavefront w loads slab w of U and of V;
+      // BK = 8, wavefront w loads slab w % 2 of U (w < 2) or of V (w >= 2)
+#pragma unroll
+      for (int j = 0; j < LPC; ++j) {
+        const bool isU = BK == 16 ? j == 0 : wave < 2;
+        const int slab = BK == 16 ? wave : (wave & 1);
+        int k = kc0 + 4 * slab + lk;
+        if (!EVEN) k = k < M ? k : M - 1;
+        const float* src = isU ? Ub + (size_t)q1c * pU + (size_t)k * N + ulane
+                               : Vb + (size_t)q1c * pV + (size_t)k * T + vlane;
+        float* dst = isU ? &An[4 * slab][0] : &Bn[4 * slab][0];
+        __builtin_amdgcn_global_load_lds((const void*)src,
+                                         (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+      }
+    } else {
+      const int k0 = kc0 + RPW * wave;
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+        const int k = EVEN || k0 + r < M ? k0 + r : M - 1;
+        const float* urow = Ub + (size_t)q1c * pU + (size_t)k * N;
+        const float* vrow = Vb + (size_t)q1c * pV + (size_t)k * T;
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(urow + ulane),
+            (__attribute__((address_space(3))) void*)&An[RPW * wave + r][0], 4, 0, 0);
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(vrow + vlane),
+            (__attribute__((address_space(3))) void*)&Bn[RPW * wave + r][0], 4, 0, 0);
+      }
+    }
+  };
+
+  // all operand reads of the chunk first, then its MFMAs
+  auto compute = [&](const Buf& Ac, const Buf& Bc, int kvalid) {
+    float af[BK / 4][2], bf[BK / 4][2];
+#pragma unroll
+    for (int kk = 0; kk < BK / 4; ++kk) {
+      const int row = kk * 4 + lk;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int col = wm * 32 + i * 16 + lr;
+        af[kk][i] = VEC ? (&Ac[0][0])[c5_swz(row, col)] : Ac[row][col];
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col = wn * 32 + j * 16 + lr;
+        bf[kk][j] = VEC ? (&Bc[0][0])[c5_swz(row, col)] : Bc[row][col];
+      }
+      if (!EVEN && kk * 4 + lk >= kvalid) af[kk][0] = af[kk][1] = bf[kk][0] = bf[kk][1] = 0.0f;
+    }
+#pragma unroll
+    for (int kk = 0; kk < BK / 4; ++kk)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[kk][i], bf[kk][j], acc[i][j], 0, 0, 0);
+  };
+
+  // w[i1c] += A^T[i1c][q1c] acc (F(3,3)'s A^T, selected for the runtime digit)
+  auto fold = [&](int q1c) {
+    const float a0 = q1c < 4 ? 1.0f : 0.0f;
+    const float a1 = q1c == 1 ? 1.0f : q1c == 2 ? -1.0f : q1c == 3 ? 2.0f : 0.0f;
+    const float a2 = q1c == 0 ? 0.0f : q1c == 3 ? 4.0f : 1.0f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        w[0][i][j] += a0 * acc[i][j];
+        w[1][i][j] += a1 * acc[i][j];
+        w[2][i][j] += a2 * acc[i][j];
+        acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+  };
+
+  // one pipeline step: wait for chunk it (own loads, then the barrier for
+  // everyone's), request chunk it + 3 (clamped to the last chunk, into the
+  // buffer read in step it - 1), multiply chunk it
+  auto step = [&](int it, const Buf& Ac, const Buf& Bc, Buf& An, Buf& Bn) {
+    wait_vmcnt<2 * LPC>();
+    __builtin_amdgcn_s_barrier();
+    const int c = it + 3;
+    request(c < total ? c : total - 1, An, Bn);
+    if constexpr (EVEN) {
+      compute(Ac, Bc, BK);
+    } else {
+      const int q1c = it / nk, kc = it - q1c * nk;
+      compute(Ac, Bc, kc == nk - 1 ? M - kc * BK : BK);
+      if (kc == nk - 1) fold(q1c);
+    }
+  };
+
+  request(0, A0, B0);
+  request(1 < total ? 1 : total - 1, A1, B1);
+  request(2 < total ? 2 : total - 1, A2, B2);
+  if constexpr (EVEN) {
+    for (int q1c = 0; q1c < 5; ++q1c) {
+      for (int kb = 0; kb < nk; kb += 4) {
+        const int c = q1c * nk + kb;
+        step(c, A0, B0, A3, B3);
+        step(c + 1, A1, B1, A0, B0);
+        step(c + 2, A2, B2, A1, B1);
+        step(c + 3, A3, B3, A2, B2);
+      }
+      fold(q1c);
+    }
+  } else {
+    for (int base = 0; base < total; base += 4) {
+      step(base, A0, B0, A3, B3);
+      if (base + 1 < total) step(base + 1, A1, B1, A0, B0);
+      if (base + 2 < total) step(base + 2, A2, B2, A1, B1);
+      if (base + 3 < total) step(base + 3, A3, B3, A2, B2);
+    }
+  }
+  wait_vmcnt<0>();   // the clamped requests of the last steps
+
+  // D layout of v_mfma_f32_16x16x4f32: lane l, register v -> row 4 (l / 16) + v, column l % 16
+  const size_t plane = (size_t)N * T;
+  float* __restrict__ Zg = Z + (size_t)gq * 3 * plane;
+#pragma unroll
+  for (int o = 0; o < 3; ++o)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = n0 + wm * 32 + i * 16 + lk * 4 + v;
+        if (row >= N) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int col = c0 + wn * 32 + j * 16 + lr;
+          if (col < T) Zg[(size_t)o * plane + (size_t)row * T + col] = w[o][i][j][v];
+        }
+      }
+}
+
+// ---- output transform: one thread per (tile, n) ----------------------------
+// Z [P/25][5][3][N][T] (level-1 columns applied) -> the level-1 rows, then
+// at depth 2 the level-2 A^T on both axes (output row i1r + 3 i2r).
+template <int NLEV>
+__global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z,
+                                                     float* __restrict__ y, int N, int Ho,
+                                                     int Wo, int th, int tw, int T) {
+  constexpr int Mn = NLEV == 1 ? 3 : 9;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int n = blockIdx.y;
+  if (t >= T) return;
+  const size_t plane = (size_t)N * T;
+  const float* __restrict__ zp = Z + (size_t)n * T + t;
+  // level-1 rows of group grp: z9[i1r][i1c] = sum_q1r A^T[i1r][q1r] Z[grp][q1r][i1c]
+  auto level1_rows = [&](int grp, float (&z9)[3][3]) {
+    float zr[5][3];
+#pragma unroll
+    for (int q = 0; q < 5; ++q)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) zr[q][c] = zp[((size_t)grp * 15 + q * 3 + c) * plane];
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        float sacc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+          if (at5(i, q) != 0.0f) sacc = fmaf(at5(i, q), zr[q][c], sacc);
+        z9[i][c] = sacc;
+      }
+  };
+  float out[Mn][Mn];
+  if constexpr (NLEV == 1) {
+    level1_rows(0, out);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 9; ++i)
+#pragma unroll
+      for (int k = 0; k < 9; ++k) out[i][k] = 0.0f;
+    // one group per iteration (not unrolled: the 75 point-plane offsets of
+    // an unrolled loop would all stay live); runtime digits select the
+    // level-2 coefficients
+#pragma unroll 1
+    for (int grp = 0; grp < 25; ++grp) {
+      const int q2r = grp / 5, q2c = grp - 5 * q2r;
+      float zv[3][3];
+      level1_rows(grp, zv);
+      float cr[3], cc[3];
+#pragma unroll
+      for (int i = 0; i < 3; ++i) {
+        cr[i] = 0.0f;
+        cc[i] = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 5; ++q) {
+          cr[i] = q2r == q ? at5(i, q) : cr[i];
+          cc[i] = q2c == q ? at5(i, q) : cc[i];
+        }
+      }
+#pragma unroll
+      for (int i2r = 0; i2r < 3; ++i2r)
+#pragma unroll
+        for (int i2c = 0; i2c < 3; ++i2c) {
+          const float cf = cr[i2r] * cc[i2c];
+#pragma unroll
+          for (int i1r = 0; i1r < 3; ++i1r)
+#pragma unroll
+            for (int i1c = 0; i1c < 3; ++i1c)
+              out[3 * i2r + i1r][3 * i2c + i1c] =
+                  fmaf(cf, zv[i1r][i1c], out[3 * i2r + i1r][3 * i2c + i1c]);
+        }
+    }
+  }
+  const int tpi = th * tw;
+  const int b = t / tpi;
+  const int r2 = t - b * tpi;
+  const int ty = r2 / tw, tx = r2 - ty * tw;
+  float* __restrict__ yo = y + ((size_t)b * N + n) * Ho * Wo;
+#pragma unroll
+  for (int i = 0; i < Mn; ++i) {
+    const int row = ty * Mn + i;
+    if (row >= Ho) continue;
+#pragma unroll
+    for (int k = 0; k < Mn; ++k) {
+      const int col = tx * Mn + k;
+      if (col < Wo) yo[(size_t)row * Wo + col] = out[i][k];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kernel_xform5(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
+  const long long nthreads = (long long)g.N * g.M;
+  dim3 grid((unsigned)((nthreads + 255) / 256));
+  if (g.n == 1)
+    hipLaunchKernelGGL(kernel_xform5<1>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads);
+  else if (g.n == 2)
+    hipLaunchKernelGGL(kernel_xform5<2>, grid, dim3(256), 0, s, w, U, g.M, g.N, g.r, nthreads);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_input_xform5(const nwg_plan_info& g, const float* x, float* V, hipStream_t s) {
+  if (g.n != 1 && g.n != 2) return hipErrorInvalidValue;
+  const int Mn = g.n == 1 ? 3 : 9, Ln = g.n == 1 ? 5 : 17;
+  // up to 64 tiles per box
+  const int RX = g.tw < 64 ? g.tw : 64;
+  int RY = 64 / RX;
+  if (RY > g.th) RY = g.th;
+  const int nbx = (g.tw + RX - 1) / RX, nby = (g.th + RY - 1) / RY;
+  const long long blocks = (long long)nbx * nby * g.B;
+  if (blocks > 0x7fffffffLL || g.M > 65535) return hipErrorInvalidValue;
+  const size_t lds = (size_t)((RY - 1) * Mn + Ln) * ((RX - 1) * Mn + Ln) * sizeof(float);
+  dim3 grid((unsigned)blocks, (unsigned)g.M);
+  const int T = (int)g.T;
+  if (g.n == 1)
+    hipLaunchKernelGGL(input_xform5<1>, grid, dim3(64), lds, s, x, V, g.M, g.H, g.W, g.pad, g.th,
+                       g.tw, T, RX, RY, nbx, nby);
+  else
+    hipLaunchKernelGGL(input_xform5<2>, grid, dim3(320), lds, s, x, V, g.M, g.H, g.W, g.pad,
+                       g.th, g.tw, T, RX, RY, nbx, nby);
+  return hipGetLastError();
+}
+
+hipError_t launch_contract5(const nwg_plan_info& g, const float* U, const float* V, float* Z,
+                            hipStream_t s) {
+  if (g.n != 1 && g.n != 2) return hipErrorInvalidValue;
+  const int T = (int)g.T;
+  const int ntb = (T + C5_BN - 1) / C5_BN, nnb = (g.N + C5_BM - 1) / C5_BM;
+  const long long blocks = (long long)ntb * nnb * (g.P / 5);
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)blocks), block(256);
+  const bool vec = g.N % 4 == 0 && T % 4 == 0 && !(((uintptr_t)U | (uintptr_t)V) & 15);
+#define NWG_C5(BK, EVEN, VEC)                                                                 \
+  hipLaunchKernelGGL((contract5<BK, EVEN, VEC>), grid, block, 0, s, U, V, Z, g.M, g.N, T, ntb, \
+                     nnb)
+  if (g.M % 64 == 0) {
+    if (vec) NWG_C5(16, true, true); else NWG_C5(16, true, false);
+  } else if (g.M % 32 == 0) {
+    if (vec) NWG_C5(8, true, true); else NWG_C5(8, true, false);
+  } else {
+    if (vec) NWG_C5(16, false, true); else NWG_C5(16, false, false);
+  }
+#undef NWG_C5
+  return hipGetLastError();
+}
+
+hipError_t launch_output_xform5(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s) {
+  if (g.N > 65535) return hipErrorInvalidValue;
+  const int T = (int)g.T;
+  dim3 grid((unsigned)((T + 255) / 256), (unsigned)g.N);
+  if (g.n == 1)
+    hipLaunchKernelGGL(output_xform5<1>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo, g.th, g.tw,
+                       T);
+  else if (g.n == 2)
+    hipLaunchKernelGGL(output_xform5<2>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo, g.th, g.tw,
+                       T);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace nwg

@@ -67,8 +67,8 @@ namespace {
 // contraction lost more (4.73 -> 5.6-6.6 ms over its parts) than the hidden
 // input transform saved; every part count from 2 to 16 made the step slower.
 bool pipeline_allowed(const nwg_plan_info& g) {
-  return g.n == 4 && !g.depthwise && !g.fused_input && g.M % 32 == 0 && g.N % 64 == 0 &&
-         g.T % 64 == 0;
+  return g.tile == NWG_TILE_F2X2_3X3 && g.n == 4 && !g.depthwise && !g.fused_input &&
+         g.M % 32 == 0 && g.N % 64 == 0 && g.T % 64 == 0;
 }
 
 // depthwise: M = N = C channels, one r x r kernel each, no channel sum.
@@ -83,8 +83,13 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     set_error("invalid shape B=%d M=%d N=%d H=%d W=%d r=%d pad=%d", B, M, N, H, W, r, pad);
     return NWG_EINVAL;
   }
-  if (tile != NWG_TILE_F2X2_3X3) {
-    set_error("unsupported tile %d (only NWG_TILE_F2X2_3X3)", tile);
+  if (tile != NWG_TILE_F2X2_3X3 && tile != NWG_TILE_F3X3_3X3) {
+    set_error("unsupported tile %d (NWG_TILE_F2X2_3X3 or NWG_TILE_F3X3_3X3)", tile);
+    return NWG_EUNSUPPORTED;
+  }
+  const bool f33 = tile == NWG_TILE_F3X3_3X3;
+  if (f33 && depthwise) {
+    set_error("depthwise plans use the F(2x2,3x3) tile");
     return NWG_EUNSUPPORTED;
   }
   const long long Ho = (long long)H + 2LL * pad - r + 1, Wo = (long long)W + 2LL * pad - r + 1;
@@ -92,7 +97,10 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     set_error("kernel %d larger than padded input %dx%d (pad %d)", r, H, W, pad);
     return NWG_EINVAL;
   }
-  const int m = nwg::kOut, rb = nwg::kTaps, l = nwg::kBase;
+  // base F(m, rb): F(2,3) or F(3,3); F(3,3) is kept to depth 2 (r <= 9),
+  // where its fp32 error stays near 1e-6
+  const int m = f33 ? 3 : nwg::kOut, rb = nwg::kTaps, l = m + rb - 1;
+  const int max_depth = f33 ? 2 : NWG_MAX_DEPTH;
   int n = 0, Mn = 1, Kn = 1;
   int strides[NWG_MAX_DEPTH + 1] = {0};
   if (r > 1) {
@@ -102,9 +110,9 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     Kn = rb;
     while (Kn < r) {
       const int s = Mn < Kn ? Mn : Kn;
-      if (n >= NWG_MAX_DEPTH) {
-        set_error("kernel size %d needs nesting depth > %d (r <= 31 supported)", r,
-                  NWG_MAX_DEPTH);
+      if (n >= max_depth) {
+        set_error("kernel size %d needs nesting depth > %d (r <= %d supported on this tile)", r,
+                  max_depth, f33 ? 9 : 31);
         return NWG_EUNSUPPORTED;
       }
       strides[n] = s;
@@ -140,8 +148,11 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     g->ewmm_mults = (long long)B * N * Mk * Ho * Wo;
     g->contract_flop = 2.0 * B * N * (double)Mk * Ho * Wo;
   } else {
-    // the contraction writes the level-1 output transform of Yhat: P/4 values per (n, t)
-    const double u = f * P * Mk * N, v = f * P * M * g->T, yh = f * (P / 4) * N * g->T;
+    // the contraction writes Yhat after (part of) the level-1 output
+    // transform: per (n, t) P/4 values for F(2,3) (both axes), 3 P/5 for
+    // F(3,3) (columns only)
+    const double zpts = f33 ? (double)(P / 5) * 3 : (double)(P / 4);
+    const double u = f * P * Mk * N, v = f * P * M * g->T, yh = f * zpts * N * g->T;
     if (u > 1e13 || v > 1e13 || yh > 1e13 || g->T > 0x7fffffffLL / 64) {
       set_error("workspace too large");
       return NWG_EUNSUPPORTED;
@@ -155,8 +166,9 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
   // one or two output channels (or depthwise) at depth 3-4: the fused kernel
   // never forms V.  Few channels (or depthwise) at depth 1-2: one kernel
   // x -> y, neither V nor Z.
-  g->fused_input = nwg::input_contract_applies(*g) ? 1 : 0;
-  g->fused_conv = (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
+  g->fused_input = !f33 && nwg::input_contract_applies(*g) ? 1 : 0;
+  g->fused_conv =
+      !f33 && (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
   const bool no_v = g->fused_input || depthwise || g->fused_conv;
   const bool no_z = g->fused_conv;
   g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : g->yhat_bytes);
@@ -234,7 +246,22 @@ hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* 
   if (g.depthwise)
     return g.n == 0 ? nwg::launch_dw_scale(g, V, U, Z, s) : nwg::launch_dw_contract(g, U, V, Z, s);
   if (g.n == 0) return nwg::launch_gemm_depth0(depth0_args(g, U, V, Z), s);
+  if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_contract5(g, U, V, Z, s);
   return nwg::launch_contract_fused(U, V, Z, g.M, g.N, (int)g.T, g.P / 16, s);
+}
+
+// stage launchers by tile (depth >= 1)
+hipError_t launch_kxform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
+  if (g.tile == NWG_TILE_F3X3_3X3 && g.n > 0) return nwg::launch_kernel_xform5(g, w, U, s);
+  return nwg::launch_kernel_xform(kernel_geometry(g), w, U, s);
+}
+hipError_t launch_ixform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s) {
+  if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_input_xform5(g, x, V, s);
+  return nwg::launch_input_xform(g, x, V, s);
+}
+hipError_t launch_oxform(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s) {
+  if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_output_xform5(g, Z, y, s);
+  return nwg::launch_output_xform(g, Z, y, s);
 }
 
 // Input transform and contraction in `parts` pieces on two streams: part k's
@@ -285,14 +312,14 @@ int run_pipelined(nwg_plan* p, const float* x, hipStream_t s) {
 int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, float* U,
                          hipStream_t s) {
   return timed(p, 0, s, "kernel transform launch",
-               [&] { return nwg::launch_kernel_xform(kernel_geometry(g), w, U, s); });
+               [&] { return launch_kxform(g, w, U, s); });
 }
 
 }  // namespace
 
 extern "C" {
 
-const char* nwg_version(void) { return "nwg 0.1 (F(2x2,3x3) nested, gfx950)"; }
+const char* nwg_version(void) { return "nwg 0.2 (nested F(2x2,3x3) and F(3x3,3x3), gfx950)"; }
 
 const char* nwg_last_error(void) { return g_last_error.c_str(); }
 
@@ -398,8 +425,7 @@ int nwg_kernel_transform(const nwg_plan* p, const float* w, float* U, void* stre
     set_error("NULL argument to nwg_kernel_transform");
     return NWG_EINVAL;
   }
-  return check_hip(nwg::launch_kernel_xform(kernel_geometry(p->info), w, U, (hipStream_t)stream),
-                   "kernel transform launch");
+  return check_hip(launch_kxform(p->info, w, U, (hipStream_t)stream), "kernel transform launch");
 }
 
 int nwg_input_transform(const nwg_plan* p, const float* x, float* V, void* stream) {
@@ -411,7 +437,7 @@ int nwg_input_transform(const nwg_plan* p, const float* x, float* V, void* strea
     set_error("depth 0 (r = 1) has no input transform");
     return NWG_EINVAL;
   }
-  return check_hip(nwg::launch_input_xform(p->info, x, V, (hipStream_t)stream),
+  return check_hip(launch_ixform(p->info, x, V, (hipStream_t)stream),
                    "input transform launch");
 }
 
@@ -430,8 +456,9 @@ int nwg_input_contract(const nwg_plan* p, const float* x, const float* U, float*
     set_error("NULL argument to nwg_input_contract");
     return NWG_EINVAL;
   }
-  if (!nwg::input_contract_applies(p->info)) {
-    set_error("fused input transform + contraction needs depth 3 or 4 and N <= 2 or a "
+  if (p->info.tile != NWG_TILE_F2X2_3X3 || !nwg::input_contract_applies(p->info)) {
+    set_error("fused input transform + contraction needs the F(2x2,3x3) tile, depth 3 or 4 "
+              "and N <= 2 or a "
               "depthwise plan (depth %d, N = %d)", p->info.n, p->info.N);
     return NWG_EUNSUPPORTED;
   }
@@ -448,7 +475,7 @@ int nwg_output_transform(const nwg_plan* p, const float* Yh, float* y, void* str
     set_error("depth 0 (r = 1) has no output transform");
     return NWG_EINVAL;
   }
-  return check_hip(nwg::launch_output_xform(p->info, Yh, y, (hipStream_t)stream),
+  return check_hip(launch_oxform(p->info, Yh, y, (hipStream_t)stream),
                    "output transform launch");
 }
 
@@ -497,14 +524,14 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
     rc = run_pipelined(p, x, s);
   } else {
     rc = timed(p, 1, s, "input transform launch",
-               [&] { return nwg::launch_input_xform(g, x, p->V, s); });
+               [&] { return launch_ixform(g, x, p->V, s); });
     if (rc != NWG_OK) return rc;
     rc = timed(p, 2, s, "contraction launch",
                [&] { return launch_contract(g, p->U, p->V, p->Yh, s); });
   }
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",
-               [&] { return nwg::launch_output_xform(g, p->Yh, y, s); });
+               [&] { return launch_oxform(g, p->Yh, y, s); });
 }
 
 int nwg_plan_set_pipeline(nwg_plan* p, int parts) {

@@ -18,6 +18,24 @@ namespace nwg {
 //   A^T rows: y0 = v0 + v1 + v2, y1 = v1 - v2 - v3
 // ---------------------------------------------------------------------------
 
+// Work-group i of G -> logical block: the dispatcher deals work-groups
+// round-robin over the 8 XCDs (i % 8); this numbering gives each XCD a
+// contiguous run of logical blocks, so blocks that share operand tiles
+// share one L2.
+__device__ __forceinline__ long long xcd_remap(long long i, long long G) {
+  const long long q = G / 8, rem = G % 8;
+  const long long xcd = i % 8, slot = i / 8;
+  return xcd < rem ? xcd * (q + 1) + slot : rem * (q + 1) + (xcd - rem) * q + slot;
+}
+
+// Wait until at most N vector-memory loads of this wavefront are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 constexpr int kBase = 4;   // l
 constexpr int kOut = 2;    // m
 constexpr int kTaps = 3;   // r of the base
@@ -110,6 +128,12 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
 bool input_contract_applies(const nwg_plan_info& g);
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* U, float* Z,
                                  hipStream_t s);
+// the F(3,3) tile (depth 1-2): U [P][M][N], V [P][M][T], Z [P/25][9][N][T]
+hipError_t launch_kernel_xform5(const nwg_plan_info& g, const float* w, float* U, hipStream_t s);
+hipError_t launch_input_xform5(const nwg_plan_info& g, const float* x, float* V, hipStream_t s);
+hipError_t launch_contract5(const nwg_plan_info& g, const float* U, const float* V, float* Z,
+                            hipStream_t s);
+hipError_t launch_output_xform5(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s);
 // few channels at depth 1-2 (dense): x -> y in one kernel
 bool small_conv_applies(const nwg_plan_info& g);
 hipError_t launch_small_conv(const nwg_plan_info& g, const float* x, const float* U, float* y,

@@ -16,6 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libnwg.so")
 
 NWG_TILE_F2X2_3X3 = 0
+NWG_TILE_F3X3_3X3 = 1
 NWG_OK, NWG_EINVAL, NWG_ENOMEM, NWG_EHIP, NWG_EUNSUPPORTED = 0, -1, -2, -3, -4
 NWG_MAX_DEPTH = 4
 
@@ -168,21 +169,30 @@ class Plan:
     def __exit__(self, *exc):
         self.close()
 
-    # shapes of the Winograd-domain buffers (quad-interleaved, see include/nwg.h)
+    # shapes of the Winograd-domain buffers (F(2x2,3x3): quad-interleaved;
+    # F(3x3,3x3): plain; see include/nwg.h)
+    @property
+    def _f33(self):
+        return self.info["tile"] == NWG_TILE_F3X3_3X3 and self.info["n"] > 0
+
     @property
     def u_shape(self):
         i = self.info
         mk = 1 if i["depthwise"] else i["M"]
-        return (i["P"] // 4, mk, i["N"], 4) if i["n"] else (mk, i["N"])
+        if not i["n"]:
+            return (mk, i["N"])
+        return (i["P"], mk, i["N"]) if self._f33 else (i["P"] // 4, mk, i["N"], 4)
 
     @property
     def v_shape(self):
         i = self.info
-        return (i["P"] // 4, i["M"], i["T"], 4)
+        return (i["P"], i["M"], i["T"]) if self._f33 else (i["P"] // 4, i["M"], i["T"], 4)
 
     @property
     def z_shape(self):
         i = self.info
+        if self._f33:
+            return (i["P"] // 25, 5, 3, i["N"], i["T"])
         return (i["P"] // 16, i["N"], i["T"], 4)
 
     @property

@@ -9,12 +9,13 @@ transform.
 """
 import numpy as np
 
-from oracle.nested import base_f23, point_permutation
+from oracle.nested import base_f23, point_permutation, toom_cook_base
 
 
-def to_lib_points(a, n):
-    """oracle [..., P1, P1] -> [..., P] in the library's point order."""
-    perm = point_permutation(n)
+def to_lib_points(a, n, l=4):
+    """oracle [..., P1, P1] -> [..., P] in the library's point order (base-l
+    digits)."""
+    perm = point_permutation(n, l)
     return a[..., perm[:, 0], perm[:, 1]]
 
 
@@ -31,3 +32,19 @@ def level1(yh_pnt):
     g = yh_pnt.reshape(P // 16, 4, 4, N, T)
     z = np.einsum("iq,jr,gqrnt->gntij", AT, AT, g)
     return np.ascontiguousarray(z.reshape(P // 16, N, T, 4))
+
+
+def f33_base():
+    """F(3,3) from the Toom-Cook points 0, 1, -1, 2 (and infinity), the base of
+    the library's F(3x3, 3x3) tile."""
+    return toom_cook_base(3, 3, [0, 1, -1, 2])
+
+
+def level1_f33(yh_pnt):
+    """F(3,3) tile: [P][N][T] -> Z [P/25][5][3][N][T] with
+    Z[g][q1r][i1c] = sum_{q1c} A^T[i1c][q1c] Yhat[25 g + 5 q1r + q1c] (the
+    oracle's A^T along the level-1 columns only)."""
+    AT = f33_base().AT.astype(np.float64)
+    P, N, T = yh_pnt.shape
+    g = yh_pnt.reshape(P // 25, 5, 5, N, T)
+    return np.ascontiguousarray(np.einsum("jr,gqrnt->gqjnt", AT, g))

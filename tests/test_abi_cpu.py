@@ -172,3 +172,31 @@ def test_fused_conv_flag():
     for r, want in [(3, 1), (7, 1), (9, 0), (1, 0)]:
         g = nwg.plan_geometry_depthwise(2, 6, 40, 40, r, (r - 1) // 2)
         assert g["fused_conv"] == want, r
+
+
+@pytest.mark.parametrize("r", list(range(1, 12)))
+def test_f33_geometry_matches_oracle_levels(r):
+    from oracle.nested import toom_cook_base
+    B, M, N, H, W = 2, 3, 5, 40, 37
+    pad = (r - 1) // 2
+    tile = nwg.NWG_TILE_F3X3_3X3
+    if r > 9:
+        with pytest.raises(nwg.NwgError):
+            nwg.plan_geometry(B, M, N, H, W, r, pad, tile)
+        return
+    g = nwg.plan_geometry(B, M, N, H, W, r, pad, tile)
+    lv = nesting_levels(toom_cook_base(3, 3, [0, 1, -1, 2]), r)
+    assert g["tile"] == tile
+    assert g["n"] == lv.n and g["Mn"] == lv.Mn and g["Kn"] == lv.Kn
+    assert g["strides"][:lv.n] == lv.strides
+    if lv.n:
+        assert (g["m"], g["rb"], g["l"], g["Ln"]) == (3, 3, 5, lv.Ln)
+        P, T = 25 ** lv.n, B * g["th"] * g["tw"]
+        assert g["P"] == P and g["T"] == T
+        assert g["u_bytes"] == 4 * P * M * N and g["v_bytes"] == 4 * P * M * T
+        assert g["yhat_bytes"] == 4 * (P // 25) * 15 * N * T
+        assert g["workspace_bytes"] == g["u_bytes"] + g["v_bytes"] + g["yhat_bytes"]
+    # never fused, even where the F(2x2,3x3) tile would be
+    assert g["fused_input"] == 0 and g["fused_conv"] == 0 and g["pipeline_parts"] == 1
+    with pytest.raises(nwg.NwgError):
+        nwg.plan_geometry_depthwise(B, 4, H, W, r, pad, tile)
