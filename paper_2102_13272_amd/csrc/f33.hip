@@ -135,12 +135,23 @@ __global__ __launch_bounds__(320) void input_xform5(const float* __restrict__ x,
   const int r0 = ty0 * Mn - pad, c0 = tx0 * Mn - pad;
   const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
   const int nth = blockDim.x;
-  for (int e = threadIdx.x; e < BH * BW; e += nth) {
-    const int row = e / BW, col = e - row * BW;
-    const int gr = r0 + row, gc = c0 + col;
-    float v = 0.0f;
-    if (gr >= 0 && gr < H && gc >= 0 && gc < W) v = xp[(size_t)gr * W + gc];
-    box[e] = v;
+  const int nbox = BH * BW;
+  // batches of FB loads per thread, all issued before the first LDS store,
+  // so that the fill waits for memory once per batch, not once per element
+  constexpr int FB = 8;
+  for (int e0 = threadIdx.x; e0 < nbox; e0 += FB * nth) {
+    float v[FB];
+#pragma unroll
+    for (int u = 0; u < FB; ++u) {
+      const int e = e0 + u * nth;
+      const int row = e / BW, col = e - row * BW;
+      const int gr = r0 + row, gc = c0 + col;
+      v[u] = 0.0f;
+      if (e < nbox && gr >= 0 && gr < H && gc >= 0 && gc < W) v[u] = xp[(size_t)gr * W + gc];
+    }
+#pragma unroll
+    for (int u = 0; u < FB; ++u)
+      if (e0 + u * nth < nbox) box[e0 + u * nth] = v[u];
   }
   __syncthreads();
   const int s = threadIdx.x & 63;                      // tile within the box (<= 64)
@@ -476,13 +487,8 @@ __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z
   if (t >= T) return;
   const size_t plane = (size_t)N * T;
   const float* __restrict__ zp = Z + (size_t)n * T + t;
-  // level-1 rows of group grp: z9[i1r][i1c] = sum_q1r A^T[i1r][q1r] Z[grp][q1r][i1c]
-  auto level1_rows = [&](int grp, float (&z9)[3][3]) {
-    float zr[5][3];
-#pragma unroll
-    for (int q = 0; q < 5; ++q)
-#pragma unroll
-      for (int c = 0; c < 3; ++c) zr[q][c] = zp[((size_t)grp * 15 + q * 3 + c) * plane];
+  // level-1 rows: z9[i1r][i1c] = sum_q1r A^T[i1r][q1r] zr[q1r][i1c]
+  auto level1_rows = [&](const float (&zr)[5][3], float (&z9)[3][3]) {
 #pragma unroll
     for (int i = 0; i < 3; ++i)
 #pragma unroll
@@ -496,43 +502,61 @@ __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z
   };
   float out[Mn][Mn];
   if constexpr (NLEV == 1) {
-    level1_rows(0, out);
+    float zr[5][3];
+#pragma unroll
+    for (int q = 0; q < 5; ++q)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) zr[q][c] = zp[(size_t)(q * 3 + c) * plane];
+    level1_rows(zr, out);
   } else {
 #pragma unroll
     for (int i = 0; i < 9; ++i)
 #pragma unroll
       for (int k = 0; k < 9; ++k) out[i][k] = 0.0f;
-    // one group per iteration (not unrolled: the 75 point-plane offsets of
-    // an unrolled loop would all stay live); runtime digits select the
-    // level-2 coefficients
+    // one level-2 row digit q2r per iteration: its 5 groups' 75 values are
+    // loaded together (one wait for memory per row digit).  The plane
+    // stride is made opaque so the loop-invariant offsets of the 75 loads
+    // are not all precomputed and kept in scalar registers.
+    const float* zq = zp;
 #pragma unroll 1
-    for (int grp = 0; grp < 25; ++grp) {
-      const int q2r = grp / 5, q2c = grp - 5 * q2r;
-      float zv[3][3];
-      level1_rows(grp, zv);
-      float cr[3], cc[3];
+    for (int q2r = 0; q2r < 5; ++q2r) {
+      float zr[5][5][3];
+      size_t pl = plane;
+      asm volatile("" : "+s"(pl));
+#pragma unroll
+      for (int q2c = 0; q2c < 5; ++q2c)
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+#pragma unroll
+          for (int c = 0; c < 3; ++c) {
+            zr[q2c][q][c] = *zq;
+            zq += pl;
+          }
+      float cr[3];
 #pragma unroll
       for (int i = 0; i < 3; ++i) {
         cr[i] = 0.0f;
-        cc[i] = 0.0f;
 #pragma unroll
-        for (int q = 0; q < 5; ++q) {
-          cr[i] = q2r == q ? at5(i, q) : cr[i];
-          cc[i] = q2c == q ? at5(i, q) : cc[i];
-        }
+        for (int q = 0; q < 5; ++q) cr[i] = q2r == q ? at5(i, q) : cr[i];
       }
 #pragma unroll
-      for (int i2r = 0; i2r < 3; ++i2r)
+      for (int q2c = 0; q2c < 5; ++q2c) {
+        float zv[3][3];
+        level1_rows(zr[q2c], zv);
 #pragma unroll
-        for (int i2c = 0; i2c < 3; ++i2c) {
-          const float cf = cr[i2r] * cc[i2c];
+        for (int i2r = 0; i2r < 3; ++i2r)
 #pragma unroll
-          for (int i1r = 0; i1r < 3; ++i1r)
+          for (int i2c = 0; i2c < 3; ++i2c) {
+            if (at5(i2c, q2c) == 0.0f) continue;
+            const float cf = cr[i2r] * at5(i2c, q2c);
 #pragma unroll
-            for (int i1c = 0; i1c < 3; ++i1c)
-              out[3 * i2r + i1r][3 * i2c + i1c] =
-                  fmaf(cf, zv[i1r][i1c], out[3 * i2r + i1r][3 * i2c + i1c]);
-        }
+            for (int i1r = 0; i1r < 3; ++i1r)
+#pragma unroll
+              for (int i1c = 0; i1c < 3; ++i1c)
+                out[3 * i2r + i1r][3 * i2c + i1c] =
+                    fmaf(cf, zv[i1r][i1c], out[3 * i2r + i1r][3 * i2c + i1c]);
+          }
+      }
     }
   }
   const int tpi = th * tw;
