@@ -47,8 +47,9 @@ def stage_bytes_flops(info: dict):
     if info["n"] == 0:
         return {"kernel_transform": (w + 4 * mk * N, 0.0),
                 "contraction": (x + y + 4 * mk * N, flop)}
-    # Z: the contraction's output after the first output level, P/4 values per (n, t)
-    U, V, Yh = 4 * P * mk * N, 4 * P * M * T, 4 * (P // 4) * N * T
+    # Z: the contraction's output after (part of) the first output level: P/4
+    # values per (n, t) on F(2x2,3x3), 3P/5 on F(3x3,3x3) (the plan's yhat_bytes)
+    U, V, Yh = info["u_bytes"], info["v_bytes"], info["yhat_bytes"]
     if info.get("fused_conv"):
         # one kernel: x and U in, y out
         return {"kernel_transform": (w + U, 0.0), "contraction": (x + U + y, flop)}
@@ -191,6 +192,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5_r31")
+    ap.add_argument("--tile", choices=["f23", "f33"], default="f23",
+                    help="Winograd base: F(2x2,3x3) nests (any r <= 31), or F(3x3,3x3) nests "
+                         "for the dense layers with r <= 9 (others keep F(2x2,3x3))")
     ap.add_argument("--pipeline-parts", type=int, default=0,
                     help="input-transform/contraction pieces on two streams (0: the library's "
                          "default for each plan, 1: off)")
@@ -236,8 +240,13 @@ def main():
     x, ws = make_workload(args.workload)
     xd = torch.from_numpy(x).to("cuda")
     wds = [torch.from_numpy(w).to("cuda") for w in ws]
-    plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, depthwise=L.depthwise)
-             for L in wl.layers]
+    def tile_for(L):
+        if args.tile == "f33" and not L.depthwise and L.r <= 9:
+            return nwg.NWG_TILE_F3X3_3X3
+        return nwg.NWG_TILE_F2X2_3X3
+
+    plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, tile=tile_for(L),
+                      depthwise=L.depthwise) for L in wl.layers]
     if args.pipeline_parts:
         for p in plans:
             if p.info["pipeline_parts"] > 1 or args.pipeline_parts == 1:
@@ -328,14 +337,17 @@ def main():
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4)}
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
-    roof["traffic"] = measured_traffic(args.workload, dom) if len(plans) == 1 else None
+    roof["traffic"] = (measured_traffic(args.workload, dom)
+                       if len(plans) == 1 and args.tile == "f23" else None)
 
     L0 = wl.layers[0]
     cfg = {"workload": args.workload, "layers": len(wl.layers), "B": L0.B,
            "M": L0.M, "N": wl.layers[-1].N, "H": L0.H, "W": L0.W,
            "r": [L.r for L in wl.layers] if len(wl.layers) > 1 else L0.r,
            "pad": [L.pad for L in wl.layers] if len(wl.layers) > 1 else L0.pad,
-           "base": "F(2x2,3x3)", "nesting_depth": [p.info["n"] for p in plans],
+           "base": [("F(3x3,3x3)" if p.info["tile"] == nwg.NWG_TILE_F3X3_3X3 else "F(2x2,3x3)")
+                    for p in plans] if args.tile == "f33" else "F(2x2,3x3)",
+           "nesting_depth": [p.info["n"] for p in plans],
            "pipeline_parts": [p.info["pipeline_parts"] for p in plans]}
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
