@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
 PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
+PEAK_BF16_MFMA_TFLOPS = 2500.0  # MI355X dense bf16 matrix
 METRIC = "direct-conv-equiv TFLOP/s & fraction of fp32 MFMA/HBM roofline, 1 MI355X"
 STAGES = ["kernel_transform", "input_transform", "contraction", "output_transform"]
 CSRC = os.path.join(ROOT, "paper_2102_13272_amd", "csrc")
@@ -195,6 +196,9 @@ def main():
     ap.add_argument("--tile", choices=["f23", "f33"], default="f23",
                     help="Winograd base: F(2x2,3x3) nests (any r <= 31), or F(3x3,3x3) nests "
                          "for the dense layers with r <= 9 (others keep F(2x2,3x3))")
+    ap.add_argument("--precision", choices=["fp32", "bf16_split"], default="fp32",
+                    help="contraction arithmetic: fp32 MFMA, or the two-term bf16 split of U "
+                         "and V on bf16 MFMA with fp32 accumulation (plans that can take it)")
     ap.add_argument("--pipeline-parts", type=int, default=0,
                     help="input-transform/contraction pieces on two streams (0: the library's "
                          "default for each plan, 1: off)")
@@ -251,6 +255,12 @@ def main():
         for p in plans:
             if p.info["pipeline_parts"] > 1 or args.pipeline_parts == 1:
                 p.set_pipeline(args.pipeline_parts)
+    if args.precision == "bf16_split":
+        for p in plans:
+            try:
+                p.set_precision(nwg.NWG_PRECISION_BF16_SPLIT)
+            except nwg.NwgError:
+                pass            # this layer keeps fp32
     outs = [torch.empty(p.y_shape, dtype=torch.float32, device="cuda") for p in plans]
     stream = torch.cuda.current_stream()
 
@@ -325,12 +335,17 @@ def main():
     dom = max(stages, key=lambda k: stages[k]["ms_total"])
     s = stages[dom]
     avg_s = s["ms_total"] * 1e-3 / s["launches"]
-    ai = s["flop"] / s["bytes"] if s["bytes"] else 0.0
-    ridge = PEAK_FP32_MFMA_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    # split precision: the MFMAs run on bf16 and execute 4 partial products
+    # per algorithmic multiply-add
+    split = args.precision == "bf16_split"
+    peak_mm = PEAK_BF16_MFMA_TFLOPS if split else PEAK_FP32_MFMA_TFLOPS
+    flop_x = 4.0 if split else 1.0
+    ai = flop_x * s["flop"] / s["bytes"] if s["bytes"] else 0.0
+    ridge = peak_mm * 1e12 / (PEAK_HBM_GBS * 1e9)
     if dom == "contraction" and ai > ridge:
-        ach = s["flop"] / s["launches"] / avg_s / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_FP32_MFMA_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / PEAK_FP32_MFMA_TFLOPS, 4)}
+        ach = flop_x * s["flop"] / s["launches"] / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak_mm,
+                "unit": "TFLOP/s", "frac": round(ach / peak_mm, 4)}
     else:
         ach = s["bytes"] / s["launches"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
@@ -338,7 +353,7 @@ def main():
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
     roof["traffic"] = (measured_traffic(args.workload, dom)
-                       if len(plans) == 1 and args.tile == "f23" else None)
+                       if len(plans) == 1 and args.tile == "f23" and not split else None)
 
     L0 = wl.layers[0]
     cfg = {"workload": args.workload, "layers": len(wl.layers), "B": L0.B,
@@ -352,7 +367,9 @@ def main():
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": ("f32" if all(p.info["precision"] == nwg.NWG_PRECISION_FP32 for p in plans)
+                  else "bf16-split/f32-acc"),
         "data": "synthetic", "config": cfg, "roofline": roof,
         "stages": detail,
         "kernel_transform_ms_once": round(kx_ms, 4),

@@ -87,6 +87,17 @@ enum {
 
 #define NWG_MAX_DEPTH 4   /* r <= 31 */
 
+/* Arithmetic of the Winograd-domain contraction (nwg_plan_set_precision).
+ *   NWG_PRECISION_FP32: fp32 operands, fp32 MFMA (v_mfma_f32_16x16x4f32).
+ *   NWG_PRECISION_BF16_SPLIT: every U and V value is stored as a two-term
+ *     bf16 split v ~ hi + lo (hi = bf16(v), lo = bf16(v - hi), round to
+ *     nearest even; hi + lo keeps 16 significant bits), packed in one 32-bit
+ *     word with hi in the low half, so U and V keep their fp32 layouts and
+ *     sizes.  The contraction forms all four partial products
+ *     (hi + lo)(hi + lo) on bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32
+ *     accumulation; Z and y stay fp32. */
+enum { NWG_PRECISION_FP32 = 0, NWG_PRECISION_BF16_SPLIT = 1 };
+
 /* Plan geometry, as computed by the level recurrence (Sec. III.B). */
 typedef struct nwg_plan_info {
   int B, M, N, H, W, r, pad, tile;
@@ -110,6 +121,8 @@ typedef struct nwg_plan_info {
                                    depthwise at depth 1-2); the plan holds only U */
   int pipeline_parts;           /* 1, or the parts nwg_conv2d splits the input transform
                                    and contraction into (nwg_plan_set_pipeline) */
+  int precision;                /* NWG_PRECISION_FP32 (default) or NWG_PRECISION_BF16_SPLIT
+                                   (nwg_plan_set_precision) */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).
@@ -205,6 +218,19 @@ int nwg_output_transform(const nwg_plan* plan, const float* Z, float* y, void* s
  * NWG_EINVAL for other values, NWG_EUNSUPPORTED for a plan that cannot
  * split.  Timing records each piece (counts then grow by `parts`). */
 int nwg_plan_set_pipeline(nwg_plan* plan, int parts);
+
+/* Contraction arithmetic (see NWG_PRECISION_*), for dense F(2x2,3x3) plans at
+ * depth 1-4 whose contraction takes full 64-wide tiles (M % 32 == 0,
+ * N % 64 == 0, T >= 64) and that are neither fused nor pipelined.  With
+ * NWG_PRECISION_BF16_SPLIT, nwg_kernel_transform and nwg_input_transform
+ * write U and V as packed (hi, lo) pairs in the fp32 layouts, and
+ * nwg_contract reads them so; nwg_output_transform is unchanged.  The cached
+ * transformed weights are invalidated: the next nwg_conv2d (or
+ * nwg_plan_set_weights) transforms w again.  NWG_EINVAL for an unknown
+ * precision, NWG_EUNSUPPORTED for a plan that cannot take it (nothing
+ * changes then).  Measured error of the split path on the workloads: see the
+ * library's tests; about 1e-5 relative L2 at depth 4 (fp32: about 1e-7). */
+int nwg_plan_set_precision(nwg_plan* plan, int precision);
 
 /* --- Per-stage timing ------------------------------------------------------
  * When enabled, nwg_conv2d records HIP events around each of its launches on

@@ -330,7 +330,10 @@ struct DeepLoader {
   }
 };
 
-template <int BM, int BN, int WM, int WN, int BKD, int STAGES>
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
 struct DeepTile {
   static constexpr int NT = 64 * WM * WN;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -352,6 +355,10 @@ struct DeepTile {
   }
 
   __device__ __forceinline__ void compute(const float4 (*Ac)[BM], const float4 (*Bc)[BN]) {
+    if constexpr (SPLIT) {
+      compute_split(Ac, Bc);
+      return;
+    }
 #pragma unroll
     for (int kk = 0; kk < BKD / 4; ++kk) {
       float4 af[FM], bf[FN];
@@ -368,6 +375,48 @@ struct DeepTile {
           acc[2][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].z, bf[j].z, acc[2][i][j], 0, 0, 0);
           acc[3][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].w, bf[j].w, acc[3][i][j], 0, 0, 0);
         }
+    }
+  }
+
+  // Split precision: every LDS word is a packed (hi, lo) bf16 pair.  One
+  // v_mfma_f32_16x16x32_bf16 per point takes the chunk's 8 channels: lane
+  // group g = l / 16 holds channels 2g and 2g + 1, four K elements each,
+  // so that every channel contributes all four partial products:
+  //   U side (A): Uhi Ulo Uhi Ulo      (the pair word, twice)
+  //   V side (B): Vhi Vlo Vlo Vhi      (the pair word, then its halves swapped)
+  // and the sum over K is sum_m (Uhi + Ulo)(Vhi + Vlo), accumulated in fp32.
+  __device__ __forceinline__ void compute_split(const float4 (*Ac)[BM], const float4 (*Bc)[BN]) {
+    static_assert(BKD == 8, "one bf16 MFMA (K = 32) per 8-channel chunk");
+    float4 ua[FM][2], vb[FN][2];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) ua[i][c] = Ac[2 * lk + c][wm * WTM + i * 16 + lr];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) vb[j][c] = Bc[2 * lk + c][wn * WTN + j * 16 + lr];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      bf16x8 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const uint32_t w0 = __float_as_uint(reinterpret_cast<const float*>(&ua[i][0])[q]);
+        const uint32_t w1 = __float_as_uint(reinterpret_cast<const float*>(&ua[i][1])[q]);
+        a[i] = __builtin_bit_cast(bf16x8, u32x4{w0, w0, w1, w1});
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const uint32_t w0 = __float_as_uint(reinterpret_cast<const float*>(&vb[j][0])[q]);
+        const uint32_t w1 = __float_as_uint(reinterpret_cast<const float*>(&vb[j][1])[q]);
+        b[j] = __builtin_bit_cast(bf16x8, u32x4{w0, __builtin_amdgcn_alignbit(w0, w0, 16), w1,
+                                                __builtin_amdgcn_alignbit(w1, w1, 16)});
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[q][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[q][i][j], 0, 0, 0);
     }
   }
 
@@ -402,11 +451,11 @@ struct DeepTile {
   }
 };
 
-template <int BM, int BN, int WM, int WN, int BKD, int STAGES>
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2))) void contract_deep(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
     int N, int T, int ntb, int nnb) {
-  using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES>;
+  using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
   static_assert(STAGES >= 2 && STAGES <= 4, "2 to 4 stages");
@@ -490,7 +539,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
   }
 }
 
-template <int BM, int BN, int WM, int WN, int BKD, int STAGES>
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT = false>
 hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, int T,
                        long long G, hipStream_t s) {
   // T need not be a multiple of BN: the last column tile is ragged
@@ -500,7 +549,7 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
     return hipErrorInvalidValue;
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES, SPLIT>), dim3((unsigned)blocks),
                      dim3(64 * WM * WN), 0, s, (const float4*)U, (const float4*)V, (float4*)Z,
                      M, N, T, ntb, nnb);
   return hipGetLastError();
@@ -686,7 +735,13 @@ hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                                 long long G, hipStream_t s) {
+                                 long long G, hipStream_t s, bool split) {
+  // split precision: the deep pipeline only (full 64-row tiles, whole sweeps)
+  if (split) {
+    if (M % 32 || N % 64 || T < 64) return hipErrorInvalidValue;
+    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4, true>(U, V, Z, M, N, T, G, s);
+    return launch_deep<64, 64, 2, 2, 8, 4, true>(U, V, Z, M, N, T, G, s);
+  }
   // full 64-row tiles and whole 4-stage K sweeps: the deep pipeline; a
   // ragged T takes 64-column tiles (the last one partly recomputed)
   if (M % 32 == 0 && N % 64 == 0) {

@@ -37,6 +37,7 @@ namespace {
 // store of its 256 points as 64 quads.  Point digits (q2r, q2c, q1r, q1c),
 // most significant first; vb points at the branch's first quad for this
 // (m, t), qstride is the distance between quads (M*T float4).
+template <bool SPLIT>
 __device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* __restrict__ vb,
                                              size_t qstride) {
 #pragma unroll
@@ -63,14 +64,14 @@ __device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* _
       for (int q2c = 0; q2c < 4; ++q2c) {
         const int quad = q2r * 16 + q2c * 4 + q1r;
         vb[(size_t)quad * qstride] =
-            make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+            store_quad<SPLIT>(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
       }
     }
   }
 }
 
 // ---- depth 1: union box of tiles in LDS, one thread per tile ----------------
-template <int NLEV>
+template <int NLEV, bool SPLIT>
 __global__ __launch_bounds__(256) void input_xform_box(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
     int tw, int T, long long qstride, int RX, int RY, int nbx, int nby) {
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(256) void input_xform_box(
     }
 #pragma unroll
     for (int q1r = 0; q1r < 4; ++q1r)
-      vb[(size_t)q1r * qstride] = make_float4(Rw[q1r][0], Rw[q1r][1], Rw[q1r][2], Rw[q1r][3]);
+      vb[(size_t)q1r * qstride] = store_quad<SPLIT>(Rw[q1r][0], Rw[q1r][1], Rw[q1r][2], Rw[q1r][3]);
   }
 }
 
@@ -136,6 +137,7 @@ __global__ __launch_bounds__(256) void input_xform_box(
 // the tile's 10 x 10 window (4 window rows per output row) and the two
 // levels along the columns to the result, storing 4 quads.  The work-group's
 // 16 tiles form a box of RX x RY tiles whose windows are staged in LDS.
+template <bool SPLIT>
 __global__ __launch_bounds__(256) void input_xform_d2(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
     int tw, int T, long long qstride, int RX, int RY, int nbx, int nby) {
@@ -183,12 +185,12 @@ __global__ __launch_bounds__(256) void input_xform_d2(
   for (int q2c = 0; q2c < 4; ++q2c) {
     const int quad = q2r * 16 + q2c * 4 + q1r;
     vb[(size_t)quad * qstride] =
-        make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+        store_quad<SPLIT>(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
   }
 }
 
 // ---- depth 3 and 4: 16 tiles per work-group, per-tile windows in LDS -------
-template <int NLEV>
+template <int NLEV, bool SPLIT>
 __global__ __launch_bounds__(256) void input_xform_tiles(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
     int tw, int T, long long qstride, int q4_0, int nq4) {
@@ -310,7 +312,7 @@ __global__ __launch_bounds__(256) void input_xform_tiles(
     }
   // 256-point block of this branch: (q4r, q4c, q3r, q3c) at depth 4, (q3r, q3c) at depth 3
   const int branch = q4 * 16 + slot;
-  inner2_store(S, V + (size_t)branch * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+  inner2_store<SPLIT>(S, V + (size_t)branch * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
 }
 
 }  // namespace
@@ -319,6 +321,8 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
                               int part, int nparts) {
   float4* V = reinterpret_cast<float4*>(Vf);
   if ((uintptr_t)Vf & 15) return hipErrorInvalidValue;
+  // split precision: every quad holds the four values' bf16 (hi, lo) pairs
+  const bool split = g.precision == NWG_PRECISION_BF16_SPLIT;
   const long long qstride = (long long)g.M * g.T;   // float4 quads between consecutive quads
   const int T = (int)g.T;
   if (g.n >= 3) {
@@ -335,12 +339,15 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
     const long long nwg = (g.T + 15) / 16 * g.M * nq4;
     if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
     dim3 grid((unsigned)nwg);
-    if (g.n == 3)
-      hipLaunchKernelGGL(input_xform_tiles<3>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
-                         g.pad, g.th, g.tw, T, qstride, q4_0, nq4);
-    else
-      hipLaunchKernelGGL(input_xform_tiles<4>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
-                         g.pad, g.th, g.tw, T, qstride, q4_0, nq4);
+#define NWG_TILES(L, SP)                                                                       \
+  hipLaunchKernelGGL((input_xform_tiles<L, SP>), grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,  \
+                     g.pad, g.th, g.tw, T, qstride, q4_0, nq4)
+    if (g.n == 3) {
+      if (split) NWG_TILES(3, true); else NWG_TILES(3, false);
+    } else {
+      if (split) NWG_TILES(4, true); else NWG_TILES(4, false);
+    }
+#undef NWG_TILES
   } else if (g.n == 2) {
     if (nparts != 1) return hipErrorInvalidValue;
     const int Mn = 4, Ln = 10;
@@ -350,8 +357,12 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
     const int nbx = (g.tw + RX - 1) / RX, nby = (g.th + RY - 1) / RY;
     const size_t lds = (size_t)((RY - 1) * Mn + Ln) * ((RX - 1) * Mn + Ln) * sizeof(float);
     dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)g.M);
-    hipLaunchKernelGGL(input_xform_d2, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W, g.pad, g.th,
-                       g.tw, T, qstride, RX, RY, nbx, nby);
+    if (split)
+      hipLaunchKernelGGL(input_xform_d2<true>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
+                         g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby);
+    else
+      hipLaunchKernelGGL(input_xform_d2<false>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
+                         g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby);
   } else {
     if (nparts != 1) return hipErrorInvalidValue;
     const int Mn = 1 << g.n, Ln = 3 * Mn - 2;
@@ -371,8 +382,12 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
     const int nbx = (g.tw + RX - 1) / RX, nby = (g.th + RY - 1) / RY;
     const size_t lds = (size_t)((RY - 1) * Mn + Ln) * ((RX - 1) * Mn + Ln) * sizeof(float);
     dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)g.M);
-    hipLaunchKernelGGL(input_xform_box<1>, grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W, g.pad,
-                       g.th, g.tw, T, qstride, RX, RY, nbx, nby);
+    if (split)
+      hipLaunchKernelGGL((input_xform_box<1, true>), grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W,
+                         g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby);
+    else
+      hipLaunchKernelGGL((input_xform_box<1, false>), grid, dim3(tpb), lds, s, x, V, g.M, g.H,
+                         g.W, g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby);
   }
   return hipGetLastError();
 }

@@ -294,4 +294,24 @@ hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U,
   return hipGetLastError();
 }
 
+// Split precision: every fp32 value becomes its packed bf16 (hi, lo) pair,
+// in place (4 values per thread; n need not be a multiple of 4).
+__global__ __launch_bounds__(256) void split_pairs_kernel(float* __restrict__ buf, size_t n) {
+  const size_t i = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i + 4 <= n) {
+    float4 v = *reinterpret_cast<const float4*>(buf + i);
+    *reinterpret_cast<float4*>(buf + i) = store_quad<true>(v.x, v.y, v.z, v.w);
+  } else {
+    for (size_t e = i; e < n; ++e) buf[e] = __uint_as_float(split_pair(buf[e]));
+  }
+}
+
+hipError_t launch_split_pairs(float* buf, size_t n, hipStream_t s) {
+  if (((uintptr_t)buf & 15) || n == 0) return hipErrorInvalidValue;
+  const size_t blocks = (n + 1023) / 1024;
+  if (blocks > 0x7fffffffULL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(split_pairs_kernel, dim3((unsigned)blocks), dim3(256), 0, s, buf, n);
+  return hipGetLastError();
+}
+
 }  // namespace nwg

@@ -67,7 +67,8 @@ namespace {
 // contraction lost more (4.73 -> 5.6-6.6 ms over its parts) than the hidden
 // input transform saved; every part count from 2 to 16 made the step slower.
 bool pipeline_allowed(const nwg_plan_info& g) {
-  return g.tile == NWG_TILE_F2X2_3X3 && g.n == 4 && !g.depthwise && !g.fused_input &&
+  return g.tile == NWG_TILE_F2X2_3X3 && g.precision == NWG_PRECISION_FP32 && g.n == 4 &&
+         !g.depthwise && !g.fused_input &&
          g.M % 32 == 0 && g.N % 64 == 0 && g.T % 64 == 0;
 }
 
@@ -173,6 +174,7 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
   const bool no_z = g->fused_conv;
   g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : g->yhat_bytes);
   g->pipeline_parts = 1;
+  g->precision = NWG_PRECISION_FP32;
   return NWG_OK;
 }
 
@@ -247,13 +249,17 @@ hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* 
     return g.n == 0 ? nwg::launch_dw_scale(g, V, U, Z, s) : nwg::launch_dw_contract(g, U, V, Z, s);
   if (g.n == 0) return nwg::launch_gemm_depth0(depth0_args(g, U, V, Z), s);
   if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_contract5(g, U, V, Z, s);
-  return nwg::launch_contract_fused(U, V, Z, g.M, g.N, (int)g.T, g.P / 16, s);
+  return nwg::launch_contract_fused(U, V, Z, g.M, g.N, (int)g.T, g.P / 16, s,
+                                    g.precision == NWG_PRECISION_BF16_SPLIT);
 }
 
 // stage launchers by tile (depth >= 1)
 hipError_t launch_kxform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
   if (g.tile == NWG_TILE_F3X3_3X3 && g.n > 0) return nwg::launch_kernel_xform5(g, w, U, s);
-  return nwg::launch_kernel_xform(kernel_geometry(g), w, U, s);
+  const hipError_t e = nwg::launch_kernel_xform(kernel_geometry(g), w, U, s);
+  if (e != hipSuccess || g.precision != NWG_PRECISION_BF16_SPLIT) return e;
+  // split precision: the fp32 U just written becomes its (hi, lo) pairs
+  return nwg::launch_split_pairs(U, g.u_bytes / sizeof(float), s);
 }
 hipError_t launch_ixform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s) {
   if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_input_xform5(g, x, V, s);
@@ -532,6 +538,31 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",
                [&] { return launch_oxform(g, p->Yh, y, s); });
+}
+
+int nwg_plan_set_precision(nwg_plan* p, int precision) {
+  if (!p) {
+    set_error("NULL plan");
+    return NWG_EINVAL;
+  }
+  if (precision != NWG_PRECISION_FP32 && precision != NWG_PRECISION_BF16_SPLIT) {
+    set_error("unknown precision %d", precision);
+    return NWG_EINVAL;
+  }
+  const nwg_plan_info& g = p->info;
+  if (precision == NWG_PRECISION_BF16_SPLIT &&
+      (g.tile != NWG_TILE_F2X2_3X3 || g.n < 1 || g.depthwise || g.fused_input || g.fused_conv ||
+       g.pipeline_parts > 1 || g.M % 32 || g.N % 64 || g.T < 64)) {
+    set_error("split precision needs a dense, unfused, unpipelined F(2x2,3x3) plan at depth "
+              ">= 1 with M %% 32 == 0, N %% 64 == 0 and T >= 64 (M = %d, N = %d, T = %lld)",
+              g.M, g.N, g.T);
+    return NWG_EUNSUPPORTED;
+  }
+  if (precision != g.precision) {
+    p->info.precision = precision;
+    p->weights_valid = false;
+  }
+  return NWG_OK;
 }
 
 int nwg_plan_set_pipeline(nwg_plan* p, int parts) {

@@ -36,6 +36,31 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// ---------------------------------------------------------------------------
+// Two-term bf16 split (precision NWG_PRECISION_BF16_SPLIT): v ~ hi + lo with
+// hi = bf16(v) and lo = bf16(v - hi), both rounded to nearest even; packed
+// in one 32-bit word, hi in the low half.  hi + lo carries 16 significant
+// bits of v.  Finite inputs (a NaN or infinity gives an unspecified pair).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t bf16_rne_bits(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t split_pair(float v) {
+  const uint32_t hi = bf16_rne_bits(v);
+  const uint32_t lo = bf16_rne_bits(v - __uint_as_float(hi << 16));
+  return hi | (lo << 16);
+}
+// a Winograd-domain quad as stored: fp32 values, or their split pairs
+template <bool SPLIT>
+__device__ __forceinline__ float4 store_quad(float a, float b, float c, float d) {
+  if constexpr (SPLIT)
+    return make_float4(__uint_as_float(split_pair(a)), __uint_as_float(split_pair(b)),
+                       __uint_as_float(split_pair(c)), __uint_as_float(split_pair(d)));
+  else
+    return make_float4(a, b, c, d);
+}
+
 constexpr int kBase = 4;   // l
 constexpr int kOut = 2;    // m
 constexpr int kTaps = 3;   // r of the base
@@ -122,8 +147,11 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, 
 // depth 0: y[b] = U^T x[b]
 hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s);
 // depth >= 1: Z = level-1 A^T of (U^T V per point); G = P / 16 groups
+// split = true: U, V hold bf16 (hi, lo) pairs (precision NWG_PRECISION_BF16_SPLIT)
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                                 long long G, hipStream_t s);
+                                 long long G, hipStream_t s, bool split = false);
+// in place: every fp32 value of buf (n values) -> its packed bf16 (hi, lo) pair
+hipError_t launch_split_pairs(float* buf, size_t n, hipStream_t s);
 // depth 3-4 and N <= 2: x, U -> Z without forming V
 bool input_contract_applies(const nwg_plan_info& g);
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* U, float* Z,

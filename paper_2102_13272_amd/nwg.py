@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(_HERE, "libnwg.so")
 
 NWG_TILE_F2X2_3X3 = 0
 NWG_TILE_F3X3_3X3 = 1
+NWG_PRECISION_FP32 = 0
+NWG_PRECISION_BF16_SPLIT = 1
 NWG_OK, NWG_EINVAL, NWG_ENOMEM, NWG_EHIP, NWG_EUNSUPPORTED = 0, -1, -2, -3, -4
 NWG_MAX_DEPTH = 4
 
@@ -36,7 +38,7 @@ class nwg_plan_info(ctypes.Structure):
         ("ewmm_mults", ctypes.c_longlong), ("direct_flop", ctypes.c_double),
         ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
         ("depthwise", ctypes.c_int), ("fused_conv", ctypes.c_int),
-        ("pipeline_parts", ctypes.c_int),
+        ("pipeline_parts", ctypes.c_int), ("precision", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -64,6 +66,7 @@ SIGNATURES = [
     ("nwg_input_contract", _I, [_P, _P, _P, _P, _P]),
     ("nwg_output_transform", _I, [_P, _P, _P, _P]),
     ("nwg_plan_set_pipeline", _I, [_P, _I]),
+    ("nwg_plan_set_precision", _I, [_P, _I]),
     ("nwg_plan_set_timing", _I, [_P, _I]),
     ("nwg_plan_get_timing", _I, [_P, ctypes.POINTER(ctypes.c_double),
                                  ctypes.POINTER(ctypes.c_longlong)]),
@@ -230,6 +233,13 @@ class Plan:
 
     def set_pipeline(self, parts: int):
         _check(self._lib.nwg_plan_set_pipeline(self.handle, int(parts)), "nwg_plan_set_pipeline")
+        info = nwg_plan_info()
+        _check(self._lib.nwg_plan_query(self.handle, ctypes.byref(info)), "nwg_plan_query")
+        self.info = info.as_dict()
+
+    def set_precision(self, precision: int):
+        _check(self._lib.nwg_plan_set_precision(self.handle, int(precision)),
+               "nwg_plan_set_precision")
         info = nwg_plan_info()
         _check(self._lib.nwg_plan_query(self.handle, ctypes.byref(info)), "nwg_plan_query")
         self.info = info.as_dict()
