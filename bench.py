@@ -193,9 +193,10 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5_r31")
-    ap.add_argument("--tile", choices=["f23", "f33"], default="f23",
-                    help="Winograd base: F(2x2,3x3) nests (any r <= 31), or F(3x3,3x3) nests "
-                         "for the dense layers with r <= 9 (others keep F(2x2,3x3))")
+    ap.add_argument("--tile", choices=["f23", "f33", "auto"], default="f23",
+                    help="Winograd base: F(2x2,3x3) nests (any r <= 31); F(3x3,3x3) nests for "
+                         "the dense layers with r <= 9 (others keep F(2x2,3x3)); or the "
+                         "library's per-layer choice (NWG_TILE_AUTO)")
     ap.add_argument("--precision", choices=["fp32", "bf16_split"], default="fp32",
                     help="contraction arithmetic: fp32 MFMA, or the two-term bf16 split of U "
                          "and V on bf16 MFMA with fp32 accumulation (plans that can take it)")
@@ -245,6 +246,8 @@ def main():
     xd = torch.from_numpy(x).to("cuda")
     wds = [torch.from_numpy(w).to("cuda") for w in ws]
     def tile_for(L):
+        if args.tile == "auto":
+            return nwg.NWG_TILE_AUTO
         if args.tile == "f33" and not L.depthwise and L.r <= 9:
             return nwg.NWG_TILE_F3X3_3X3
         return nwg.NWG_TILE_F2X2_3X3
@@ -353,7 +356,8 @@ def main():
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
     roof["traffic"] = (measured_traffic(args.workload, dom)
-                       if len(plans) == 1 and args.tile == "f23" and not split else None)
+                       if len(plans) == 1 and all(p.info["tile"] == nwg.NWG_TILE_F2X2_3X3
+                                                  for p in plans) and not split else None)
 
     L0 = wl.layers[0]
     cfg = {"workload": args.workload, "layers": len(wl.layers), "B": L0.B,
@@ -361,7 +365,7 @@ def main():
            "r": [L.r for L in wl.layers] if len(wl.layers) > 1 else L0.r,
            "pad": [L.pad for L in wl.layers] if len(wl.layers) > 1 else L0.pad,
            "base": [("F(3x3,3x3)" if p.info["tile"] == nwg.NWG_TILE_F3X3_3X3 else "F(2x2,3x3)")
-                    for p in plans] if args.tile == "f33" else "F(2x2,3x3)",
+                    for p in plans] if args.tile != "f23" else "F(2x2,3x3)",
            "nesting_depth": [p.info["n"] for p in plans],
            "pipeline_parts": [p.info["pipeline_parts"] for p in plans]}
     out = {

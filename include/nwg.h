@@ -73,9 +73,20 @@ typedef struct nwg_plan nwg_plan;
  *         columns only: Z[g][q1r][i1c][n][t] = sum over q1c of
  *         A^T[i1c][q1c] Yhat[25g + 5 q1r + q1c][n][t]
  *     (A^T rows [1,1,1,1,0], [0,1,-1,2,0], [0,1,1,4,1]).
- *     Depth 0 (r = 1) is the plain contraction as for F(2x2, 3x3).  Never
- *     fused (fused_input = fused_conv = 0, pipeline_parts = 1). */
-enum { NWG_TILE_F2X2_3X3 = 0, NWG_TILE_F3X3_3X3 = 1 };
+ *     Depth 0 (r = 1) is the plain contraction as for F(2x2, 3x3).  With one
+ *     output channel at depth 2, nwg_conv2d runs a fused kernel (x -> Z
+ *     without V, fused_input = 1; the plan holds U and per input-channel-group
+ *     partial sums of Z instead of V and Z) and the output transform; the
+ *     stage calls keep the layouts above, and nwg_input_contract is not
+ *     available on this tile.  Otherwise fused_input = fused_conv = 0 and
+ *     pipeline_parts = 1.
+ *   NWG_TILE_AUTO: the plan takes F(3x3,3x3) where it measured faster on
+ *     MI355X -- one output channel at depth 2 (the fused kernel; unless the
+ *     F(2x2,3x3) plan runs the layer in one kernel), or M, N >= 32 and either
+ *     r = 8..9 (one nesting level fewer) or r <= 3 -- and F(2x2,3x3)
+ *     otherwise (always for depthwise plans and r > 9).  info.tile reports
+ *     the tile taken. */
+enum { NWG_TILE_F2X2_3X3 = 0, NWG_TILE_F3X3_3X3 = 1, NWG_TILE_AUTO = -1 };
 
 enum {
   NWG_OK = 0,
@@ -113,8 +124,10 @@ typedef struct nwg_plan_info {
   long long ewmm_mults;         /* general multiplications per call: P*T*M*N */
   double direct_flop;           /* 2*B*N*M*Ho*Wo*r*r */
   double contract_flop;         /* 2*P*M*N*T (n = 0: 2*B*N*M*Ho*Wo) */
-  int fused_input;              /* 1: nwg_conv2d runs nwg_input_contract (depth 3-4,
-                                   N <= 2, or depthwise) and the plan holds no V */
+  int fused_input;              /* 1: nwg_conv2d fuses the input transform into the
+                                   contraction (F(2x2,3x3): nwg_input_contract, depth 3-4,
+                                   N <= 2, or depthwise; F(3x3,3x3): depth 2, N = 1) and
+                                   the plan holds no V */
   int depthwise;                /* 1: depthwise plan (see nwg_plan_create_depthwise) */
   int fused_conv;               /* 1: nwg_conv2d runs one kernel x -> y (depth 1 with
                                    M <= 8, N <= 16; depth 2 with M <= 2, M N <= 64;

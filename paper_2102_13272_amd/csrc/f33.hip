@@ -477,10 +477,14 @@ __global__ __launch_bounds__(256) void contract5(const float* __restrict__ U,
 // ---- output transform: one thread per (tile, n) ----------------------------
 // Z [P/25][5][3][N][T] (level-1 columns applied) -> the level-1 rows, then
 // at depth 2 the level-2 A^T on both axes (output row i1r + 3 i2r).
-template <int NLEV>
+// FOLD9 (the fused kernel's parts, depth 2): Z9 [P/25][3][3][N][T], level 1
+// already applied on both axes.  parts > 1: the sum of `parts` buffers
+// zpart floats apart.
+template <int NLEV, bool FOLD9 = false>
 __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z,
                                                      float* __restrict__ y, int N, int Ho,
-                                                     int Wo, int th, int tw, int T) {
+                                                     int Wo, int th, int tw, int T, int parts,
+                                                     size_t zpart) {
   constexpr int Mn = NLEV == 1 ? 3 : 9;
   const int t = blockIdx.x * 256 + threadIdx.x;
   const int n = blockIdx.y;
@@ -506,7 +510,11 @@ __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z
 #pragma unroll
     for (int q = 0; q < 5; ++q)
 #pragma unroll
-      for (int c = 0; c < 3; ++c) zr[q][c] = zp[(size_t)(q * 3 + c) * plane];
+      for (int c = 0; c < 3; ++c) {
+        float v = 0.0f;
+        for (int k = 0; k < parts; ++k) v += zp[(size_t)k * zpart + (size_t)(q * 3 + c) * plane];
+        zr[q][c] = v;
+      }
     level1_rows(zr, out);
   } else {
 #pragma unroll
@@ -520,18 +528,58 @@ __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z
     const float* zq = zp;
 #pragma unroll 1
     for (int q2r = 0; q2r < 5; ++q2r) {
-      float zr[5][5][3];
+      float zv9[5][3][3];
       size_t pl = plane;
       asm volatile("" : "+s"(pl));
+      if constexpr (FOLD9) {
 #pragma unroll
-      for (int q2c = 0; q2c < 5; ++q2c)
+        for (int q2c = 0; q2c < 5; ++q2c)
 #pragma unroll
-        for (int q = 0; q < 5; ++q)
+          for (int i = 0; i < 3; ++i)
 #pragma unroll
-          for (int c = 0; c < 3; ++c) {
-            zr[q2c][q][c] = *zq;
-            zq += pl;
-          }
+            for (int c = 0; c < 3; ++c) {
+              zv9[q2c][i][c] = *zq;
+              zq += pl;
+            }
+        for (int k = 1; k < parts; ++k) {
+          const float* zk = zq - 45 * pl + (size_t)k * zpart;
+#pragma unroll
+          for (int q2c = 0; q2c < 5; ++q2c)
+#pragma unroll
+            for (int i = 0; i < 3; ++i)
+#pragma unroll
+              for (int c = 0; c < 3; ++c) {
+                zv9[q2c][i][c] += *zk;
+                zk += pl;
+              }
+        }
+      } else {
+        float zr[5][5][3];
+#pragma unroll
+        for (int q2c = 0; q2c < 5; ++q2c)
+#pragma unroll
+          for (int q = 0; q < 5; ++q)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+              zr[q2c][q][c] = *zq;
+              zq += pl;
+            }
+        // partial sums of a channel-split contraction (parts > 1)
+        for (int k = 1; k < parts; ++k) {
+          const float* zk = zq - 75 * pl + (size_t)k * zpart;
+#pragma unroll
+          for (int q2c = 0; q2c < 5; ++q2c)
+#pragma unroll
+            for (int q = 0; q < 5; ++q)
+#pragma unroll
+              for (int c = 0; c < 3; ++c) {
+                zr[q2c][q][c] += *zk;
+                zk += pl;
+              }
+        }
+#pragma unroll
+        for (int q2c = 0; q2c < 5; ++q2c) level1_rows(zr[q2c], zv9[q2c]);
+      }
       float cr[3];
 #pragma unroll
       for (int i = 0; i < 3; ++i) {
@@ -541,8 +589,7 @@ __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z
       }
 #pragma unroll
       for (int q2c = 0; q2c < 5; ++q2c) {
-        float zv[3][3];
-        level1_rows(zr[q2c], zv);
+        const float (&zv)[3][3] = zv9[q2c];
 #pragma unroll
         for (int i2r = 0; i2r < 3; ++i2r)
 #pragma unroll
@@ -573,6 +620,144 @@ __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z
       const int col = tx * Mn + k;
       if (col < Wo) yo[(size_t)row * Wo + col] = out[i][k];
     }
+  }
+}
+
+// ---- fused input transform + contraction: depth 2, one output channel -----
+// x -> Z with no V in memory (the F(3,3) counterpart of the F(2,3) fused
+// kernel): work-group = a box of up to 64 tiles of one image and a group of
+// input channels; wavefront q2r (5 of them) and lane = tile, as in the input
+// transform.  Per channel the box and U[.][m][0] are staged in LDS; each
+// lane forms its 125 points (q2c, q1r, q1c), multiplies them by U (LDS
+// broadcast reads) and folds level 1 on both axes into 45 accumulators
+// acc[q2c][i1r][i1c].  Channel group cg writes its partial Z9 (P/25 x 9
+// values per tile: level 1 fully applied) to part cg; the output
+// transform adds the parts.
+__global__ __launch_bounds__(320) void input_contract5(
+    const float* __restrict__ x, const float* __restrict__ U, float* __restrict__ Zp, int M,
+    int H, int W, int pad, int th, int tw, int T, int RX, int RY, int nbx, int nby, int mper,
+    size_t zpart) {
+  constexpr int Mn = 9, Ln = 17, P = 625;
+  extern __shared__ float lds[];
+  const int BH = (RY - 1) * Mn + Ln, BW = (RX - 1) * Mn + Ln;
+  const int nbox = BH * BW;
+  float* box = lds;
+  float* Us = lds + nbox;
+  int bid = blockIdx.x;
+  const int bx = bid % nbx;
+  bid /= nbx;
+  const int by = bid % nby;
+  const int b = bid / nby;
+  const int cg = blockIdx.y;
+  const int m0 = cg * mper, m1 = M < m0 + mper ? M : m0 + mper;
+  const int ty0 = by * RY, tx0 = bx * RX;
+  const int r0 = ty0 * Mn - pad, c0 = tx0 * Mn - pad;
+  const int s = threadIdx.x & 63;
+  const int q2r = threadIdx.x >> 6;
+  const int ly = s / RX, lx = s - ly * RX;
+  const int ty = ty0 + ly, tx = tx0 + lx;
+  const bool active = s < RX * RY && ty < th && tx < tw;
+  float c2v[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int q = 0; q < 5; ++q)
+#pragma unroll
+    for (int a2 = 0; a2 < 5; ++a2) c2v[a2] = q2r == q ? bt5(q, a2) : c2v[a2];
+  float acc[5][3][3];   // [q2c][i1r][i1c]
+#pragma unroll
+  for (int i = 0; i < 5; ++i)
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+      for (int k = 0; k < 3; ++k) acc[i][j][k] = 0.0f;
+
+  for (int m = m0; m < m1; ++m) {
+    const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
+    constexpr int FB = 8;
+    for (int e0 = threadIdx.x; e0 < nbox; e0 += FB * 320) {
+      float v[FB];
+#pragma unroll
+      for (int u = 0; u < FB; ++u) {
+        const int e = e0 + u * 320;
+        const int row = e / BW, col = e - row * BW;
+        const int gr = r0 + row, gc = c0 + col;
+        v[u] = 0.0f;
+        if (e < nbox && gr >= 0 && gr < H && gc >= 0 && gc < W) v[u] = xp[(size_t)gr * W + gc];
+      }
+#pragma unroll
+      for (int u = 0; u < FB; ++u)
+        if (e0 + u * 320 < nbox) box[e0 + u * 320] = v[u];
+    }
+    for (int e = threadIdx.x; e < P; e += 320) Us[e] = U[(size_t)e * M + m];
+    __syncthreads();
+    if (active) {
+      const float* win = box + ly * Mn * BW + lx * Mn;
+      float Rw[5][17];
+#pragma unroll
+      for (int a1 = 0; a1 < 5; ++a1) {
+#pragma unroll
+        for (int c = 0; c < 17; ++c) Rw[a1][c] = 0.0f;
+#pragma unroll
+        for (int a2 = 0; a2 < 5; ++a2) {
+          const float* rowp = win + (a1 + 3 * a2) * BW;
+#pragma unroll
+          for (int c = 0; c < 17; ++c) Rw[a1][c] = fmaf(c2v[a2], rowp[c], Rw[a1][c]);
+        }
+      }
+      const float* ub = Us + q2r * 125;
+#pragma unroll
+      for (int q1r = 0; q1r < 5; ++q1r) {
+        float R[17];
+#pragma unroll
+        for (int c = 0; c < 17; ++c) {
+          float sr = 0.0f;
+#pragma unroll
+          for (int a1 = 0; a1 < 5; ++a1)
+            if (bt5(q1r, a1) != 0.0f) sr = fmaf(bt5(q1r, a1), Rw[a1][c], sr);
+          R[c] = sr;
+        }
+#pragma unroll
+        for (int q2c = 0; q2c < 5; ++q2c) {
+          float v5[5];
+#pragma unroll
+          for (int b1 = 0; b1 < 5; ++b1) {
+            float s2 = 0.0f;
+#pragma unroll
+            for (int b2 = 0; b2 < 5; ++b2)
+              if (bt5(q2c, b2) != 0.0f) s2 = fmaf(bt5(q2c, b2), R[b1 + 3 * b2], s2);
+            v5[b1] = s2;
+          }
+          float o[5];
+          bt5_vec(v5, o);
+          const float* up = ub + (q2c * 5 + q1r) * 5;   // the same LDS word for every lane
+          float pr[5];
+#pragma unroll
+          for (int q1c = 0; q1c < 5; ++q1c) pr[q1c] = up[q1c] * o[q1c];
+#pragma unroll
+          for (int i1c = 0; i1c < 3; ++i1c) {
+            float wc = 0.0f;
+#pragma unroll
+            for (int q1c = 0; q1c < 5; ++q1c)
+              if (at5(i1c, q1c) != 0.0f) wc = fmaf(at5(i1c, q1c), pr[q1c], wc);
+#pragma unroll
+            for (int i1r = 0; i1r < 3; ++i1r)
+              if (at5(i1r, q1r) != 0.0f)
+                acc[q2c][i1r][i1c] = fmaf(at5(i1r, q1r), wc, acc[q2c][i1r][i1c]);
+          }
+        }
+      }
+    }
+    __syncthreads();   // the next channel's fill overwrites box and Us
+  }
+  if (active) {
+    const int t = (b * th + ty) * tw + tx;
+    float* __restrict__ zp = Zp + (size_t)cg * zpart + t;
+#pragma unroll
+    for (int q2c = 0; q2c < 5; ++q2c)
+#pragma unroll
+      for (int i1r = 0; i1r < 3; ++i1r)
+#pragma unroll
+        for (int i1c = 0; i1c < 3; ++i1c)
+          zp[(size_t)((q2r * 5 + q2c) * 9 + i1r * 3 + i1c) * T] = acc[q2c][i1r][i1c];
   }
 }
 
@@ -635,18 +820,107 @@ hipError_t launch_contract5(const nwg_plan_info& g, const float* U, const float*
   return hipGetLastError();
 }
 
-hipError_t launch_output_xform5(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s) {
-  if (g.N > 65535) return hipErrorInvalidValue;
+hipError_t launch_output_xform5(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s,
+                                int parts, bool fold9) {
+  if (g.N > 65535 || parts < 1 || (fold9 && g.n != 2)) return hipErrorInvalidValue;
   const int T = (int)g.T;
+  // parts lie back to back: Z9 parts of P/25 x 9 values per (n, t), else Z
+  const size_t zpart = fold9 ? (size_t)(g.P / 25) * 9 * g.N * g.T : g.yhat_bytes / sizeof(float);
   dim3 grid((unsigned)((T + 255) / 256), (unsigned)g.N);
   if (g.n == 1)
     hipLaunchKernelGGL(output_xform5<1>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo, g.th, g.tw,
-                       T);
+                       T, parts, zpart);
+  else if (g.n == 2 && fold9)
+    hipLaunchKernelGGL((output_xform5<2, true>), grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo,
+                       g.th, g.tw, T, parts, zpart);
   else if (g.n == 2)
     hipLaunchKernelGGL(output_xform5<2>, grid, dim3(256), 0, s, Z, y, g.N, g.Ho, g.Wo, g.th, g.tw,
-                       T);
+                       T, parts, zpart);
   else
     return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// Sum of the fused kernel's partial Z9 buffers into the first one (one
+// thread per 4 consecutive values: all of them in flight at once, where the
+// output transform alone has one thread per tile and output channel).
+__global__ __launch_bounds__(256) void sum_parts_kernel(float* __restrict__ Z, size_t n,
+                                                        size_t zpart, int parts) {
+  const size_t i = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= n) return;
+  if (i + 4 <= n && !(zpart & 3)) {
+    float4 a = *reinterpret_cast<const float4*>(Z + i);
+    for (int k = 1; k < parts; ++k) {
+      const float4 b = *reinterpret_cast<const float4*>(Z + (size_t)k * zpart + i);
+      a.x += b.x;
+      a.y += b.y;
+      a.z += b.z;
+      a.w += b.w;
+    }
+    *reinterpret_cast<float4*>(Z + i) = a;
+  } else {
+    for (size_t e = i; e < n && e < i + 4; ++e) {
+      float a = Z[e];
+      for (int k = 1; k < parts; ++k) a += Z[(size_t)k * zpart + e];
+      Z[e] = a;
+    }
+  }
+}
+
+hipError_t launch_sum_parts(float* Z, size_t n, int parts, hipStream_t s) {
+  if (parts <= 1) return hipSuccess;
+  if ((uintptr_t)Z & 15) return hipErrorInvalidValue;
+  const size_t blocks = (n + 1023) / 1024;
+  if (blocks > 0x7fffffffULL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sum_parts_kernel, dim3((unsigned)blocks), dim3(256), 0, s, Z, n, n, parts);
+  return hipGetLastError();
+}
+
+// The fused depth-2 kernel: dense F(3,3) plans with one output channel.
+bool input_contract5_applies(const nwg_plan_info& g) {
+  return g.tile == NWG_TILE_F3X3_3X3 && g.n == 2 && g.N == 1 && !g.depthwise;
+}
+
+namespace {
+struct IC5Shape {
+  int RX, RY, nbx, nby, groups, mper;
+  size_t lds;
+};
+IC5Shape ic5_shape(const nwg_plan_info& g) {
+  IC5Shape c;
+  c.RX = g.tw < 64 ? g.tw : 64;
+  c.RY = 64 / c.RX;
+  if (c.RY > g.th) c.RY = g.th;
+  c.nbx = (g.tw + c.RX - 1) / c.RX;
+  c.nby = (g.th + c.RY - 1) / c.RY;
+  // input-channel groups: about 512 work-groups in all, at least 2 channels each
+  const long long boxes = (long long)c.nbx * c.nby * g.B;
+  long long want = (512 + boxes - 1) / boxes;
+  const long long maxg = (g.M + 1) / 2;
+  if (want > maxg) want = maxg;
+  if (want < 1) want = 1;
+  c.mper = (int)((g.M + want - 1) / want);
+  c.groups = (g.M + c.mper - 1) / c.mper;
+  c.lds = (size_t)(((c.RY - 1) * 9 + 17) * ((c.RX - 1) * 9 + 17) + 625) * sizeof(float);
+  return c;
+}
+}  // namespace
+
+int input_contract5_parts(const nwg_plan_info& g) { return ic5_shape(g).groups; }
+
+size_t input_contract5_zbytes(const nwg_plan_info& g) {
+  return (size_t)ic5_shape(g).groups * (size_t)(g.P / 25) * 9 * g.N * g.T * sizeof(float);
+}
+
+hipError_t launch_input_contract5(const nwg_plan_info& g, const float* x, const float* U,
+                                  float* Zp, hipStream_t s) {
+  if (!input_contract5_applies(g)) return hipErrorInvalidValue;
+  const IC5Shape c = ic5_shape(g);
+  const long long blocks = (long long)c.nbx * c.nby * g.B;
+  if (blocks > 0x7fffffffLL || c.groups > 65535 || c.lds > 160 * 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(input_contract5, dim3((unsigned)blocks, (unsigned)c.groups), dim3(320), c.lds,
+                     s, x, U, Zp, g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T, c.RX, c.RY, c.nbx,
+                     c.nby, c.mper, (size_t)(g.P / 25) * 9 * g.N * g.T);
   return hipGetLastError();
 }
 

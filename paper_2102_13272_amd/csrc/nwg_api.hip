@@ -73,8 +73,44 @@ bool pipeline_allowed(const nwg_plan_info& g) {
 }
 
 // depthwise: M = N = C channels, one r x r kernel each, no channel sum.
+// bytes of the plan's Z buffer: the stage-call Z, or the fused F(3,3)
+// kernel's partial Z9 buffers
+size_t zalloc_bytes(const nwg_plan_info& g) {
+  if (g.fused_input && g.tile == NWG_TILE_F3X3_3X3) return nwg::input_contract5_zbytes(g);
+  return g.yhat_bytes;
+}
+
+int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile,
+                          int depthwise, nwg_plan_info* g);
+
+// NWG_TILE_AUTO: F(3x3,3x3) where it measured faster than F(2x2,3x3) --
+// the fused one-output-channel kernel at depth 2 (unless F(2,3) runs the
+// layer in one kernel), or both channel counts >= 32 and either a nesting
+// level saved (r = 8, 9) or depth 1 (r <= 3); F(2x2,3x3) otherwise.
 int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile, int depthwise,
                      nwg_plan_info* g) {
+  if (tile != NWG_TILE_AUTO)
+    return compute_geometry_tile(B, M, N, H, W, r, pad, tile, depthwise, g);
+  nwg_plan_info a, b;
+  const int ra = compute_geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F2X2_3X3, depthwise, &a);
+  if (ra != NWG_OK || depthwise || r > 9 || r == 1) {
+    if (g) *g = a;
+    return ra;
+  }
+  if (compute_geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F3X3_3X3, 0, &b) != NWG_OK) {
+    set_error("");
+    *g = a;
+    return NWG_OK;
+  }
+  const bool big = M >= 32 && N >= 32;
+  const bool pick = (b.fused_input && !a.fused_conv) || (big && a.n > b.n) ||
+                    (big && a.n == 1 && !a.fused_conv);
+  *g = pick ? b : a;
+  return NWG_OK;
+}
+
+int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile,
+                          int depthwise, nwg_plan_info* g) {
   if (!g) {
     set_error("output pointer is NULL");
     return NWG_EINVAL;
@@ -167,12 +203,12 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
   // one or two output channels (or depthwise) at depth 3-4: the fused kernel
   // never forms V.  Few channels (or depthwise) at depth 1-2: one kernel
   // x -> y, neither V nor Z.
-  g->fused_input = !f33 && nwg::input_contract_applies(*g) ? 1 : 0;
+  g->fused_input = (f33 ? nwg::input_contract5_applies(*g) : nwg::input_contract_applies(*g)) ? 1 : 0;
   g->fused_conv =
       !f33 && (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
   const bool no_v = g->fused_input || depthwise || g->fused_conv;
   const bool no_z = g->fused_conv;
-  g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : g->yhat_bytes);
+  g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : zalloc_bytes(*g));
   g->pipeline_parts = 1;
   g->precision = NWG_PRECISION_FP32;
   return NWG_OK;
@@ -372,7 +408,7 @@ nwg_plan* create_plan(const nwg_plan_info& g) {
   const bool no_v = g.fused_input || g.depthwise || g.fused_conv;
   const bool no_z = g.fused_conv;
   if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, no_v ? 0 : g.v_bytes, "V") ||
-      !alloc(&p->Yh, no_z ? 0 : g.yhat_bytes, "Yhat")) {
+      !alloc(&p->Yh, no_z ? 0 : zalloc_bytes(g), "Yhat")) {
     nwg_plan_destroy(p);
     // keep the allocation message
     return nullptr;
@@ -523,7 +559,18 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
     });
   }
   int rc;
-  if (g.fused_input) {
+  if (g.fused_input && g.tile == NWG_TILE_F3X3_3X3) {
+    // partial Z9 per input-channel group, summed by the output transform
+    const int parts = nwg::input_contract5_parts(g);
+    rc = timed(p, 2, s, "fused input transform + contraction launch", [&] {
+      const hipError_t e = nwg::launch_input_contract5(g, x, p->U, p->Yh, s);
+      if (e != hipSuccess) return e;
+      return nwg::launch_sum_parts(p->Yh, (size_t)(g.P / 25) * 9 * g.N * g.T, parts, s);
+    });
+    if (rc != NWG_OK) return rc;
+    return timed(p, 3, s, "output transform launch",
+                 [&] { return nwg::launch_output_xform5(g, p->Yh, y, s, 1, true); });
+  } else if (g.fused_input) {
     rc = timed(p, 2, s, "fused input transform + contraction launch",
                [&] { return nwg::launch_input_contract(g, x, p->U, p->Yh, s); });
   } else if (g.pipeline_parts > 1) {

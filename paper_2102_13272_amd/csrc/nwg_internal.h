@@ -161,7 +161,17 @@ hipError_t launch_kernel_xform5(const nwg_plan_info& g, const float* w, float* U
 hipError_t launch_input_xform5(const nwg_plan_info& g, const float* x, float* V, hipStream_t s);
 hipError_t launch_contract5(const nwg_plan_info& g, const float* U, const float* V, float* Z,
                             hipStream_t s);
-hipError_t launch_output_xform5(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s);
+// parts > 1 / fold9: the fused kernel's partial Z9 buffers (see f33.hip)
+hipError_t launch_output_xform5(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s,
+                                int parts = 1, bool fold9 = false);
+// fused x -> partial Z9 (depth 2, N = 1): applies / number of parts / bytes
+bool input_contract5_applies(const nwg_plan_info& g);
+int input_contract5_parts(const nwg_plan_info& g);
+size_t input_contract5_zbytes(const nwg_plan_info& g);
+hipError_t launch_input_contract5(const nwg_plan_info& g, const float* x, const float* U,
+                                  float* Zp, hipStream_t s);
+// Z[i] += Z[k n + i] for k = 1 .. parts-1 (n floats per part)
+hipError_t launch_sum_parts(float* Z, size_t n, int parts, hipStream_t s);
 // few channels at depth 1-2 (dense): x -> y in one kernel
 bool small_conv_applies(const nwg_plan_info& g);
 hipError_t launch_small_conv(const nwg_plan_info& g, const float* x, const float* U, float* y,

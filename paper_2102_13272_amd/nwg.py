@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libnwg.so")
 
 NWG_TILE_F2X2_3X3 = 0
 NWG_TILE_F3X3_3X3 = 1
+NWG_TILE_AUTO = -1
 NWG_PRECISION_FP32 = 0
 NWG_PRECISION_BF16_SPLIT = 1
 NWG_OK, NWG_EINVAL, NWG_ENOMEM, NWG_EHIP, NWG_EUNSUPPORTED = 0, -1, -2, -3, -4

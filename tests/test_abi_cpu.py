@@ -200,3 +200,22 @@ def test_f33_geometry_matches_oracle_levels(r):
     assert g["fused_input"] == 0 and g["fused_conv"] == 0 and g["pipeline_parts"] == 1
     with pytest.raises(nwg.NwgError):
         nwg.plan_geometry_depthwise(B, 4, H, W, r, pad, tile)
+
+
+@pytest.mark.parametrize("shape,tile", [
+    ((4, 32, 1, 256, 256, 9, 4), 1),      # one output channel at depth 2: fused F(3,3)
+    ((4, 1, 32, 256, 256, 5, 2), 0),      # F(2,3) runs it in one kernel
+    ((8, 64, 64, 56, 56, 9, 4), 1),       # depth 3 -> 2
+    ((8, 64, 64, 56, 56, 7, 3), 0),       # same depth: F(2,3)
+    ((8, 64, 64, 56, 56, 3, 1), 1),       # depth 1, wide channels
+    ((4, 5, 5, 256, 256, 3, 1), 0),       # few channels
+    ((16, 128, 128, 56, 56, 31, 15), 0),  # r > 9
+    ((1, 32, 32, 64, 64, 1, 0), 0),       # 1x1
+])
+def test_auto_tile_choice(shape, tile):
+    g = nwg.plan_geometry(*shape, tile=nwg.NWG_TILE_AUTO)
+    assert g["tile"] == tile
+    ref = nwg.plan_geometry(*shape, tile=tile)
+    assert g == ref
+    d = nwg.plan_geometry_depthwise(4, 16, 64, 64, 9, 4, tile=nwg.NWG_TILE_AUTO)
+    assert d["tile"] == nwg.NWG_TILE_F2X2_3X3 and d["depthwise"] == 1

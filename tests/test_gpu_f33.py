@@ -32,8 +32,10 @@ def _conv(x, w, pad):
     B, M, H, W = x.shape
     N, _, r, _ = w.shape
     with nwg.Plan(B, M, N, H, W, r, pad, tile=F33) as plan:
-        assert plan.info["tile"] == F33 and plan.info["fused_input"] == 0
-        assert plan.info["fused_conv"] == 0
+        i = plan.info
+        assert i["tile"] == F33 and i["fused_conv"] == 0
+        # one output channel at depth 2: the fused kernel, no V
+        assert i["fused_input"] == (1 if (i["n"] == 2 and N == 1) else 0)
         y = torch.full(plan.y_shape, float("nan"), device="cuda")
         plan.conv2d(dev(x), dev(w), y)
         torch.cuda.synchronize()
@@ -62,6 +64,12 @@ E2E = [
     (4, 20, 12, 17, 17, 4, 1),
     (4, 64, 64, 30, 30, 3, 1),
     (4, 96, 132, 46, 46, 9, 4),
+    # N = 1 at depth 2: the fused kernel (one or several input-channel
+    # groups, ragged boxes, M = 1 and odd M)
+    (1, 1, 1, 23, 21, 4, 2),
+    (2, 5, 1, 40, 35, 9, 4),
+    (3, 32, 1, 70, 50, 7, 3),
+    (1, 33, 1, 100, 90, 9, 0),
 ]
 
 
@@ -116,6 +124,16 @@ def test_f33_stages_match_cpu_nested_reference(case):
         # rows, level-2 rows and columns): rounding reaches ~1e-6 of max|y|
         assert_close(y.cpu().numpy(), output_transform(Yh_ref, g), rel_tol=1e-6,
                      abs_frac=1e-5, what="y")
+
+
+def test_f33_fused_plan_holds_no_v():
+    with nwg.Plan(4, 32, 1, 256, 256, 9, 4, tile=F33) as plan:
+        i = plan.info
+        assert i["fused_input"] == 1 and i["n"] == 2
+        z9 = (i["P"] // 25) * 9 * i["T"] * 4
+        parts = (i["workspace_bytes"] - i["u_bytes"]) // z9
+        assert parts >= 1 and i["workspace_bytes"] == i["u_bytes"] + parts * z9
+        assert i["workspace_bytes"] < i["v_bytes"]
 
 
 def test_f33_rejects_deep_kernels_and_fused_calls():

@@ -64,12 +64,15 @@ def test_sr_stack_per_layer_and_end_to_end():
         p.close()
 
 
-def test_large_kernel_workload_sampled():
+@pytest.mark.parametrize("precision", [nwg.NWG_PRECISION_FP32, nwg.NWG_PRECISION_BF16_SPLIT],
+                         ids=["fp32", "bf16_split"])
+def test_large_kernel_workload_sampled(precision):
     name = "c5_r31"
     L = WORKLOADS[name].layers[0]
     x, (w,) = make_workload(name)
-    print(f"workload {name}", flush=True)
+    print(f"workload {name} precision {precision}", flush=True)
     with nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad) as plan:
+        plan.set_precision(precision)
         y = _gpu_layer(plan, dev(x), w)
         torch.cuda.synchronize()
         yh = y.cpu().numpy()
