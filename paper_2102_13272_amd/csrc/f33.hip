@@ -672,7 +672,9 @@ __global__ __launch_bounds__(320) void input_contract5(
 
   for (int m = m0; m < m1; ++m) {
     const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
-    constexpr int FB = 8;
+    // batches of FB loads per thread (a 64-tile box of 9 x 9 tiles is
+    // about 7000 floats: one batch), all issued before the LDS stores
+    constexpr int FB = 24;
     for (int e0 = threadIdx.x; e0 < nbox; e0 += FB * 320) {
       float v[FB];
 #pragma unroll
