@@ -200,6 +200,9 @@ def main():
     ap.add_argument("--precision", choices=["fp32", "bf16_split"], default="fp32",
                     help="contraction arithmetic: fp32 MFMA, or the two-term bf16 split of U "
                          "and V on bf16 MFMA with fp32 accumulation (plans that can take it)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the step as replays of one HIP graph holding every layer's "
+                         "launches (per-kernel times still come from an eager timed region)")
     ap.add_argument("--pipeline-parts", type=int, default=0,
                     help="input-transform/contraction pieces on two streams (0: the library's "
                          "default for each plan, 1: off)")
@@ -267,10 +270,10 @@ def main():
     outs = [torch.empty(p.y_shape, dtype=torch.float32, device="cuda") for p in plans]
     stream = torch.cuda.current_stream()
 
-    def step():
+    def step(s=None):
         cur = xd
         for p, w, y in zip(plans, wds, outs):
-            p.conv2d(cur, w, y, stream)
+            p.conv2d(cur, w, y, s or stream)
             cur = y
 
     # warm-up (includes the one kernel transform per layer), then timed steps
@@ -292,6 +295,26 @@ def main():
     ms_total = e0.elapsed_time(e1)
     ms_step = ms_total / args.steps
     timing = [p.get_timing() for p in plans]
+    ms_step_eager = ms_step
+    if args.graph:
+        # one step captured (weights already transformed, timing off: the
+        # captured work is exactly the step's kernels), then K replays timed
+        for p in plans:
+            p.set_timing(False)
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=cap):
+            step(torch.cuda.current_stream())
+        graph.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        ms_step = g0.elapsed_time(g1) / args.steps
 
     direct_flop = float(sum(L.direct_flop for L in wl.layers))
     value = direct_flop / (ms_step * 1e-3) / 1e12
@@ -367,7 +390,8 @@ def main():
            "base": [("F(3x3,3x3)" if p.info["tile"] == nwg.NWG_TILE_F3X3_3X3 else "F(2x2,3x3)")
                     for p in plans] if args.tile != "f23" else "F(2x2,3x3)",
            "nesting_depth": [p.info["n"] for p in plans],
-           "pipeline_parts": [p.info["pipeline_parts"] for p in plans]}
+           "pipeline_parts": [p.info["pipeline_parts"] for p in plans],
+           "launch": "hip-graph replay" if args.graph else "eager"}
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
@@ -380,6 +404,8 @@ def main():
         "value_incl_kernel_transform": round(direct_flop / ((ms_step + kx_ms) * 1e-3) / 1e12, 3),
         "direct_flop_per_step": direct_flop,
     }
+    if args.graph:
+        out["ms_per_step_eager"] = round(ms_step_eager, 4)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
     for p in plans:
