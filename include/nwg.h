@@ -86,7 +86,18 @@ typedef struct nwg_plan nwg_plan;
  *     r = 8..9 (one nesting level fewer) or r <= 3 -- and F(2x2,3x3)
  *     otherwise (always for depthwise plans and r > 9).  info.tile reports
  *     the tile taken. */
-enum { NWG_TILE_F2X2_3X3 = 0, NWG_TILE_F3X3_3X3 = 1, NWG_TILE_AUTO = -1 };
+/*   NWG_TILE_LD_F2X2_3X3: the linear decomposition of Sec. II.B (Fig. 2),
+ *     the method the paper compares nesting with, on the same F(2x2,3x3)
+ *     kernels: the r x r kernel is cut into c x c sub-kernels of 3 x 3
+ *     (c = ceil(r/3), zero-padded at the end), sub-kernel (cu, cv) meets the
+ *     input window moved by (3 cu, 3 cv), and the Winograd-domain products
+ *     of all sub-kernels and input channels are summed before one output
+ *     transform.  The plan is a depth-1 plan (n = 1, P = 16, M_n = 2,
+ *     K_n = 3c, L_n = 3c + 1, info.ld_c = c) whose contraction runs over
+ *     M c^2 channels, channel (cu c + cv) M + m: U [4][M c^2][N][4],
+ *     V [4][M c^2][T][4], Z [1][N][T][4].  Dense fp32 plans only. */
+enum { NWG_TILE_F2X2_3X3 = 0, NWG_TILE_F3X3_3X3 = 1, NWG_TILE_LD_F2X2_3X3 = 2,
+       NWG_TILE_AUTO = -1 };
 
 enum {
   NWG_OK = 0,
@@ -136,6 +147,7 @@ typedef struct nwg_plan_info {
                                    and contraction into (nwg_plan_set_pipeline) */
   int precision;                /* NWG_PRECISION_FP32 (default) or NWG_PRECISION_BF16_SPLIT
                                    (nwg_plan_set_precision) */
+  int ld_c;                     /* NWG_TILE_LD_F2X2_3X3: sub-kernels per axis c; else 0 */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).

@@ -454,7 +454,7 @@ struct DeepTile {
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2))) void contract_deep(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
-    int N, int T, int ntb, int nnb) {
+    int N, int T, int ntb, int nnb, int ks) {
   using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
@@ -468,17 +468,23 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
   const int tb = (int)(bid % ntb);
   bid /= ntb;
   const int nb = (int)(bid % nnb);
-  const long long g = bid / nnb;
+  bid /= nnb;
+  // K slices (ks > 1): slice sk takes channels [sk M/ks, (sk+1) M/ks) and
+  // writes its partial Z to part sk (parts of G N T quads, back to back)
+  const int sk = (int)(bid % ks);
+  const long long g = bid / ks;
+  const long long G = (long long)gridDim.x / ((long long)ntb * nnb * ks);
+  const int mk = M / ks;
   const int n0 = nb * BM, c0 = tb * BN;
 
   Tile tile;
   tile.quadU = (size_t)M * N;
   tile.quadV = (size_t)M * T;
-  tile.Ug = U + (size_t)(4 * g) * tile.quadU;
-  tile.Vg = V + (size_t)(4 * g) * tile.quadV;
+  tile.Ug = U + (size_t)(4 * g) * tile.quadU + (size_t)sk * mk * N;
+  tile.Vg = V + (size_t)(4 * g) * tile.quadV + (size_t)sk * mk * T;
   tile.N = N;
   tile.T = T;
-  tile.nk = M / BKD;
+  tile.nk = mk / BKD;
   tile.total = 4 * tile.nk;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -522,7 +528,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
     tile.fold(q1r);
   }
 
-  float4* __restrict__ Zg = Z + (size_t)g * N * T;
+  float4* __restrict__ Zg = Z + (size_t)(sk * G + g) * N * T;
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -541,17 +547,17 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
 
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT = false>
 hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, int T,
-                       long long G, hipStream_t s) {
+                       long long G, hipStream_t s, int ks = 1) {
   // T need not be a multiple of BN: the last column tile is ragged
   const int ntb = (T + BN - 1) / BN, nnb = N / BM;
-  const long long blocks = (long long)ntb * nnb * G;
-  if (N % BM || M % (BKD * STAGES) || blocks <= 0 || blocks > 0x7fffffffLL)
+  const long long blocks = (long long)ntb * nnb * G * ks;
+  if (ks < 1 || N % BM || M % (BKD * STAGES * ks) || blocks <= 0 || blocks > 0x7fffffffLL)
     return hipErrorInvalidValue;
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
   hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES, SPLIT>), dim3((unsigned)blocks),
                      dim3(64 * WM * WN), 0, s, (const float4*)U, (const float4*)V, (float4*)Z,
-                     M, N, T, ntb, nnb);
+                     M, N, T, ntb, nnb, ks);
   return hipGetLastError();
 }
 
@@ -735,12 +741,17 @@ hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                                 long long G, hipStream_t s, bool split) {
-  // split precision: the deep pipeline only (full 64-row tiles, whole sweeps)
-  if (split) {
-    if (M % 32 || N % 64 || T < 64) return hipErrorInvalidValue;
-    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4, true>(U, V, Z, M, N, T, G, s);
-    return launch_deep<64, 64, 2, 2, 8, 4, true>(U, V, Z, M, N, T, G, s);
+                                 long long G, hipStream_t s, bool split, int ks) {
+  // split precision and K slices: the deep pipeline only (full 64-row
+  // tiles, whole sweeps)
+  if (split || ks > 1) {
+    if (M % (32 * ks) || N % 64 || T < 64) return hipErrorInvalidValue;
+    if (split) {
+      if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4, true>(U, V, Z, M, N, T, G, s, ks);
+      return launch_deep<64, 64, 2, 2, 8, 4, true>(U, V, Z, M, N, T, G, s, ks);
+    }
+    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s, ks);
+    return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s, ks);
   }
   // full 64-row tiles and whole 4-stage K sweeps: the deep pipeline; a
   // ragged T takes 64-column tiles (the last one partly recomputed)

@@ -74,11 +74,21 @@ __device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* _
 template <int NLEV, bool SPLIT>
 __global__ __launch_bounds__(256) void input_xform_box(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
-    int tw, int T, long long qstride, int RX, int RY, int nbx, int nby) {
+    int tw, int T, long long qstride, int RX, int RY, int nbx, int nby, int ldc) {
   constexpr int Mn = 1 << NLEV;
   constexpr int Ln = 3 * Mn - 2;
   extern __shared__ float lds[];
-  const int m = blockIdx.y;
+  // V channel mv; in a linear-decomposition plan (ldc > 0) it is
+  // (sub-kernel (cu, cv), input channel m), mv = (cu ldc + cv) M + m, and the
+  // window moves by (3 cu, 3 cv)
+  const int mv = blockIdx.y;
+  int m = mv, sr = 0, sc = 0;
+  if (ldc > 0) {
+    m = mv % M;
+    const int sub = mv / M;
+    sr = 3 * (sub / ldc);
+    sc = 3 * (sub % ldc);
+  }
   int bid = blockIdx.x;
   const int bx = bid % nbx;
   bid /= nbx;
@@ -86,7 +96,7 @@ __global__ __launch_bounds__(256) void input_xform_box(
   const int b = bid / nby;
   const int ty0 = by * RY, tx0 = bx * RX;
   const int BH = (RY - 1) * Mn + Ln, BW = (RX - 1) * Mn + Ln;
-  const int r0 = ty0 * Mn - pad, c0 = tx0 * Mn - pad;
+  const int r0 = ty0 * Mn - pad + sr, c0 = tx0 * Mn - pad + sc;
   const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
   const int nth = blockDim.x;
   for (int e = threadIdx.x; e < BH * BW; e += nth) {
@@ -104,7 +114,7 @@ __global__ __launch_bounds__(256) void input_xform_box(
   if (ty >= th || tx >= tw) return;
   const int t = (b * th + ty) * tw + tx;
   const float* win = lds + ly * Mn * BW + lx * Mn;
-  float4* vb = V + (size_t)m * T + t;
+  float4* vb = V + (size_t)mv * T + t;
   static_assert(NLEV == 1, "the box kernel serves depth 1");
   {
     float X[4][4], Rw[4][4];
@@ -323,7 +333,9 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
   if ((uintptr_t)Vf & 15) return hipErrorInvalidValue;
   // split precision: every quad holds the four values' bf16 (hi, lo) pairs
   const bool split = g.precision == NWG_PRECISION_BF16_SPLIT;
-  const long long qstride = (long long)g.M * g.T;   // float4 quads between consecutive quads
+  // V channels: M, or M c^2 for a linear-decomposition plan (c = ld_c)
+  const long long mv = (long long)g.M * (g.ld_c > 0 ? g.ld_c * g.ld_c : 1);
+  const long long qstride = mv * g.T;   // float4 quads between consecutive quads
   const int T = (int)g.T;
   if (g.n >= 3) {
     const size_t lds = (size_t)16 * (22 * 22 + 1) * sizeof(float);
@@ -364,7 +376,7 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
       hipLaunchKernelGGL(input_xform_d2<false>, grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,
                          g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby);
   } else {
-    if (nparts != 1) return hipErrorInvalidValue;
+    if (nparts != 1 || mv > 65535) return hipErrorInvalidValue;
     const int Mn = 1 << g.n, Ln = 3 * Mn - 2;
     // tiles per work-group: 256, or 64 when that leaves too few work-groups
     int tpb = 256;
@@ -372,7 +384,7 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
       const int RX = g.tw < tpb ? g.tw : tpb;
       int RY = tpb / RX;
       if (RY > g.th) RY = g.th;
-      const long long nwg = (long long)((g.tw + RX - 1) / RX) * ((g.th + RY - 1) / RY) * g.B * g.M;
+      const long long nwg = (long long)((g.tw + RX - 1) / RX) * ((g.th + RY - 1) / RY) * g.B * mv;
       if (nwg >= 1024 || tpb == 64) break;
       tpb = 64;
     }
@@ -381,13 +393,13 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
     if (RY > g.th) RY = g.th;
     const int nbx = (g.tw + RX - 1) / RX, nby = (g.th + RY - 1) / RY;
     const size_t lds = (size_t)((RY - 1) * Mn + Ln) * ((RX - 1) * Mn + Ln) * sizeof(float);
-    dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)g.M);
+    dim3 grid((unsigned)(nbx * nby * g.B), (unsigned)mv);
     if (split)
       hipLaunchKernelGGL((input_xform_box<1, true>), grid, dim3(tpb), lds, s, x, V, g.M, g.H, g.W,
-                         g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby);
+                         g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby, g.ld_c);
     else
       hipLaunchKernelGGL((input_xform_box<1, false>), grid, dim3(tpb), lds, s, x, V, g.M, g.H,
-                         g.W, g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby);
+                         g.W, g.pad, g.th, g.tw, T, qstride, RX, RY, nbx, nby, g.ld_c);
   }
   return hipGetLastError();
 }

@@ -294,6 +294,54 @@ hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U,
   return hipGetLastError();
 }
 
+// Linear decomposition (Sec. II.B): one thread per (output channel n,
+// decomposed channel mv = (cu c + cv) M + m).  Sub-kernel (cu, cv) is
+// w[n][m][3 cu .. 3 cu + 2][3 cv .. 3 cv + 2], zero past r; G of F(2,3) on
+// both axes gives 16 values stored as the 4 quads of a depth-1 plan.
+__global__ __launch_bounds__(256) void kernel_xform_ld(const float* __restrict__ w,
+                                                       float* __restrict__ U, int M, int N, int r,
+                                                       int c, long long nthreads) {
+  const long long id = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (id >= nthreads) return;
+  const int nn = (int)(id % N);
+  const int mv = (int)(id / N);
+  const int m = mv % M, sub = mv / M;
+  const int u0 = 3 * (sub / c), v0 = 3 * (sub % c);
+  const float* __restrict__ wk = w + ((size_t)nn * M + m) * r * r;
+  float k[3][3];
+#pragma unroll
+  for (int u = 0; u < 3; ++u)
+#pragma unroll
+    for (int v = 0; v < 3; ++v)
+      k[u][v] = (u0 + u < r && v0 + v < r) ? wk[(u0 + u) * r + v0 + v] : 0.0f;
+  float rows[3][4];
+#pragma unroll
+  for (int u = 0; u < 3; ++u) g_one(k[u][0], k[u][1], k[u][2], rows[u]);
+  const size_t MN = (size_t)M * c * c * N;
+  float4* ub = reinterpret_cast<float4*>(U) + (size_t)mv * N + nn;
+  float o[4][4];   // [q1r][q1c]
+#pragma unroll
+  for (int q1c = 0; q1c < 4; ++q1c) {
+    float cc[4];
+    g_one(rows[0][q1c], rows[1][q1c], rows[2][q1c], cc);
+#pragma unroll
+    for (int q1r = 0; q1r < 4; ++q1r) o[q1r][q1c] = cc[q1r];
+  }
+#pragma unroll
+  for (int q1r = 0; q1r < 4; ++q1r)
+    ub[(size_t)q1r * MN] = make_float4(o[q1r][0], o[q1r][1], o[q1r][2], o[q1r][3]);
+}
+
+hipError_t launch_kernel_xform_ld(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
+  if (g.ld_c < 1 || ((uintptr_t)U & 15)) return hipErrorInvalidValue;
+  const long long nthreads = (long long)g.N * g.M * g.ld_c * g.ld_c;
+  const long long blocks = (nthreads + 255) / 256;
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(kernel_xform_ld, dim3((unsigned)blocks), dim3(256), 0, s, w, U, g.M, g.N,
+                     g.r, g.ld_c, nthreads);
+  return hipGetLastError();
+}
+
 // Split precision: every fp32 value becomes its packed bf16 (hi, lo) pair,
 // in place (4 values per thread; n need not be a multiple of 4).
 __global__ __launch_bounds__(256) void split_pairs_kernel(float* __restrict__ buf, size_t n) {

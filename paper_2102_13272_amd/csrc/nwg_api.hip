@@ -73,15 +73,82 @@ bool pipeline_allowed(const nwg_plan_info& g) {
 }
 
 // depthwise: M = N = C channels, one r x r kernel each, no channel sum.
-// bytes of the plan's Z buffer: the stage-call Z, or the fused F(3,3)
-// kernel's partial Z9 buffers
+// K slices of a linear-decomposition plan's contraction: its grid has one
+// level-1 group, so with few tiles the M c^2 channels are split (a divisor
+// of M c^2 / 32, up to 64 slices) until there are about 1024 work-groups
+int ld_kslices(const nwg_plan_info& g) {
+  if (g.ld_c <= 0) return 1;
+  const long long mk = (long long)g.M * g.ld_c * g.ld_c;
+  if (mk % 32 || g.N % 64 || g.T < 64) return 1;
+  const long long ntb = g.T % 128 == 0 ? g.T / 128 : (g.T + 63) / 64;
+  const long long wgs = ntb * (g.N / 64);
+  const long long units = mk / 32;
+  int best = 1;
+  for (int sl = 1; sl <= 64 && sl <= units; ++sl) {
+    if (units % sl) continue;
+    best = sl;
+    if (wgs * sl >= 1024) break;
+  }
+  return best;
+}
+
+// bytes of the plan's Z buffer: the stage-call Z, the fused F(3,3) kernel's
+// partial Z9 buffers, or a linear-decomposition plan's K-slice parts
 size_t zalloc_bytes(const nwg_plan_info& g) {
   if (g.fused_input && g.tile == NWG_TILE_F3X3_3X3) return nwg::input_contract5_zbytes(g);
+  if (g.ld_c > 0) return (size_t)ld_kslices(g) * g.yhat_bytes;
   return g.yhat_bytes;
 }
 
 int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile,
                           int depthwise, nwg_plan_info* g);
+
+// Linear decomposition (Sec. II.B) on F(2,3): a depth-1 plan over M c^2
+// contraction channels, c = ceil(r/3) sub-kernels per axis.
+int ld_geometry(int B, int M, int N, int H, int W, int r, int pad, int depthwise,
+                nwg_plan_info* g) {
+  if (depthwise) {
+    set_error("the linear-decomposition tile serves dense plans");
+    return NWG_EUNSUPPORTED;
+  }
+  const long long Ho = (long long)H + 2LL * pad - r + 1, Wo = (long long)W + 2LL * pad - r + 1;
+  if (Ho <= 0 || Wo <= 0) {
+    set_error("kernel %d larger than padded input %dx%d (pad %d)", r, H, W, pad);
+    return NWG_EINVAL;
+  }
+  const int c = (r + 2) / 3;
+  g->B = B; g->M = M; g->N = N; g->H = H; g->W = W; g->r = r; g->pad = pad;
+  g->tile = NWG_TILE_LD_F2X2_3X3;
+  g->Ho = (int)Ho;
+  g->Wo = (int)Wo;
+  g->n = 1;
+  g->m = 2; g->rb = 3; g->l = 4;
+  g->strides[0] = 1;
+  g->Mn = 2;
+  g->Kn = 3 * c;
+  g->Ln = 3 * c + 1;
+  g->th = (int)((Ho + 1) / 2);
+  g->tw = (int)((Wo + 1) / 2);
+  g->T = (long long)B * g->th * g->tw;
+  g->P = 16;
+  g->ld_c = c;
+  const double mk = (double)M * c * c, f = (double)sizeof(float);
+  const double u = f * 16 * mk * N, v = f * 16 * mk * g->T, yh = f * 4 * N * (double)g->T;
+  if (u > 1e13 || v > 1e13 || g->T > 0x7fffffffLL / 64 || mk > 65535) {
+    set_error("workspace too large (or more than 65535 decomposed channels)");
+    return NWG_EUNSUPPORTED;
+  }
+  g->u_bytes = (size_t)u;
+  g->v_bytes = (size_t)v;
+  g->yhat_bytes = (size_t)yh;
+  g->direct_flop = 2.0 * B * N * (double)M * Ho * Wo * r * r;
+  g->ewmm_mults = (long long)(16 * (double)g->T * mk * N);
+  g->contract_flop = 2.0 * 16 * mk * N * (double)g->T;
+  g->pipeline_parts = 1;
+  g->precision = NWG_PRECISION_FP32;
+  g->workspace_bytes = g->u_bytes + g->v_bytes + zalloc_bytes(*g);
+  return NWG_OK;
+}
 
 // NWG_TILE_AUTO: F(3x3,3x3) where it measured faster than F(2x2,3x3) --
 // the fused one-output-channel kernel at depth 2 (unless F(2,3) runs the
@@ -120,10 +187,11 @@ int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int
     set_error("invalid shape B=%d M=%d N=%d H=%d W=%d r=%d pad=%d", B, M, N, H, W, r, pad);
     return NWG_EINVAL;
   }
-  if (tile != NWG_TILE_F2X2_3X3 && tile != NWG_TILE_F3X3_3X3) {
-    set_error("unsupported tile %d (NWG_TILE_F2X2_3X3 or NWG_TILE_F3X3_3X3)", tile);
+  if (tile != NWG_TILE_F2X2_3X3 && tile != NWG_TILE_F3X3_3X3 && tile != NWG_TILE_LD_F2X2_3X3) {
+    set_error("unsupported tile %d", tile);
     return NWG_EUNSUPPORTED;
   }
+  if (tile == NWG_TILE_LD_F2X2_3X3) return ld_geometry(B, M, N, H, W, r, pad, depthwise, g);
   const bool f33 = tile == NWG_TILE_F3X3_3X3;
   if (f33 && depthwise) {
     set_error("depthwise plans use the F(2x2,3x3) tile");
@@ -279,19 +347,26 @@ nwg_plan_info kernel_geometry(const nwg_plan_info& g) {
   return k;
 }
 
+// ks > 1 (linear-decomposition plans, nwg_conv2d only): K slices writing
+// partial Z buffers that launch_sum_parts adds
 hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* V, float* Z,
-                           hipStream_t s) {
+                           hipStream_t s, int ks = 1) {
   if (g.depthwise)
     return g.n == 0 ? nwg::launch_dw_scale(g, V, U, Z, s) : nwg::launch_dw_contract(g, U, V, Z, s);
   if (g.n == 0) return nwg::launch_gemm_depth0(depth0_args(g, U, V, Z), s);
   if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_contract5(g, U, V, Z, s);
-  return nwg::launch_contract_fused(U, V, Z, g.M, g.N, (int)g.T, g.P / 16, s,
-                                    g.precision == NWG_PRECISION_BF16_SPLIT);
+  // linear decomposition: the contraction runs over M c^2 channels
+  const int mk = g.ld_c > 0 ? g.M * g.ld_c * g.ld_c : g.M;
+  const hipError_t e = nwg::launch_contract_fused(U, V, Z, mk, g.N, (int)g.T, g.P / 16, s,
+                                                  g.precision == NWG_PRECISION_BF16_SPLIT, ks);
+  if (e != hipSuccess || ks == 1) return e;
+  return nwg::launch_sum_parts(Z, (size_t)(g.P / 4) * g.N * g.T, ks, s);
 }
 
 // stage launchers by tile (depth >= 1)
 hipError_t launch_kxform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
   if (g.tile == NWG_TILE_F3X3_3X3 && g.n > 0) return nwg::launch_kernel_xform5(g, w, U, s);
+  if (g.tile == NWG_TILE_LD_F2X2_3X3) return nwg::launch_kernel_xform_ld(g, w, U, s);
   const hipError_t e = nwg::launch_kernel_xform(kernel_geometry(g), w, U, s);
   if (e != hipSuccess || g.precision != NWG_PRECISION_BF16_SPLIT) return e;
   // split precision: the fp32 U just written becomes its (hi, lo) pairs
@@ -580,7 +655,7 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
                [&] { return launch_ixform(g, x, p->V, s); });
     if (rc != NWG_OK) return rc;
     rc = timed(p, 2, s, "contraction launch",
-               [&] { return launch_contract(g, p->U, p->V, p->Yh, s); });
+               [&] { return launch_contract(g, p->U, p->V, p->Yh, s, ld_kslices(g)); });
   }
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",

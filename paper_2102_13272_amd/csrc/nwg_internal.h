@@ -147,9 +147,13 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* V, 
 // depth 0: y[b] = U^T x[b]
 hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s);
 // depth >= 1: Z = level-1 A^T of (U^T V per point); G = P / 16 groups
-// split = true: U, V hold bf16 (hi, lo) pairs (precision NWG_PRECISION_BF16_SPLIT)
+// linear decomposition: U [4][M c^2][N][4] from the c x c sub-kernels of w
+hipError_t launch_kernel_xform_ld(const nwg_plan_info& g, const float* w, float* U, hipStream_t s);
+// split = true: U, V hold bf16 (hi, lo) pairs (precision NWG_PRECISION_BF16_SPLIT).
+// ks > 1: K slices of M / ks channels (deep path: M % (32 ks) == 0, N % 64 == 0,
+// T >= 64), slice k writing its partial Z to Z + k G N T 4 floats.
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                                 long long G, hipStream_t s, bool split = false);
+                                 long long G, hipStream_t s, bool split = false, int ks = 1);
 // in place: every fp32 value of buf (n values) -> its packed bf16 (hi, lo) pair
 hipError_t launch_split_pairs(float* buf, size_t n, hipStream_t s);
 // depth 3-4 and N <= 2: x, U -> Z without forming V

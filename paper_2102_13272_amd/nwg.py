@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libnwg.so")
 
 NWG_TILE_F2X2_3X3 = 0
 NWG_TILE_F3X3_3X3 = 1
+NWG_TILE_LD_F2X2_3X3 = 2
 NWG_TILE_AUTO = -1
 NWG_PRECISION_FP32 = 0
 NWG_PRECISION_BF16_SPLIT = 1
@@ -39,7 +40,7 @@ class nwg_plan_info(ctypes.Structure):
         ("ewmm_mults", ctypes.c_longlong), ("direct_flop", ctypes.c_double),
         ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
         ("depthwise", ctypes.c_int), ("fused_conv", ctypes.c_int),
-        ("pipeline_parts", ctypes.c_int), ("precision", ctypes.c_int),
+        ("pipeline_parts", ctypes.c_int), ("precision", ctypes.c_int), ("ld_c", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -180,9 +181,15 @@ class Plan:
         return self.info["tile"] == NWG_TILE_F3X3_3X3 and self.info["n"] > 0
 
     @property
+    def _mv(self):
+        """channels of V (and of the contraction): M, or M c^2 for the linear decomposition"""
+        i = self.info
+        return i["M"] * i["ld_c"] ** 2 if i["ld_c"] else i["M"]
+
+    @property
     def u_shape(self):
         i = self.info
-        mk = 1 if i["depthwise"] else i["M"]
+        mk = 1 if i["depthwise"] else self._mv
         if not i["n"]:
             return (mk, i["N"])
         return (i["P"], mk, i["N"]) if self._f33 else (i["P"] // 4, mk, i["N"], 4)
@@ -190,7 +197,7 @@ class Plan:
     @property
     def v_shape(self):
         i = self.info
-        return (i["P"], i["M"], i["T"]) if self._f33 else (i["P"] // 4, i["M"], i["T"], 4)
+        return (i["P"], i["M"], i["T"]) if self._f33 else (i["P"] // 4, self._mv, i["T"], 4)
 
     @property
     def z_shape(self):

@@ -107,10 +107,16 @@ WORKLOADS = {
         "fanin_normal", 6000,
         note="depthwise 7x7 on 54 channels of 83x83 (the shape of Table I's depth-wise row), "
              "B=8, same padding"),
+    "srcnn_955": Workload(
+        "srcnn_955", [Layer(1, 1, 64, 256, 256, 9, 4), Layer(1, 64, 32, 256, 256, 5, 2),
+                      Layer(1, 32, 1, 256, 256, 5, 2)], "uniform_01", "fanin_normal", 7000,
+        layer_seeds=[7001, 7002, 7003],
+        note="the three SRCNN layers of Table I as one chain, (Cout, Cin, H, W) = "
+             "(64, 1, 256, 256), (32, 64, 256, 256), (1, 32, 256, 256), same padding"),
 }
 
 # Order in which the workloads are listed (1-based index k matches seed 1000*k).
-ORDER = ["c1_r4_valid", "c2_r7", "c3_r13", "c4_sr_stack", "c5_r31", "dw7_pnasnet"]
+ORDER = ["c1_r4_valid", "c2_r7", "c3_r13", "c4_sr_stack", "c5_r31", "dw7_pnasnet", "srcnn_955"]
 
 
 def _draw(rng: np.random.Generator, shape, dist: str, fan_in: int = 1) -> np.ndarray:

@@ -6,6 +6,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 from oracle.nested import base_f23, nesting_levels
@@ -76,7 +77,8 @@ def test_geometry_of_the_five_workloads():
               "c5_r31": [(4, 256, 65536)],
               "c4_sr_stack": [(2, 16384, 256), (0, 65536, 1)] + [(1, 65536, 16)] * 4
               + [(0, 65536, 1), (3, 4096, 4096)],
-              "dw7_pnasnet": [(2, 8 * 21 * 21, 256)]}
+              "dw7_pnasnet": [(2, 8 * 21 * 21, 256)],
+              "srcnn_955": [(3, 32 * 32, 4096), (2, 64 * 64, 256), (2, 64 * 64, 256)]}
     for name, wl in WORKLOADS.items():
         got = []
         for L in wl.layers:
@@ -219,3 +221,46 @@ def test_auto_tile_choice(shape, tile):
     assert g == ref
     d = nwg.plan_geometry_depthwise(4, 16, 64, 64, 9, 4, tile=nwg.NWG_TILE_AUTO)
     assert d["tile"] == nwg.NWG_TILE_F2X2_3X3 and d["depthwise"] == 1
+
+
+@pytest.mark.parametrize("r", [1, 2, 3, 4, 7, 9, 13, 31])
+def test_ld_geometry_and_counts(r):
+    from oracle.counts import ld_per_output
+    B, M, N, H, W = 2, 3, 5, 40, 37
+    pad = (r - 1) // 2
+    g = nwg.plan_geometry(B, M, N, H, W, r, pad, nwg.NWG_TILE_LD_F2X2_3X3)
+    c = -(-r // 3)
+    Ho, Wo = H + 2 * pad - r + 1, W + 2 * pad - r + 1
+    assert g["tile"] == nwg.NWG_TILE_LD_F2X2_3X3 and g["ld_c"] == c
+    assert (g["n"], g["P"], g["Mn"], g["Kn"], g["Ln"]) == (1, 16, 2, 3 * c, 3 * c + 1)
+    assert (g["th"], g["tw"]) == (-(-Ho // 2), -(-Wo // 2))
+    T = B * g["th"] * g["tw"]
+    assert g["T"] == T
+    assert g["u_bytes"] == 4 * 16 * M * c * c * N and g["v_bytes"] == 4 * 16 * M * c * c * T
+    assert g["yhat_bytes"] == 4 * 4 * N * T
+    # Sec. II.B's count, (l/m)^2 ceil(R/r)^2 multiplications per output and channel pair
+    per_out = ld_per_output(2, 3, r)
+    assert g["ewmm_mults"] == per_out * (T * 4) * M * N
+    assert g["fused_input"] == 0 and g["fused_conv"] == 0
+
+
+def test_ld_multiplications_match_the_oracle_loop():
+    from oracle.lindecomp import ld_conv2d
+    from oracle.nested import MultCounter
+    rng = np.random.default_rng(0)
+    B, M, N, H, W, r, pad = 1, 2, 3, 9, 8, 5, 2
+    x = rng.standard_normal((B, M, H, W))
+    w = rng.standard_normal((N, M, r, r))
+    cnt = MultCounter()
+    ld_conv2d(x, w, pad, counter=cnt)
+    g = nwg.plan_geometry(B, M, N, H, W, r, pad, nwg.NWG_TILE_LD_F2X2_3X3)
+    assert g["ewmm_mults"] == cnt.count
+
+
+def test_ld_workspace_holds_the_k_slices():
+    # C3-shaped layer: 7 x 1 column tiles, so the M c^2 = 1600 channels are
+    # cut into slices whose partial Z the plan holds
+    g = nwg.plan_geometry(8, 64, 64, 56, 56, 13, 6, nwg.NWG_TILE_LD_F2X2_3X3)
+    parts = (g["workspace_bytes"] - g["u_bytes"] - g["v_bytes"]) // g["yhat_bytes"]
+    assert parts > 1 and (64 * 25 // 32) % parts == 0
+    assert g["workspace_bytes"] == g["u_bytes"] + g["v_bytes"] + parts * g["yhat_bytes"]

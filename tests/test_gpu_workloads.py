@@ -42,12 +42,17 @@ def test_single_layer_workload_full_oracle(name):
         assert_close(y.cpu().numpy(), direct_conv2d(x, w, L.pad), what=name)
 
 
-def test_sr_stack_per_layer_and_end_to_end():
-    name = "c4_sr_stack"
+@pytest.mark.parametrize("name,tile", [("c4_sr_stack", nwg.NWG_TILE_F2X2_3X3),
+                                       ("c4_sr_stack", nwg.NWG_TILE_AUTO),
+                                       ("srcnn_955", nwg.NWG_TILE_F2X2_3X3),
+                                       ("srcnn_955", nwg.NWG_TILE_AUTO),
+                                       ("srcnn_955", nwg.NWG_TILE_LD_F2X2_3X3)],
+                         ids=["c4_f23", "c4_auto", "srcnn_f23", "srcnn_auto", "srcnn_ld"])
+def test_sr_stack_per_layer_and_end_to_end(name, tile):
     wl = WORKLOADS[name]
     x, ws = make_workload(name)
-    print(f"workload {name}", flush=True)
-    plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad) for L in wl.layers]
+    print(f"workload {name} tile {tile}", flush=True)
+    plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, tile=tile) for L in wl.layers]
     cur_dev = dev(x)
     ref64 = x.astype(np.float64)
     for i, (L, w, plan) in enumerate(zip(wl.layers, ws, plans)):
