@@ -51,6 +51,10 @@ def stage_bytes_flops(info: dict):
     # Z: the contraction's output after (part of) the first output level: P/4
     # values per (n, t) on F(2x2,3x3), 3P/5 on F(3x3,3x3) (the plan's yhat_bytes)
     U, V, Yh = info["u_bytes"], info["v_bytes"], info["yhat_bytes"]
+    if info.get("fused_output"):
+        # input transform, then the output transform that forms the contraction
+        return {"kernel_transform": (w + U, 0.0), "input_transform": (x + V, 0.0),
+                "contraction": (U + V + y, flop)}
     if info.get("fused_conv"):
         # one kernel: x and U in, y out
         return {"kernel_transform": (w + U, 0.0), "contraction": (x + U + y, flop)}

@@ -78,14 +78,16 @@ typedef struct nwg_plan nwg_plan;
  *     without V, fused_input = 1; the plan holds U and per input-channel-group
  *     partial sums of Z instead of V and Z) and the output transform; the
  *     stage calls keep the layouts above, and nwg_input_contract is not
- *     available on this tile.  Otherwise fused_input = fused_conv = 0 and
+ *     available on this tile.  With one or two input channels (and not that
+ *     case) the output transform forms the contraction itself from V and U
+ *     (fused_output = 1, no Z).  Otherwise fused_input = fused_conv = 0 and
  *     pipeline_parts = 1.
  *   NWG_TILE_AUTO: the plan takes F(3x3,3x3) where it measured faster on
- *     MI355X -- one output channel at depth 2 (the fused kernel; unless the
- *     F(2x2,3x3) plan runs the layer in one kernel), or M, N >= 32 and either
- *     r = 8..9 (one nesting level fewer) or r <= 3 -- and F(2x2,3x3)
- *     otherwise (always for depthwise plans and r > 9).  info.tile reports
- *     the tile taken. */
+ *     MI355X -- one output channel at depth 2 or one or two input channels
+ *     (its fused kernels; unless the F(2x2,3x3) plan runs the layer in one
+ *     kernel), or M, N >= 32 and either r = 8..9 (one nesting level fewer)
+ *     or r <= 3 -- and F(2x2,3x3) otherwise (always for depthwise plans and
+ *     r > 9).  info.tile reports the tile taken. */
 /*   NWG_TILE_LD_F2X2_3X3: the linear decomposition of Sec. II.B (Fig. 2),
  *     the method the paper compares nesting with, on the same F(2x2,3x3)
  *     kernels: the r x r kernel is cut into c x c sub-kernels of 3 x 3
@@ -148,6 +150,10 @@ typedef struct nwg_plan_info {
   int precision;                /* NWG_PRECISION_FP32 (default) or NWG_PRECISION_BF16_SPLIT
                                    (nwg_plan_set_precision) */
   int ld_c;                     /* NWG_TILE_LD_F2X2_3X3: sub-kernels per axis c; else 0 */
+  int fused_output;             /* 1: nwg_conv2d forms the contraction inside the output
+                                   transform (F(3x3,3x3), M <= 2, not fused_input): input
+                                   transform, then one kernel V -> y (timed as the
+                                   contraction, index 2); the plan holds no Z */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).

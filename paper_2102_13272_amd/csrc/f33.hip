@@ -623,6 +623,137 @@ __global__ __launch_bounds__(256) void output_xform5(const float* __restrict__ Z
   }
 }
 
+// ---- contraction fused into the output transform: one or two input channels
+// With M <= 2 the contraction is one or two multiply-adds per point, while Z
+// would hold 3P/5 values per (output channel, tile): the output transform
+// forms each point's sum from V and U itself and no Z reaches memory.
+// Thread per (tile, n); U[.][.][n] (P x M values) is staged in LDS and read
+// as broadcasts; V reads are coalesced over the tiles of a wavefront.
+template <int NLEV, int MM>
+__global__ __launch_bounds__(256) void contract_output5(const float* __restrict__ V,
+                                                        const float* __restrict__ U,
+                                                        float* __restrict__ y, int N, int Ho,
+                                                        int Wo, int th, int tw, int T) {
+  constexpr int Mn = NLEV == 1 ? 3 : 9;
+  constexpr int P = NLEV == 1 ? 25 : 625;
+  __shared__ float Us[P * MM];
+  const int n = blockIdx.y;
+  for (int e = threadIdx.x; e < P * MM; e += 256) {
+    const int p = e / MM, m = e - p * MM;
+    Us[e] = U[((size_t)p * MM + m) * N + n];
+  }
+  __syncthreads();
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= T) return;
+  const float* __restrict__ vp = V + t;
+  // the 25 points of group grp, their V values in vv -> level 1 on both axes
+  auto group = [&](int grp, const float (&vv)[25][MM], float (&z9)[3][3]) {
+    float zr[5][3];
+#pragma unroll
+    for (int q1r = 0; q1r < 5; ++q1r) {
+      float a[5];
+#pragma unroll
+      for (int q1c = 0; q1c < 5; ++q1c) {
+        const int p = grp * 25 + q1r * 5 + q1c;
+        float sacc = 0.0f;
+#pragma unroll
+        for (int m = 0; m < MM; ++m) sacc = fmaf(Us[p * MM + m], vv[q1r * 5 + q1c][m], sacc);
+        a[q1c] = sacc;
+      }
+#pragma unroll
+      for (int i1c = 0; i1c < 3; ++i1c) {
+        float sc = 0.0f;
+#pragma unroll
+        for (int q1c = 0; q1c < 5; ++q1c)
+          if (at5(i1c, q1c) != 0.0f) sc = fmaf(at5(i1c, q1c), a[q1c], sc);
+        zr[q1r][i1c] = sc;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 3; ++i)
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        float sacc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 5; ++q)
+          if (at5(i, q) != 0.0f) sacc = fmaf(at5(i, q), zr[q][c], sacc);
+        z9[i][c] = sacc;
+      }
+  };
+  auto load_group = [&](int grp, float (&vv)[25][MM]) {
+#pragma unroll
+    for (int k = 0; k < 25; ++k)
+#pragma unroll
+      for (int m = 0; m < MM; ++m) vv[k][m] = vp[((size_t)(grp * 25 + k) * MM + m) * T];
+  };
+  float out[Mn][Mn];
+  if constexpr (NLEV == 1) {
+    float vv[25][MM];
+    load_group(0, vv);
+    group(0, vv, out);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 9; ++i)
+#pragma unroll
+      for (int k = 0; k < 9; ++k) out[i][k] = 0.0f;
+    // one group per iteration (batching three groups' loads measured slower)
+    constexpr int GB = 1;
+#pragma unroll 1
+    for (int g0 = 0; g0 < 25; g0 += GB) {
+      float vv[GB][25][MM];
+#pragma unroll
+      for (int j = 0; j < GB; ++j) load_group(g0 + j < 25 ? g0 + j : 24, vv[j]);
+#pragma unroll
+      for (int j = 0; j < GB; ++j) {
+        // past the last group (25 is not a multiple of GB): q2r = 5 selects
+        // zero coefficients, the data are group 24's
+        const int grp = g0 + j;
+        const int q2r = grp / 5, q2c = grp - 5 * q2r;
+        float zv[3][3];
+        group(grp < 25 ? grp : 24, vv[j], zv);
+        float cr[3], cc[3];
+#pragma unroll
+        for (int i = 0; i < 3; ++i) {
+          cr[i] = 0.0f;
+          cc[i] = 0.0f;
+#pragma unroll
+          for (int q = 0; q < 5; ++q) {
+            cr[i] = q2r == q ? at5(i, q) : cr[i];
+            cc[i] = q2c == q ? at5(i, q) : cc[i];
+          }
+        }
+#pragma unroll
+        for (int i2r = 0; i2r < 3; ++i2r)
+#pragma unroll
+          for (int i2c = 0; i2c < 3; ++i2c) {
+            const float cf = cr[i2r] * cc[i2c];
+#pragma unroll
+            for (int i1r = 0; i1r < 3; ++i1r)
+#pragma unroll
+              for (int i1c = 0; i1c < 3; ++i1c)
+                out[3 * i2r + i1r][3 * i2c + i1c] =
+                    fmaf(cf, zv[i1r][i1c], out[3 * i2r + i1r][3 * i2c + i1c]);
+          }
+      }
+    }
+  }
+  const int tpi = th * tw;
+  const int b = t / tpi;
+  const int r2 = t - b * tpi;
+  const int ty = r2 / tw, tx = r2 - ty * tw;
+  float* __restrict__ yo = y + ((size_t)b * N + n) * Ho * Wo;
+#pragma unroll
+  for (int i = 0; i < Mn; ++i) {
+    const int row = ty * Mn + i;
+    if (row >= Ho) continue;
+#pragma unroll
+    for (int k = 0; k < Mn; ++k) {
+      const int col = tx * Mn + k;
+      if (col < Wo) yo[(size_t)row * Wo + col] = out[i][k];
+    }
+  }
+}
+
 // ---- fused input transform + contraction: depth 2, one output channel -----
 // x -> Z with no V in memory (the F(3,3) counterpart of the F(2,3) fused
 // kernel): work-group = a box of up to 64 tiles of one image and a group of
@@ -923,6 +1054,30 @@ hipError_t launch_input_contract5(const nwg_plan_info& g, const float* x, const 
   hipLaunchKernelGGL(input_contract5, dim3((unsigned)blocks, (unsigned)c.groups), dim3(320), c.lds,
                      s, x, U, Zp, g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T, c.RX, c.RY, c.nbx,
                      c.nby, c.mper, (size_t)(g.P / 25) * 9 * g.N * g.T);
+  return hipGetLastError();
+}
+
+// The contraction fused into the output transform: F(3,3) plans with one or
+// two input channels that do not take the fused one-output-channel kernel.
+bool contract_output5_applies(const nwg_plan_info& g) {
+  return g.tile == NWG_TILE_F3X3_3X3 && (g.n == 1 || g.n == 2) && g.M <= 2 && !g.depthwise &&
+         !input_contract5_applies(g);
+}
+
+hipError_t launch_contract_output5(const nwg_plan_info& g, const float* V, const float* U,
+                                   float* y, hipStream_t s) {
+  if (!contract_output5_applies(g) || g.N > 65535) return hipErrorInvalidValue;
+  const int T = (int)g.T;
+  dim3 grid((unsigned)((T + 255) / 256), (unsigned)g.N);
+#define NWG_CO5(L, MM)                                                                          \
+  hipLaunchKernelGGL((contract_output5<L, MM>), grid, dim3(256), 0, s, V, U, y, g.N, g.Ho, g.Wo, \
+                     g.th, g.tw, T)
+  if (g.n == 1) {
+    if (g.M == 1) NWG_CO5(1, 1); else NWG_CO5(1, 2);
+  } else {
+    if (g.M == 1) NWG_CO5(2, 1); else NWG_CO5(2, 2);
+  }
+#undef NWG_CO5
   return hipGetLastError();
 }
 

@@ -170,8 +170,8 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
     return NWG_OK;
   }
   const bool big = M >= 32 && N >= 32;
-  const bool pick = (b.fused_input && !a.fused_conv) || (big && a.n > b.n) ||
-                    (big && a.n == 1 && !a.fused_conv);
+  const bool pick = ((b.fused_input || b.fused_output) && !a.fused_conv) ||
+                    (big && a.n > b.n) || (big && a.n == 1 && !a.fused_conv);
   *g = pick ? b : a;
   return NWG_OK;
 }
@@ -274,8 +274,9 @@ int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int
   g->fused_input = (f33 ? nwg::input_contract5_applies(*g) : nwg::input_contract_applies(*g)) ? 1 : 0;
   g->fused_conv =
       !f33 && (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
+  g->fused_output = nwg::contract_output5_applies(*g) ? 1 : 0;
   const bool no_v = g->fused_input || depthwise || g->fused_conv;
-  const bool no_z = g->fused_conv;
+  const bool no_z = g->fused_conv || g->fused_output;
   g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : zalloc_bytes(*g));
   g->pipeline_parts = 1;
   g->precision = NWG_PRECISION_FP32;
@@ -481,7 +482,7 @@ nwg_plan* create_plan(const nwg_plan_info& g) {
     return true;
   };
   const bool no_v = g.fused_input || g.depthwise || g.fused_conv;
-  const bool no_z = g.fused_conv;
+  const bool no_z = g.fused_conv || g.fused_output;
   if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, no_v ? 0 : g.v_bytes, "V") ||
       !alloc(&p->Yh, no_z ? 0 : zalloc_bytes(g), "Yhat")) {
     nwg_plan_destroy(p);
@@ -654,6 +655,9 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
     rc = timed(p, 1, s, "input transform launch",
                [&] { return launch_ixform(g, x, p->V, s); });
     if (rc != NWG_OK) return rc;
+    if (g.fused_output)
+      return timed(p, 2, s, "contraction + output transform launch",
+                   [&] { return nwg::launch_contract_output5(g, p->V, p->U, y, s); });
     rc = timed(p, 2, s, "contraction launch",
                [&] { return launch_contract(g, p->U, p->V, p->Yh, s, ld_kslices(g)); });
   }

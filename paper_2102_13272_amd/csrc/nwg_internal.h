@@ -174,6 +174,11 @@ int input_contract5_parts(const nwg_plan_info& g);
 size_t input_contract5_zbytes(const nwg_plan_info& g);
 hipError_t launch_input_contract5(const nwg_plan_info& g, const float* x, const float* U,
                                   float* Zp, hipStream_t s);
+// F(3,3) with M <= 2 (and not the fused N = 1 kernel): V -> y, the
+// contraction formed inside the output transform (no Z)
+bool contract_output5_applies(const nwg_plan_info& g);
+hipError_t launch_contract_output5(const nwg_plan_info& g, const float* V, const float* U,
+                                   float* y, hipStream_t s);
 // Z[i] += Z[k n + i] for k = 1 .. parts-1 (n floats per part)
 hipError_t launch_sum_parts(float* Z, size_t n, int parts, hipStream_t s);
 // few channels at depth 1-2 (dense): x -> y in one kernel

@@ -41,6 +41,7 @@ class nwg_plan_info(ctypes.Structure):
         ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
         ("depthwise", ctypes.c_int), ("fused_conv", ctypes.c_int),
         ("pipeline_parts", ctypes.c_int), ("precision", ctypes.c_int), ("ld_c", ctypes.c_int),
+        ("fused_output", ctypes.c_int),
     ]
 
     def as_dict(self):

@@ -34,8 +34,13 @@ def _conv(x, w, pad):
     with nwg.Plan(B, M, N, H, W, r, pad, tile=F33) as plan:
         i = plan.info
         assert i["tile"] == F33 and i["fused_conv"] == 0
-        # one output channel at depth 2: the fused kernel, no V
+        # one output channel at depth 2: the fused kernel, no V; else one or
+        # two input channels: the output transform forms the contraction, no Z
         assert i["fused_input"] == (1 if (i["n"] == 2 and N == 1) else 0)
+        fo = 1 if (i["n"] >= 1 and M <= 2 and not i["fused_input"]) else 0
+        assert i["fused_output"] == fo
+        if fo:
+            assert i["workspace_bytes"] == i["u_bytes"] + i["v_bytes"]
         y = torch.full(plan.y_shape, float("nan"), device="cuda")
         plan.conv2d(dev(x), dev(w), y)
         torch.cuda.synchronize()
@@ -70,6 +75,10 @@ E2E = [
     (2, 5, 1, 40, 35, 9, 4),
     (3, 32, 1, 70, 50, 7, 3),
     (1, 33, 1, 100, 90, 9, 0),
+    # one or two input channels: the contraction inside the output transform
+    (1, 1, 64, 70, 66, 9, 4),
+    (2, 2, 33, 31, 29, 3, 1),
+    (1, 2, 5, 44, 40, 7, 3),
 ]
 
 
