@@ -8,7 +8,7 @@
 // kernel is zero.  G of F(2,3) along every axis gives U[p][m][n].
 //
 // Depth <= 2: one thread per (output channel, input channel).  Depth 3 and
-// 4: see kernel_xform_lds below.  Per outer branch the outer levels (3 and
+// 4: see kernel_xform_sep below.  Per outer branch the outer levels (3 and
 // 4) fold the reordered kernel into a 9 x 9 sub-kernel over the digits
 // (k2, k1) of each axis, and the two inner levels (9 -> 16 per axis) run in
 // registers.  U is quad-interleaved, U[p/4][m][n][p%4] (p%4 is
@@ -169,94 +169,129 @@ __global__ __launch_bounds__(256) void kernel_xform(const float* __restrict__ w,
   }
 }
 
-// Depth 3 and 4: a work-group takes 16 consecutive output channels of one
-// input channel; their r x r kernels sit in LDS (odd stride per kernel, so
-// the 16 channels of a quarter-wave read 16 different banks).  Thread
-// (channel, slot) handles the outer branches slot, slot + 16, ...; the
-// quarter-wave's 16 channels store 256 contiguous bytes per quad.
-template <int NLEV>
-__global__ __launch_bounds__(256) void kernel_xform_lds(const float* __restrict__ w,
+// ---- depth 3 and 4, separable: rows of the outer levels first -------------
+// Work-group (NW wavefronts; NW = 4 at depth 3, where there are 4 column
+// branches, and 8 at depth 4, since its LDS allows one work-group per CU):
+// 16 output channels of one input channel, their kernels in LDS
+// zero-padded to K x K (K = 2^(NLEV+1) - 1, odd, so the 16 channels of a
+// quarter-wave sit in different banks).  The outer levels (3, and 4 at depth
+// 4) are applied along the rows for 4 outer row branches at a time
+// (wavefront w takes branch w % 4 of the batch, so its G coefficients are
+// uniform and zero terms are skipped by a scalar branch), leaving
+// Rw[branch][channel][inner row digits (k2, k1)][column] in LDS.  Then
+// wavefront w takes the outer column branches w, w + NW, ... and its lanes
+// (channel, row branch) fold the columns into the 9 x 9 sub-kernel S over the
+// inner digits, run the two inner levels in registers and store 64 quads;
+// the 16 channels of a quarter-wave store 256 contiguous bytes per quad.
+// Every tap index is a compile-time constant.
+template <int NLEV, int NW>
+__global__ __launch_bounds__(NW * 64) void kernel_xform_sep(const float* __restrict__ w,
                                                         float* __restrict__ U, int M, int N,
                                                         int r) {
-  extern __shared__ float wl[];
+  constexpr int K = (2 << NLEV) - 1;        // padded taps per axis
+  constexpr int KS = K * K;                 // LDS stride per channel (odd)
+  constexpr int RS = 9 * K;                 // Rw stride per (branch, channel) (odd)
+  constexpr int NRB = NLEV == 4 ? 16 : 4;   // outer row (and column) branches
+  constexpr int NA = NLEV == 4 ? 3 : 1;     // level-4 digits per axis
+  extern __shared__ float lds[];
+  float* wl = lds;                          // [16][K][K]
+  float* Rw = lds + 16 * KS;                // [4][16][9][K]
   const int m = blockIdx.y;
   const int n0 = blockIdx.x * 16;
-  const int rr = r * r;
-  const int kstride = (rr & 1) ? rr : rr + 1;   // odd stride >= r*r
-  for (int e = threadIdx.x; e < 16 * rr; e += 256) {
-    const int c = e / rr, k = e - c * rr;
+  for (int e = threadIdx.x; e < 16 * KS; e += NW * 64) {
+    const int c = e / KS, k = e - c * KS;
+    const int u = k / K, v = k - u * K;
     const int nn = n0 + c;
-    wl[c * kstride + k] = nn < N ? w[((size_t)nn * M + m) * rr + k] : 0.0f;
+    wl[e] = (nn < N && u < r && v < r) ? w[((size_t)nn * M + m) * r * r + u * r + v] : 0.0f;
   }
-  __syncthreads();
-  const int cl = threadIdx.x & 15, slot = threadIdx.x >> 4;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int cl = lane & 15, rbb = lane >> 4;
   const int nn = n0 + cl;
-  if (nn >= N) return;                      // no barrier below
-  const float* wk = wl + cl * kstride;
   const size_t MN = (size_t)M * N;
-  constexpr int NB = NLEV == 4 ? 256 : 16;  // outer branches
-  for (int branch = slot; branch < NB; branch += 16) {
-    int qr3, qc3, qr4 = 0, qc4 = 0;
-    if (NLEV == 3) {
-      qr3 = branch >> 2;
-      qc3 = branch & 3;
-    } else {
-      qr4 = branch >> 6;
-      qc4 = (branch >> 4) & 3;
-      qr3 = (branch >> 2) & 3;
-      qc3 = branch & 3;
-    }
-    float S[9][9];
+  for (int rb0 = 0; rb0 < NRB; rb0 += 4) {
+    __syncthreads();                        // wl ready / previous batch's Rw read
+    // rows: wavefront w takes row branch rb0 + w % 4; the NW / 4 wavefronts
+    // of a branch share its (channel, column) elements
+    {
+      const int rb = rb0 + (wave & 3);
+      const int qr3 = rb & 3, qr4 = rb >> 2;
+      float* rwb = Rw + (wave & 3) * 16 * RS;
+      for (int e = lane + 64 * (wave >> 2); e < 16 * K; e += 64 * (NW / 4)) {
+        const int c = e / K, col = e - c * K;
+        const float* wc = wl + c * KS + col;
+        float acc[9];
 #pragma unroll
-    for (int i = 0; i < 9; ++i)
+        for (int i = 0; i < 9; ++i) acc[i] = 0.0f;
 #pragma unroll
-      for (int j = 0; j < 9; ++j) S[i][j] = 0.0f;
-    const int n4 = NLEV == 4 ? 3 : 1;
-    for (int a4 = 0; a4 < n4; ++a4)
-      for (int a3 = 0; a3 < 3; ++a3) {
-        float gr = g_coef(qr3, a3);
-        if (NLEV == 4) gr *= g_coef(qr4, a4);
-        if (gr == 0.0f) continue;
-        for (int b4 = 0; b4 < n4; ++b4)
-          for (int b3 = 0; b3 < 3; ++b3) {
-            float gc = gr * g_coef(qc3, b3);
-            if (NLEV == 4) gc *= g_coef(qc4, b4);
-            if (gc == 0.0f) continue;
+        for (int a4 = 0; a4 < NA; ++a4)
+#pragma unroll
+          for (int a3 = 0; a3 < 3; ++a3) {
+            const float cf = (NLEV == 4 ? g_coef(qr4, a4) : 1.0f) * g_coef(qr3, a3);
+            if (cf == 0.0f) continue;       // uniform: scalar branch
 #pragma unroll
             for (int ir = 0; ir < 9; ++ir) {
-              const int tr = canonical_tap<NLEV>(a4, a3, ir / 3, ir % 3);
-              if (tr < 0 || tr >= r) continue;
-#pragma unroll
-              for (int ic = 0; ic < 9; ++ic) {
-                const int tc = canonical_tap<NLEV>(b4, b3, ic / 3, ic % 3);
-                if (tc < 0 || tc >= r) continue;
-                S[ir][ic] += gc * wk[tr * r + tc];
-              }
+              const int tap = canonical_tap<NLEV>(a4, a3, ir / 3, ir % 3);
+              if (tap >= 0) acc[ir] = fmaf(cf, wc[tap * K], acc[ir]);
             }
           }
+#pragma unroll
+        for (int ir = 0; ir < 9; ++ir) rwb[c * RS + ir * K + col] = acc[ir];
       }
-    float4* ub = reinterpret_cast<float4*>(U) + (size_t)branch * 64 * MN + (size_t)m * N + nn;
+    }
+    __syncthreads();
+    // columns: wavefront w takes column branches w, w + NW, ...; lane
+    // (channel cl, row branch rb0 + rbb)
+    const int rb = rb0 + rbb;
+    const int qr3 = rb & 3, qr4 = rb >> 2;
+    const float* rwl = Rw + (rbb * 16 + cl) * RS;
+    for (int cb = wave; cb < NRB; cb += NW) {
+      const int qc3 = cb & 3, qc4 = cb >> 2;
+      float S[9][9];
 #pragma unroll
-    for (int rho = 0; rho < 16; ++rho) {
-      const int q2r = rho >> 2, q1r = rho & 3;
-      float rowv[9];
+      for (int i = 0; i < 9; ++i)
 #pragma unroll
-      for (int ic = 0; ic < 9; ++ic) {
-        float sacc = 0.0f;
+        for (int j = 0; j < 9; ++j) S[i][j] = 0.0f;
 #pragma unroll
-        for (int ir = 0; ir < 9; ++ir) {
-          const float c = g_coef(q2r, ir / 3) * g_coef(q1r, ir % 3);
-          if (c != 0.0f) sacc += c * S[ir][ic];
+      for (int b4 = 0; b4 < NA; ++b4)
+#pragma unroll
+        for (int b3 = 0; b3 < 3; ++b3) {
+          const float cf = (NLEV == 4 ? g_coef(qc4, b4) : 1.0f) * g_coef(qc3, b3);
+          if (cf == 0.0f) continue;         // uniform: scalar branch
+#pragma unroll
+          for (int ic = 0; ic < 9; ++ic) {
+            const int tap = canonical_tap<NLEV>(b4, b3, ic / 3, ic % 3);
+            if (tap < 0) continue;
+#pragma unroll
+            for (int ir = 0; ir < 9; ++ir) S[ir][ic] = fmaf(cf, rwl[ir * K + tap], S[ir][ic]);
+          }
         }
-        rowv[ic] = sacc;
-      }
-      float o[16];
-      g_inner2(rowv, o);
+      if (nn < N) {
+        const int branch = NLEV == 4 ? ((qr4 * 4 + qc4) * 4 + qr3) * 4 + qc3 : qr3 * 4 + qc3;
+        float4* ub = reinterpret_cast<float4*>(U) + (size_t)branch * 64 * MN + (size_t)m * N + nn;
 #pragma unroll
-      for (int q2c = 0; q2c < 4; ++q2c) {
-        const int quad = q2r * 16 + q2c * 4 + q1r;
-        ub[(size_t)quad * MN] =
-            make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+        for (int rho = 0; rho < 16; ++rho) {
+          const int q2r = rho >> 2, q1r = rho & 3;
+          float rowv[9];
+#pragma unroll
+          for (int ic = 0; ic < 9; ++ic) {
+            float sacc = 0.0f;
+#pragma unroll
+            for (int ir = 0; ir < 9; ++ir) {
+              const float c = g_coef(q2r, ir / 3) * g_coef(q1r, ir % 3);
+              if (c != 0.0f) sacc += c * S[ir][ic];
+            }
+            rowv[ic] = sacc;
+          }
+          float o[16];
+          g_inner2(rowv, o);
+#pragma unroll
+          for (int q2c = 0; q2c < 4; ++q2c) {
+            const int quad = q2r * 16 + q2c * 4 + q1r;
+            ub[(size_t)quad * MN] =
+                make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+          }
+        }
       }
     }
   }
@@ -266,21 +301,17 @@ __global__ __launch_bounds__(256) void kernel_xform_lds(const float* __restrict_
 
 hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
   if (g.n >= 3) {
-    const int rr = g.r * g.r;
-    const size_t lds = (size_t)16 * ((rr & 1) ? rr : rr + 1) * sizeof(float);
+    const int K = (2 << g.n) - 1;
+    const size_t lds = ((size_t)16 * K * K + (size_t)64 * 9 * K) * sizeof(float);
     dim3 grid((unsigned)((g.N + 15) / 16), (unsigned)g.M);
-    hipError_t e;
-    if (g.n == 3) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&kernel_xform_lds<3>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(kernel_xform_lds<3>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
-    } else {
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&kernel_xform_lds<4>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(kernel_xform_lds<4>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
-    }
+    const void* fn = g.n == 3 ? reinterpret_cast<const void*>(&kernel_xform_sep<3, 4>)
+                              : reinterpret_cast<const void*>(&kernel_xform_sep<4, 8>);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    if (g.n == 3)
+      hipLaunchKernelGGL((kernel_xform_sep<3, 4>), grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
+    else
+      hipLaunchKernelGGL((kernel_xform_sep<4, 8>), grid, dim3(512), lds, s, w, U, g.M, g.N, g.r);
     return hipGetLastError();
   }
   const long long nthreads = (long long)g.N * g.M;
