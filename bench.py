@@ -369,6 +369,11 @@ def main():
                                       and name == "contraction" else {}),
                                    **({"fused_conv": True} if p.info["fused_conv"]
                                       and name == "contraction" else {})})
+    # split precision: the MFMAs run on bf16 and execute 4 partial products
+    # per algorithmic multiply-add
+    split = args.precision == "bf16_split"
+    peak_mm = PEAK_BF16_MFMA_TFLOPS if split else PEAK_FP32_MFMA_TFLOPS
+    flop_x = 4.0 if split else 1.0
     detail = {}
     for name, s in stages.items():
         sec = s["ms_total"] * 1e-3
@@ -378,18 +383,13 @@ def main():
                         "launches_per_step": s["launches"] // args.steps,
                         "GB_s": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
                         "TFLOP_s": round(tfs, 2),
-                        "mfma_frac": round(tfs / PEAK_FP32_MFMA_TFLOPS, 4),
+                        "mfma_frac": round(flop_x * tfs / peak_mm, 4),
                         "per_layer": s["per_layer"]}
 
     # dominant kernel: largest time share of the step
     dom = max(stages, key=lambda k: stages[k]["ms_total"])
     s = stages[dom]
     avg_s = s["ms_total"] * 1e-3 / s["launches"]
-    # split precision: the MFMAs run on bf16 and execute 4 partial products
-    # per algorithmic multiply-add
-    split = args.precision == "bf16_split"
-    peak_mm = PEAK_BF16_MFMA_TFLOPS if split else PEAK_FP32_MFMA_TFLOPS
-    flop_x = 4.0 if split else 1.0
     ai = flop_x * s["flop"] / s["bytes"] if s["bytes"] else 0.0
     ridge = peak_mm * 1e12 / (PEAK_HBM_GBS * 1e9)
     if dom == "contraction" and ai > ridge:

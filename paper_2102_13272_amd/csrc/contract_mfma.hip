@@ -545,6 +545,142 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
   }
 }
 
+// Persistent form of contract_deep: one work-group per CU slot walks a list
+// of (column tile, row tile, K slice, group) items, and its load pipeline
+// runs on across items, so the first chunks of item i+1 stream in while
+// item i's last chunks are multiplied and its Z tile is stored (a fresh
+// work-group would start with an empty pipeline).  Items are numbered as
+// in contract_deep; XCD x takes a contiguous range of them (the split of
+// xcd_remap) and its wpx work-groups stride through that range, so the
+// tiles that share a group's U and V run together on one L2.
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2))) void contract_deep_persist(
+    const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
+    int N, int T, int ntb, int nnb, int ks, long long G, int wpx) {
+  using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
+  constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
+  static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
+  static_assert(STAGES == 4, "4 stages");
+  __shared__ float4 A0[BKD][BM], A1[BKD][BM], A2[BKD][BM], A3[BKD][BM];
+  __shared__ float4 B0[BKD][BN], B1[BKD][BN], B2[BKD][BN], B3[BKD][BN];
+
+  // this work-group's items: first + i * wpx, i < mine
+  const long long items = (long long)ntb * nnb * ks * G;
+  const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
+  const long long q = items / 8, rem = items % 8;
+  const long long xstart = xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q;
+  const long long xcount = q + (xcd < rem ? 1 : 0);
+  const int mine = xcount > j ? (int)((xcount - 1 - j) / wpx + 1) : 0;
+  if (mine == 0) return;                    // uniform over the work-group
+  const long long first = xstart + j;
+  const int mk = M / ks;
+
+  Tile tile;
+  tile.quadU = (size_t)M * N;
+  tile.quadV = (size_t)M * T;
+  tile.N = N;
+  tile.T = T;
+  tile.nk = mk / BKD;
+  tile.total = 4 * tile.nk;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  tile.wm = wave / WN;
+  tile.wn = wave % WN;
+  tile.lr = lane & 15;
+  tile.lk = lane >> 4;
+#pragma unroll
+  for (int o = 0; o < 4; ++o)
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int jj = 0; jj < FN; ++jj) {
+        tile.out[o][i][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+        tile.acc[o][i][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+
+  // request cursor: item ri, chunk rc (tile.Ug / tile.Vg and the loaders
+  // follow the requested item)
+  int ri = 0, rc = 0;
+  auto set_req_item = [&](int i) {
+    long long b = first + (long long)i * wpx;
+    const int tb = (int)(b % ntb);
+    b /= ntb;
+    const int nb = (int)(b % nnb);
+    b /= nnb;
+    const int sk = (int)(b % ks);
+    const long long g = b / ks;
+    tile.Ug = U + (size_t)(4 * g) * tile.quadU + (size_t)sk * mk * N;
+    tile.Vg = V + (size_t)(4 * g) * tile.quadV + (size_t)sk * mk * T;
+    tile.da.init(N, nb * BM, N);
+    tile.db.init(T, tb * BN, T);
+  };
+  // past the last item the last chunk is requested again, into a buffer
+  // that is never read, so every step issues the same loads
+  auto request_next = [&](float4 (*An)[BM], float4 (*Bn)[BN]) {
+    tile.request(rc, An, Bn);
+    if (rc + 1 < tile.total) {
+      ++rc;
+    } else if (ri + 1 < mine) {
+      ++ri;
+      rc = 0;
+      set_req_item(ri);
+    }
+  };
+  auto step = [&](const float4 (*Ac)[BM], const float4 (*Bc)[BN], float4 (*An)[BM],
+                  float4 (*Bn)[BN]) {
+    wait_vmcnt<(STAGES - 2) * Tile::LPC>();
+    __builtin_amdgcn_s_barrier();
+    request_next(An, Bn);
+    tile.compute(Ac, Bc);
+  };
+
+  set_req_item(0);
+  request_next(A0, B0);
+  request_next(A1, B1);
+  request_next(A2, B2);
+  for (int it = 0; it < mine; ++it) {
+    for (int q1r = 0; q1r < 4; ++q1r) {
+      for (int kb = 0; kb < tile.nk; kb += STAGES) {
+        step(A0, B0, A3, B3);
+        step(A1, B1, A0, B0);
+        step(A2, B2, A1, B1);
+        step(A3, B3, A2, B2);
+      }
+      tile.fold(q1r);
+    }
+    long long b = first + (long long)it * wpx;
+    const int tb = (int)(b % ntb);
+    b /= ntb;
+    const int nb = (int)(b % nnb);
+    b /= nnb;
+    const int sk = (int)(b % ks);
+    const long long g = b / ks;
+    const int n0 = nb * BM, c0 = tb * BN;
+    float4* __restrict__ Zg = Z + (size_t)(sk * G + g) * N * T;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = n0 + tile.wm * WTM + i * 16 + tile.lk * 4 + v;
+#pragma unroll
+        for (int jj = 0; jj < FN; ++jj) {
+          const int col = c0 + tile.wn * WTN + jj * 16 + tile.lr;
+          if (col < T)
+            Zg[(size_t)row * T + col] = make_float4(tile.out[0][i][jj][v], tile.out[1][i][jj][v],
+                                                    tile.out[2][i][jj][v], tile.out[3][i][jj][v]);
+        }
+      }
+    }
+#pragma unroll
+    for (int o = 0; o < 4; ++o)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int jj = 0; jj < FN; ++jj) tile.out[o][i][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  wait_vmcnt<0>();                          // the clamped tail loads land before exit
+}
+
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT = false>
 hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, int T,
                        long long G, hipStream_t s, int ks = 1) {
@@ -555,6 +691,30 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
     return hipErrorInvalidValue;
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
+  if (STAGES == 4) {
+    // one work-group per CU slot when every slot gets at least 4 items
+    static int occ = -1;
+    if (occ < 0) {
+      int b = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+              &b, reinterpret_cast<const void*>(&contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT>),
+              64 * WM * WN, 0) != hipSuccess)
+        b = 0;
+      occ = b;
+    }
+    int dev = 0, cus = 0;
+    if (occ > 0 && hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus >= 8) {
+      const int wpx = cus / 8 * occ;
+      if (blocks >= 4LL * 8 * wpx) {
+        hipLaunchKernelGGL((contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT>),
+                           dim3((unsigned)(8 * wpx)), dim3(64 * WM * WN), 0, s, (const float4*)U,
+                           (const float4*)V, (float4*)Z, M, N, T, ntb, nnb, ks, G, wpx);
+        return hipGetLastError();
+      }
+    }
+  }
   hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES, SPLIT>), dim3((unsigned)blocks),
                      dim3(64 * WM * WN), 0, s, (const float4*)U, (const float4*)V, (float4*)Z,
                      M, N, T, ntb, nnb, ks);

@@ -301,6 +301,7 @@ __global__ __launch_bounds__(NW * 64) void kernel_xform_sep(const float* __restr
 
 hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
   if (g.n >= 3) {
+    if (g.M > 65535) return hipErrorInvalidValue;   // grid.y
     const int K = (2 << g.n) - 1;
     const size_t lds = ((size_t)16 * K * K + (size_t)64 * 9 * K) * sizeof(float);
     dim3 grid((unsigned)((g.N + 15) / 16), (unsigned)g.M);

@@ -164,13 +164,17 @@ def test_fused_input_contract_rejects_other_shapes():
                                          (64, 32, 128, 1), (16, 16, 128, 2), (32, 48, 256, 1),
                                          (128, 64, 192, 1), (64, 96, 256, 1), (128, 32, 128, 2),
                                          # deep path with a ragged last column tile
-                                         (64, 32, 100, 1), (128, 64, 200, 2), (64, 64, 65, 1)])
+                                         (64, 32, 100, 1), (128, 64, 200, 2), (64, 64, 65, 1),
+                                         # persistent deep path (at least 4 tiles per CU slot):
+                                         # 64 x 128 tiles, 4 per slot; 64 x 64 tiles with a
+                                         # ragged last one and 4 or 5 tiles per slot
+                                         (128, 64, 256, 3), (64, 32, 520, 3)])
 def test_contraction_matches_numpy(N, M, T, depth):
     """Z = level-1 A^T of (U[p]^T V[p]) for ragged shapes, through nwg_contract.
 
-    Depth 1 (P = 16) uses B = T images of 2x2 with r = 2 (one tile each);
-    depth 2 (P = 256) uses B = T images of 4x4 with r = 4; depth 0 (r = 1)
-    uses one image of 1 x T, where V is x and the result is y.
+    Depth d = 1, 2, 3 (P = 16, 256, 4096) uses B = T images of 2^d x 2^d with
+    r = 2^d (one tile each); depth 0 (r = 1) uses one image of 1 x T, where V
+    is x and the result is y.
     """
     rng = np.random.default_rng(N * 1000 + M * 10 + T)
     if depth == 0:
@@ -181,13 +185,13 @@ def test_contraction_matches_numpy(N, M, T, depth):
         out = torch.empty((N, T), device="cuda")
         plan.contract(dev(U), dev(V), out)
     else:
-        side = 2 if depth == 1 else 4
+        side = 2 ** depth
         plan = nwg.Plan(T, M, N, side, side, side, 0)
         P = plan.info["P"]
         assert plan.info["n"] == depth and plan.info["T"] == T
         U = rng.standard_normal((P, M, N))
         V = rng.standard_normal((P, M, T))
-        ref = _level1(np.einsum("pmn,pmt->pnt", U, V))
+        ref = _level1(np.matmul(U.transpose(0, 2, 1), V))
         out = torch.empty(plan.z_shape, device="cuda")
         plan.contract(dev(_quads(U)), dev(_quads(V)), out)
     torch.cuda.synchronize()
