@@ -197,11 +197,13 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5_r31")
-    ap.add_argument("--tile", choices=["f23", "f33", "auto", "ld"], default="f23",
+    ap.add_argument("--tile", choices=["f23", "f33", "auto", "ld", "mix"], default="f23",
                     help="Winograd base: F(2x2,3x3) nests (any r <= 31); F(3x3,3x3) nests for "
                          "the dense layers with r <= 9 (others keep F(2x2,3x3)); the "
-                         "library's per-layer choice (NWG_TILE_AUTO); or the linear "
-                         "decomposition on F(2x2,3x3) (Sec. II.B) for the dense layers with r > 1")
+                         "library's per-layer choice (NWG_TILE_AUTO); the linear "
+                         "decomposition on F(2x2,3x3) (Sec. II.B) for the dense layers with "
+                         "r > 1; or the mixed nest (F(2,3) at levels 1-2, F(3,3) above) for "
+                         "the dense layers with r >= 8")
     ap.add_argument("--precision", choices=["fp32", "bf16_split"], default="fp32",
                     help="contraction arithmetic: fp32 MFMA, or the two-term bf16 split of U "
                          "and V on bf16 MFMA with fp32 accumulation (plans that can take it)")
@@ -260,6 +262,8 @@ def main():
             return nwg.NWG_TILE_F3X3_3X3
         if args.tile == "ld" and not L.depthwise and L.r > 1:
             return nwg.NWG_TILE_LD_F2X2_3X3
+        if args.tile == "mix" and not L.depthwise and L.r >= 8:
+            return nwg.NWG_TILE_MIX_F23_F33
         return nwg.NWG_TILE_F2X2_3X3
 
     plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, tile=tile_for(L),
@@ -412,7 +416,8 @@ def main():
            "r": [L.r for L in wl.layers] if len(wl.layers) > 1 else L0.r,
            "pad": [L.pad for L in wl.layers] if len(wl.layers) > 1 else L0.pad,
            "base": [{nwg.NWG_TILE_F3X3_3X3: "F(3x3,3x3)",
-                     nwg.NWG_TILE_LD_F2X2_3X3: "linear decomposition on F(2x2,3x3)"}.get(
+                     nwg.NWG_TILE_LD_F2X2_3X3: "linear decomposition on F(2x2,3x3)",
+                     nwg.NWG_TILE_MIX_F23_F33: "mixed F(2,3)/F(3,3) nest"}.get(
                          p.info["tile"], "F(2x2,3x3)") for p in plans]
                     if args.tile != "f23" else "F(2x2,3x3)",
            "nesting_depth": [p.info["n"] for p in plans],

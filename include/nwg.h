@@ -98,8 +98,26 @@ typedef struct nwg_plan nwg_plan;
  *     K_n = 3c, L_n = 3c + 1, info.ld_c = c) whose contraction runs over
  *     M c^2 channels, channel (cu c + cv) M + m: U [4][M c^2][N][4],
  *     V [4][M c^2][T][4], Z [1][N][T][4].  Dense fp32 plans only. */
+/*   NWG_TILE_MIX_F23_F33: a nest with a different base per level (the level
+ *     recurrence of Sec. III.B does not need the levels to share a base):
+ *     F(2,3) at levels 1 and 2 and F(3,3) (the points above) at the
+ *     info.outer33 = n - 2 levels above them, strides 1, 2, 4, 12:
+ *       r = 8..15:  n = 3, M_n = 12, K_n = 15, L_n = 26, P = 80^2 = 6400;
+ *       r = 16..39: n = 4, M_n = 36, K_n = 39, L_n = 74, P = 400^2 = 160000
+ *     (31 x 31: 123 general multiplications per output, 256 with four F(2,3)
+ *     levels).  Point digits (q_n^row, q_n^col, ..., q_1^row, q_1^col), most
+ *     significant first, radix 5 at the F(3,3) levels and 4 at the F(2,3)
+ *     ones, so the quad layouts of F(2x2,3x3) hold unchanged (U [P/4][M][N][4],
+ *     V [P/4][M][T][4], Z [P/16][N][T][4]).  At n = 4 the input and the
+ *     output transform also use a scratch buffer of max(25*676*M*T,
+ *     25*144*N*T) floats (the level-4 blocks of the input windows, the
+ *     level-3 blocks of the output tiles) that the plan holds after its Z
+ *     (counted in workspace_bytes), also for the stage calls, which therefore
+ *     must not overlap on one plan.
+ *     Dense fp32 plans; r <= 7 gives the F(2x2,3x3) plan (info.tile reports
+ *     it).  No fused paths (fused_input = fused_conv = fused_output = 0). */
 enum { NWG_TILE_F2X2_3X3 = 0, NWG_TILE_F3X3_3X3 = 1, NWG_TILE_LD_F2X2_3X3 = 2,
-       NWG_TILE_AUTO = -1 };
+       NWG_TILE_MIX_F23_F33 = 3, NWG_TILE_AUTO = -1 };
 
 enum {
   NWG_OK = 0,
@@ -154,6 +172,8 @@ typedef struct nwg_plan_info {
                                    transform (F(3x3,3x3), M <= 2, not fused_input): input
                                    transform, then one kernel V -> y (timed as the
                                    contraction, index 2); the plan holds no Z */
+  int outer33;                  /* NWG_TILE_MIX_F23_F33: F(3,3) levels above the two
+                                   F(2,3) levels (1 or 2); else 0 */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only).

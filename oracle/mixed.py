@@ -110,13 +110,17 @@ def split_tap_mixed(k: int, lv: MixedLevels) -> List[int]:
 
 
 def input_matrix(lv: MixedLevels) -> np.ndarray:
+    """(B_1^T (x) ... (x) B_n^T) S, S the 0/1 map of the reordered slice
+    D[a] = x[sum_j s_{j-1} a_j]: column a of the Kronecker product is added
+    to column sum_j s_{j-1} a_j (the product with S, one 1 per row of S)."""
     radices = [b.l for b in lv.bases]
-    S = np.zeros((lv.P1, lv.Ln), dtype=object)
-    S[:] = Fraction(0)
-    for row in range(lv.P1):
-        a = _digits(row, radices)
-        S[row, sum(s * aj for s, aj in zip(lv.strides, a))] = Fraction(1)
-    return _kron([b.BT for b in lv.bases]).dot(S)
+    K = _kron([b.BT for b in lv.bases])
+    out = np.zeros((lv.P1, lv.Ln), dtype=object)
+    out[:] = Fraction(0)
+    for col in range(lv.P1):
+        a = _digits(col, radices)
+        out[:, sum(s * aj for s, aj in zip(lv.strides, a))] += K[:, col]
+    return out
 
 
 def kernel_matrix(lv: MixedLevels) -> np.ndarray:

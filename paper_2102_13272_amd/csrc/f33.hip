@@ -27,38 +27,6 @@ namespace {
 
 constexpr int L5 = 5;
 
-// B^T[q][a], G[q][k], A^T[i][q] of F(3,3)
-__device__ __forceinline__ float bt5(int q, int a) {
-  constexpr float T[5][5] = {{1.0f, -0.5f, -1.0f, 0.5f, 0.0f},
-                             {0.0f, 1.0f, 0.5f, -0.5f, 0.0f},
-                             {0.0f, -1.0f / 3.0f, 0.5f, -1.0f / 6.0f, 0.0f},
-                             {0.0f, -1.0f / 6.0f, 0.0f, 1.0f / 6.0f, 0.0f},
-                             {0.0f, 2.0f, -1.0f, -2.0f, 1.0f}};
-  return T[q][a];
-}
-__device__ __forceinline__ float g5(int q, int k) {
-  constexpr float G[5][3] = {{1.0f, 0.0f, 0.0f}, {1.0f, 1.0f, 1.0f}, {1.0f, -1.0f, 1.0f},
-                             {1.0f, 2.0f, 4.0f}, {0.0f, 0.0f, 1.0f}};
-  return G[q][k];
-}
-__host__ __device__ constexpr float at5(int i, int q) {
-  return i == 0 ? (q == 4 ? 0.0f : 1.0f)
-       : i == 1 ? (q == 0 ? 0.0f : q == 1 ? 1.0f : q == 2 ? -1.0f : q == 3 ? 2.0f : 0.0f)
-                : (q == 0 ? 0.0f : q == 3 ? 4.0f : 1.0f);
-}
-
-// B^T along a length-5 vector
-__device__ __forceinline__ void bt5_vec(const float (&v)[5], float (&o)[5]) {
-#pragma unroll
-  for (int q = 0; q < 5; ++q) {
-    float s = 0.0f;
-#pragma unroll
-    for (int a = 0; a < 5; ++a)
-      if (bt5(q, a) != 0.0f) s = fmaf(bt5(q, a), v[a], s);
-    o[q] = s;
-  }
-}
-
 // ---- kernel transform: one thread per (n, m) --------------------------------
 // w (r x r, zero-padded to K_n x K_n at its end) -> U[p][m][n].  Tap k splits
 // as k = k1 + 3 k2 (k1, k2 < 3).  For every pair of row digits (q2r, q1r)

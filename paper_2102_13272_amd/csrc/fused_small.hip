@@ -335,7 +335,7 @@ hipError_t launch_ics(const nwg_plan_info& g, const float* x, const float4* U, f
 }  // namespace
 
 bool input_contract_applies(const nwg_plan_info& g) {
-  return g.n >= 3 && g.n <= 4 && (g.depthwise || g.N <= 2);
+  return g.tile == NWG_TILE_F2X2_3X3 && g.n >= 3 && g.n <= 4 && (g.depthwise || g.N <= 2);
 }
 
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* Uf,

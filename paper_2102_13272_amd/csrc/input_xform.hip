@@ -33,43 +33,6 @@
 namespace nwg {
 namespace {
 
-// 2D inner transform (two levels per axis) of a 10 x 10 sub-window S and
-// store of its 256 points as 64 quads.  Point digits (q2r, q2c, q1r, q1c),
-// most significant first; vb points at the branch's first quad for this
-// (m, t), qstride is the distance between quads (M*T float4).
-template <bool SPLIT>
-__device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* __restrict__ vb,
-                                             size_t qstride) {
-#pragma unroll
-  for (int q2r = 0; q2r < 4; ++q2r) {
-    // level 2 along rows (stride 2): Z[u][j], u = 0..3
-    float Z[4][10];
-    const int a0 = 2 * bt_tap0(q2r), a1 = 2 * bt_tap1(q2r);
-    const float s0 = bt_sign0(q2r), s1 = bt_sign1(q2r);
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int j = 0; j < 10; ++j) Z[u][j] = s0 * S[u + a0][j] + s1 * S[u + a1][j];
-#pragma unroll
-    for (int q1r = 0; q1r < 4; ++q1r) {
-      // level 1 along rows (stride 1)
-      float R[10];
-      const int b0 = bt_tap0(q1r), b1 = bt_tap1(q1r);
-      const float t0 = bt_sign0(q1r), t1 = bt_sign1(q1r);
-#pragma unroll
-      for (int j = 0; j < 10; ++j) R[j] = t0 * Z[b0][j] + t1 * Z[b1][j];
-      float o[16];
-      bt_inner2(R, o);  // columns: index q2c*4 + q1c
-#pragma unroll
-      for (int q2c = 0; q2c < 4; ++q2c) {
-        const int quad = q2r * 16 + q2c * 4 + q1r;
-        vb[(size_t)quad * qstride] =
-            store_quad<SPLIT>(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
-      }
-    }
-  }
-}
-
 // ---- depth 1: union box of tiles in LDS, one thread per tile ----------------
 template <int NLEV, bool SPLIT>
 __global__ __launch_bounds__(256) void input_xform_box(

@@ -40,26 +40,6 @@ __device__ __forceinline__ int canonical_tap(int k4, int k3, int k2, int k1) {
   return ok ? tap : -1;
 }
 
-// inner G transform (level 2 over k2, level 1 over k1) of a 9-vector
-// indexed k2*3 + k1 -> 16 values indexed q2*4 + q1
-__device__ __forceinline__ void g_inner2(const float (&v)[9], float (&out)[16]) {
-  float h[4][3];
-#pragma unroll
-  for (int k1 = 0; k1 < 3; ++k1) {
-    float o[4];
-    g_one(v[0 * 3 + k1], v[1 * 3 + k1], v[2 * 3 + k1], o);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) h[q][k1] = o[q];
-  }
-#pragma unroll
-  for (int q2 = 0; q2 < 4; ++q2) {
-    float o[4];
-    g_one(h[q2][0], h[q2][1], h[q2][2], o);
-#pragma unroll
-    for (int q1 = 0; q1 < 4; ++q1) out[q2 * 4 + q1] = o[q1];
-  }
-}
-
 template <int NLEV>
 __global__ __launch_bounds__(256) void kernel_xform(const float* __restrict__ w,
                                                     float* __restrict__ U, int M, int N, int r,

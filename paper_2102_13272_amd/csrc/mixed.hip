@@ -1,0 +1,552 @@
+// Nested Winograd with a different base per level (Sec. III.B's level
+// recurrence does not need the levels to share a base; Sec. V.A names F(2,3)
+// and F(3,3) among its bases): F(2,3) at levels 1 and 2, F(3,3) at the NO =
+// 1 or 2 levels above them.  The recurrence s_j = min(M_j, K_j) gives
+// strides 1, 2, 4, 12 and
+//   NO = 1: M_n = 12, K_n = 15, L_n = 26, 20 points per axis (r = 8..15),
+//   NO = 2: M_n = 36, K_n = 39, L_n = 74, 100 points per axis (r = 16..39).
+// A 31 x 31 kernel then costs (400 / 36)^2 = 123 general multiplications per
+// output instead of (256 / 16)^2 = 256 for four F(2,3) levels.
+//
+// Point digits (q_n^row, q_n^col, ..., q_1^row, q_1^col), most significant
+// first, radix 5 at the F(3,3) levels and 4 at the F(2,3) ones.  With the
+// outer branch ob = (q4r, q4c, q3r, q3c) (or (q3r, q3c)) the layouts are the
+// F(2x2,3x3) quad layouts: U[P/4][M][N][4], V[P/4][M][T][4] with quad
+// 64 ob + 16 q2r + 4 q2c + q1r, and Z[P/16][N][T][4] from the unchanged
+// contraction (group g = 16 ob + 4 q2r + q2c after the level-1 A^T).
+//
+//   kernel transform : one thread per (output channel, outer branch), the
+//                      16 output channels of a work-group in LDS, padded to
+//                      K_n x K_n; the outer G rows fold the kernel into the
+//                      9 x 9 sub-kernel of the two F(2,3) levels.
+//   input transform  : 16 tiles x 25 level-3 branches per work-group; at
+//                      NO = 2 the work-group owns one level-4 branch, whose
+//                      B^T rows the LDS fill applies (74 x 74 -> 26 x 26).
+//                      Level 3 runs per output row (rows, then columns), the
+//                      two F(2,3) levels in registers (10 x 10 -> 16 x 16).
+//   output transform : levels 2 and 3 per (tile, level-4 branch, channel)
+//                      into a 12 x 12 block; at NO = 1 that is the output
+//                      tile, at NO = 2 a second kernel applies level 4 to
+//                      the 25 blocks (held in a scratch buffer Z3).
+#include "nwg_internal.h"
+
+namespace nwg {
+namespace {
+
+constexpr int kStride3 = 4, kStride4 = 12;
+
+// Tap of the axis multi-index (k4, k3, k2, k1) (digits < 3, strides 12, 4, 2,
+// 1), or -1 when the multi-index is not the greedy split of its tap
+// (outermost digit first, each as large as allowed).
+template <int NO>
+__host__ __device__ constexpr int mix_tap(int k4, int k3, int k2, int k1) {
+  const int tap = kStride4 * k4 + kStride3 * k3 + 2 * k2 + k1;
+  int rem = tap;
+  int d4 = 0;
+  if (NO == 2) {
+    d4 = rem / kStride4 < 2 ? rem / kStride4 : 2;
+    rem -= kStride4 * d4;
+  }
+  const int d3 = rem / kStride3 < 2 ? rem / kStride3 : 2;
+  rem -= kStride3 * d3;
+  const int d2 = rem / 2 < 2 ? rem / 2 : 2;
+  rem -= 2 * d2;
+  const bool ok = rem == k1 && d2 == k2 && d3 == k3 && (NO == 1 ? k4 == 0 : d4 == k4);
+  return ok ? tap : -1;
+}
+
+// F(3,3) rows with a runtime row index, as selects over compile-time rows
+__device__ __forceinline__ void g5_row(int q, float (&c)[3]) {
+#pragma unroll
+  for (int k = 0; k < 3; ++k) c[k] = 0.0f;
+#pragma unroll
+  for (int qq = 0; qq < 5; ++qq)
+#pragma unroll
+    for (int k = 0; k < 3; ++k) c[k] = q == qq ? g5(qq, k) : c[k];
+}
+__device__ __forceinline__ void bt5_row(int q, float (&c)[5]) {
+#pragma unroll
+  for (int a = 0; a < 5; ++a) c[a] = 0.0f;
+#pragma unroll
+  for (int qq = 0; qq < 5; ++qq)
+#pragma unroll
+    for (int a = 0; a < 5; ++a) c[a] = q == qq ? bt5(qq, a) : c[a];
+}
+
+// ---- kernel transform -------------------------------------------------------
+template <int NO>
+__global__ __launch_bounds__(256) void kernel_xform_mix(const float* __restrict__ w,
+                                                        float* __restrict__ U, int M, int N,
+                                                        int r) {
+  constexpr int K = NO == 2 ? 39 : 15;      // padded taps per axis (odd)
+  constexpr int KS = K * K;
+  constexpr int NA = NO == 2 ? 3 : 1;       // level-4 digits per axis
+  constexpr int NB = NO == 2 ? 625 : 25;    // outer branches
+  extern __shared__ float wl[];             // [16][K][K]
+  const int m = blockIdx.y;
+  const int n0 = blockIdx.x * 16;
+  for (int e = threadIdx.x; e < 16 * KS; e += 256) {
+    const int c = e / KS, k = e - c * KS;
+    const int u = k / K, v = k - u * K;
+    const int nn = n0 + c;
+    wl[e] = (nn < N && u < r && v < r) ? w[((size_t)nn * M + m) * r * r + u * r + v] : 0.0f;
+  }
+  __syncthreads();
+  const int cl = threadIdx.x & 15, slot = threadIdx.x >> 4;
+  const int nn = n0 + cl;
+  if (nn >= N) return;                      // no barrier below
+  const float* wk = wl + cl * KS;
+  const size_t MN = (size_t)M * N;
+  for (int b = slot; b < NB; b += 16) {
+    const int q3c = b % 5, q3r = (b / 5) % 5;
+    const int q4c = NO == 2 ? (b / 25) % 5 : 0, q4r = NO == 2 ? b / 125 : 0;
+    float c3r[3], c3c[3], c4r[3], c4c[3];
+    g5_row(q3r, c3r);
+    g5_row(q3c, c3c);
+    g5_row(q4r, c4r);
+    g5_row(q4c, c4c);
+    float cr[NA][3], cc[NA][3];
+#pragma unroll
+    for (int a4 = 0; a4 < NA; ++a4)
+#pragma unroll
+      for (int a3 = 0; a3 < 3; ++a3) {
+        cr[a4][a3] = (NO == 2 ? c4r[a4] : 1.0f) * c3r[a3];
+        cc[a4][a3] = (NO == 2 ? c4c[a4] : 1.0f) * c3c[a3];
+      }
+    // S[ir][ic] over the inner digits (k2, k1) of each axis
+    float S[9][9];
+#pragma unroll
+    for (int i = 0; i < 9; ++i)
+#pragma unroll
+      for (int j = 0; j < 9; ++j) S[i][j] = 0.0f;
+#pragma unroll
+    for (int a4 = 0; a4 < NA; ++a4)
+#pragma unroll
+      for (int a3 = 0; a3 < 3; ++a3)
+#pragma unroll
+        for (int ir = 0; ir < 9; ++ir) {
+          const int tr = mix_tap<NO>(a4, a3, ir / 3, ir % 3);
+          if (tr < 0) continue;
+          // the row's taps folded over the outer column digits
+          float rowv[9];
+#pragma unroll
+          for (int ic = 0; ic < 9; ++ic) rowv[ic] = 0.0f;
+#pragma unroll
+          for (int b4 = 0; b4 < NA; ++b4)
+#pragma unroll
+            for (int b3 = 0; b3 < 3; ++b3)
+#pragma unroll
+              for (int ic = 0; ic < 9; ++ic) {
+                const int tc = mix_tap<NO>(b4, b3, ic / 3, ic % 3);
+                if (tc < 0) continue;
+                rowv[ic] = fmaf(cc[b4][b3], wk[tr * K + tc], rowv[ic]);
+              }
+#pragma unroll
+          for (int ic = 0; ic < 9; ++ic) S[ir][ic] = fmaf(cr[a4][a3], rowv[ic], S[ir][ic]);
+        }
+    // the two F(2,3) levels: 64 quads of this outer branch
+    float4* ub = reinterpret_cast<float4*>(U) + (size_t)b * 64 * MN + (size_t)m * N + nn;
+#pragma unroll
+    for (int rho = 0; rho < 16; ++rho) {
+      const int q2r = rho >> 2, q1r = rho & 3;
+      float rowv[9];
+#pragma unroll
+      for (int ic = 0; ic < 9; ++ic) {
+        float sacc = 0.0f;
+#pragma unroll
+        for (int ir = 0; ir < 9; ++ir) {
+          const float c = g_coef(q2r, ir / 3) * g_coef(q1r, ir % 3);
+          if (c != 0.0f) sacc += c * S[ir][ic];
+        }
+        rowv[ic] = sacc;
+      }
+      float o[16];
+      g_inner2(rowv, o);
+#pragma unroll
+      for (int q2c = 0; q2c < 4; ++q2c) {
+        const int quad = q2r * 16 + q2c * 4 + q1r;
+        ub[(size_t)quad * MN] =
+            make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+      }
+    }
+  }
+}
+
+// ---- input transform --------------------------------------------------------
+// Depth 4 runs in two kernels.  input_mix_l4 applies the level-4 B^T rows
+// (q4r along the rows, q4c along the columns, stride 12) to every tile's
+// 74 x 74 window: X4[q4][m][t][26 x 26].
+// input_xform_mix then takes 16 tiles x 25 level-3 branches per work-group:
+// the 16 tiles' 26 x 26 blocks (X4 at depth 4, the raw windows at depth 3)
+// go to LDS, level 3 runs per output row (rows, then columns) and the two
+// F(2,3) levels in registers (10 x 10 -> 16 x 16).
+constexpr int kL3 = 26;                     // window side left for levels 1..3
+constexpr int kWS = kL3 * kL3 + 1;          // odd per-tile stride in LDS
+
+__global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
+                                                    float* __restrict__ X4, int M, int H, int W,
+                                                    int pad, int th, int tw, int T) {
+  // work-group (tile t, channel m): the 74 x 74 window, then the level-4 B^T
+  // along the rows (5 row branches of 26 x 74), then along the columns (25
+  // branches of 26 x 26), separably through LDS
+  constexpr int LW = 74, LS = 75;           // window side, odd LDS stride
+  __shared__ float win[LW * LS];
+  __shared__ float rw[5 * kL3 * LS];
+  const int t = blockIdx.x, m = blockIdx.y;
+  const int tpi = th * tw;
+  const int b = t / tpi;
+  const int r2 = t - b * tpi;
+  const int ty = r2 / tw, tx = r2 - ty * tw;
+  const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
+  const int gr0 = ty * 36 - pad, gc0 = tx * 36 - pad;
+  for (int e = threadIdx.x; e < LW * LW; e += 256) {
+    const int i = e / LW, j = e - i * LW;
+    const int gr = gr0 + i, gc = gc0 + j;
+    win[i * LS + j] = (gr >= 0 && gr < H && gc >= 0 && gc < W) ? xp[(size_t)gr * W + gc] : 0.0f;
+  }
+  __syncthreads();
+  // rows: rw[q4r][i][c] = sum_a B^T[q4r][a] win[i + 12 a][c]
+  for (int e = threadIdx.x; e < kL3 * LW; e += 256) {
+    const int i = e / LW, c = e - i * LW;
+    float v[5];
+#pragma unroll
+    for (int a = 0; a < 5; ++a) v[a] = win[(i + kStride4 * a) * LS + c];
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+      float sacc = 0.0f;
+#pragma unroll
+      for (int a = 0; a < 5; ++a)
+        if (bt5(q, a) != 0.0f) sacc = fmaf(bt5(q, a), v[a], sacc);
+      rw[(q * kL3 + i) * LS + c] = sacc;
+    }
+  }
+  __syncthreads();
+  // columns: X4[5 q4r + q4c][m][t][i][j] = sum_b B^T[q4c][b] rw[q4r][i][j + 12 b]
+  const size_t bstride = (size_t)M * T * kL3 * kL3;   // between level-4 branches
+  float* __restrict__ dst = X4 + ((size_t)m * T + t) * kL3 * kL3;
+  for (int e = threadIdx.x; e < 5 * kL3 * kL3; e += 256) {
+    const int q4r = e / (kL3 * kL3), k = e - q4r * (kL3 * kL3);
+    const int i = k / kL3, j = k - i * kL3;
+    float v[5];
+#pragma unroll
+    for (int bb = 0; bb < 5; ++bb) v[bb] = rw[(q4r * kL3 + i) * LS + j + kStride4 * bb];
+#pragma unroll
+    for (int q = 0; q < 5; ++q) {
+      float sacc = 0.0f;
+#pragma unroll
+      for (int bb = 0; bb < 5; ++bb)
+        if (bt5(q, bb) != 0.0f) sacc = fmaf(bt5(q, bb), v[bb], sacc);
+      dst[(size_t)(q4r * 5 + q) * bstride + k] = sacc;
+    }
+  }
+}
+
+// 400 threads: 16 tiles x 25 level-3 branches.  Work-group -> (level-4
+// branch q4 (NO = 2), 16-tile chunk, channel m), q4 fastest, numbered so that
+// each XCD takes a contiguous range.
+template <int NO>
+__global__ __launch_bounds__(400) void input_xform_mix(
+    const float* __restrict__ x, const float* __restrict__ X4, float4* __restrict__ V, int M,
+    int H, int W, int pad, int th, int tw, int T, long long qstride) {
+  constexpr int Mn = NO == 2 ? 36 : 12;
+  constexpr int KK = kL3 * kL3;
+  constexpr int PER = (16 * KK + 399) / 400;  // fill values per thread
+  extern __shared__ float lds[];            // [16][kWS]
+  long long lid;
+  {
+    const long long G = (long long)gridDim.x, i = blockIdx.x;
+    const long long q = G / 8, rem = G % 8, xcd = i % 8, sl = i / 8;
+    lid = xcd < rem ? xcd * (q + 1) + sl : rem * (q + 1) + (xcd - rem) * q + sl;
+  }
+  const int q4 = NO == 2 ? (int)(lid % 25) : 0;
+  const long long rest = NO == 2 ? lid / 25 : lid;
+  const int nchunk = (T + 15) / 16;
+  const int t0 = (int)(rest % nchunk) * 16;
+  const int m = (int)(rest / nchunk);
+  const int nt = T - t0 < 16 ? T - t0 : 16;   // tiles of this chunk
+  // fill: all loads first (PER in flight per thread), then the LDS writes
+  {
+    float v[PER];
+    if (NO == 2) {
+      // X4[q4][m][t0 .. t0 + nt) is contiguous
+      const float* src = X4 + (((size_t)q4 * M + m) * T + t0) * KK;
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int e = threadIdx.x + 400 * u;
+        v[u] = e < nt * KK ? src[e] : 0.0f;
+      }
+    } else {
+      const int tpi = th * tw;
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int e = threadIdx.x + 400 * u;
+        const int tl = e / KK, k = e - tl * KK;
+        const int i = k / kL3, j = k - i * kL3;
+        float val = 0.0f;
+        if (tl < nt) {
+          const int t = t0 + tl;
+          const int b = t / tpi;
+          const int r2 = t - b * tpi;
+          const int ty = r2 / tw, tx = r2 - ty * tw;
+          const int gr = ty * Mn - pad + i, gc = tx * Mn - pad + j;
+          if (gr >= 0 && gr < H && gc >= 0 && gc < W)
+            val = x[(((size_t)b * M + m) * H + gr) * W + gc];
+        }
+        v[u] = val;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = threadIdx.x + 400 * u;
+      if (e < 16 * KK) {
+        const int tl = e / KK, k = e - tl * KK;
+        lds[tl * kWS + k] = v[u];
+      }
+    }
+  }
+  __syncthreads();
+  const int tl = threadIdx.x & 15, slot = threadIdx.x >> 4;   // slot = 5 q3r + q3c
+  const int t = t0 + tl;
+  if (t >= T) return;                       // no barrier below
+  float ca[5], cb[5];
+  bt5_row(slot / 5, ca);
+  bt5_row(slot % 5, cb);
+  const float* win = lds + tl * kWS;
+  // level 3 (stride 4): per output row, the rows' taps, then the columns'
+  float S[10][10];
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    float tr[kL3];
+#pragma unroll
+    for (int c = 0; c < kL3; ++c) {
+      float s = 0.0f;
+#pragma unroll
+      for (int a = 0; a < 5; ++a) s = fmaf(ca[a], win[(i + kStride3 * a) * kL3 + c], s);
+      tr[c] = s;
+    }
+#pragma unroll
+    for (int j = 0; j < 10; ++j) {
+      float s = 0.0f;
+#pragma unroll
+      for (int b = 0; b < 5; ++b) s = fmaf(cb[b], tr[j + kStride3 * b], s);
+      S[i][j] = s;
+    }
+    // one output row at a time: keeps the row's 130 LDS reads from being
+    // hoisted across rows (register pressure)
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  const int ob = q4 * 25 + slot;
+  inner2_store<false>(S, V + (size_t)ob * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+}
+
+// ---- output transform -------------------------------------------------------
+// Levels 2 and 3: thread (tile t, level-4 branch q4, channel n), lanes on
+// consecutive tiles.  Over the 25 level-3 branches, level2_reduce gives each
+// branch's 4 x 4 block and the level-3 A^T accumulates the 12 x 12 block
+// acc[i3r][i3c][rr][cc] (row 4 i3r + rr, column 4 i3c + cc).  FINAL (NO = 1):
+// that block is the output tile; else it goes to Z3[q4][e][n][t], e = 12 row
+// + column.
+template <bool FINAL>
+__global__ __launch_bounds__(64) void output_xform_mix23(
+    const float4* __restrict__ Z, float* __restrict__ out, int N, int Ho, int Wo, int th, int tw,
+    int T, long long gstride) {
+  const int t = blockIdx.x * 64 + threadIdx.x;
+  const int q4 = blockIdx.y;
+  const int n = blockIdx.z;
+  if (t >= T) return;
+  float acc[3][3][16];
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int b = 0; b < 3; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
+  const float4* zt = Z + (size_t)n * T + t;
+  // a runtime loop over the 25 branches (one branch's 16 quads in flight at
+  // a time: the 144 accumulators leave no room for more)
+#pragma unroll 1
+  for (int q3 = 0; q3 < 25; ++q3) {
+    const int q3r = q3 / 5, q3c = q3 - 5 * q3r;
+    const int ob = q4 * 25 + q3;
+    float po[4][4];
+    level2_reduce(zt + (size_t)ob * 16 * gstride, (size_t)gstride, po);
+    float cr[3], cc[3];
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      cr[i] = at5(i, q3r);
+      cc[i] = at5(i, q3c);
+    }
+#pragma unroll
+    for (int i3r = 0; i3r < 3; ++i3r)
+#pragma unroll
+      for (int i3c = 0; i3c < 3; ++i3c) {
+        const float c = cr[i3r] * cc[i3c];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i3r][i3c][e] = fmaf(c, po[e >> 2][e & 3], acc[i3r][i3c][e]);
+      }
+  }
+  if constexpr (FINAL) {
+    const int tpi = th * tw;
+    const int b = t / tpi;
+    const int r2 = t - b * tpi;
+    const int ty = r2 / tw, tx = r2 - ty * tw;
+    float* yo = out + ((size_t)b * N + n) * Ho * Wo;
+#pragma unroll
+    for (int i3r = 0; i3r < 3; ++i3r)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int row = ty * 12 + 4 * i3r + rr;
+        if (row >= Ho) continue;
+#pragma unroll
+        for (int i3c = 0; i3c < 3; ++i3c)
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const int col = tx * 12 + 4 * i3c + cc;
+            if (col < Wo) yo[(size_t)row * Wo + col] = acc[i3r][i3c][rr * 4 + cc];
+          }
+      }
+  } else {
+    const size_t es = (size_t)N * T;        // between consecutive e
+    float* z3 = out + (size_t)q4 * 144 * es + (size_t)n * T + t;
+#pragma unroll
+    for (int i3r = 0; i3r < 3; ++i3r)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+        for (int i3c = 0; i3c < 3; ++i3c)
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const int e = (4 * i3r + rr) * 12 + 4 * i3c + cc;
+            z3[(size_t)e * es] = acc[i3r][i3c][rr * 4 + cc];
+          }
+  }
+}
+
+// Level 4 (NO = 2): thread (tile t, block element e, channel n) combines the
+// 25 level-4 branches of Z3 into the 3 x 3 blocks of the 36 x 36 tile.
+__global__ __launch_bounds__(64) void output_xform_mix4(const float* __restrict__ Z3,
+                                                        float* __restrict__ y, int N, int Ho,
+                                                        int Wo, int th, int tw, int T) {
+  const int t = blockIdx.x * 64 + threadIdx.x;
+  const int e = blockIdx.y;
+  const int n = blockIdx.z;
+  if (t >= T) return;
+  const size_t es = (size_t)N * T;
+  const float* zp = Z3 + (size_t)e * es + (size_t)n * T + t;
+  float h[5][3];                            // [q4r][i4c]
+#pragma unroll
+  for (int q4r = 0; q4r < 5; ++q4r) {
+    float v[5];
+#pragma unroll
+    for (int q4c = 0; q4c < 5; ++q4c) v[q4c] = zp[(size_t)(q4r * 5 + q4c) * 144 * es];
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      float s = 0.0f;
+#pragma unroll
+      for (int q = 0; q < 5; ++q)
+        if (at5(i, q) != 0.0f) s = fmaf(at5(i, q), v[q], s);
+      h[q4r][i] = s;
+    }
+  }
+  const int tpi = th * tw;
+  const int b = t / tpi;
+  const int r2 = t - b * tpi;
+  const int ty = r2 / tw, tx = r2 - ty * tw;
+  const int er = e / 12, ec = e - er * 12;
+  float* yo = y + ((size_t)b * N + n) * Ho * Wo;
+#pragma unroll
+  for (int i4r = 0; i4r < 3; ++i4r) {
+    const int row = ty * 36 + 12 * i4r + er;
+    if (row >= Ho) continue;
+#pragma unroll
+    for (int i4c = 0; i4c < 3; ++i4c) {
+      const int col = tx * 36 + 12 * i4c + ec;
+      if (col >= Wo) continue;
+      float s = 0.0f;
+#pragma unroll
+      for (int q = 0; q < 5; ++q)
+        if (at5(i4r, q) != 0.0f) s = fmaf(at5(i4r, q), h[q][i4c], s);
+      yo[(size_t)row * Wo + col] = s;
+    }
+  }
+}
+
+}  // namespace
+
+int mix_outer_levels(const nwg_plan_info& g) {
+  return g.tile == NWG_TILE_MIX_F23_F33 ? g.n - 2 : 0;
+}
+
+size_t mix_scratch_bytes(const nwg_plan_info& g) {
+  if (mix_outer_levels(g) != 2) return 0;
+  const size_t z3 = (size_t)25 * 144 * g.N * g.T * sizeof(float);
+  const size_t x4 = (size_t)25 * g.M * g.T * kL3 * kL3 * sizeof(float);
+  return z3 > x4 ? z3 : x4;
+}
+
+hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float* U,
+                                   hipStream_t s) {
+  const int no = mix_outer_levels(g);
+  if ((no != 1 && no != 2) || g.M > 65535 || ((uintptr_t)U & 15)) return hipErrorInvalidValue;
+  const int K = no == 2 ? 39 : 15;
+  const size_t lds = (size_t)16 * K * K * sizeof(float);
+  dim3 grid((unsigned)((g.N + 15) / 16), (unsigned)g.M);
+  const void* fn = no == 2 ? reinterpret_cast<const void*>(&kernel_xform_mix<2>)
+                           : reinterpret_cast<const void*>(&kernel_xform_mix<1>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  if (no == 2)
+    hipLaunchKernelGGL(kernel_xform_mix<2>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
+  else
+    hipLaunchKernelGGL(kernel_xform_mix<1>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
+  return hipGetLastError();
+}
+
+hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float* Vf,
+                                  float* X4, hipStream_t s) {
+  const int no = mix_outer_levels(g);
+  if ((no != 1 && no != 2) || ((uintptr_t)Vf & 15) || (no == 2 && !X4))
+    return hipErrorInvalidValue;
+  float4* V = reinterpret_cast<float4*>(Vf);
+  const long long qstride = (long long)g.M * g.T;
+  const long long nwg = (g.T + 15) / 16 * g.M * (no == 2 ? 25 : 1);
+  if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
+  const size_t lds = (size_t)16 * kWS * sizeof(float);
+  if (no == 2) {
+    if (g.M > 65535) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(input_mix_l4, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x, X4,
+                       g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(input_xform_mix<2>, dim3((unsigned)nwg), dim3(400), lds, s, x, X4, V, g.M,
+                       g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride);
+  } else {
+    hipLaunchKernelGGL(input_xform_mix<1>, dim3((unsigned)nwg), dim3(400), lds, s, x, X4, V, g.M,
+                       g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_output_xform_mix(const nwg_plan_info& g, const float* Zf, float* y,
+                                   float* Z3, hipStream_t s) {
+  const int no = mix_outer_levels(g);
+  if ((no != 1 && no != 2) || ((uintptr_t)Zf & 15) || g.N > 65535) return hipErrorInvalidValue;
+  const float4* Z = reinterpret_cast<const float4*>(Zf);
+  const long long gstride = (long long)g.N * g.T;
+  const unsigned tb = (unsigned)((g.T + 63) / 64);
+  if (no == 1) {
+    hipLaunchKernelGGL(output_xform_mix23<true>, dim3(tb, 1, (unsigned)g.N), dim3(64), 0, s, Z, y,
+                       g.N, g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride);
+    return hipGetLastError();
+  }
+  if (!Z3) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(output_xform_mix23<false>, dim3(tb, 25, (unsigned)g.N), dim3(64), 0, s, Z,
+                     Z3, g.N, g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(output_xform_mix4, dim3(tb, 144, (unsigned)g.N), dim3(64), 0, s, Z3, y, g.N,
+                     g.Ho, g.Wo, g.th, g.tw, (int)g.T);
+  return hipGetLastError();
+}
+
+}  // namespace nwg

@@ -97,6 +97,8 @@ int ld_kslices(const nwg_plan_info& g) {
 size_t zalloc_bytes(const nwg_plan_info& g) {
   if (g.fused_input && g.tile == NWG_TILE_F3X3_3X3) return nwg::input_contract5_zbytes(g);
   if (g.ld_c > 0) return (size_t)ld_kslices(g) * g.yhat_bytes;
+  // mixed nest at depth 4: Z, then the scratch of its transforms
+  if (g.tile == NWG_TILE_MIX_F23_F33) return g.yhat_bytes + nwg::mix_scratch_bytes(g);
   return g.yhat_bytes;
 }
 
@@ -187,11 +189,24 @@ int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int
     set_error("invalid shape B=%d M=%d N=%d H=%d W=%d r=%d pad=%d", B, M, N, H, W, r, pad);
     return NWG_EINVAL;
   }
-  if (tile != NWG_TILE_F2X2_3X3 && tile != NWG_TILE_F3X3_3X3 && tile != NWG_TILE_LD_F2X2_3X3) {
+  if (tile != NWG_TILE_F2X2_3X3 && tile != NWG_TILE_F3X3_3X3 && tile != NWG_TILE_LD_F2X2_3X3 &&
+      tile != NWG_TILE_MIX_F23_F33) {
     set_error("unsupported tile %d", tile);
     return NWG_EUNSUPPORTED;
   }
   if (tile == NWG_TILE_LD_F2X2_3X3) return ld_geometry(B, M, N, H, W, r, pad, depthwise, g);
+  const bool mix = tile == NWG_TILE_MIX_F23_F33;
+  if (mix && depthwise) {
+    set_error("the mixed F(2,3)/F(3,3) nest serves dense plans");
+    return NWG_EUNSUPPORTED;
+  }
+  // up to 7 taps the mixed nest has only its two F(2,3) levels
+  if (mix && r <= 7)
+    return compute_geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F2X2_3X3, 0, g);
+  if (mix && r > 39) {
+    set_error("kernel size %d exceeds the mixed nest's 39 taps", r);
+    return NWG_EUNSUPPORTED;
+  }
   const bool f33 = tile == NWG_TILE_F3X3_3X3;
   if (f33 && depthwise) {
     set_error("depthwise plans use the F(2x2,3x3) tile");
@@ -204,15 +219,19 @@ int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int
   }
   // base F(m, rb): F(2,3) or F(3,3); F(3,3) is kept to depth 2 (r <= 9),
   // where its fp32 error stays near 1e-6
+  // (the mixed nest: F(2,3) at levels 1-2, F(3,3) above)
   const int m = f33 ? 3 : nwg::kOut, rb = nwg::kTaps, l = m + rb - 1;
   const int max_depth = f33 ? 2 : NWG_MAX_DEPTH;
+  auto level_m = [&](int j) { return mix && j >= 2 ? 3 : m; };   // level j + 1
   int n = 0, Mn = 1, Kn = 1;
   int strides[NWG_MAX_DEPTH + 1] = {0};
+  long long P1 = 1;   // Winograd points per axis
   if (r > 1) {
     strides[0] = 1;
     n = 1;
     Mn = m;
     Kn = rb;
+    P1 = l;
     while (Kn < r) {
       const int s = Mn < Kn ? Mn : Kn;
       if (n >= max_depth) {
@@ -220,9 +239,11 @@ int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int
                   max_depth, f33 ? 9 : 31);
         return NWG_EUNSUPPORTED;
       }
+      const int mj = level_m(n);
       strides[n] = s;
-      Mn += s * (m - 1);
+      Mn += s * (mj - 1);
       Kn += s * (rb - 1);
+      P1 *= mj + rb - 1;
       ++n;
     }
   }
@@ -241,9 +262,9 @@ int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int
   g->th = (int)((Ho + Mn - 1) / Mn);
   g->tw = (int)((Wo + Mn - 1) / Mn);
   g->T = (long long)B * g->th * g->tw;
-  long long P = 1;
-  for (int j = 0; j < 2 * n; ++j) P *= l;
+  const long long P = P1 * P1;
   g->P = P;
+  g->outer33 = mix ? n - 2 : 0;
   const double f = (double)sizeof(float);
   g->direct_flop = 2.0 * B * N * (double)Mk * Ho * Wo * r * r;
   if (n == 0) {
@@ -273,7 +294,7 @@ int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int
   // x -> y, neither V nor Z.
   g->fused_input = (f33 ? nwg::input_contract5_applies(*g) : nwg::input_contract_applies(*g)) ? 1 : 0;
   g->fused_conv =
-      !f33 && (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
+      !f33 && !mix && (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
   g->fused_output = nwg::contract_output5_applies(*g) ? 1 : 0;
   const bool no_v = g->fused_input || depthwise || g->fused_conv;
   const bool no_z = g->fused_conv || g->fused_output;
@@ -367,19 +388,29 @@ hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* 
 // stage launchers by tile (depth >= 1)
 hipError_t launch_kxform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
   if (g.tile == NWG_TILE_F3X3_3X3 && g.n > 0) return nwg::launch_kernel_xform5(g, w, U, s);
+  if (g.tile == NWG_TILE_MIX_F23_F33) return nwg::launch_kernel_xform_mix(g, w, U, s);
   if (g.tile == NWG_TILE_LD_F2X2_3X3) return nwg::launch_kernel_xform_ld(g, w, U, s);
   const hipError_t e = nwg::launch_kernel_xform(kernel_geometry(g), w, U, s);
   if (e != hipSuccess || g.precision != NWG_PRECISION_BF16_SPLIT) return e;
   // split precision: the fp32 U just written becomes its (hi, lo) pairs
   return nwg::launch_split_pairs(U, g.u_bytes / sizeof(float), s);
 }
-hipError_t launch_ixform(const nwg_plan_info& g, const float* x, float* V, hipStream_t s) {
+hipError_t launch_ixform(const nwg_plan_info& g, const float* x, float* V, float* scratch,
+                         hipStream_t s) {
   if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_input_xform5(g, x, V, s);
+  if (g.tile == NWG_TILE_MIX_F23_F33) return nwg::launch_input_xform_mix(g, x, V, scratch, s);
   return nwg::launch_input_xform(g, x, V, s);
 }
-hipError_t launch_oxform(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s) {
+// Z3 (and X4 above): the mixed nest's depth-4 scratch (the plan's, after its Z)
+hipError_t launch_oxform(const nwg_plan_info& g, const float* Z, float* y, float* Z3,
+                         hipStream_t s) {
   if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_output_xform5(g, Z, y, s);
+  if (g.tile == NWG_TILE_MIX_F23_F33) return nwg::launch_output_xform_mix(g, Z, y, Z3, s);
   return nwg::launch_output_xform(g, Z, y, s);
+}
+float* mix_scratch(const nwg_plan* p) {
+  return p->Yh && nwg::mix_scratch_bytes(p->info) ? p->Yh + p->info.yhat_bytes / sizeof(float)
+                                                   : nullptr;
 }
 
 // Input transform and contraction in `parts` pieces on two streams: part k's
@@ -437,7 +468,9 @@ int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, fl
 
 extern "C" {
 
-const char* nwg_version(void) { return "nwg 0.2 (nested F(2x2,3x3) and F(3x3,3x3), gfx950)"; }
+const char* nwg_version(void) {
+  return "nwg 0.3 (nested F(2x2,3x3), F(3x3,3x3) and mixed F(2,3)/F(3,3), gfx950)";
+}
 
 const char* nwg_last_error(void) { return g_last_error.c_str(); }
 
@@ -555,7 +588,7 @@ int nwg_input_transform(const nwg_plan* p, const float* x, float* V, void* strea
     set_error("depth 0 (r = 1) has no input transform");
     return NWG_EINVAL;
   }
-  return check_hip(launch_ixform(p->info, x, V, (hipStream_t)stream),
+  return check_hip(launch_ixform(p->info, x, V, mix_scratch(p), (hipStream_t)stream),
                    "input transform launch");
 }
 
@@ -593,7 +626,7 @@ int nwg_output_transform(const nwg_plan* p, const float* Yh, float* y, void* str
     set_error("depth 0 (r = 1) has no output transform");
     return NWG_EINVAL;
   }
-  return check_hip(launch_oxform(p->info, Yh, y, (hipStream_t)stream),
+  return check_hip(launch_oxform(p->info, Yh, y, mix_scratch(p), (hipStream_t)stream),
                    "output transform launch");
 }
 
@@ -653,7 +686,7 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
     rc = run_pipelined(p, x, s);
   } else {
     rc = timed(p, 1, s, "input transform launch",
-               [&] { return launch_ixform(g, x, p->V, s); });
+               [&] { return launch_ixform(g, x, p->V, mix_scratch(p), s); });
     if (rc != NWG_OK) return rc;
     if (g.fused_output)
       return timed(p, 2, s, "contraction + output transform launch",
@@ -663,7 +696,7 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
   }
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",
-               [&] { return launch_oxform(g, p->Yh, y, s); });
+               [&] { return launch_oxform(g, p->Yh, y, mix_scratch(p), s); });
 }
 
 int nwg_plan_set_precision(nwg_plan* p, int precision) {

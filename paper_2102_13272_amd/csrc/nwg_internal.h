@@ -125,6 +125,127 @@ __host__ __device__ constexpr float at_coef(int i, int q) {
                 : (q == 0 ? 0.0f : (q == 1 ? 1.0f : -1.0f));
 }
 
+// ---- helpers shared by the F(2,3) kernels ----------------------------------
+
+// inner G transform (level 2 over k2, level 1 over k1) of a 9-vector
+// indexed k2*3 + k1 -> 16 values indexed q2*4 + q1
+__device__ __forceinline__ void g_inner2(const float (&v)[9], float (&out)[16]) {
+  float h[4][3];
+#pragma unroll
+  for (int k1 = 0; k1 < 3; ++k1) {
+    float o[4];
+    g_one(v[0 * 3 + k1], v[1 * 3 + k1], v[2 * 3 + k1], o);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) h[q][k1] = o[q];
+  }
+#pragma unroll
+  for (int q2 = 0; q2 < 4; ++q2) {
+    float o[4];
+    g_one(h[q2][0], h[q2][1], h[q2][2], o);
+#pragma unroll
+    for (int q1 = 0; q1 < 4; ++q1) out[q2 * 4 + q1] = o[q1];
+  }
+}
+
+// Level 2 for one branch: 16 quads (q2r, q2c) -> 4x4 partial tile
+// po[rr][cc], rr = i1r + 2*i2r, cc = i1c + 2*i2c.  zb points at the branch's
+// first quad for this (n, t); gstride is the distance between groups.
+__device__ __forceinline__ void level2_reduce(const float4* __restrict__ zb, size_t gstride,
+                                              float (&po)[4][4]) {
+  float4 v[4][4];
+#pragma unroll
+  for (int q2r = 0; q2r < 4; ++q2r)
+#pragma unroll
+    for (int q2c = 0; q2c < 4; ++q2c) v[q2r][q2c] = zb[(size_t)(q2r * 4 + q2c) * gstride];
+  // along columns: h[q2r][i2c] (float4 over (i1r, i1c))
+  float4 h[4][2];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    h[q][0] = v[q][0] + v[q][1] + v[q][2];
+    h[q][1] = v[q][1] - v[q][2] - v[q][3];
+  }
+#pragma unroll
+  for (int i2c = 0; i2c < 2; ++i2c) {
+    const float4 e0 = h[0][i2c] + h[1][i2c] + h[2][i2c];   // i2r = 0
+    const float4 e1 = h[1][i2c] - h[2][i2c] - h[3][i2c];   // i2r = 1
+    po[0][2 * i2c + 0] = e0.x;  po[0][2 * i2c + 1] = e0.y;
+    po[1][2 * i2c + 0] = e0.z;  po[1][2 * i2c + 1] = e0.w;
+    po[2][2 * i2c + 0] = e1.x;  po[2][2 * i2c + 1] = e1.y;
+    po[3][2 * i2c + 0] = e1.z;  po[3][2 * i2c + 1] = e1.w;
+  }
+}
+
+// 2D inner transform (two levels per axis) of a 10 x 10 sub-window S and
+// store of its 256 points as 64 quads.  Point digits (q2r, q2c, q1r, q1c),
+// most significant first; vb points at the branch's first quad for this
+// (m, t), qstride is the distance between quads (M*T float4).
+template <bool SPLIT>
+__device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* __restrict__ vb,
+                                             size_t qstride) {
+#pragma unroll
+  for (int q2r = 0; q2r < 4; ++q2r) {
+    // level 2 along rows (stride 2): Z[u][j], u = 0..3
+    float Z[4][10];
+    const int a0 = 2 * bt_tap0(q2r), a1 = 2 * bt_tap1(q2r);
+    const float s0 = bt_sign0(q2r), s1 = bt_sign1(q2r);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < 10; ++j) Z[u][j] = s0 * S[u + a0][j] + s1 * S[u + a1][j];
+#pragma unroll
+    for (int q1r = 0; q1r < 4; ++q1r) {
+      // level 1 along rows (stride 1)
+      float R[10];
+      const int b0 = bt_tap0(q1r), b1 = bt_tap1(q1r);
+      const float t0 = bt_sign0(q1r), t1 = bt_sign1(q1r);
+#pragma unroll
+      for (int j = 0; j < 10; ++j) R[j] = t0 * Z[b0][j] + t1 * Z[b1][j];
+      float o[16];
+      bt_inner2(R, o);  // columns: index q2c*4 + q1c
+#pragma unroll
+      for (int q2c = 0; q2c < 4; ++q2c) {
+        const int quad = q2r * 16 + q2c * 4 + q1r;
+        vb[(size_t)quad * qstride] =
+            store_quad<SPLIT>(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+      }
+    }
+  }
+}
+
+// ---- F(3,3): B^T, G, A^T (Toom-Cook points 0, 1, -1, 2, infinity) ----------
+
+// B^T[q][a], G[q][k], A^T[i][q] of F(3,3)
+__device__ __forceinline__ float bt5(int q, int a) {
+  constexpr float T[5][5] = {{1.0f, -0.5f, -1.0f, 0.5f, 0.0f},
+                             {0.0f, 1.0f, 0.5f, -0.5f, 0.0f},
+                             {0.0f, -1.0f / 3.0f, 0.5f, -1.0f / 6.0f, 0.0f},
+                             {0.0f, -1.0f / 6.0f, 0.0f, 1.0f / 6.0f, 0.0f},
+                             {0.0f, 2.0f, -1.0f, -2.0f, 1.0f}};
+  return T[q][a];
+}
+__device__ __forceinline__ float g5(int q, int k) {
+  constexpr float G[5][3] = {{1.0f, 0.0f, 0.0f}, {1.0f, 1.0f, 1.0f}, {1.0f, -1.0f, 1.0f},
+                             {1.0f, 2.0f, 4.0f}, {0.0f, 0.0f, 1.0f}};
+  return G[q][k];
+}
+__host__ __device__ constexpr float at5(int i, int q) {
+  return i == 0 ? (q == 4 ? 0.0f : 1.0f)
+       : i == 1 ? (q == 0 ? 0.0f : q == 1 ? 1.0f : q == 2 ? -1.0f : q == 3 ? 2.0f : 0.0f)
+                : (q == 0 ? 0.0f : q == 3 ? 4.0f : 1.0f);
+}
+
+// B^T along a length-5 vector
+__device__ __forceinline__ void bt5_vec(const float (&v)[5], float (&o)[5]) {
+#pragma unroll
+  for (int q = 0; q < 5; ++q) {
+    float s = 0.0f;
+#pragma unroll
+    for (int a = 0; a < 5; ++a)
+      if (bt5(q, a) != 0.0f) s = fmaf(bt5(q, a), v[a], s);
+    o[q] = s;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Plan
 // ---------------------------------------------------------------------------
@@ -139,6 +260,19 @@ struct ContractArgs {
   long long batch;
 };
 
+// mixed nest (NWG_TILE_MIX_F23_F33): F(3,3) levels above the two F(2,3)
+// levels, and the bytes of the depth-4 scratch (0 below depth 4) that the
+// input transform (level-4 blocks X4) and the output transform (level-3
+// blocks Z3) use in turn
+int mix_outer_levels(const nwg_plan_info& g);
+size_t mix_scratch_bytes(const nwg_plan_info& g);
+hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float* U,
+                                   hipStream_t s);
+// X4, Z3: mix_scratch_bytes(g) of scratch at depth 4 (may be NULL at depth 3)
+hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float* V, float* X4,
+                                  hipStream_t s);
+hipError_t launch_output_xform_mix(const nwg_plan_info& g, const float* Z, float* y, float* Z3,
+                                   hipStream_t s);
 hipError_t launch_kernel_xform(const nwg_plan_info& g, const float* w, float* U, hipStream_t s);
 // part/nparts: at depth 4, the level-4 branches [16 part/nparts, 16 (part+1)/nparts)
 // (V quads [4096 part/nparts, ...)); other depths take nparts = 1

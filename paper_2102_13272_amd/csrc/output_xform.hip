@@ -21,34 +21,6 @@
 namespace nwg {
 namespace {
 
-// Level 2 for one branch: 16 quads (q2r, q2c) -> 4x4 partial tile
-// po[rr][cc], rr = i1r + 2*i2r, cc = i1c + 2*i2c.  zb points at the branch's
-// first quad for this (n, t); gstride is the distance between groups.
-__device__ __forceinline__ void level2_reduce(const float4* __restrict__ zb, size_t gstride,
-                                              float (&po)[4][4]) {
-  float4 v[4][4];
-#pragma unroll
-  for (int q2r = 0; q2r < 4; ++q2r)
-#pragma unroll
-    for (int q2c = 0; q2c < 4; ++q2c) v[q2r][q2c] = zb[(size_t)(q2r * 4 + q2c) * gstride];
-  // along columns: h[q2r][i2c] (float4 over (i1r, i1c))
-  float4 h[4][2];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    h[q][0] = v[q][0] + v[q][1] + v[q][2];
-    h[q][1] = v[q][1] - v[q][2] - v[q][3];
-  }
-#pragma unroll
-  for (int i2c = 0; i2c < 2; ++i2c) {
-    const float4 e0 = h[0][i2c] + h[1][i2c] + h[2][i2c];   // i2r = 0
-    const float4 e1 = h[1][i2c] - h[2][i2c] - h[3][i2c];   // i2r = 1
-    po[0][2 * i2c + 0] = e0.x;  po[0][2 * i2c + 1] = e0.y;
-    po[1][2 * i2c + 0] = e0.z;  po[1][2 * i2c + 1] = e0.w;
-    po[2][2 * i2c + 0] = e1.x;  po[2][2 * i2c + 1] = e1.y;
-    po[3][2 * i2c + 0] = e1.z;  po[3][2 * i2c + 1] = e1.w;
-  }
-}
-
 // ---- depth 1 and 2: one thread per tile -----------------------------------
 template <int NLEV>
 __global__ __launch_bounds__(256) void output_xform_tile(

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libnwg.so")
 NWG_TILE_F2X2_3X3 = 0
 NWG_TILE_F3X3_3X3 = 1
 NWG_TILE_LD_F2X2_3X3 = 2
+NWG_TILE_MIX_F23_F33 = 3
 NWG_TILE_AUTO = -1
 NWG_PRECISION_FP32 = 0
 NWG_PRECISION_BF16_SPLIT = 1
@@ -41,7 +42,7 @@ class nwg_plan_info(ctypes.Structure):
         ("contract_flop", ctypes.c_double), ("fused_input", ctypes.c_int),
         ("depthwise", ctypes.c_int), ("fused_conv", ctypes.c_int),
         ("pipeline_parts", ctypes.c_int), ("precision", ctypes.c_int), ("ld_c", ctypes.c_int),
-        ("fused_output", ctypes.c_int),
+        ("fused_output", ctypes.c_int), ("outer33", ctypes.c_int),
     ]
 
     def as_dict(self):

@@ -48,3 +48,27 @@ def level1_f33(yh_pnt):
     P, N, T = yh_pnt.shape
     g = yh_pnt.reshape(P // 25, 5, 5, N, T)
     return np.ascontiguousarray(np.einsum("jr,gqrnt->gqjnt", AT, g))
+
+
+def mixed_chain():
+    """The library's mixed nest: F(2,3) at levels 1 and 2, F(3,3) above."""
+    f23, f33 = base_f23(), f33_base()
+    return [f23, f23, f33, f33]
+
+
+def mixed_to_lib_points(a, radices):
+    """oracle [..., P1, P1] of a mixed chain (per-axis index with level 1 most
+    significant, radices l_1..l_n) -> [..., P] in the library's order: digits
+    (q_n^row, q_n^col, ..., q_1^row, q_1^col), most significant first."""
+    n = len(radices)
+    shape = []
+    for j in range(n - 1, -1, -1):
+        shape += [radices[j], radices[j]]
+    idx = np.indices(shape).reshape(2 * n, -1)      # lib digits, most significant first
+    rows = np.zeros(idx.shape[1], dtype=np.int64)
+    cols = np.zeros(idx.shape[1], dtype=np.int64)
+    for j in range(n):                              # level j + 1, most significant first
+        k = 2 * (n - 1 - j)
+        rows = rows * radices[j] + idx[k]
+        cols = cols * radices[j] + idx[k + 1]
+    return a[..., rows, cols]

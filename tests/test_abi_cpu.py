@@ -264,3 +264,58 @@ def test_ld_workspace_holds_the_k_slices():
     parts = (g["workspace_bytes"] - g["u_bytes"] - g["v_bytes"]) // g["yhat_bytes"]
     assert parts > 1 and (64 * 25 // 32) % parts == 0
     assert g["workspace_bytes"] == g["u_bytes"] + g["v_bytes"] + parts * g["yhat_bytes"]
+
+
+@pytest.mark.parametrize("r", [1, 3, 5, 7, 8, 9, 13, 15, 16, 23, 31, 39, 40])
+def test_mixed_geometry_matches_oracle_chain(r):
+    """NWG_TILE_MIX_F23_F33: the library's recurrence with F(2,3) at levels 1-2
+    and F(3,3) above equals the oracle's mixed-chain levels (oracle.mixed)."""
+    from oracle.mixed import mixed_levels, mults_per_output
+    from oracle.nested import toom_cook_base
+    B, M, N, H, W = 2, 3, 5, 80, 77
+    pad = (r - 1) // 2
+    tile = nwg.NWG_TILE_MIX_F23_F33
+    if r > 39:
+        with pytest.raises(nwg.NwgError):
+            nwg.plan_geometry(B, M, N, H, W, r, pad, tile)
+        return
+    g = nwg.plan_geometry(B, M, N, H, W, r, pad, tile)
+    if r <= 7:        # only the two F(2,3) levels: the F(2x2,3x3) plan
+        assert g == nwg.plan_geometry(B, M, N, H, W, r, pad)
+        assert g["tile"] == nwg.NWG_TILE_F2X2_3X3 and g["outer33"] == 0
+        return
+    f23, f33 = base_f23(), toom_cook_base(3, 3, [0, 1, -1, 2])
+    lv = mixed_levels([f23, f23, f33, f33], r)
+    assert g["tile"] == tile and g["outer33"] == lv.n - 2
+    assert g["n"] == lv.n and g["Mn"] == lv.Mn and g["Kn"] == lv.Kn and g["Ln"] == lv.Ln
+    assert g["strides"] == lv.strides
+    assert (g["m"], g["rb"], g["l"]) == (2, 3, 4)
+    P, T = lv.P1 ** 2, B * g["th"] * g["tw"]
+    assert g["P"] == P and g["T"] == T
+    assert g["th"] == -(-(H + 2 * pad - r + 1) // lv.Mn)
+    assert g["u_bytes"] == 4 * P * M * N and g["v_bytes"] == 4 * P * M * T
+    assert g["yhat_bytes"] == 4 * (P // 4) * N * T
+    # depth 4: scratch for the level-4 input blocks (26 x 26 per branch, tile
+    # and channel) and the level-3 output blocks (12 x 12 per branch, tile
+    # and channel), used in turn
+    scratch = 4 * max(25 * 676 * M * T, 25 * 144 * N * T) if lv.n == 4 else 0
+    assert g["workspace_bytes"] == g["u_bytes"] + g["v_bytes"] + g["yhat_bytes"] + scratch
+    assert g["ewmm_mults"] == P * T * M * N
+    # per output and channel pair: prod l_j^2 / M_n^2, the oracle's count
+    assert mults_per_output([f23, f23, f33, f33], r) == \
+        __import__("fractions").Fraction(P, lv.Mn ** 2)
+    assert g["fused_input"] == 0 and g["fused_conv"] == 0 and g["fused_output"] == 0
+    # one output channel would take the fused kernel on the F(2x2,3x3) tile
+    g1 = nwg.plan_geometry(B, M, 1, H, W, r, pad, tile)
+    assert g1["fused_input"] == 0
+    with pytest.raises(nwg.NwgError):
+        nwg.plan_geometry_depthwise(B, 4, H, W, r, pad, tile)
+
+
+def test_mixed_geometry_of_the_31x31_workload():
+    g = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15, nwg.NWG_TILE_MIX_F23_F33)
+    assert (g["n"], g["Mn"], g["Kn"], g["Ln"], g["P"]) == (4, 36, 39, 74, 160000)
+    assert (g["th"], g["tw"], g["T"]) == (2, 2, 64)
+    # 1.64x fewer contraction FLOPs than four F(2,3) levels (65536 points x 256 tiles)
+    f23 = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15)
+    assert f23["P"] * f23["T"] / (g["P"] * g["T"]) == pytest.approx(1.6384)

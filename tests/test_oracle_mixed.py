@@ -55,6 +55,8 @@ CHAINS = [
     ("F22,F43", [F22, F43], [3, 5, 6]),          # M_2 = 8 > K_2 = 6
     ("F44,F23", [F44, F23], [5, 8, 12]),         # M_2 = 8, K_2 = 12
     ("F23,F22,F33", [F23, F22, F33], [5, 6, 13]),  # depth 2 for 5, 3 for 6 and 13
+    # the GPU's mixed nest at depth 3: M_3 = 12, K_3 = 15 (strides 1, 2, 4)
+    ("F23,F23,F33", [F23, F23, F33], [8, 13, 15]),
 ]
 
 
@@ -102,3 +104,21 @@ def test_best_mixed_chain_never_loses_to_one_base():
 def test_short_chain_is_an_error():
     with pytest.raises(ValueError):
         mixed_levels([F23], 5)
+
+
+@pytest.mark.parametrize("r", [16, 31, 39])
+def test_gpu_mixed_nest_at_depth_4_equals_direct_in_fp64(r):
+    """The GPU's mixed nest F(2,3), F(2,3), F(3,3), F(3,3) (strides 1, 2, 4, 12,
+    M_4 = 36, K_4 = 39, 400 points per axis): exact rationals are too slow at
+    this size, so fp64 against the direct oracle, whose only error is the
+    rounding of B^T's thirds and sixths (a dropped term or a wrong sign or
+    index gives O(1) errors)."""
+    chain = [F23, F23, F33, F33]
+    lv = mixed_levels(chain, r)
+    assert (lv.n, lv.strides, lv.Mn, lv.Kn, lv.P1) == (4, [1, 2, 4, 12], 36, 39, 400)
+    pad = (r - 1) // 2
+    x, w = _ints((1, 2, 40, 45), r), _ints((2, 2, r, r), 70 + r)
+    y = nested_conv2d_mixed(x, w, pad, chain)
+    ref = direct_conv2d(x, w, pad)
+    assert y.shape == ref.shape
+    assert np.max(np.abs(y - ref)) <= 1e-9 * np.max(np.abs(ref))
