@@ -77,38 +77,43 @@ def source_hash(files):
     return h.hexdigest()[:16]
 
 
-KERNEL_SOURCES = {"input_transform": ["input_xform.hip", "nwg_internal.h"],
+KERNEL_SOURCES = {"input_transform": ["input_xform.hip", "mixed.hip", "nwg_internal.h"],
                   "contraction": ["contract_mfma.hip", "nwg_internal.h"],
-                  "output_transform": ["output_xform.hip", "nwg_internal.h"],
-                  "kernel_transform": ["kernel_xform.hip", "nwg_internal.h"]}
+                  "output_transform": ["output_xform.hip", "mixed.hip", "nwg_internal.h"],
+                  "kernel_transform": ["kernel_xform.hip", "mixed.hip", "nwg_internal.h"]}
 
 
-def measured_traffic(workload: str, stage: str):
+def measured_traffic(workload: str, stage: str, tile: str):
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    was taken on the current kernel source with the same --tile; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}_{tile}.json")
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         d = json.load(fh)
     ent = d.get("kernels", {}).get(stage)
+    if d.get("tile", "f23") != tile:
+        return None
     if not ent or ent.get("source_hash") != source_hash(KERNEL_SOURCES[stage]):
         return None
     return ent.get("hbm_bytes_per_launch")
 
 
 STAGE_OF_KERNEL = [("contract", "contraction"), ("gemm_mfma", "contraction"),
-                   ("input_xform", "input_transform"), ("output_xform", "output_transform"),
-                   ("kernel_xform", "kernel_transform")]
+                   ("input_xform", "input_transform"), ("input_mix", "input_transform"),
+                   ("output_xform", "output_transform"), ("kernel_xform", "kernel_transform")]
 
 
-def traffic_from_counters(workload: str, fetch_csv: str, write_csv: str, copy_mib: int):
+def traffic_from_counters(workload: str, tile: str, fetch_csv: str, write_csv: str,
+                          copy_mib: int):
     """HBM bytes per launch of each stage from two rocprofv3 --pmc runs.
 
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by what the same
     counters read for the plain device-to-device copy of `copy_mib` MiB that
     `--calibrate-copy-mib` performs at the start of the profiled run.
-    Writes profiles/traffic_<workload>.json and returns its content.
+    A stage that runs several kernels (the mixed nest's input and output
+    transforms) gets their sum.  Writes profiles/traffic_<workload>_<tile>.json
+    and returns its content.
     """
     import csv
     from collections import defaultdict
@@ -129,7 +134,7 @@ def traffic_from_counters(workload: str, fetch_csv: str, write_csv: str, copy_mi
         raise SystemExit("no copy-kernel dispatch in the counter files (run with --calibrate-copy-mib)")
     fscale = copy_bytes / (cf[0][0] * 1024.0)
     wscale = copy_bytes / (cw[0][0] * 1024.0)
-    out = {"workload": workload, "copy_calibration_bytes": copy_bytes,
+    out = {"workload": workload, "tile": tile, "copy_calibration_bytes": copy_bytes,
            "fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4), "kernels": {}}
     for name in fetch:
         stage = next((st for key, st in STAGE_OF_KERNEL if key in name), None)
@@ -139,11 +144,15 @@ def traffic_from_counters(workload: str, fetch_csv: str, write_csv: str, copy_mi
         w = sum(write[name]) / len(write[name]) * 1024.0 * wscale
         short = name.split("::")[-1].split("(")[0] if "(anonymous namespace)::" in name else name
         short = name.split("(anonymous namespace)::")[-1].split("(")[0] if "(anonymous namespace)::" in name else short
-        out["kernels"][stage] = {"kernel": short[:120], "dispatches": len(fetch[name]),
-                                 "fetch_bytes": round(f), "write_bytes": round(w),
-                                 "hbm_bytes_per_launch": round(f + w),
-                                 "source_hash": source_hash(KERNEL_SOURCES[stage])}
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+        ent = out["kernels"].setdefault(stage, {"kernel": "", "dispatches": len(fetch[name]),
+                                                "fetch_bytes": 0, "write_bytes": 0,
+                                                "hbm_bytes_per_launch": 0,
+                                                "source_hash": source_hash(KERNEL_SOURCES[stage])})
+        ent["kernel"] = (ent["kernel"] + " + " if ent["kernel"] else "") + short[:120]
+        ent["fetch_bytes"] += round(f)
+        ent["write_bytes"] += round(w)
+        ent["hbm_bytes_per_launch"] += round(f + w)
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}_{tile}.json")
     with open(path, "w") as fh:
         json.dump(out, fh, indent=1)
     return out
@@ -197,7 +206,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c5_r31")
-    ap.add_argument("--tile", choices=["f23", "f33", "auto", "ld", "mix"], default="f23",
+    ap.add_argument("--tile", choices=["f23", "f33", "auto", "ld", "mix"], default="auto",
                     help="Winograd base: F(2x2,3x3) nests (any r <= 31); F(3x3,3x3) nests for "
                          "the dense layers with r <= 9 (others keep F(2x2,3x3)); the "
                          "library's per-layer choice (NWG_TILE_AUTO); the linear "
@@ -221,11 +230,12 @@ def main():
                          "known size, to scale hardware byte counters)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="no GPU work: turn two rocprofv3 --pmc counter files (FETCH_SIZE, "
-                         "WRITE_SIZE) of a --calibrate-copy-mib run into profiles/traffic_*.json")
+                         "WRITE_SIZE) of a --calibrate-copy-mib run into "
+                         "profiles/traffic_<workload>_<tile>.json")
     args = ap.parse_args()
     if args.traffic_from:
-        res = traffic_from_counters(args.workload, args.traffic_from[0], args.traffic_from[1],
-                                    args.calibrate_copy_mib or 1024)
+        res = traffic_from_counters(args.workload, args.tile, args.traffic_from[0],
+                                    args.traffic_from[1], args.calibrate_copy_mib or 1024)
         print(json.dumps(res, indent=1))
         return
     if args.gpus != 1:
@@ -406,9 +416,8 @@ def main():
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4)}
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
-    roof["traffic"] = (measured_traffic(args.workload, dom)
-                       if len(plans) == 1 and all(p.info["tile"] == nwg.NWG_TILE_F2X2_3X3
-                                                  for p in plans) and not split else None)
+    roof["traffic"] = (measured_traffic(args.workload, dom, args.tile)
+                       if len(plans) == 1 and not split else None)
 
     L0 = wl.layers[0]
     cfg = {"workload": args.workload, "layers": len(wl.layers), "B": L0.B,
@@ -438,6 +447,33 @@ def main():
     }
     if args.graph:
         out["ms_per_step_eager"] = round(ms_step_eager, 4)
+    if any(p.info["tile"] != nwg.NWG_TILE_F2X2_3X3 for p in plans):
+        # the same workload with every layer on F(2x2,3x3) nests, timed the
+        # same way (eager), for comparison
+        f23 = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, depthwise=L.depthwise)
+               for L in wl.layers]
+        outs2 = [torch.empty(p.y_shape, dtype=torch.float32, device="cuda") for p in f23]
+
+        def step2():
+            cur = xd
+            for p, w, y in zip(f23, wds, outs2):
+                p.conv2d(cur, w, y, stream)
+                cur = y
+        for _ in range(max(1, args.warmup)):
+            step2()
+        torch.cuda.synchronize()
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record(stream)
+        for _ in range(args.steps):
+            step2()
+        f1.record(stream)
+        torch.cuda.synchronize()
+        ms2 = f0.elapsed_time(f1) / args.steps
+        out["f2x2_3x3_only"] = {"ms_per_step": round(ms2, 4),
+                                "value": round(direct_flop / (ms2 * 1e-3) / 1e12, 3)}
+        for p in f23:
+            p.close()
+        del outs2
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
     for p in plans:

@@ -86,8 +86,9 @@ typedef struct nwg_plan nwg_plan;
  *     MI355X -- one output channel at depth 2 or one or two input channels
  *     (its fused kernels; unless the F(2x2,3x3) plan runs the layer in one
  *     kernel), or M, N >= 32 and either r = 8..9 (one nesting level fewer)
- *     or r <= 3 -- and F(2x2,3x3) otherwise (always for depthwise plans and
- *     r > 9).  info.tile reports the tile taken. */
+ *     or r <= 3 --, the mixed nest NWG_TILE_MIX_F23_F33 (below) for dense
+ *     plans with r = 16..31 and M, N >= 32, and F(2x2,3x3) otherwise
+ *     (always for depthwise plans).  info.tile reports the tile taken. */
 /*   NWG_TILE_LD_F2X2_3X3: the linear decomposition of Sec. II.B (Fig. 2),
  *     the method the paper compares nesting with, on the same F(2x2,3x3)
  *     kernels: the r x r kernel is cut into c x c sub-kernels of 3 x 3

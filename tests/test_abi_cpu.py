@@ -211,7 +211,9 @@ def test_f33_geometry_matches_oracle_levels(r):
     ((8, 64, 64, 56, 56, 7, 3), 0),       # same depth: F(2,3)
     ((8, 64, 64, 56, 56, 3, 1), 1),       # depth 1, wide channels
     ((4, 5, 5, 256, 256, 3, 1), 0),       # few channels
-    ((16, 128, 128, 56, 56, 31, 15), 0),  # r > 9
+    ((16, 128, 128, 56, 56, 31, 15), 3),  # depth 4, wide channels: the mixed nest
+    ((2, 16, 128, 56, 56, 31, 15), 0),    # depth 4, M < 32
+    ((8, 64, 64, 56, 56, 13, 6), 0),      # depth 3
     ((1, 32, 32, 64, 64, 1, 0), 0),       # 1x1
 ])
 def test_auto_tile_choice(shape, tile):

@@ -56,7 +56,6 @@ E2E = [
     (1, 2, 3, 75, 40, 31, 15),
     (1, 2, 2, 45, 45, 39, 19),
     (2, 33, 20, 40, 40, 23, 11),
-    (64, 32, 64, 36, 36, 31, 15),
 ]
 
 
@@ -66,6 +65,39 @@ def test_mixed_conv2d_matches_direct_oracle(case):
     L, x, w = make_case(B, M, N, H, W, r, pad, seed=7 * sum(case))
     print(f"mixed case {case}", flush=True)
     assert_close(_conv(x, w, pad), direct_conv2d(x, w, pad), what=str(case))
+
+
+def _sampled(x, w, pad, y, seed, edges):
+    """y against the direct oracle at 1500 random outputs plus the corners
+    and both sides of the tile edges given (rows and columns)."""
+    B, N, Ho, Wo = y.shape
+    rng = np.random.default_rng(seed)
+    pts = {(int(rng.integers(B)), int(rng.integers(N)), int(rng.integers(Ho)),
+            int(rng.integers(Wo))) for _ in range(1500)}
+    for b in (0, B - 1):
+        for n in (0, N - 1):
+            for i in edges + [0, Ho - 1]:
+                for j in edges + [0, Wo - 1]:
+                    if i < Ho and j < Wo:
+                        pts.add((b, n, i, j))
+    pts = sorted(pts)
+    ref = direct_conv2d_points(x, w, pad, pts)
+    got = np.array([y[p] for p in pts], dtype=np.float64)
+    assert_close(got, ref, what="sampled outputs")
+
+
+# the deep contraction at depth 4 (T = 64, 10000 groups: the persistent
+# form), 64 x 64 blocks (N = 64) and 128 x 64 blocks (N = 128); full outputs
+# are too slow for the CPU oracle here, so sampled outputs
+BIG = [(64, 32, 64, 36, 36, 31, 15), (64, 32, 128, 36, 36, 31, 15)]
+
+
+@pytest.mark.parametrize("case", BIG, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
+def test_mixed_conv2d_deep_contraction_sampled(case):
+    B, M, N, H, W, r, pad = case
+    L, x, w = make_case(B, M, N, H, W, r, pad, seed=7 * sum(case))
+    print(f"mixed case {case}", flush=True)
+    _sampled(x, w, pad, _conv(x, w, pad), 13, [11, 12, 35])
 
 
 def _stage_refs(x, w, pad):
@@ -176,16 +208,6 @@ def test_large_kernel_workload_sampled_on_the_mixed_nest():
         torch.cuda.synchronize()
         yh = y.cpu().numpy()
     assert np.isfinite(yh).all()
-    rng = np.random.default_rng(9)
-    pts = {(int(rng.integers(L.B)), int(rng.integers(L.N)), int(rng.integers(L.Ho)),
-            int(rng.integers(L.Wo))) for _ in range(1500)}
-    # corners and both sides of the 36-pixel tile edge (ragged second tile)
-    for b in (0, L.B - 1):
-        for n in (0, L.N - 1):
-            for i in (0, 11, 12, 35, 36, L.Ho - 1):
-                for j in (0, 23, 24, 35, 36, L.Wo - 1):
-                    pts.add((b, n, i, j))
-    pts = sorted(pts)
-    ref = direct_conv2d_points(x, w, L.pad, pts)
-    got = np.array([yh[p] for p in pts], dtype=np.float64)
-    assert_close(got, ref, what=name)
+    # both sides of the 12-pixel level-3 blocks and the 36-pixel tile edge
+    # (a ragged second tile)
+    _sampled(x, w, L.pad, yh, 9, [11, 12, 23, 24, 35, 36])

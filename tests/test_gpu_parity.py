@@ -168,7 +168,9 @@ def test_fused_input_contract_rejects_other_shapes():
                                          # persistent deep path (at least 4 tiles per CU slot):
                                          # 64 x 128 tiles, 4 per slot; 64 x 64 tiles with a
                                          # ragged last one and 4 or 5 tiles per slot
-                                         (128, 64, 256, 3), (64, 32, 520, 3)])
+                                         (128, 64, 256, 3), (64, 32, 520, 3),
+                                         # 128 x 64 blocks (T = 64, N % 128 == 0)
+                                         (128, 32, 64, 2), (256, 64, 64, 1)])
 def test_contraction_matches_numpy(N, M, T, depth):
     """Z = level-1 A^T of (U[p]^T V[p]) for ragged shapes, through nwg_contract.
 
