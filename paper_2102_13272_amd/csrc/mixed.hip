@@ -199,10 +199,24 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
   const int ty = r2 / tw, tx = r2 - ty * tw;
   const float* __restrict__ xp = x + ((size_t)b * M + m) * H * W;
   const int gr0 = ty * 36 - pad, gc0 = tx * 36 - pad;
-  for (int e = threadIdx.x; e < LW * LW; e += 256) {
-    const int i = e / LW, j = e - i * LW;
-    const int gr = gr0 + i, gc = gc0 + j;
-    win[i * LS + j] = (gr >= 0 && gr < H && gc >= 0 && gc < W) ? xp[(size_t)gr * W + gc] : 0.0f;
+  {
+    // all of a thread's loads first (22 in flight), then the LDS writes
+    constexpr int PER = (LW * LW + 255) / 256;
+    float v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int i = e / LW, j = e - i * LW;
+      const int gr = gr0 + i, gc = gc0 + j;
+      v[u] = (e < LW * LW && gr >= 0 && gr < H && gc >= 0 && gc < W) ? xp[(size_t)gr * W + gc]
+                                                                    : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = threadIdx.x + 256 * u;
+      const int i = e / LW, j = e - i * LW;
+      if (e < LW * LW) win[i * LS + j] = v[u];
+    }
   }
   __syncthreads();
   // rows: rw[q4r][i][c] = sum_a B^T[q4r][a] win[i + 12 a][c]
@@ -241,16 +255,18 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
   }
 }
 
-// 400 threads: 16 tiles x 25 level-3 branches.  Work-group -> (level-4
-// branch q4 (NO = 2), 16-tile chunk, channel m), q4 fastest, numbered so that
-// each XCD takes a contiguous range.
+// 256 threads: 16 tiles x 16 slots, slot s taking the level-3 branches s
+// and s + 16 (< 25), so that two work-groups share a CU (one's stores
+// overlap the other's fill and arithmetic).  Work-group -> (level-4 branch
+// q4 (NO = 2), 16-tile chunk, channel m), q4 fastest, numbered so that each
+// XCD takes a contiguous range.
 template <int NO>
-__global__ __launch_bounds__(400) void input_xform_mix(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix(
     const float* __restrict__ x, const float* __restrict__ X4, float4* __restrict__ V, int M,
     int H, int W, int pad, int th, int tw, int T, long long qstride) {
   constexpr int Mn = NO == 2 ? 36 : 12;
   constexpr int KK = kL3 * kL3;
-  constexpr int PER = (16 * KK + 399) / 400;  // fill values per thread
+  constexpr int PER = (16 * KK + 255) / 256;  // fill values per thread
   extern __shared__ float lds[];            // [16][kWS]
   long long lid;
   {
@@ -272,14 +288,14 @@ __global__ __launch_bounds__(400) void input_xform_mix(
       const float* src = X4 + (((size_t)q4 * M + m) * T + t0) * KK;
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int e = threadIdx.x + 400 * u;
+        const int e = threadIdx.x + 256 * u;
         v[u] = e < nt * KK ? src[e] : 0.0f;
       }
     } else {
       const int tpi = th * tw;
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int e = threadIdx.x + 400 * u;
+        const int e = threadIdx.x + 256 * u;
         const int tl = e / KK, k = e - tl * KK;
         const int i = k / kL3, j = k - i * kL3;
         float val = 0.0f;
@@ -297,7 +313,7 @@ __global__ __launch_bounds__(400) void input_xform_mix(
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      const int e = threadIdx.x + 400 * u;
+      const int e = threadIdx.x + 256 * u;
       if (e < 16 * KK) {
         const int tl = e / KK, k = e - tl * KK;
         lds[tl * kWS + k] = v[u];
@@ -305,13 +321,14 @@ __global__ __launch_bounds__(400) void input_xform_mix(
     }
   }
   __syncthreads();
-  const int tl = threadIdx.x & 15, slot = threadIdx.x >> 4;   // slot = 5 q3r + q3c
+  const int tl = threadIdx.x & 15;
   const int t = t0 + tl;
   if (t >= T) return;                       // no barrier below
+  const float* win = lds + tl * kWS;
+  for (int slot = threadIdx.x >> 4; slot < 25; slot += 16) {   // slot = 5 q3r + q3c
   float ca[5], cb[5];
   bt5_row(slot / 5, ca);
   bt5_row(slot % 5, cb);
-  const float* win = lds + tl * kWS;
   // level 3 (stride 4): per output row, the rows' taps, then the columns'
   float S[10][10];
 #pragma unroll
@@ -337,6 +354,7 @@ __global__ __launch_bounds__(400) void input_xform_mix(
   }
   const int ob = q4 * 25 + slot;
   inner2_store<false>(S, V + (size_t)ob * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+  }
 }
 
 // ---- output transform -------------------------------------------------------
@@ -518,10 +536,10 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
                        g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(input_xform_mix<2>, dim3((unsigned)nwg), dim3(400), lds, s, x, X4, V, g.M,
+    hipLaunchKernelGGL(input_xform_mix<2>, dim3((unsigned)nwg), dim3(256), lds, s, x, X4, V, g.M,
                        g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride);
   } else {
-    hipLaunchKernelGGL(input_xform_mix<1>, dim3((unsigned)nwg), dim3(400), lds, s, x, X4, V, g.M,
+    hipLaunchKernelGGL(input_xform_mix<1>, dim3((unsigned)nwg), dim3(256), lds, s, x, X4, V, g.M,
                        g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride);
   }
   return hipGetLastError();
