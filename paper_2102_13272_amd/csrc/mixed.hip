@@ -16,9 +16,9 @@
 // contraction (group g = 16 ob + 4 q2r + q2c after the level-1 A^T).
 //
 //   kernel transform : one thread per (output channel, outer branch), the
-//                      16 output channels of a work-group in LDS, padded to
-//                      K_n x K_n; the outer G rows fold the kernel into the
-//                      9 x 9 sub-kernel of the two F(2,3) levels.
+//                      16 output channels of a 512-thread work-group in LDS,
+//                      padded to K_n x K_n; the outer G rows fold the kernel
+//                      into the 9 x 9 sub-kernel of the two F(2,3) levels.
 //   input transform  : 16 tiles x 25 level-3 branches per work-group; at
 //                      NO = 2 the work-group owns one level-4 branch, whose
 //                      B^T rows the LDS fill applies (74 x 74 -> 26 x 26).
@@ -75,7 +75,7 @@ __device__ __forceinline__ void bt5_row(int q, float (&c)[5]) {
 
 // ---- kernel transform -------------------------------------------------------
 template <int NO>
-__global__ __launch_bounds__(256) void kernel_xform_mix(const float* __restrict__ w,
+__global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict__ w,
                                                         float* __restrict__ U, int M, int N,
                                                         int r) {
   constexpr int K = NO == 2 ? 39 : 15;      // padded taps per axis (odd)
@@ -85,19 +85,19 @@ __global__ __launch_bounds__(256) void kernel_xform_mix(const float* __restrict_
   extern __shared__ float wl[];             // [16][K][K]
   const int m = blockIdx.y;
   const int n0 = blockIdx.x * 16;
-  for (int e = threadIdx.x; e < 16 * KS; e += 256) {
+  for (int e = threadIdx.x; e < 16 * KS; e += 512) {
     const int c = e / KS, k = e - c * KS;
     const int u = k / K, v = k - u * K;
     const int nn = n0 + c;
     wl[e] = (nn < N && u < r && v < r) ? w[((size_t)nn * M + m) * r * r + u * r + v] : 0.0f;
   }
   __syncthreads();
-  const int cl = threadIdx.x & 15, slot = threadIdx.x >> 4;
+  const int cl = threadIdx.x & 15, slot = threadIdx.x >> 4;   // 32 slots
   const int nn = n0 + cl;
   if (nn >= N) return;                      // no barrier below
   const float* wk = wl + cl * KS;
   const size_t MN = (size_t)M * N;
-  for (int b = slot; b < NB; b += 16) {
+  for (int b = slot; b < NB; b += 32) {
     const int q3c = b % 5, q3r = (b / 5) % 5;
     const int q4c = NO == 2 ? (b / 25) % 5 : 0, q4r = NO == 2 ? b / 125 : 0;
     float c3r[3], c3c[3], c4r[3], c4c[3];
@@ -514,9 +514,9 @@ hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   if (no == 2)
-    hipLaunchKernelGGL(kernel_xform_mix<2>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
+    hipLaunchKernelGGL(kernel_xform_mix<2>, grid, dim3(512), lds, s, w, U, g.M, g.N, g.r);
   else
-    hipLaunchKernelGGL(kernel_xform_mix<1>, grid, dim3(256), lds, s, w, U, g.M, g.N, g.r);
+    hipLaunchKernelGGL(kernel_xform_mix<1>, grid, dim3(512), lds, s, w, U, g.M, g.N, g.r);
   return hipGetLastError();
 }
 
