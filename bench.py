@@ -225,6 +225,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-compare", action="store_true",
+                    help="skip the all-F(2x2,3x3) comparison step (e.g. under a counter run)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="first copy a float32 buffer of this many MiB (a plain copy kernel of "
                          "known size, to scale hardware byte counters)")
@@ -447,7 +449,7 @@ def main():
     }
     if args.graph:
         out["ms_per_step_eager"] = round(ms_step_eager, 4)
-    if any(p.info["tile"] != nwg.NWG_TILE_F2X2_3X3 for p in plans):
+    if not args.no_compare and any(p.info["tile"] != nwg.NWG_TILE_F2X2_3X3 for p in plans):
         # the same workload with every layer on F(2x2,3x3) nests, timed the
         # same way (eager), for comparison
         f23 = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, depthwise=L.depthwise)
