@@ -181,7 +181,10 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
 // go to LDS, level 3 runs per output row (rows, then columns) and the two
 // F(2,3) levels in registers (10 x 10 -> 16 x 16).
 constexpr int kL3 = 26;                     // window side left for levels 1..3
-constexpr int kWS = kL3 * kL3 + 1;          // odd per-tile stride in LDS
+// per-tile stride in LDS: even, so that column pairs are 8-byte aligned
+// (float2 reads), and 678 = 38 (mod 64), so that the 16 tiles of a
+// quarter-wave start on 16 different even banks
+constexpr int kWS = kL3 * kL3 + 2;
 
 __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
                                                     float* __restrict__ X4, int M, int H, int W,
@@ -326,29 +329,46 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void i
   if (t >= T) return;                       // no barrier below
   const float* win = lds + tl * kWS;
   for (int slot = threadIdx.x >> 4; slot < 25; slot += 16) {   // slot = 5 q3r + q3c
-  float ca[5], cb[5];
-  bt5_row(slot / 5, ca);
-  bt5_row(slot % 5, cb);
-  // level 3 (stride 4): per output row, the rows' taps, then the columns'
+  // a row of B^T of F(3,3) has its nonzero taps among 4 consecutive ones,
+  // from tap 0 for row 0 and from tap 1 otherwise
+  const int q3r = slot / 5, q3c = slot - 5 * q3r;
+  const int lr = q3r == 0 ? 0 : 1, lc = q3c == 0 ? 0 : 1;
+  float ca5[5], cb5[5], ca[4], cb[4];
+  bt5_row(q3r, ca5);
+  bt5_row(q3c, cb5);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    ca[u] = lr ? ca5[u + 1] : ca5[u];
+    cb[u] = lc ? cb5[u + 1] : cb5[u];
+  }
+  // level 3 (stride 4): per output row, the rows' taps over the 22 columns
+  // the column taps need (from column 4 lc), read as float2, then the
+  // columns' taps
+  const float* wb = win + kStride3 * lr * kL3 + kStride3 * lc;
   float S[10][10];
 #pragma unroll
   for (int i = 0; i < 10; ++i) {
-    float tr[kL3];
+    float tr[22];
 #pragma unroll
-    for (int c = 0; c < kL3; ++c) {
-      float s = 0.0f;
+    for (int c = 0; c < 22; c += 2) {
+      float s0 = 0.0f, s1 = 0.0f;
 #pragma unroll
-      for (int a = 0; a < 5; ++a) s = fmaf(ca[a], win[(i + kStride3 * a) * kL3 + c], s);
-      tr[c] = s;
+      for (int u = 0; u < 4; ++u) {
+        const float2 v = *reinterpret_cast<const float2*>(wb + (i + kStride3 * u) * kL3 + c);
+        s0 = fmaf(ca[u], v.x, s0);
+        s1 = fmaf(ca[u], v.y, s1);
+      }
+      tr[c] = s0;
+      tr[c + 1] = s1;
     }
 #pragma unroll
     for (int j = 0; j < 10; ++j) {
-      float s = 0.0f;
+      float sacc = 0.0f;
 #pragma unroll
-      for (int b = 0; b < 5; ++b) s = fmaf(cb[b], tr[j + kStride3 * b], s);
-      S[i][j] = s;
+      for (int u = 0; u < 4; ++u) sacc = fmaf(cb[u], tr[j + kStride3 * u], sacc);
+      S[i][j] = sacc;
     }
-    // one output row at a time: keeps the row's 130 LDS reads from being
+    // one output row at a time: keeps the row's LDS reads from being
     // hoisted across rows (register pressure)
     __builtin_amdgcn_sched_barrier(0);
   }
