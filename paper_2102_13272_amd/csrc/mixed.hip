@@ -24,10 +24,11 @@
 //                      B^T rows the LDS fill applies (74 x 74 -> 26 x 26).
 //                      Level 3 runs per output row (rows, then columns), the
 //                      two F(2,3) levels in registers (10 x 10 -> 16 x 16).
-//   output transform : levels 2 and 3 per (tile, level-4 branch, channel)
-//                      into a 12 x 12 block; at NO = 1 that is the output
-//                      tile, at NO = 2 a second kernel applies level 4 to
-//                      the 25 blocks (held in a scratch buffer Z3).
+//   output transform : NO = 1: levels 2 and 3 per (tile, 4 x 4 output
+//                      block, channel), straight to y.  NO = 2: levels 2
+//                      and 3 per (tile, level-4 branch, channel) into a
+//                      12 x 12 block held in a scratch buffer Z3, then a
+//                      second kernel applies level 4 to the 25 blocks.
 #include "nwg_internal.h"
 
 namespace nwg {
@@ -381,13 +382,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void i
 // Levels 2 and 3: thread (tile t, level-4 branch q4, channel n), lanes on
 // consecutive tiles.  Over the 25 level-3 branches, level2_reduce gives each
 // branch's 4 x 4 block and the level-3 A^T accumulates the 12 x 12 block
-// acc[i3r][i3c][rr][cc] (row 4 i3r + rr, column 4 i3c + cc).  FINAL (NO = 1):
-// that block is the output tile; else it goes to Z3[q4][e][n][t], e = 12 row
-// + column.
-template <bool FINAL>
-__global__ __launch_bounds__(64) void output_xform_mix23(
-    const float4* __restrict__ Z, float* __restrict__ out, int N, int Ho, int Wo, int th, int tw,
-    int T, long long gstride) {
+// acc[i3r][i3c][rr][cc] (row 4 i3r + rr, column 4 i3c + cc), which goes to
+// Z3[q4][e][n][t], e = 12 row + column (depth 4).
+__global__ __launch_bounds__(64) void output_xform_mix23(const float4* __restrict__ Z,
+                                                         float* __restrict__ out, int N, int T,
+                                                         long long gstride) {
   const int t = blockIdx.x * 64 + threadIdx.x;
   const int q4 = blockIdx.y;
   const int n = blockIdx.z;
@@ -423,40 +422,65 @@ __global__ __launch_bounds__(64) void output_xform_mix23(
         for (int e = 0; e < 16; ++e) acc[i3r][i3c][e] = fmaf(c, po[e >> 2][e & 3], acc[i3r][i3c][e]);
       }
   }
-  if constexpr (FINAL) {
-    const int tpi = th * tw;
-    const int b = t / tpi;
-    const int r2 = t - b * tpi;
-    const int ty = r2 / tw, tx = r2 - ty * tw;
-    float* yo = out + ((size_t)b * N + n) * Ho * Wo;
+  const size_t es = (size_t)N * T;          // between consecutive e
+  float* z3 = out + (size_t)q4 * 144 * es + (size_t)n * T + t;
 #pragma unroll
-    for (int i3r = 0; i3r < 3; ++i3r)
+  for (int i3r = 0; i3r < 3; ++i3r)
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int row = ty * 12 + 4 * i3r + rr;
-        if (row >= Ho) continue;
+    for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
-        for (int i3c = 0; i3c < 3; ++i3c)
+      for (int i3c = 0; i3c < 3; ++i3c)
 #pragma unroll
-          for (int cc = 0; cc < 4; ++cc) {
-            const int col = tx * 12 + 4 * i3c + cc;
-            if (col < Wo) yo[(size_t)row * Wo + col] = acc[i3r][i3c][rr * 4 + cc];
-          }
-      }
-  } else {
-    const size_t es = (size_t)N * T;        // between consecutive e
-    float* z3 = out + (size_t)q4 * 144 * es + (size_t)n * T + t;
+        for (int cc = 0; cc < 4; ++cc) {
+          const int e = (4 * i3r + rr) * 12 + 4 * i3c + cc;
+          z3[(size_t)e * es] = acc[i3r][i3c][rr * 4 + cc];
+        }
+}
+
+// Depth 3 (NO = 1): levels 2 and 3 straight to y, one thread per (tile t,
+// output block (i3r, i3c), channel n), lanes on consecutive tiles: over the
+// level-3 branches whose A^T coefficient for its block is nonzero (a
+// work-group-uniform test), level2_reduce gives the branch's 4 x 4 block and
+// the thread accumulates its own 4 x 4 output block.  Nine times the threads
+// of a (tile, channel) split (the 144 accumulators of output_xform_mix23 leave
+// one wavefront per CU on layers of a few hundred tiles).
+__global__ __launch_bounds__(64) void output_xform_mix3(const float4* __restrict__ Z,
+                                                        float* __restrict__ y, int N, int Ho,
+                                                        int Wo, int th, int tw, int T,
+                                                        long long gstride) {
+  const int t = blockIdx.x * 64 + threadIdx.x;
+  const int blk = blockIdx.y;               // 3 i3r + i3c
+  const int n = blockIdx.z;
+  if (t >= T) return;
+  const int i3r = blk / 3, i3c = blk - 3 * i3r;
+  float acc[16];
 #pragma unroll
-    for (int i3r = 0; i3r < 3; ++i3r)
+  for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+  const float4* zt = Z + (size_t)n * T + t;
+#pragma unroll 1
+  for (int q3 = 0; q3 < 25; ++q3) {
+    const int q3r = q3 / 5, q3c = q3 - 5 * q3r;
+    const float c = at5(i3r, q3r) * at5(i3c, q3c);
+    if (c == 0.0f) continue;                // uniform over the work-group
+    float po[4][4];
+    level2_reduce(zt + (size_t)q3 * 16 * gstride, (size_t)gstride, po);
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
+    for (int e = 0; e < 16; ++e) acc[e] = fmaf(c, po[e >> 2][e & 3], acc[e]);
+  }
+  const int tpi = th * tw;
+  const int b = t / tpi;
+  const int r2 = t - b * tpi;
+  const int ty = r2 / tw, tx = r2 - ty * tw;
+  float* yo = y + ((size_t)b * N + n) * Ho * Wo;
 #pragma unroll
-        for (int i3c = 0; i3c < 3; ++i3c)
+  for (int rr = 0; rr < 4; ++rr) {
+    const int row = ty * 12 + 4 * i3r + rr;
+    if (row >= Ho) continue;
 #pragma unroll
-          for (int cc = 0; cc < 4; ++cc) {
-            const int e = (4 * i3r + rr) * 12 + 4 * i3c + cc;
-            z3[(size_t)e * es] = acc[i3r][i3c][rr * 4 + cc];
-          }
+    for (int cc = 0; cc < 4; ++cc) {
+      const int col = tx * 12 + 4 * i3c + cc;
+      if (col < Wo) yo[(size_t)row * Wo + col] = acc[rr * 4 + cc];
+    }
   }
 }
 
@@ -573,13 +597,13 @@ hipError_t launch_output_xform_mix(const nwg_plan_info& g, const float* Zf, floa
   const long long gstride = (long long)g.N * g.T;
   const unsigned tb = (unsigned)((g.T + 63) / 64);
   if (no == 1) {
-    hipLaunchKernelGGL(output_xform_mix23<true>, dim3(tb, 1, (unsigned)g.N), dim3(64), 0, s, Z, y,
-                       g.N, g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride);
+    hipLaunchKernelGGL(output_xform_mix3, dim3(tb, 9, (unsigned)g.N), dim3(64), 0, s, Z, y, g.N,
+                       g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride);
     return hipGetLastError();
   }
   if (!Z3) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(output_xform_mix23<false>, dim3(tb, 25, (unsigned)g.N), dim3(64), 0, s, Z,
-                     Z3, g.N, g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride);
+  hipLaunchKernelGGL(output_xform_mix23, dim3(tb, 25, (unsigned)g.N), dim3(64), 0, s, Z, Z3, g.N,
+                     (int)g.T, gstride);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(output_xform_mix4, dim3(tb, 144, (unsigned)g.N), dim3(64), 0, s, Z3, y, g.N,
