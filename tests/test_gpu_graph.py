@@ -6,7 +6,8 @@ it.  The graph is replayed several times, with eager work of the program
 and synchronisations between the replays, and each replay is compared with
 the eager output bit for bit.  Covers a chain of layers that takes every
 kind of launch (fused small-channel kernels, 1x1 GEMMs, the fused F(3,3)
-kernel with its partial sums, the three-kernel path).
+kernel with its partial sums, the three-kernel path, the mixed nest with its
+scratch buffer).
 """
 import numpy as np
 import pytest
@@ -31,6 +32,8 @@ CHAIN = [(1, 32, 5, 2, nwg.NWG_TILE_F2X2_3X3),     # single-kernel depth 2
          (32, 5, 1, 0, nwg.NWG_TILE_F2X2_3X3),     # 1x1 GEMM
          (5, 5, 3, 1, nwg.NWG_TILE_F2X2_3X3),      # single-kernel depth 1
          (5, 64, 7, 3, nwg.NWG_TILE_F2X2_3X3),     # three kernels, depth 2
+         (64, 64, 17, 8, nwg.NWG_TILE_MIX_F23_F33),  # mixed nest, depth 4 (scratch)
+         (64, 64, 13, 6, nwg.NWG_TILE_MIX_F23_F33),  # mixed nest, depth 3
          (64, 64, 9, 4, nwg.NWG_TILE_F3X3_3X3),    # F(3,3) three kernels
          (64, 1, 9, 4, nwg.NWG_TILE_AUTO)]         # fused F(3,3), partial sums
 
