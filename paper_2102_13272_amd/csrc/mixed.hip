@@ -383,7 +383,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void i
 // consecutive tiles.  Over the 25 level-3 branches, level2_reduce gives each
 // branch's 4 x 4 block and the level-3 A^T accumulates the 12 x 12 block
 // acc[i3r][i3c][rr][cc] (row 4 i3r + rr, column 4 i3c + cc), which goes to
-// Z3[q4][e][n][t], e = 12 row + column (depth 4).
+// Z3[q4][n][t][e], e = 12 row + column (depth 4).
 __global__ __launch_bounds__(64) void output_xform_mix23(const float4* __restrict__ Z,
                                                          float* __restrict__ out, int N, int T,
                                                          long long gstride) {
@@ -422,19 +422,18 @@ __global__ __launch_bounds__(64) void output_xform_mix23(const float4* __restric
         for (int e = 0; e < 16; ++e) acc[i3r][i3c][e] = fmaf(c, po[e >> 2][e & 3], acc[i3r][i3c][e]);
       }
   }
-  const size_t es = (size_t)N * T;          // between consecutive e
-  float* z3 = out + (size_t)q4 * 144 * es + (size_t)n * T + t;
+  // Z3[q4][n][t][e], e = 12 row + column: a thread's 144 values are one
+  // contiguous block (36 float4)
+  float4* z3 = reinterpret_cast<float4*>(out + (((size_t)q4 * N + n) * T + t) * 144);
 #pragma unroll
   for (int i3r = 0; i3r < 3; ++i3r)
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
-      for (int i3c = 0; i3c < 3; ++i3c)
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          const int e = (4 * i3r + rr) * 12 + 4 * i3c + cc;
-          z3[(size_t)e * es] = acc[i3r][i3c][rr * 4 + cc];
-        }
+      for (int i3c = 0; i3c < 3; ++i3c) {
+        const float* a = &acc[i3r][i3c][rr * 4];
+        z3[(4 * i3r + rr) * 3 + i3c] = make_float4(a[0], a[1], a[2], a[3]);
+      }
 }
 
 // Depth 3 (NO = 1): levels 2 and 3 straight to y, one thread per (tile t,
@@ -484,30 +483,34 @@ __global__ __launch_bounds__(64) void output_xform_mix3(const float4* __restrict
   }
 }
 
-// Level 4 (NO = 2): thread (tile t, block element e, channel n) combines the
-// 25 level-4 branches of Z3 into the 3 x 3 blocks of the 36 x 36 tile.
-__global__ __launch_bounds__(64) void output_xform_mix4(const float* __restrict__ Z3,
-                                                        float* __restrict__ y, int N, int Ho,
-                                                        int Wo, int th, int tw, int T) {
-  const int t = blockIdx.x * 64 + threadIdx.x;
-  const int e = blockIdx.y;
-  const int n = blockIdx.z;
-  if (t >= T) return;
-  const size_t es = (size_t)N * T;
-  const float* zp = Z3 + (size_t)e * es + (size_t)n * T + t;
+// Level 4 (NO = 2): thread (block element e, tile t, channel n), lanes on
+// consecutive e (contiguous Z3 reads, 12-column runs of y), combines the 25
+// level-4 branches of Z3 into the 3 x 3 blocks of the 36 x 36 tile.
+__global__ __launch_bounds__(256) void output_xform_mix4(const float* __restrict__ Z3,
+                                                         float* __restrict__ y, int N, int Ho,
+                                                         int Wo, int th, int tw, int T,
+                                                         long long total) {
+  const long long id = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (id >= total) return;
+  const int e = (int)(id % 144);
+  const long long nt = id / 144;            // n T + t
+  const int t = (int)(nt % T);
+  const int n = (int)(nt / T);
+  const size_t bs = (size_t)N * T * 144;    // between level-4 branches
+  const float* zp = Z3 + (size_t)nt * 144 + e;
   float h[5][3];                            // [q4r][i4c]
 #pragma unroll
   for (int q4r = 0; q4r < 5; ++q4r) {
     float v[5];
 #pragma unroll
-    for (int q4c = 0; q4c < 5; ++q4c) v[q4c] = zp[(size_t)(q4r * 5 + q4c) * 144 * es];
+    for (int q4c = 0; q4c < 5; ++q4c) v[q4c] = zp[(size_t)(q4r * 5 + q4c) * bs];
 #pragma unroll
     for (int i = 0; i < 3; ++i) {
-      float s = 0.0f;
+      float sacc = 0.0f;
 #pragma unroll
       for (int q = 0; q < 5; ++q)
-        if (at5(i, q) != 0.0f) s = fmaf(at5(i, q), v[q], s);
-      h[q4r][i] = s;
+        if (at5(i, q) != 0.0f) sacc = fmaf(at5(i, q), v[q], sacc);
+      h[q4r][i] = sacc;
     }
   }
   const int tpi = th * tw;
@@ -524,11 +527,11 @@ __global__ __launch_bounds__(64) void output_xform_mix4(const float* __restrict_
     for (int i4c = 0; i4c < 3; ++i4c) {
       const int col = tx * 36 + 12 * i4c + ec;
       if (col >= Wo) continue;
-      float s = 0.0f;
+      float sacc = 0.0f;
 #pragma unroll
       for (int q = 0; q < 5; ++q)
-        if (at5(i4r, q) != 0.0f) s = fmaf(at5(i4r, q), h[q][i4c], s);
-      yo[(size_t)row * Wo + col] = s;
+        if (at5(i4r, q) != 0.0f) sacc = fmaf(at5(i4r, q), h[q][i4c], sacc);
+      yo[(size_t)row * Wo + col] = sacc;
     }
   }
 }
@@ -606,8 +609,11 @@ hipError_t launch_output_xform_mix(const nwg_plan_info& g, const float* Zf, floa
                      (int)g.T, gstride);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(output_xform_mix4, dim3(tb, 144, (unsigned)g.N), dim3(64), 0, s, Z3, y, g.N,
-                     g.Ho, g.Wo, g.th, g.tw, (int)g.T);
+  const long long total = 144LL * g.N * g.T;
+  const long long blocks = (total + 255) / 256;
+  if (blocks > 0x7fffffffLL || ((uintptr_t)Z3 & 15)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(output_xform_mix4, dim3((unsigned)blocks), dim3(256), 0, s, Z3, y, g.N, g.Ho,
+                     g.Wo, g.th, g.tw, (int)g.T, total);
   return hipGetLastError();
 }
 
