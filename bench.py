@@ -325,6 +325,11 @@ def main():
         except nwg.NwgError:
             kx_ms += ms[0]      # no stage call (depth 0, depthwise): first call
 
+    # the timed steps run with the library's per-stage events off (recording
+    # them puts work between the launches); a second pass of K steps with
+    # them on gives the per-stage times
+    for p in plans:
+        p.set_timing(False)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
@@ -334,7 +339,14 @@ def main():
     torch.cuda.synchronize()
     ms_total = e0.elapsed_time(e1)
     ms_step = ms_total / args.steps
+    for p in plans:
+        p.set_timing(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
     timing = [p.get_timing() for p in plans]
+    for p in plans:
+        p.set_timing(False)
     ms_step_eager = ms_step
     if args.graph:
         # one step captured (weights already transformed, timing off: the
