@@ -56,6 +56,9 @@ E2E = [
     (1, 2, 3, 75, 40, 31, 15),
     (1, 2, 2, 45, 45, 39, 19),
     (2, 33, 20, 40, 40, 23, 11),
+    (3, 4, 5, 37, 50, 20, 0),       # no padding, rectangular, B = 3
+    (1, 6, 7, 90, 30, 12, 5),       # depth 3, a tall image (8 x 3 tiles)
+    (1, 65, 17, 40, 40, 16, 8),     # M = 65, N = 17: ragged kernel-transform blocks
 ]
 
 
