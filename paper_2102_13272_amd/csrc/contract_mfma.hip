@@ -453,8 +453,10 @@ struct DeepTile {
   }
 };
 
+// Two wavefronts per SIMD for 32 x 32 wavefront tiles; a 64 x 32 tile (eight
+// accumulator sets of 8 floatx4) needs the whole register file, one per SIMD.
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
-__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2))) void contract_deep(
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((BM / WM) * (BN / WN) > 1024 ? 1 : 2))) void contract_deep(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
     int N, int T, int ntb, int nnb, int ks) {
   using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
@@ -556,7 +558,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2)
 // xcd_remap) and its wpx work-groups stride through that range, so the
 // tiles that share a group's U and V run together on one L2.
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
-__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(2))) void contract_deep_persist(
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((BM / WM) * (BN / WN) > 1024 ? 1 : 2))) void contract_deep_persist(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
     int N, int T, int ntb, int nnb, int ks, long long G, int wpx) {
   using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
@@ -921,8 +923,8 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
     if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s);
     // T = 64 with N a multiple of 128 (e.g. the mixed nest's 31x31 layer):
     // 128 x 64 blocks, so that V is read once per group (3.52 -> 3.44 ms)
-    if (T == 64 && N % 128 == 0)
-      return launch_deep<128, 64, 4, 2, 8, 4>(U, V, Z, M, N, T, G, s);
+    if (T == 64 && N % 128 == 0)   // four wavefronts of 64 x 32 (one per SIMD): 3.43 -> 3.38 ms
+      return launch_deep<128, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
     if (T >= 64) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
   }
   // small problems (fewer than 256 work-groups with the wide tiles, e.g.
