@@ -116,7 +116,7 @@ def _stage_refs(x, w, pad):
     th, tw = -(-Ho // Mn), -(-Wo // Mn)
     wp = np.zeros((N, M, lv.Kn, lv.Kn))
     wp[:, :, :r, :r] = w
-    U = np.einsum("pk,nmkl,ql->nmpq", KG, wp, KG)
+    U = np.einsum("pk,nmkl,ql->nmpq", KG, wp, KG, optimize=True)
     Hp, Wp = (th - 1) * Mn + Ln, (tw - 1) * Mn + Ln
     xp = np.zeros((B, M, max(Hp, H + pad), max(Wp, W + pad)))
     xp[:, :, pad:pad + H, pad:pad + W] = x
@@ -124,13 +124,13 @@ def _stage_refs(x, w, pad):
     for ty in range(th):
         for tx in range(tw):
             X = xp[:, :, ty * Mn:ty * Mn + Ln, tx * Mn:tx * Mn + Ln]
-            V[:, ty, tx] = np.einsum("pk,bmkl,ql->bmpq", IB, X, IB)
+            V[:, ty, tx] = np.einsum("pk,bmkl,ql->bmpq", IB, X, IB, optimize=True)
     Yh = ewmm(U, V)
     y = np.zeros((B, N, th * Mn, tw * Mn))
     for ty in range(th):
         for tx in range(tw):
             y[:, :, ty * Mn:(ty + 1) * Mn, tx * Mn:(tx + 1) * Mn] = \
-                np.einsum("ip,bnpq,jq->bnij", OA, Yh[:, ty, tx], OA)
+                np.einsum("ip,bnpq,jq->bnij", OA, Yh[:, ty, tx], OA, optimize=True)
     return lv, U, V, Yh, y[:, :, :Ho, :Wo]
 
 
