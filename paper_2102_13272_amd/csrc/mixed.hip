@@ -19,8 +19,9 @@
 //                      16 output channels of a 512-thread work-group in LDS,
 //                      padded to K_n x K_n; the outer G rows fold the kernel
 //                      into the 9 x 9 sub-kernel of the two F(2,3) levels.
-//   input transform  : 16 tiles x 25 level-3 branches per work-group; at
-//                      NO = 2 the work-group owns one level-4 branch, whose
+//   input transform  : 16 (NO = 1) or 32 (NO = 2) tiles x 25 level-3
+//                      branches per work-group; at NO = 2 the work-group
+//                      owns one level-4 branch, whose
 //                      B^T rows the LDS fill applies (74 x 74 -> 26 x 26).
 //                      Level 3 runs per output row (rows, then columns), the
 //                      two F(2,3) levels in registers (10 x 10 -> 16 x 16).
@@ -177,14 +178,15 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
 // Depth 4 runs in two kernels.  input_mix_l4 applies the level-4 B^T rows
 // (q4r along the rows, q4c along the columns, stride 12) to every tile's
 // 74 x 74 window: X4[q4][m][t][26 x 26].
-// input_xform_mix then takes 16 tiles x 25 level-3 branches per work-group:
-// the 16 tiles' 26 x 26 blocks (X4 at depth 4, the raw windows at depth 3)
+// input_xform_mix then takes TPW tiles (32 at depth 4, 16 at depth 3) x 25
+// level-3 branches per work-group: their 26 x 26 blocks (X4 at depth 4, the
+// raw windows at depth 3)
 // go to LDS, level 3 runs per output row (rows, then columns) and the two
 // F(2,3) levels in registers (10 x 10 -> 16 x 16).
 constexpr int kL3 = 26;                     // window side left for levels 1..3
 // per-tile stride in LDS: even, so that column pairs are 8-byte aligned
-// (float2 reads), and 678 = 38 (mod 64), so that the 16 tiles of a
-// quarter-wave start on 16 different even banks
+// (float2 reads), and 678 = 38 (mod 64), so that 32 consecutive tiles
+// start on 32 different even banks
 constexpr int kWS = kL3 * kL3 + 2;
 
 __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
@@ -259,19 +261,22 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
   }
 }
 
-// 256 threads: 16 tiles x 16 slots, slot s taking the level-3 branches s
-// and s + 16 (< 25), so that two work-groups share a CU (one's stores
-// overlap the other's fill and arithmetic).  Work-group -> (level-4 branch
-// q4 (NO = 2), 16-tile chunk, channel m), q4 fastest, numbered so that each
-// XCD takes a contiguous range.
+// 16 TPW threads: TPW tiles x 16 slots, slot s taking the level-3 branches s
+// and s + 16 (< 25); two wavefronts per SIMD (one work-group's stores
+// overlap another's fill and arithmetic).  At depth 4, 32 tiles (512
+// threads, one work-group per CU) write each point's V row in 512-byte runs:
+// 1.394 -> 1.372 ms on the 31 x 31 layer against 16 tiles.  Work-group ->
+// (level-4 branch q4 (NO = 2), TPW-tile chunk, channel m), q4 fastest,
+// numbered so that each XCD takes a contiguous range.
 template <int NO>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix(
+__global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix(
     const float* __restrict__ x, const float* __restrict__ X4, float4* __restrict__ V, int M,
     int H, int W, int pad, int th, int tw, int T, long long qstride) {
   constexpr int Mn = NO == 2 ? 36 : 12;
   constexpr int KK = kL3 * kL3;
-  constexpr int PER = (16 * KK + 255) / 256;  // fill values per thread
-  extern __shared__ float lds[];            // [16][kWS]
+  constexpr int TPW = NO == 2 ? 32 : 16, NT = 16 * TPW;   // tiles, threads per work-group
+  constexpr int PER = (TPW * KK + NT - 1) / NT;  // fill values per thread
+  extern __shared__ float lds[];            // [TPW][kWS]
   long long lid;
   {
     const long long G = (long long)gridDim.x, i = blockIdx.x;
@@ -280,10 +285,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void i
   }
   const int q4 = NO == 2 ? (int)(lid % 25) : 0;
   const long long rest = NO == 2 ? lid / 25 : lid;
-  const int nchunk = (T + 15) / 16;
-  const int t0 = (int)(rest % nchunk) * 16;
+  const int nchunk = (T + TPW - 1) / TPW;
+  const int t0 = (int)(rest % nchunk) * TPW;
   const int m = (int)(rest / nchunk);
-  const int nt = T - t0 < 16 ? T - t0 : 16;   // tiles of this chunk
+  const int nt = T - t0 < TPW ? T - t0 : TPW;   // tiles of this chunk
   // fill: all loads first (PER in flight per thread), then the LDS writes
   {
     float v[PER];
@@ -292,14 +297,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void i
       const float* src = X4 + (((size_t)q4 * M + m) * T + t0) * KK;
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int e = threadIdx.x + 256 * u;
+        const int e = threadIdx.x + NT * u;
         v[u] = e < nt * KK ? src[e] : 0.0f;
       }
     } else {
       const int tpi = th * tw;
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int e = threadIdx.x + 256 * u;
+        const int e = threadIdx.x + NT * u;
         const int tl = e / KK, k = e - tl * KK;
         const int i = k / kL3, j = k - i * kL3;
         float val = 0.0f;
@@ -317,19 +322,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void i
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      const int e = threadIdx.x + 256 * u;
-      if (e < 16 * KK) {
+      const int e = threadIdx.x + NT * u;
+      if (e < TPW * KK) {
         const int tl = e / KK, k = e - tl * KK;
         lds[tl * kWS + k] = v[u];
       }
     }
   }
   __syncthreads();
-  const int tl = threadIdx.x & 15;
+  const int tl = threadIdx.x & (TPW - 1);
   const int t = t0 + tl;
   if (t >= T) return;                       // no barrier below
   const float* win = lds + tl * kWS;
-  for (int slot = threadIdx.x >> 4; slot < 25; slot += 16) {   // slot = 5 q3r + q3c
+  for (int slot = threadIdx.x / TPW; slot < 25; slot += 16) {   // slot = 5 q3r + q3c
   // a row of B^T of F(3,3) has its nonzero taps among 4 consecutive ones,
   // from tap 0 for row 0 and from tap 1 otherwise
   const int q3r = slot / 5, q3c = slot - 5 * q3r;
@@ -574,16 +579,20 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
     return hipErrorInvalidValue;
   float4* V = reinterpret_cast<float4*>(Vf);
   const long long qstride = (long long)g.M * g.T;
-  const long long nwg = (g.T + 15) / 16 * g.M * (no == 2 ? 25 : 1);
+  const int tpw = no == 2 ? 32 : 16;       // tiles per work-group (TPW)
+  const long long nwg = (g.T + tpw - 1) / tpw * g.M * (no == 2 ? 25 : 1);
   if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
-  const size_t lds = (size_t)16 * kWS * sizeof(float);
+  const size_t lds = (size_t)tpw * kWS * sizeof(float);
   if (no == 2) {
     if (g.M > 65535) return hipErrorInvalidValue;
     hipLaunchKernelGGL(input_mix_l4, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x, X4,
                        g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(input_xform_mix<2>, dim3((unsigned)nwg), dim3(256), lds, s, x, X4, V, g.M,
+    const hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_mix<2>),
+                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (ea != hipSuccess) return ea;
+    hipLaunchKernelGGL(input_xform_mix<2>, dim3((unsigned)nwg), dim3(512), lds, s, x, X4, V, g.M,
                        g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride);
   } else {
     hipLaunchKernelGGL(input_xform_mix<1>, dim3((unsigned)nwg), dim3(256), lds, s, x, X4, V, g.M,
