@@ -59,6 +59,7 @@ E2E = [
     (3, 4, 5, 37, 50, 20, 0),       # no padding, rectangular, B = 3
     (1, 6, 7, 90, 30, 12, 5),       # depth 3, a tall image (8 x 3 tiles)
     (1, 65, 17, 40, 40, 16, 8),     # M = 65, N = 17: ragged kernel-transform blocks
+    (10, 2, 3, 72, 72, 31, 15),     # depth 4, T = 40: a full 32-tile input chunk and a ragged one
 ]
 
 
