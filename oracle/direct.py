@@ -42,11 +42,14 @@ def direct_conv2d(x, w, pad: int = 0) -> np.ndarray:
     B, M, H, W, N, r, Ho, Wo = _check(x, w, pad)
     xp = np.pad(x, ((0, 0), (0, 0), (pad, pad), (pad, pad)))
     xpt = xp.transpose(1, 0, 2, 3)            # [M][B][Hp][Wp]
+    # taps outermost, so that each tap's N x M matrix is contiguous and the
+    # product goes to BLAS (numpy multiplies a strided view with its own loop)
+    wt = np.ascontiguousarray(w.transpose(2, 3, 0, 1))   # [r][r][N][M]
     y = np.zeros((N, B * Ho * Wo), dtype=np.float64)
     for u in range(r):
         for v in range(r):
             win = np.ascontiguousarray(xpt[:, :, u:u + Ho, v:v + Wo]).reshape(M, -1)
-            y += w[:, :, u, v] @ win
+            y += wt[u, v] @ win
     return y.reshape(N, B, Ho, Wo).transpose(1, 0, 2, 3).copy()
 
 
