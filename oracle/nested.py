@@ -479,36 +479,3 @@ def nested_depthwise_conv2d(x, w, pad: int = 0, base: Optional[Base] = None,
     V = input_transform(x, gx, exact)
     Yh = ewmm_depthwise(U, V, counter)
     return output_transform(Yh, gx, exact)
-
-
-# ---------------------------------------------------------------------------
-# Point ordering used by the GPU library's Winograd-domain buffers
-# ---------------------------------------------------------------------------
-
-def point_permutation(n: int, l: int = 4) -> np.ndarray:
-    """Map the library's flat point index p to this module's (row, column) point.
-
-    The library orders the P = l^(2n) points of a tile by the base-l digits
-    (q_n^row, q_n^col, q_{n-1}^row, q_{n-1}^col, ..., q_1^row, q_1^col), most
-    significant first, where q_j is the level-j index.  This module indexes a
-    point as [pi_row, pi_col] with pi = (q_1, ..., q_n), q_1 most significant.
-    Returns an int array perm of shape (P, 2) with perm[p] = (pi_row, pi_col).
-    """
-    P = l ** (2 * n)
-    perm = np.zeros((P, 2), dtype=np.int64)
-    for p in range(P):
-        digits = []
-        rem = p
-        for _ in range(2 * n):
-            digits.append(rem % l)
-            rem //= l
-        digits = digits[::-1]       # most significant first
-        q_row = {n - k: digits[2 * k] for k in range(n)}      # level index -> digit
-        q_col = {n - k: digits[2 * k + 1] for k in range(n)}
-        pr = 0
-        pc = 0
-        for j in range(1, n + 1):   # q_1 most significant in this module
-            pr = pr * l + q_row[j]
-            pc = pc * l + q_col[j]
-        perm[p] = (pr, pc)
-    return perm

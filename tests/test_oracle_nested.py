@@ -10,7 +10,7 @@ import pytest
 
 from oracle.direct import brute_force_conv2d, direct_conv2d
 from oracle.nested import (base_f23, ewmm, geometry, input_transform, kernel_transform,
-                           nested_conv2d, output_transform, point_permutation, toom_cook_base)
+                           nested_conv2d, output_transform, toom_cook_base)
 
 INT_CASES = [  # B, M, N, H, W, r, pad  (depth n from r: 1->0, 2-3->1, 4-7->2, 8-15->3, 16-31->4)
     (2, 3, 2, 7, 9, 1, 0),
@@ -75,10 +75,3 @@ def test_stage_shapes_and_composition():
     assert g.lv.n == 2 and (g.th, g.tw) == (3, 3)
     assert U.shape == (4, 3, 16, 16) and V.shape == (2, 3, 3, 3, 16, 16) and Yh.shape == (2, 3, 3, 4, 16, 16)
     assert np.array_equal(output_transform(Yh, g), direct_conv2d(x, w, 3))
-
-
-@pytest.mark.parametrize("n", [1, 2, 3])
-def test_point_permutation_is_bijection(n):
-    perm = point_permutation(n)
-    assert len({tuple(p) for p in perm}) == 4 ** (2 * n)
-    assert perm.min() == 0 and perm.max() == 4 ** n - 1
