@@ -158,133 +158,109 @@ def traffic_from_counters(workload: str, tile: str, fetch_csv: str, write_csv: s
     return out
 
 
-def cpu_baseline(workload: str, target_s: float):
-    """The fp64 oracle timed on this host's cores over a bounded sample."""
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return max([d.get("num_threads", 1) for d in threadpool_info()
+                    if d.get("user_api") == "blas"] or [1])
+    except Exception:
+        return os.cpu_count() or 1
+
+
+def host_cores() -> dict:
+    """The host's logical CPUs (os.cpu_count, like nproc without a mask) and
+    the ones this process may run on (sched_getaffinity, what nproc prints)."""
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except Exception:
+        usable = os.cpu_count() or 1
+    return {"cpu_count": os.cpu_count() or 1, "nproc": usable}
+
+
+REL_L2, MAX_ABS_FRAC = 1e-4, 1e-3     # the fp32 bar against the fp64 oracle
+
+
+def cpu_baseline(workload: str, target_s: float, outputs=None):
+    """The fp64 oracle timed on this host's cores over a bounded sample of the
+    workload (whole images, all channels, every layer), and the parity of the
+    GPU outputs of the same run (a dict of name -> numpy [B][N][Ho][Wo] of the
+    last layer) on the sampled images: rel-L2 and max-abs over all their
+    outputs, against the fp32 bar.  Returns (baseline, {name: parity})."""
     from oracle.direct import direct_conv2d, direct_depthwise_conv2d
     from paper_2102_13272_amd.workloads import WORKLOADS, make_workload
 
     def conv(L, xs, w):
         return (direct_depthwise_conv2d if L.depthwise else direct_conv2d)(xs, w, L.pad)
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([d.get("num_threads", 1) for d in threadpool_info()
-                       if d.get("user_api") == "blas"] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
     wl = WORKLOADS[workload]
     x, ws = make_workload(workload)
+    B = wl.layers[0].B
     flop = 0.0
+    refs = []
     t0 = time.perf_counter()
-    images = 0
-    if len(wl.layers) == 1:
-        L = wl.layers[0]
-        for b in range(L.B):
-            conv(L, x[b:b + 1], ws[0])
+    for b in range(B):
+        cur = x[b:b + 1].astype(np.float64)
+        for L, w in zip(wl.layers, ws):
+            cur = conv(L, cur, w)
             flop += L.direct_flop / L.B
-            images += 1
-            if time.perf_counter() - t0 >= target_s:
-                break
-        sample = f"{images} of {L.B} images of the workload, all channels"
-    else:
-        for b in range(wl.layers[0].B):
-            cur = x[b:b + 1].astype(np.float64)
-            for L, w in zip(wl.layers, ws):
-                cur = conv(L, cur, w)
-                flop += L.direct_flop / L.B
-            images += 1
-            if time.perf_counter() - t0 >= target_s:
-                break
-        sample = f"{images} of {wl.layers[0].B} images through all {len(wl.layers)} layers"
+        refs.append(cur[0])
+        if time.perf_counter() - t0 >= target_s:
+            break
     dt = time.perf_counter() - t0
-    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": sample, "seconds": round(dt, 3)}
+    images = len(refs)
+    what = "all channels" if len(wl.layers) == 1 else f"through all {len(wl.layers)} layers"
+    base = {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": blas_threads(), "kind": "oracle",
+            "sample": f"{images} of {B} images of the workload, {what}",
+            "seconds": round(dt, 3), **{"host_" + k: v for k, v in host_cores().items()}}
+    ref = np.stack(refs)
+    den = np.linalg.norm(ref)
+    scale = float(np.abs(ref).max())
+    parity = {}
+    for key, y in (outputs or {}).items():
+        got = np.asarray(y[:images], dtype=np.float64)
+        rel = float(np.linalg.norm(got - ref) / (den if den > 0 else 1.0))
+        mabs = float(np.abs(got - ref).max())
+        ok = bool(np.isfinite(got).all() and rel <= REL_L2 and mabs <= MAX_ABS_FRAC * scale)
+        parity[key] = {"rel_l2": rel, "max_abs_over_max": mabs / scale if scale else mabs,
+                       "images": images, "outputs": int(ref.size), "ok": ok,
+                       "bar": {"rel_l2": REL_L2, "max_abs_over_max": MAX_ABS_FRAC},
+                       "oracle": "fp64 direct correlation"}
+    return base, parity
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c5_r31")
-    ap.add_argument("--tile", choices=["f23", "f33", "auto", "ld", "mix"], default="auto",
-                    help="Winograd base: F(2x2,3x3) nests (any r <= 31); F(3x3,3x3) nests for "
-                         "the dense layers with r <= 9 (others keep F(2x2,3x3)); the "
-                         "library's per-layer choice (NWG_TILE_AUTO); the linear "
-                         "decomposition on F(2x2,3x3) (Sec. II.B) for the dense layers with "
-                         "r > 1; or the mixed nest (F(2,3) at levels 1-2, F(3,3) above) for "
-                         "the dense layers with r >= 8")
-    ap.add_argument("--precision", choices=["fp32", "bf16_split"], default="fp32",
-                    help="contraction arithmetic: fp32 MFMA, or the two-term bf16 split of U "
-                         "and V on bf16 MFMA with fp32 accumulation (plans that can take it)")
-    ap.add_argument("--graph", action="store_true",
-                    help="time the step as replays of one HIP graph holding every layer's "
-                         "launches (per-kernel times still come from an eager timed region)")
-    ap.add_argument("--pipeline-parts", type=int, default=0,
-                    help="input-transform/contraction pieces on two streams (0: the library's "
-                         "default for each plan, 1: off)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="approximate CPU time for the oracle baseline sample")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-compare", action="store_true",
-                    help="skip the all-F(2x2,3x3) comparison step (e.g. under a counter run)")
-    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
-                    help="first copy a float32 buffer of this many MiB (a plain copy kernel of "
-                         "known size, to scale hardware byte counters)")
-    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="no GPU work: turn two rocprofv3 --pmc counter files (FETCH_SIZE, "
-                         "WRITE_SIZE) of a --calibrate-copy-mib run into "
-                         "profiles/traffic_<workload>_<tile>.json")
-    args = ap.parse_args()
-    if args.traffic_from:
-        res = traffic_from_counters(args.workload, args.tile, args.traffic_from[0],
-                                    args.traffic_from[1], args.calibrate_copy_mib or 1024)
-        print(json.dumps(res, indent=1))
-        return
-    if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); the path "
-              f"shards over output tiles or Winograd points, which is not built here.",
-              file=sys.stderr)
-        sys.exit(2)
+TILE_NAMES = {0: "F(2x2,3x3)", 1: "F(3x3,3x3)", 2: "linear decomposition on F(2x2,3x3)",
+              3: "mixed F(2,3)/F(3,3) nest"}
 
-    import torch
-    from paper_2102_13272_amd import nwg
+
+def run_workload(torch, nwg, name: str, tile: str, precision: str, steps: int, warmup: int,
+                 pipeline_parts: int = 0, graph: bool = False) -> dict:
+    """Plans for every layer of the workload, warm-up (which transforms the
+    weights once), K timed steps with the library's per-stage events off, then
+    K more with them on for the per-stage times.  Returns the measurements, the
+    plans (open) and the last layer's output tensor of the timed run."""
     from paper_2102_13272_amd.workloads import WORKLOADS, make_workload
-
-    if not torch.cuda.is_available():
-        print("bench.py: no GPU visible", file=sys.stderr)
-        sys.exit(1)
-    nwg.load_library()
-    torch.cuda.set_device(0)
-    if args.calibrate_copy_mib > 0:
-        n = args.calibrate_copy_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-    wl = WORKLOADS[args.workload]
-    x, ws = make_workload(args.workload)
+    wl = WORKLOADS[name]
+    x, ws = make_workload(name)
     xd = torch.from_numpy(x).to("cuda")
     wds = [torch.from_numpy(w).to("cuda") for w in ws]
+
     def tile_for(L):
-        if args.tile == "auto":
+        if tile == "auto":
             return nwg.NWG_TILE_AUTO
-        if args.tile == "f33" and not L.depthwise and L.r <= 9:
+        if tile == "f33" and not L.depthwise and L.r <= 9:
             return nwg.NWG_TILE_F3X3_3X3
-        if args.tile == "ld" and not L.depthwise and L.r > 1:
+        if tile == "ld" and not L.depthwise and L.r > 1:
             return nwg.NWG_TILE_LD_F2X2_3X3
-        if args.tile == "mix" and not L.depthwise and L.r >= 8:
+        if tile == "mix" and not L.depthwise and L.r >= 8:
             return nwg.NWG_TILE_MIX_F23_F33
         return nwg.NWG_TILE_F2X2_3X3
 
     plans = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, tile=tile_for(L),
                       depthwise=L.depthwise) for L in wl.layers]
-    if args.pipeline_parts:
+    if pipeline_parts:
         for p in plans:
-            if p.info["pipeline_parts"] > 1 or args.pipeline_parts == 1:
-                p.set_pipeline(args.pipeline_parts)
-    if args.precision == "bf16_split":
+            if p.info["pipeline_parts"] > 1 or pipeline_parts == 1:
+                p.set_pipeline(pipeline_parts)
+    if precision == "bf16_split":
         for p in plans:
             try:
                 p.set_precision(nwg.NWG_PRECISION_BF16_SPLIT)
@@ -302,7 +278,7 @@ def main():
     # warm-up (includes the one kernel transform per layer), then timed steps
     for p in plans:
         p.set_timing(True)
-    for _ in range(max(1, args.warmup)):
+    for _ in range(max(1, warmup)):
         step()
     torch.cuda.synchronize()
     warm = [p.get_timing() for p in plans]
@@ -333,166 +309,271 @@ def main():
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     e1.record(stream)
     torch.cuda.synchronize()
-    ms_total = e0.elapsed_time(e1)
-    ms_step = ms_total / args.steps
+    ms_step = e0.elapsed_time(e1) / steps
+    y_timed = outs[-1].cpu().numpy()
     for p in plans:
         p.set_timing(True)
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     torch.cuda.synchronize()
     timing = [p.get_timing() for p in plans]
     for p in plans:
         p.set_timing(False)
     ms_step_eager = ms_step
-    if args.graph:
+    if graph:
         # one step captured (weights already transformed, timing off: the
         # captured work is exactly the step's kernels), then K replays timed
-        for p in plans:
-            p.set_timing(False)
         cap = torch.cuda.Stream()
         cap.wait_stream(stream)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=cap):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
             step(torch.cuda.current_stream())
-        graph.replay()
+        g.replay()
         torch.cuda.synchronize()
         g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         g0.record(stream)
-        for _ in range(args.steps):
-            graph.replay()
+        for _ in range(steps):
+            g.replay()
         g1.record(stream)
         torch.cuda.synchronize()
-        ms_step = g0.elapsed_time(g1) / args.steps
+        ms_step = g0.elapsed_time(g1) / steps
 
     direct_flop = float(sum(L.direct_flop for L in wl.layers))
-    value = direct_flop / (ms_step * 1e-3) / 1e12
-
     # per-stage accounting summed over layers
     stages = {}
     for p, (ms, cnt) in zip(plans, timing):
         bf = stage_bytes_flops(p.info)
         parts = p.info["pipeline_parts"]
-        for si, name in enumerate(STAGES):
-            if name == "kernel_transform" or cnt[si] == 0:
+        for si, sname in enumerate(STAGES):
+            if sname == "kernel_transform" or cnt[si] == 0:
                 continue
-            b, f = bf[name]
-            if name in ("input_transform", "contraction") and parts > 1:
+            b, f = bf[sname]
+            if sname in ("input_transform", "contraction") and parts > 1:
                 # the two-stream pipeline launches these in `parts` pieces
                 b, f = b / parts, f / parts
-            s = stages.setdefault(name, {"ms_total": 0.0, "launches": 0, "bytes": 0.0,
-                                         "flop": 0.0, "per_layer": []})
-            s["ms_total"] += ms[si]
-            s["launches"] += cnt[si]
-            s["bytes"] += b * cnt[si]
-            s["flop"] += f * cnt[si]
-            s["per_layer"].append({"r": p.info["r"], "n": p.info["n"],
-                                   "avg_us": round(1e3 * ms[si] / cnt[si], 2),
-                                   **({"pieces": parts} if parts > 1 and name in (
-                                       "input_transform", "contraction") else {}),
-                                   **({"fused_input": True} if p.info["fused_input"]
-                                      and name == "contraction" else {}),
-                                   **({"fused_conv": True} if p.info["fused_conv"]
-                                      and name == "contraction" else {})})
+            st = stages.setdefault(sname, {"ms_total": 0.0, "launches": 0, "bytes": 0.0,
+                                           "flop": 0.0, "per_layer": []})
+            st["ms_total"] += ms[si]
+            st["launches"] += cnt[si]
+            st["bytes"] += b * cnt[si]
+            st["flop"] += f * cnt[si]
+            st["per_layer"].append({"r": p.info["r"], "n": p.info["n"],
+                                    "avg_us": round(1e3 * ms[si] / cnt[si], 2),
+                                    **({"pieces": parts} if parts > 1 and sname in (
+                                        "input_transform", "contraction") else {}),
+                                    **({"fused_input": True} if p.info["fused_input"]
+                                       and sname == "contraction" else {}),
+                                    **({"fused_conv": True} if p.info["fused_conv"]
+                                       and sname == "contraction" else {})})
     # split precision: the MFMAs run on bf16 and execute 4 partial products
     # per algorithmic multiply-add
-    split = args.precision == "bf16_split"
+    split = any(p.info["precision"] == nwg.NWG_PRECISION_BF16_SPLIT for p in plans)
     peak_mm = PEAK_BF16_MFMA_TFLOPS if split else PEAK_FP32_MFMA_TFLOPS
     flop_x = 4.0 if split else 1.0
     detail = {}
-    for name, s in stages.items():
-        sec = s["ms_total"] * 1e-3
-        gbs = s["bytes"] / sec / 1e9
-        tfs = s["flop"] / sec / 1e12
-        detail[name] = {"ms_per_step": round(s["ms_total"] / args.steps, 4),
-                        "launches_per_step": s["launches"] // args.steps,
-                        "GB_s": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
-                        "TFLOP_s": round(tfs, 2),
-                        "mfma_frac": round(flop_x * tfs / peak_mm, 4),
-                        "per_layer": s["per_layer"]}
+    for sname, st in stages.items():
+        sec = st["ms_total"] * 1e-3
+        gbs = st["bytes"] / sec / 1e9
+        tfs = st["flop"] / sec / 1e12
+        detail[sname] = {"ms_per_step": round(st["ms_total"] / steps, 4),
+                         "launches_per_step": st["launches"] // steps,
+                         "GB_s": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+                         "TFLOP_s": round(tfs, 2),
+                         "mfma_frac": round(flop_x * tfs / peak_mm, 4),
+                         "per_layer": st["per_layer"]}
 
     # dominant kernel: largest time share of the step
     dom = max(stages, key=lambda k: stages[k]["ms_total"])
-    s = stages[dom]
-    avg_s = s["ms_total"] * 1e-3 / s["launches"]
-    ai = flop_x * s["flop"] / s["bytes"] if s["bytes"] else 0.0
+    st = stages[dom]
+    avg_s = st["ms_total"] * 1e-3 / st["launches"]
+    ai = flop_x * st["flop"] / st["bytes"] if st["bytes"] else 0.0
     ridge = peak_mm * 1e12 / (PEAK_HBM_GBS * 1e9)
     if dom == "contraction" and ai > ridge:
-        ach = flop_x * s["flop"] / s["launches"] / avg_s / 1e12
+        ach = flop_x * st["flop"] / st["launches"] / avg_s / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak_mm,
                 "unit": "TFLOP/s", "frac": round(ach / peak_mm, 4)}
     else:
-        ach = s["bytes"] / s["launches"] / avg_s / 1e9
+        ach = st["bytes"] / st["launches"] / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4)}
     roof["kernel"] = dom
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
-    roof["traffic"] = (measured_traffic(args.workload, dom, args.tile)
-                       if len(plans) == 1 and not split else None)
+    traffic = measured_traffic(name, dom, tile) if len(plans) == 1 and not split else None
+    roof["traffic"] = traffic
+    roof["traffic_source"] = (f"profiles/traffic_{name}_{tile}.json: rocprofv3 FETCH_SIZE and "
+                              f"WRITE_SIZE of this kernel source, scaled by a device copy"
+                              if traffic is not None else None)
 
     L0 = wl.layers[0]
-    cfg = {"workload": args.workload, "layers": len(wl.layers), "B": L0.B,
+    cfg = {"workload": name, "layers": len(wl.layers), "B": L0.B,
            "M": L0.M, "N": wl.layers[-1].N, "H": L0.H, "W": L0.W,
            "r": [L.r for L in wl.layers] if len(wl.layers) > 1 else L0.r,
            "pad": [L.pad for L in wl.layers] if len(wl.layers) > 1 else L0.pad,
-           "base": [{nwg.NWG_TILE_F3X3_3X3: "F(3x3,3x3)",
-                     nwg.NWG_TILE_LD_F2X2_3X3: "linear decomposition on F(2x2,3x3)",
-                     nwg.NWG_TILE_MIX_F23_F33: "mixed F(2,3)/F(3,3) nest"}.get(
-                         p.info["tile"], "F(2x2,3x3)") for p in plans]
-                    if args.tile != "f23" else "F(2x2,3x3)",
+           "base": [TILE_NAMES.get(p.info["tile"], "F(2x2,3x3)") for p in plans]
+                   if tile != "f23" else "F(2x2,3x3)",
            "nesting_depth": [p.info["n"] for p in plans],
            "pipeline_parts": [p.info["pipeline_parts"] for p in plans],
-           "launch": "hip-graph replay" if args.graph else "eager"}
+           "launch": "hip-graph replay" if graph else "eager"}
+    return {"plans": plans, "ms_step": ms_step, "ms_step_eager": ms_step_eager,
+            "value": direct_flop / (ms_step * 1e-3) / 1e12, "direct_flop": direct_flop,
+            "stages": detail, "roofline": roof, "config": cfg, "kx_ms": kx_ms,
+            "kx_first_ms": kx_first_ms, "split": split, "y": y_timed}
+
+
+def close(res):
+    for p in res["plans"]:
+        p.close()
+    res["plans"] = []
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c5_r31")
+    ap.add_argument("--tile", choices=["f23", "f33", "auto", "ld", "mix"], default="auto",
+                    help="Winograd base: F(2x2,3x3) nests (any r <= 31); F(3x3,3x3) nests for "
+                         "the dense layers with r <= 9 (others keep F(2x2,3x3)); the "
+                         "library's per-layer choice (NWG_TILE_AUTO); the linear "
+                         "decomposition on F(2x2,3x3) (Sec. II.B) for the dense layers with "
+                         "r > 1; or the mixed nest (F(2,3) at levels 1-2, F(3,3) above) for "
+                         "the dense layers with r >= 8")
+    ap.add_argument("--precision", choices=["fp32", "bf16_split"], default="fp32",
+                    help="contraction arithmetic: fp32 MFMA, or the two-term bf16 split of U "
+                         "and V on bf16 MFMA with fp32 accumulation (plans that can take it)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the step as replays of one HIP graph holding every layer's "
+                         "launches (per-kernel times still come from an eager timed region)")
+    ap.add_argument("--pipeline-parts", type=int, default=0,
+                    help="input-transform/contraction pieces on two streams (0: the library's "
+                         "default for each plan, 1: off)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time for the oracle baseline sample (and parity)")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle: no cpu_baseline and no parity fields")
+    ap.add_argument("--no-compare", action="store_true",
+                    help="skip the all-F(2x2,3x3) comparison step (e.g. under a counter run)")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="skip the other workloads' lines (per_config)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="first copy a float32 buffer of this many MiB (a plain copy kernel of "
+                         "known size, to scale hardware byte counters)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU work: turn two rocprofv3 --pmc counter files (FETCH_SIZE, "
+                         "WRITE_SIZE) of a --calibrate-copy-mib run into "
+                         "profiles/traffic_<workload>_<tile>.json")
+    args = ap.parse_args()
+    if args.traffic_from:
+        res = traffic_from_counters(args.workload, args.tile, args.traffic_from[0],
+                                    args.traffic_from[1], args.calibrate_copy_mib or 1024)
+        print(json.dumps(res, indent=1))
+        return
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); the path "
+              f"shards over output tiles or Winograd points, which is not built here.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2102_13272_amd import nwg
+    from paper_2102_13272_amd.workloads import WORKLOADS
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    nwg.load_library()
+    torch.cuda.set_device(0)
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    res = run_workload(torch, nwg, args.workload, args.tile, args.precision, args.steps,
+                       args.warmup, args.pipeline_parts, args.graph)
+    cfg = res["config"]
     out = {
-        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "metric": METRIC, "value": round(res["value"], 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(res["ms_step"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": ("f32" if all(p.info["precision"] == nwg.NWG_PRECISION_FP32 for p in plans)
-                  else "bf16-split/f32-acc"),
-        "data": "synthetic", "config": cfg, "roofline": roof,
-        "stages": detail,
-        "kernel_transform_ms_once": round(kx_ms, 4),
-        "kernel_transform_ms_first_call": round(kx_first_ms, 4),
-        "value_incl_kernel_transform": round(direct_flop / ((ms_step + kx_ms) * 1e-3) / 1e12, 3),
-        "direct_flop_per_step": direct_flop,
+        "dtype": "bf16-split/f32-acc" if res["split"] else "f32",
+        "data": "synthetic", "config": cfg, "roofline": res["roofline"],
+        "stages": res["stages"],
+        "kernel_transform_ms_once": round(res["kx_ms"], 4),
+        "kernel_transform_ms_first_call": round(res["kx_first_ms"], 4),
+        "value_incl_kernel_transform": round(
+            res["direct_flop"] / ((res["ms_step"] + res["kx_ms"]) * 1e-3) / 1e12, 3),
+        "direct_flop_per_step": res["direct_flop"],
     }
     if args.graph:
-        out["ms_per_step_eager"] = round(ms_step_eager, 4)
-    if not args.no_compare and any(p.info["tile"] != nwg.NWG_TILE_F2X2_3X3 for p in plans):
+        out["ms_per_step_eager"] = round(res["ms_step_eager"], 4)
+    y_main = res["y"]
+    compare_tile = any(p.info["tile"] != nwg.NWG_TILE_F2X2_3X3 for p in res["plans"])
+    close(res)
+    y_f23 = None
+    if not args.no_compare and compare_tile:
         # the same workload with every layer on F(2x2,3x3) nests, timed the
-        # same way (eager), for comparison
-        f23 = [nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, depthwise=L.depthwise)
-               for L in wl.layers]
-        outs2 = [torch.empty(p.y_shape, dtype=torch.float32, device="cuda") for p in f23]
-
-        def step2():
-            cur = xd
-            for p, w, y in zip(f23, wds, outs2):
-                p.conv2d(cur, w, y, stream)
-                cur = y
-        for _ in range(max(1, args.warmup)):
-            step2()
-        torch.cuda.synchronize()
-        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        f0.record(stream)
-        for _ in range(args.steps):
-            step2()
-        f1.record(stream)
-        torch.cuda.synchronize()
-        ms2 = f0.elapsed_time(f1) / args.steps
-        out["f2x2_3x3_only"] = {"ms_per_step": round(ms2, 4),
-                                "value": round(direct_flop / (ms2 * 1e-3) / 1e12, 3)}
-        for p in f23:
-            p.close()
-        del outs2
+        # same way in the same run, for comparison
+        r2 = run_workload(torch, nwg, args.workload, "f23", args.precision, args.steps,
+                          args.warmup)
+        out["f2x2_3x3_only"] = {
+            "ms_per_step": round(r2["ms_step"], 4), "value": round(r2["value"], 3),
+            "roofline": {k: r2["roofline"][k] for k in ("bound", "frac", "kernel")},
+            "stages": {k: {f: v[f] for f in ("ms_per_step", "GB_s", "hbm_frac", "TFLOP_s",
+                                              "mfma_frac")}
+                       for k, v in r2["stages"].items()}}
+        y_f23 = r2["y"]
+        close(r2)
+    failed = []
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
-    for p in plans:
-        p.close()
+        outs = {"timed": y_main}
+        if y_f23 is not None:
+            outs["f2x2_3x3_only"] = y_f23
+        base, par = cpu_baseline(args.workload, args.cpu_seconds, outs)
+        out["cpu_baseline"] = base
+        out["parity"] = par["timed"]
+        if "f2x2_3x3_only" in par:
+            out["f2x2_3x3_only"]["parity"] = par["f2x2_3x3_only"]
+        failed += [args.workload + ("" if k == "timed" else f" ({k})")
+                   for k, v in par.items() if not v["ok"]]
+    if not args.no_per_config and args.workload == "c5_r31":
+        # the other configs of the benchmark, each timed the same way, with its
+        # dominant kernel's roofline and (unless skipped) its parity
+        per = {}
+        for name in ("c1_r4_valid", "c2_r7", "c3_r13", "c4_sr_stack"):
+            rk = run_workload(torch, nwg, name, args.tile, args.precision, args.steps,
+                              args.warmup)
+            ent = {"ms_per_step": round(rk["ms_step"], 4), "value": round(rk["value"], 3),
+                   "unit": "TFLOP/s", "config": rk["config"],
+                   "roofline": {k: rk["roofline"][k]
+                                for k in ("bound", "achieved", "peak", "unit", "frac",
+                                          "kernel", "avg_launch_us")},
+                   "stages": {k: {f: v[f] for f in ("ms_per_step", "GB_s", "hbm_frac",
+                                                     "TFLOP_s", "mfma_frac")}
+                              for k, v in rk["stages"].items()}}
+            y_k = rk["y"]
+            close(rk)
+            if not args.no_cpu_baseline:
+                bk, pk = cpu_baseline(name, 2.0, {"timed": y_k})
+                ent["cpu_baseline"] = bk
+                ent["parity"] = pk["timed"]
+                if not pk["timed"]["ok"]:
+                    failed.append(name)
+            per[name] = ent
+        out["per_config"] = per
     print(json.dumps(out), flush=True)
+    if failed:
+        print(f"bench.py: output outside the fp32 bar against the oracle: {failed}",
+              file=sys.stderr)
+        sys.exit(3)
 
 
 if __name__ == "__main__":

@@ -48,7 +48,15 @@
  *
  * Errors: functions returning int give NWG_OK (0) or a negative status;
  * functions returning a pointer give NULL.  nwg_last_error() then returns a
- * message for the calling thread.
+ * message, and nwg_last_status() the status (for a NULL pointer: why), for
+ * the calling thread.  A launch that fails returns NWG_EHIP; a kernel that
+ * fails while it runs is reported by the stream's next synchronising call,
+ * or, with the environment variable NWG_DEBUG_SYNC set, by the call that
+ * queued it (every call then waits for each kernel it queues: a debugging
+ * aid, not for use under stream capture).
+ *
+ * Limits: each input and output map holds fewer than 2^31 values, and no
+ * tensor or workspace buffer more than 1e13 bytes (NWG_EUNSUPPORTED).
  */
 #ifndef NWG_H
 #define NWG_H
@@ -177,18 +185,29 @@ typedef struct nwg_plan_info {
                                    F(2,3) levels (1 or 2); else 0 */
 } nwg_plan_info;
 
-/* Geometry of a convolution without touching any device (host-only).
- * Returns NWG_EINVAL for a bad shape, NWG_EUNSUPPORTED for r > 31 (r > 9 on
- * NWG_TILE_F3X3_3X3) or an unknown tile. */
+/* Geometry of a convolution without touching any device (host-only): the
+ * level recurrence of Sec. III.B (the multi-level nesting paragraph; Alg. 1's
+ * expression tree read as a chain of n bases), with level strides
+ * s_j = min(M_j, K_j) where the base has m != r.  Writes *out and returns
+ * NWG_OK; NWG_EINVAL for a NULL out, a dimension <= 0, pad < 0 or a kernel
+ * larger than the padded input; NWG_EUNSUPPORTED for an unknown tile, a
+ * kernel beyond the tile's depth (r > 31 on F(2x2,3x3) and AUTO, r > 9 on
+ * F(3x3,3x3), r > 39 on the mixed nest) or a size beyond the limits above. */
 int nwg_plan_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
                       nwg_plan_info* out);
 
-/* Create a plan ("valid" convolution, pad = 0) and allocate its workspace on
- * the current device.  NULL on a bad shape, unsupported request or failed
- * allocation (see nwg_last_error). */
+/* Create a plan for the convolution of Sec. II.A ("valid": pad = 0) -- M
+ * input maps of H x W, N groups of M-channel r x r kernels, B images --
+ * computed by nested Winograd (Sec. III.B) on `tile`, and allocate its
+ * workspace on the current device (workspace_bytes; the caller's tensors
+ * are not part of it).  NULL on failure, with nwg_last_status():
+ * NWG_EINVAL / NWG_EUNSUPPORTED as for nwg_plan_geometry (and r = 1 with
+ * pad > 0: NWG_EUNSUPPORTED), NWG_ENOMEM when a device allocation fails
+ * (nothing stays allocated), NWG_EHIP when no device is available. */
 nwg_plan* nwg_plan_create(int B, int M, int N, int H, int W, int r, int tile);
 
-/* Same with explicit zero padding on all four sides ("same": pad = (r-1)/2). */
+/* Same with explicit zero padding on all four sides ("same": pad = (r-1)/2;
+ * the problem statement of Sec. II.A with the input zero-padded). */
 nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad, int tile);
 
 /* --- Depthwise convolution (Table I's depth-wise row) --------------------
@@ -216,11 +235,18 @@ void nwg_plan_destroy(nwg_plan* plan);
 /* Copy the plan's geometry into *out. */
 int nwg_plan_query(const nwg_plan* plan, nwg_plan_info* out);
 
-/* y = conv(x, w): kernel transform (only when w differs from the cached weight
- * pointer or after nwg_plan_set_weights), then the input transform, the
- * per-point channel contraction and the output transform, all queued on
- * `stream`.  For r = 1 the contraction reads x and writes y directly.
- * Mutating w in place requires nwg_plan_set_weights before the next call. */
+/* y = conv(x, w), the correlation of Sec. II.A, by the steps of Sec. III.B:
+ * the nested kernel transform (only when w differs from the cached weight
+ * pointer or after nwg_plan_set_weights), then the nested input transform,
+ * the per-point channel contraction (Sec. II.B: the M input channels summed
+ * in the Winograd domain) and the nested output transform, all queued on
+ * `stream`.  x [B][M][H][W], w [N][M][r][r], y [B][N][Ho][Wo]: contiguous
+ * fp32 device buffers of the plan's shape, 16-byte aligned, y not
+ * overlapping x or w.  For r = 1 the contraction reads x and writes y
+ * directly.  The weight cache is keyed by the pointer only: mutating w in
+ * place, or passing a new weight tensor at a freed one's address, requires
+ * nwg_plan_set_weights before the next call.  NWG_EINVAL for a NULL
+ * argument, NWG_EHIP when a launch fails. */
 int nwg_conv2d(nwg_plan* plan, const float* x, const float* w, float* y, void* stream);
 
 /* Re-run the kernel transform of w into the plan's cached U now. */
@@ -296,6 +322,11 @@ int nwg_plan_get_timing(nwg_plan* plan, double ms[4], long long count[4]);
 
 /* Message for the last error on the calling thread ("" if none). */
 const char* nwg_last_error(void);
+
+/* Status of the last error on the calling thread (NWG_OK if none): for the
+ * calls that return NULL, the reason (NWG_EINVAL, NWG_EUNSUPPORTED,
+ * NWG_ENOMEM or NWG_EHIP). */
+int nwg_last_status(void);
 
 /* Library version string. */
 const char* nwg_version(void);

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libnwg.so")
-SOURCES = ["nwg_api.hip", "kernel_xform.hip", "input_xform.hip", "contract_mfma.hip",
+SOURCES = ["plan.cpp", "nwg_api.hip", "kernel_xform.hip", "input_xform.hip", "contract_mfma.hip",
            "output_xform.hip", "fused_small.hip",
            "depthwise.hip", "small_conv.hip", "f33.hip", "mixed.hip"]
 ARCH = "gfx950"
@@ -46,7 +46,7 @@ def build(verbose: bool = False, extra_flags=()) -> str:
     os.makedirs(BUILD, exist_ok=True)
     jobs = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
         jobs.append((obj, [hipcc, *CFLAGS, *extra_flags, "-c", os.path.join(CSRC, src), "-o", obj]))
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
         outs = list(ex.map(lambda j: _run(j[1]), jobs))

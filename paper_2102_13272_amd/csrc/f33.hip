@@ -977,42 +977,6 @@ hipError_t launch_sum_parts(float* Z, size_t n, int parts, hipStream_t s) {
   return hipGetLastError();
 }
 
-// The fused depth-2 kernel: dense F(3,3) plans with one output channel.
-bool input_contract5_applies(const nwg_plan_info& g) {
-  return g.tile == NWG_TILE_F3X3_3X3 && g.n == 2 && g.N == 1 && !g.depthwise;
-}
-
-namespace {
-struct IC5Shape {
-  int RX, RY, nbx, nby, groups, mper;
-  size_t lds;
-};
-IC5Shape ic5_shape(const nwg_plan_info& g) {
-  IC5Shape c;
-  c.RX = g.tw < 64 ? g.tw : 64;
-  c.RY = 64 / c.RX;
-  if (c.RY > g.th) c.RY = g.th;
-  c.nbx = (g.tw + c.RX - 1) / c.RX;
-  c.nby = (g.th + c.RY - 1) / c.RY;
-  // input-channel groups: about 512 work-groups in all, at least 2 channels each
-  const long long boxes = (long long)c.nbx * c.nby * g.B;
-  long long want = (512 + boxes - 1) / boxes;
-  const long long maxg = (g.M + 1) / 2;
-  if (want > maxg) want = maxg;
-  if (want < 1) want = 1;
-  c.mper = (int)((g.M + want - 1) / want);
-  c.groups = (g.M + c.mper - 1) / c.mper;
-  c.lds = (size_t)(((c.RY - 1) * 9 + 17) * ((c.RX - 1) * 9 + 17) + 625) * sizeof(float);
-  return c;
-}
-}  // namespace
-
-int input_contract5_parts(const nwg_plan_info& g) { return ic5_shape(g).groups; }
-
-size_t input_contract5_zbytes(const nwg_plan_info& g) {
-  return (size_t)ic5_shape(g).groups * (size_t)(g.P / 25) * 9 * g.N * g.T * sizeof(float);
-}
-
 hipError_t launch_input_contract5(const nwg_plan_info& g, const float* x, const float* U,
                                   float* Zp, hipStream_t s) {
   if (!input_contract5_applies(g)) return hipErrorInvalidValue;
@@ -1023,13 +987,6 @@ hipError_t launch_input_contract5(const nwg_plan_info& g, const float* x, const 
                      s, x, U, Zp, g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T, c.RX, c.RY, c.nbx,
                      c.nby, c.mper, (size_t)(g.P / 25) * 9 * g.N * g.T);
   return hipGetLastError();
-}
-
-// The contraction fused into the output transform: F(3,3) plans with one or
-// two input channels that do not take the fused one-output-channel kernel.
-bool contract_output5_applies(const nwg_plan_info& g) {
-  return g.tile == NWG_TILE_F3X3_3X3 && (g.n == 1 || g.n == 2) && g.M <= 2 && !g.depthwise &&
-         !input_contract5_applies(g);
 }
 
 hipError_t launch_contract_output5(const nwg_plan_info& g, const float* V, const float* U,

@@ -334,10 +334,6 @@ hipError_t launch_ics(const nwg_plan_info& g, const float* x, const float4* U, f
 
 }  // namespace
 
-bool input_contract_applies(const nwg_plan_info& g) {
-  return g.tile == NWG_TILE_F2X2_3X3 && g.n >= 3 && g.n <= 4 && (g.depthwise || g.N <= 2);
-}
-
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* Uf,
                                  float* Zf, hipStream_t s) {
   if (!input_contract_applies(g)) return hipErrorInvalidValue;

@@ -183,7 +183,7 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
 // raw windows at depth 3)
 // go to LDS, level 3 runs per output row (rows, then columns) and the two
 // F(2,3) levels in registers (10 x 10 -> 16 x 16).
-constexpr int kL3 = 26;                     // window side left for levels 1..3
+constexpr int kL3 = kMixL3;                 // window side left for levels 1..3
 // per-tile stride in LDS: even, so that column pairs are 8-byte aligned
 // (float2 reads), and 678 = 38 (mod 64), so that 32 consecutive tiles
 // start on 32 different even banks
@@ -542,17 +542,6 @@ __global__ __launch_bounds__(256) void output_xform_mix4(const float* __restrict
 }
 
 }  // namespace
-
-int mix_outer_levels(const nwg_plan_info& g) {
-  return g.tile == NWG_TILE_MIX_F23_F33 ? g.n - 2 : 0;
-}
-
-size_t mix_scratch_bytes(const nwg_plan_info& g) {
-  if (mix_outer_levels(g) != 2) return 0;
-  const size_t z3 = (size_t)25 * 144 * g.N * g.T * sizeof(float);
-  const size_t x4 = (size_t)25 * g.M * g.T * kL3 * kL3 * sizeof(float);
-  return z3 > x4 ? z3 : x4;
-}
 
 hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float* U,
                                    hipStream_t s) {

@@ -1,7 +1,7 @@
-// Host side of the nested-Winograd library: the plan (level recurrence of
-// Sec. III.B and Alg. 1, read as a chain of n identical F(2,3) bases), the
-// workspace, the weight cache, the C ABI of include/nwg.h and per-stage
-// timing.  All device work is queued on the caller's stream.
+// Device side of the nested-Winograd plan: its workspace, the weight cache,
+// the C ABI of include/nwg.h that queues work (the geometry, level
+// recurrence and error state are in plan.cpp) and per-stage timing.  All
+// device work is queued on the caller's stream.
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
@@ -16,18 +16,7 @@
 
 namespace {
 
-thread_local std::string g_last_error;
-
-void set_error(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
-void set_error(const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_last_error = buf;
-  if (std::getenv("NWG_LOG")) std::fprintf(stderr, "nwg: %s\n", buf);
-}
+using nwg::fail;
 
 struct TimingRecord {
   int stage;
@@ -57,267 +46,27 @@ struct nwg_plan {
 
 namespace {
 
-// Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,
-// s_j = min(M_j, K_j), M_{j+1} = M_j + s_j (m-1), K_{j+1} = K_j + s_j (rb-1);
-// n is the smallest depth with K_n >= r, and r = 1 needs no level.
-// Depth-4 dense plans whose contraction takes the full-tile path can split
-// the input transform and the contraction into parts over the level-4
-// branches (contiguous ranges of points) and overlap them on two streams.
-// Off by default: on the 31x31 layer (B = 16, 128 -> 128) the overlapped
-// contraction lost more (4.73 -> 5.6-6.6 ms over its parts) than the hidden
-// input transform saved; every part count from 2 to 16 made the step slower.
-bool pipeline_allowed(const nwg_plan_info& g) {
-  return g.tile == NWG_TILE_F2X2_3X3 && g.precision == NWG_PRECISION_FP32 && g.n == 4 &&
-         !g.depthwise && !g.fused_input &&
-         g.M % 32 == 0 && g.N % 64 == 0 && g.T % 64 == 0;
-}
-
-// depthwise: M = N = C channels, one r x r kernel each, no channel sum.
-// K slices of a linear-decomposition plan's contraction: its grid has one
-// level-1 group, so with few tiles the M c^2 channels are split (a divisor
-// of M c^2 / 32, up to 64 slices) until there are about 1024 work-groups
-int ld_kslices(const nwg_plan_info& g) {
-  if (g.ld_c <= 0) return 1;
-  const long long mk = (long long)g.M * g.ld_c * g.ld_c;
-  if (mk % 32 || g.N % 64 || g.T < 64) return 1;
-  const long long ntb = g.T % 128 == 0 ? g.T / 128 : (g.T + 63) / 64;
-  const long long wgs = ntb * (g.N / 64);
-  const long long units = mk / 32;
-  int best = 1;
-  for (int sl = 1; sl <= 64 && sl <= units; ++sl) {
-    if (units % sl) continue;
-    best = sl;
-    if (wgs * sl >= 1024) break;
-  }
-  return best;
-}
-
-// bytes of the plan's Z buffer: the stage-call Z, the fused F(3,3) kernel's
-// partial Z9 buffers, or a linear-decomposition plan's K-slice parts
-size_t zalloc_bytes(const nwg_plan_info& g) {
-  if (g.fused_input && g.tile == NWG_TILE_F3X3_3X3) return nwg::input_contract5_zbytes(g);
-  if (g.ld_c > 0) return (size_t)ld_kslices(g) * g.yhat_bytes;
-  // mixed nest at depth 4: Z, then the scratch of its transforms
-  if (g.tile == NWG_TILE_MIX_F23_F33) return g.yhat_bytes + nwg::mix_scratch_bytes(g);
-  return g.yhat_bytes;
-}
-
-int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile,
-                          int depthwise, nwg_plan_info* g);
-
-// Linear decomposition (Sec. II.B) on F(2,3): a depth-1 plan over M c^2
-// contraction channels, c = ceil(r/3) sub-kernels per axis.
-int ld_geometry(int B, int M, int N, int H, int W, int r, int pad, int depthwise,
-                nwg_plan_info* g) {
-  if (depthwise) {
-    set_error("the linear-decomposition tile serves dense plans");
-    return NWG_EUNSUPPORTED;
-  }
-  const long long Ho = (long long)H + 2LL * pad - r + 1, Wo = (long long)W + 2LL * pad - r + 1;
-  if (Ho <= 0 || Wo <= 0) {
-    set_error("kernel %d larger than padded input %dx%d (pad %d)", r, H, W, pad);
-    return NWG_EINVAL;
-  }
-  const int c = (r + 2) / 3;
-  g->B = B; g->M = M; g->N = N; g->H = H; g->W = W; g->r = r; g->pad = pad;
-  g->tile = NWG_TILE_LD_F2X2_3X3;
-  g->Ho = (int)Ho;
-  g->Wo = (int)Wo;
-  g->n = 1;
-  g->m = 2; g->rb = 3; g->l = 4;
-  g->strides[0] = 1;
-  g->Mn = 2;
-  g->Kn = 3 * c;
-  g->Ln = 3 * c + 1;
-  g->th = (int)((Ho + 1) / 2);
-  g->tw = (int)((Wo + 1) / 2);
-  g->T = (long long)B * g->th * g->tw;
-  g->P = 16;
-  g->ld_c = c;
-  const double mk = (double)M * c * c, f = (double)sizeof(float);
-  const double u = f * 16 * mk * N, v = f * 16 * mk * g->T, yh = f * 4 * N * (double)g->T;
-  if (u > 1e13 || v > 1e13 || g->T > 0x7fffffffLL / 64 || mk > 65535) {
-    set_error("workspace too large (or more than 65535 decomposed channels)");
-    return NWG_EUNSUPPORTED;
-  }
-  g->u_bytes = (size_t)u;
-  g->v_bytes = (size_t)v;
-  g->yhat_bytes = (size_t)yh;
-  g->direct_flop = 2.0 * B * N * (double)M * Ho * Wo * r * r;
-  g->ewmm_mults = (long long)(16 * (double)g->T * mk * N);
-  g->contract_flop = 2.0 * 16 * mk * N * (double)g->T;
-  g->pipeline_parts = 1;
-  g->precision = NWG_PRECISION_FP32;
-  g->workspace_bytes = g->u_bytes + g->v_bytes + zalloc_bytes(*g);
-  return NWG_OK;
-}
-
-// NWG_TILE_AUTO: F(3x3,3x3) where it measured faster than F(2x2,3x3) --
-// the fused one-output-channel kernel at depth 2 (unless F(2,3) runs the
-// layer in one kernel), or both channel counts >= 32 and either a nesting
-// level saved (r = 8, 9) or depth 1 (r <= 3); the mixed nest for dense
-// layers with r = 16..31 and both channel counts >= 32 (on the 31x31
-// 128 -> 128 layer: 1.64x fewer contraction FLOPs, 294 against 231
-// TFLOP/s); F(2x2,3x3) otherwise.
-int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile, int depthwise,
-                     nwg_plan_info* g) {
-  if (tile != NWG_TILE_AUTO)
-    return compute_geometry_tile(B, M, N, H, W, r, pad, tile, depthwise, g);
-  nwg_plan_info a, b;
-  const int ra = compute_geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F2X2_3X3, depthwise, &a);
-  if (ra == NWG_OK && !depthwise && a.n == 4 && M >= 32 && N >= 32) {
-    if (compute_geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_MIX_F23_F33, 0, &b) == NWG_OK) {
-      *g = b;
-      return NWG_OK;
-    }
-    set_error("");
-  }
-  if (ra != NWG_OK || depthwise || r > 9 || r == 1) {
-    if (g) *g = a;
-    return ra;
-  }
-  if (compute_geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F3X3_3X3, 0, &b) != NWG_OK) {
-    set_error("");
-    *g = a;
-    return NWG_OK;
-  }
-  const bool big = M >= 32 && N >= 32;
-  const bool pick = ((b.fused_input || b.fused_output) && !a.fused_conv) ||
-                    (big && a.n > b.n) || (big && a.n == 1 && !a.fused_conv);
-  *g = pick ? b : a;
-  return NWG_OK;
-}
-
-int compute_geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile,
-                          int depthwise, nwg_plan_info* g) {
-  if (!g) {
-    set_error("output pointer is NULL");
-    return NWG_EINVAL;
-  }
-  std::memset(g, 0, sizeof *g);
-  if (B <= 0 || M <= 0 || N <= 0 || H <= 0 || W <= 0 || r <= 0 || pad < 0) {
-    set_error("invalid shape B=%d M=%d N=%d H=%d W=%d r=%d pad=%d", B, M, N, H, W, r, pad);
-    return NWG_EINVAL;
-  }
-  if (tile != NWG_TILE_F2X2_3X3 && tile != NWG_TILE_F3X3_3X3 && tile != NWG_TILE_LD_F2X2_3X3 &&
-      tile != NWG_TILE_MIX_F23_F33) {
-    set_error("unsupported tile %d", tile);
-    return NWG_EUNSUPPORTED;
-  }
-  if (tile == NWG_TILE_LD_F2X2_3X3) return ld_geometry(B, M, N, H, W, r, pad, depthwise, g);
-  const bool mix = tile == NWG_TILE_MIX_F23_F33;
-  if (mix && depthwise) {
-    set_error("the mixed F(2,3)/F(3,3) nest serves dense plans");
-    return NWG_EUNSUPPORTED;
-  }
-  // up to 7 taps the mixed nest has only its two F(2,3) levels
-  if (mix && r <= 7)
-    return compute_geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F2X2_3X3, 0, g);
-  if (mix && r > 39) {
-    set_error("kernel size %d exceeds the mixed nest's 39 taps", r);
-    return NWG_EUNSUPPORTED;
-  }
-  const bool f33 = tile == NWG_TILE_F3X3_3X3;
-  if (f33 && depthwise) {
-    set_error("depthwise plans use the F(2x2,3x3) tile");
-    return NWG_EUNSUPPORTED;
-  }
-  const long long Ho = (long long)H + 2LL * pad - r + 1, Wo = (long long)W + 2LL * pad - r + 1;
-  if (Ho <= 0 || Wo <= 0) {
-    set_error("kernel %d larger than padded input %dx%d (pad %d)", r, H, W, pad);
-    return NWG_EINVAL;
-  }
-  // base F(m, rb): F(2,3) or F(3,3); F(3,3) is kept to depth 2 (r <= 9),
-  // where its fp32 error stays near 1e-6
-  // (the mixed nest: F(2,3) at levels 1-2, F(3,3) above)
-  const int m = f33 ? 3 : nwg::kOut, rb = nwg::kTaps, l = m + rb - 1;
-  const int max_depth = f33 ? 2 : NWG_MAX_DEPTH;
-  auto level_m = [&](int j) { return mix && j >= 2 ? 3 : m; };   // level j + 1
-  int n = 0, Mn = 1, Kn = 1;
-  int strides[NWG_MAX_DEPTH + 1] = {0};
-  long long P1 = 1;   // Winograd points per axis
-  if (r > 1) {
-    strides[0] = 1;
-    n = 1;
-    Mn = m;
-    Kn = rb;
-    P1 = l;
-    while (Kn < r) {
-      const int s = Mn < Kn ? Mn : Kn;
-      if (n >= max_depth) {
-        set_error("kernel size %d needs nesting depth > %d (r <= %d supported on this tile)", r,
-                  max_depth, f33 ? 9 : 31);
-        return NWG_EUNSUPPORTED;
-      }
-      const int mj = level_m(n);
-      strides[n] = s;
-      Mn += s * (mj - 1);
-      Kn += s * (rb - 1);
-      P1 *= mj + rb - 1;
-      ++n;
-    }
-  }
-  g->B = B; g->M = M; g->N = N; g->H = H; g->W = W; g->r = r; g->pad = pad; g->tile = tile;
-  g->depthwise = depthwise ? 1 : 0;
-  // the kernel transform sees M_k input channels: 1 for a depthwise layer
-  const int Mk = depthwise ? 1 : M;
-  g->Ho = (int)Ho;
-  g->Wo = (int)Wo;
-  g->n = n;
-  g->m = m; g->rb = rb; g->l = l;
-  for (int j = 0; j < n; ++j) g->strides[j] = strides[j];
-  g->Mn = Mn;
-  g->Kn = Kn;
-  g->Ln = n == 0 ? 1 : Mn + Kn - 1;
-  g->th = (int)((Ho + Mn - 1) / Mn);
-  g->tw = (int)((Wo + Mn - 1) / Mn);
-  g->T = (long long)B * g->th * g->tw;
-  const long long P = P1 * P1;
-  g->P = P;
-  g->outer33 = mix ? n - 2 : 0;
-  const double f = (double)sizeof(float);
-  g->direct_flop = 2.0 * B * N * (double)Mk * Ho * Wo * r * r;
-  if (n == 0) {
-    g->u_bytes = (size_t)Mk * N * sizeof(float);
-    g->v_bytes = 0;
-    g->yhat_bytes = 0;
-    g->ewmm_mults = (long long)B * N * Mk * Ho * Wo;
-    g->contract_flop = 2.0 * B * N * (double)Mk * Ho * Wo;
-  } else {
-    // the contraction writes Yhat after (part of) the level-1 output
-    // transform: per (n, t) P/4 values for F(2,3) (both axes), 3 P/5 for
-    // F(3,3) (columns only)
-    const double zpts = f33 ? (double)(P / 5) * 3 : (double)(P / 4);
-    const double u = f * P * Mk * N, v = f * P * M * g->T, yh = f * zpts * N * g->T;
-    if (u > 1e13 || v > 1e13 || yh > 1e13 || g->T > 0x7fffffffLL / 64) {
-      set_error("workspace too large");
-      return NWG_EUNSUPPORTED;
-    }
-    g->u_bytes = (size_t)u;
-    g->v_bytes = (size_t)v;
-    g->yhat_bytes = (size_t)yh;
-    g->ewmm_mults = P * g->T * Mk * (long long)N;
-    g->contract_flop = 2.0 * P * (double)Mk * N * g->T;
-  }
-  // one or two output channels (or depthwise) at depth 3-4: the fused kernel
-  // never forms V.  Few channels (or depthwise) at depth 1-2: one kernel
-  // x -> y, neither V nor Z.
-  g->fused_input = (f33 ? nwg::input_contract5_applies(*g) : nwg::input_contract_applies(*g)) ? 1 : 0;
-  g->fused_conv =
-      !f33 && !mix && (nwg::small_conv_applies(*g) || (depthwise && (n == 1 || n == 2))) ? 1 : 0;
-  g->fused_output = nwg::contract_output5_applies(*g) ? 1 : 0;
-  const bool no_v = g->fused_input || depthwise || g->fused_conv;
-  const bool no_z = g->fused_conv || g->fused_output;
-  g->workspace_bytes = g->u_bytes + (no_v ? 0 : g->v_bytes) + (no_z ? 0 : zalloc_bytes(*g));
-  g->pipeline_parts = 1;
-  g->precision = NWG_PRECISION_FP32;
-  return NWG_OK;
+// NWG_DEBUG_SYNC set in the environment: every call waits for each kernel it
+// queues and reports a failure there, naming the kernel (not for use under
+// stream capture).
+bool debug_sync() {
+  static const bool on = std::getenv("NWG_DEBUG_SYNC") != nullptr;
+  return on;
 }
 
 int check_hip(hipError_t e, const char* what) {
   if (e == hipSuccess) return NWG_OK;
-  set_error("%s: %s", what, hipGetErrorString(e));
-  return NWG_EHIP;
+  return fail(NWG_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// A launch's status; with NWG_DEBUG_SYNC also its completion on stream s.
+int check_launch(hipError_t e, const char* what, hipStream_t s) {
+  int rc = check_hip(e, what);
+  if (rc == NWG_OK && debug_sync()) {
+    const hipError_t es = hipStreamSynchronize(s);
+    if (es != hipSuccess) rc = fail(NWG_EHIP, "%s (completion): %s", what, hipGetErrorString(es));
+  }
+  return rc;
 }
 
 hipEvent_t take_event(nwg_plan* p) {
@@ -341,8 +90,9 @@ int timed(nwg_plan* p, int stage, hipStream_t s, const char* what, F&& launch) {
   }
   // a launch whose events cannot be recorded runs untimed
   bool timed_ok = e0 && e1 && hipEventRecord(e0, s) == hipSuccess;
-  const int rc = check_hip(launch(), what);
+  const hipError_t el = launch();
   timed_ok = timed_ok && hipEventRecord(e1, s) == hipSuccess;
+  const int rc = check_launch(el, what, s);
   if (timed_ok) {
     p->pending.push_back({stage, e0, e1});
   } else {
@@ -476,60 +226,41 @@ int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, fl
 
 }  // namespace
 
-extern "C" {
-
-const char* nwg_version(void) {
-  return "nwg 0.3 (nested F(2x2,3x3), F(3x3,3x3) and mixed F(2,3)/F(3,3), gfx950)";
-}
-
-const char* nwg_last_error(void) { return g_last_error.c_str(); }
-
-int nwg_plan_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile,
-                      nwg_plan_info* out) {
-  return compute_geometry(B, M, N, H, W, r, pad, tile, 0, out);
-}
-
-int nwg_plan_geometry_depthwise(int B, int C, int H, int W, int r, int pad, int tile,
-                                nwg_plan_info* out) {
-  return compute_geometry(B, C, C, H, W, r, pad, tile, 1, out);
-}
-
-}  // extern "C"
 
 namespace {
 
 nwg_plan* create_plan(const nwg_plan_info& g) {
-  if (g.n == 0 && g.pad != 0) {
-    set_error("1x1 kernels with padding are not supported (pad must be 0 for r = 1)");
-    return nullptr;
-  }
+  if (nwg::check_plan_request(g) != NWG_OK) return nullptr;
   nwg_plan* p = new (std::nothrow) nwg_plan;
   if (!p) {
-    set_error("host allocation failed");
+    fail(NWG_ENOMEM, "host allocation of the plan failed");
     return nullptr;
   }
   p->info = g;
   if (hipGetDevice(&p->device) != hipSuccess) {
-    set_error("no HIP device available");
+    hipGetLastError();
+    fail(NWG_EHIP, "no HIP device available");
     delete p;
     return nullptr;
   }
+  // a failed hipMalloc is an allocation failure (NWG_ENOMEM), whatever the
+  // runtime's code for it; the plan is released with what it holds
   auto alloc = [&](float** ptr, size_t bytes, const char* what) {
     if (bytes == 0) return true;
-    hipError_t e = hipMalloc((void**)ptr, bytes);
+    const hipError_t e = hipMalloc((void**)ptr, bytes);
     if (e != hipSuccess) {
+      *ptr = nullptr;
       hipGetLastError();
-      set_error("hipMalloc of %s (%zu bytes) failed: %s", what, bytes, hipGetErrorString(e));
+      fail(NWG_ENOMEM, "hipMalloc of %s (%zu bytes) failed: %s", what, bytes,
+           hipGetErrorString(e));
       return false;
     }
     return true;
   };
-  const bool no_v = g.fused_input || g.depthwise || g.fused_conv;
-  const bool no_z = g.fused_conv || g.fused_output;
-  if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, no_v ? 0 : g.v_bytes, "V") ||
-      !alloc(&p->Yh, no_z ? 0 : zalloc_bytes(g), "Yhat")) {
-    nwg_plan_destroy(p);
-    // keep the allocation message
+  const size_t vb = nwg::plan_holds_v(g) ? g.v_bytes : 0;
+  const size_t zb = nwg::plan_holds_z(g) ? nwg::zalloc_bytes(g) : 0;
+  if (!alloc(&p->U, g.u_bytes, "U") || !alloc(&p->V, vb, "V") || !alloc(&p->Yh, zb, "Yhat")) {
+    nwg_plan_destroy(p);    // frees nothing it did not allocate; keeps the message
     return nullptr;
   }
   return p;
@@ -541,13 +272,13 @@ extern "C" {
 
 nwg_plan* nwg_plan_create_pad(int B, int M, int N, int H, int W, int r, int pad, int tile) {
   nwg_plan_info g;
-  if (compute_geometry(B, M, N, H, W, r, pad, tile, 0, &g) != NWG_OK) return nullptr;
+  if (nwg::compute_geometry(B, M, N, H, W, r, pad, tile, 0, &g) != NWG_OK) return nullptr;
   return create_plan(g);
 }
 
 nwg_plan* nwg_plan_create_depthwise(int B, int C, int H, int W, int r, int pad, int tile) {
   nwg_plan_info g;
-  if (compute_geometry(B, C, C, H, W, r, pad, tile, 1, &g) != NWG_OK) return nullptr;
+  if (nwg::compute_geometry(B, C, C, H, W, r, pad, tile, 1, &g) != NWG_OK) return nullptr;
   return create_plan(g);
 }
 
@@ -573,78 +304,59 @@ void nwg_plan_destroy(nwg_plan* p) {
 }
 
 int nwg_plan_query(const nwg_plan* p, nwg_plan_info* out) {
-  if (!p || !out) {
-    set_error("NULL plan or output");
-    return NWG_EINVAL;
-  }
+  if (!p || !out) return fail(NWG_EINVAL, "NULL plan or output");
   *out = p->info;
   return NWG_OK;
 }
 
 int nwg_kernel_transform(const nwg_plan* p, const float* w, float* U, void* stream) {
-  if (!p || !w || !U) {
-    set_error("NULL argument to nwg_kernel_transform");
-    return NWG_EINVAL;
-  }
-  return check_hip(launch_kxform(p->info, w, U, (hipStream_t)stream), "kernel transform launch");
+  if (!p || !w || !U)
+    return fail(NWG_EINVAL, "NULL argument to nwg_kernel_transform");
+  hipStream_t s = (hipStream_t)stream;
+  return check_launch(launch_kxform(p->info, w, U, s), "kernel transform launch", s);
 }
 
 int nwg_input_transform(const nwg_plan* p, const float* x, float* V, void* stream) {
-  if (!p || !x || !V) {
-    set_error("NULL argument to nwg_input_transform");
-    return NWG_EINVAL;
-  }
-  if (p->info.n == 0) {
-    set_error("depth 0 (r = 1) has no input transform");
-    return NWG_EINVAL;
-  }
-  return check_hip(launch_ixform(p->info, x, V, mix_scratch(p), (hipStream_t)stream),
-                   "input transform launch");
+  if (!p || !x || !V)
+    return fail(NWG_EINVAL, "NULL argument to nwg_input_transform");
+  if (p->info.n == 0)
+    return fail(NWG_EINVAL, "depth 0 (r = 1) has no input transform");
+  hipStream_t s = (hipStream_t)stream;
+  return check_launch(launch_ixform(p->info, x, V, mix_scratch(p), s), "input transform launch", s);
 }
 
 int nwg_contract(const nwg_plan* p, const float* U, const float* V, float* Yh, void* stream) {
-  if (!p || !U || !V || !Yh) {
-    set_error("NULL argument to nwg_contract");
-    return NWG_EINVAL;
-  }
-  return check_hip(launch_contract(p->info, U, V, Yh, (hipStream_t)stream),
-                   "contraction launch");
+  if (!p || !U || !V || !Yh)
+    return fail(NWG_EINVAL, "NULL argument to nwg_contract");
+  hipStream_t s = (hipStream_t)stream;
+  return check_launch(launch_contract(p->info, U, V, Yh, s), "contraction launch", s);
 }
 
 int nwg_input_contract(const nwg_plan* p, const float* x, const float* U, float* Yh,
                        void* stream) {
-  if (!p || !x || !U || !Yh) {
-    set_error("NULL argument to nwg_input_contract");
-    return NWG_EINVAL;
-  }
-  if (p->info.tile != NWG_TILE_F2X2_3X3 || !nwg::input_contract_applies(p->info)) {
-    set_error("fused input transform + contraction needs the F(2x2,3x3) tile, depth 3 or 4 "
-              "and N <= 2 or a "
-              "depthwise plan (depth %d, N = %d)", p->info.n, p->info.N);
-    return NWG_EUNSUPPORTED;
-  }
-  return check_hip(nwg::launch_input_contract(p->info, x, U, Yh, (hipStream_t)stream),
-                   "fused input transform + contraction launch");
+  if (!p || !x || !U || !Yh)
+    return fail(NWG_EINVAL, "NULL argument to nwg_input_contract");
+  if (p->info.tile != NWG_TILE_F2X2_3X3 || !nwg::input_contract_applies(p->info))
+    return fail(NWG_EUNSUPPORTED,
+                "fused input transform + contraction needs the F(2x2,3x3) tile, depth 3 or 4 "
+                "and N <= 2 or a depthwise plan (depth %d, N = %d)", p->info.n, p->info.N);
+  return check_launch(nwg::launch_input_contract(p->info, x, U, Yh, (hipStream_t)stream),
+                      "fused input transform + contraction launch", (hipStream_t)stream);
 }
 
 int nwg_output_transform(const nwg_plan* p, const float* Yh, float* y, void* stream) {
-  if (!p || !Yh || !y) {
-    set_error("NULL argument to nwg_output_transform");
-    return NWG_EINVAL;
-  }
-  if (p->info.n == 0) {
-    set_error("depth 0 (r = 1) has no output transform");
-    return NWG_EINVAL;
-  }
-  return check_hip(launch_oxform(p->info, Yh, y, mix_scratch(p), (hipStream_t)stream),
-                   "output transform launch");
+  if (!p || !Yh || !y)
+    return fail(NWG_EINVAL, "NULL argument to nwg_output_transform");
+  if (p->info.n == 0)
+    return fail(NWG_EINVAL, "depth 0 (r = 1) has no output transform");
+  hipStream_t s = (hipStream_t)stream;
+  return check_launch(launch_oxform(p->info, Yh, y, mix_scratch(p), s), "output transform launch",
+                      s);
 }
 
 int nwg_plan_set_weights(nwg_plan* p, const float* w, void* stream) {
-  if (!p || !w) {
-    set_error("NULL argument to nwg_plan_set_weights");
-    return NWG_EINVAL;
-  }
+  if (!p || !w)
+    return fail(NWG_EINVAL, "NULL argument to nwg_plan_set_weights");
   const int rc = run_kernel_transform(p, p->info, w, p->U, (hipStream_t)stream);
   if (rc == NWG_OK) {
     p->cached_w = w;
@@ -656,10 +368,8 @@ int nwg_plan_set_weights(nwg_plan* p, const float* w, void* stream) {
 }
 
 int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stream) {
-  if (!p || !x || !w || !y) {
-    set_error("NULL argument to nwg_conv2d");
-    return NWG_EINVAL;
-  }
+  if (!p || !x || !w || !y)
+    return fail(NWG_EINVAL, "NULL argument to nwg_conv2d");
   hipStream_t s = (hipStream_t)stream;
   const nwg_plan_info& g = p->info;
   if (!p->weights_valid || p->cached_w != w) {
@@ -702,7 +412,7 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
       return timed(p, 2, s, "contraction + output transform launch",
                    [&] { return nwg::launch_contract_output5(g, p->V, p->U, y, s); });
     rc = timed(p, 2, s, "contraction launch",
-               [&] { return launch_contract(g, p->U, p->V, p->Yh, s, ld_kslices(g)); });
+               [&] { return launch_contract(g, p->U, p->V, p->Yh, s, nwg::ld_kslices(g)); });
   }
   if (rc != NWG_OK) return rc;
   return timed(p, 3, s, "output transform launch",
@@ -710,23 +420,16 @@ int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stre
 }
 
 int nwg_plan_set_precision(nwg_plan* p, int precision) {
-  if (!p) {
-    set_error("NULL plan");
-    return NWG_EINVAL;
-  }
-  if (precision != NWG_PRECISION_FP32 && precision != NWG_PRECISION_BF16_SPLIT) {
-    set_error("unknown precision %d", precision);
-    return NWG_EINVAL;
-  }
+  if (!p)
+    return fail(NWG_EINVAL, "NULL plan");
+  if (precision != NWG_PRECISION_FP32 && precision != NWG_PRECISION_BF16_SPLIT)
+    return fail(NWG_EINVAL, "unknown precision %d", precision);
   const nwg_plan_info& g = p->info;
-  if (precision == NWG_PRECISION_BF16_SPLIT &&
-      (g.tile != NWG_TILE_F2X2_3X3 || g.n < 1 || g.depthwise || g.fused_input || g.fused_conv ||
-       g.pipeline_parts > 1 || g.M % 32 || g.N % 64 || g.T < 64)) {
-    set_error("split precision needs a dense, unfused, unpipelined F(2x2,3x3) plan at depth "
-              ">= 1 with M %% 32 == 0, N %% 64 == 0 and T >= 64 (M = %d, N = %d, T = %lld)",
-              g.M, g.N, g.T);
-    return NWG_EUNSUPPORTED;
-  }
+  if (precision == NWG_PRECISION_BF16_SPLIT && !nwg::split_allowed(g))
+    return fail(NWG_EUNSUPPORTED,
+                "split precision needs a dense, unfused, unpipelined F(2x2,3x3) plan at depth "
+                ">= 1 with M %% 32 == 0, N %% 64 == 0 and T >= 64 (M = %d, N = %d, T = %lld)",
+                g.M, g.N, g.T);
   if (precision != g.precision) {
     p->info.precision = precision;
     p->weights_valid = false;
@@ -735,41 +438,32 @@ int nwg_plan_set_precision(nwg_plan* p, int precision) {
 }
 
 int nwg_plan_set_pipeline(nwg_plan* p, int parts) {
-  if (!p) {
-    set_error("NULL plan");
-    return NWG_EINVAL;
-  }
+  if (!p)
+    return fail(NWG_EINVAL, "NULL plan");
   if (parts == 1) {
     p->info.pipeline_parts = 1;
     return NWG_OK;
   }
-  if (parts != 2 && parts != 4 && parts != 8 && parts != 16) {
-    set_error("pipeline parts must be 1, 2, 4, 8 or 16 (got %d)", parts);
-    return NWG_EINVAL;
-  }
-  if (!pipeline_allowed(p->info)) {
-    set_error("the two-stream pipeline needs a dense depth-4 plan with M %% 32 == 0, "
-              "N %% 64 == 0 and T %% 64 == 0");
-    return NWG_EUNSUPPORTED;
-  }
+  if (parts != 2 && parts != 4 && parts != 8 && parts != 16)
+    return fail(NWG_EINVAL, "pipeline parts must be 1, 2, 4, 8 or 16 (got %d)", parts);
+  if (!nwg::pipeline_allowed(p->info))
+    return fail(NWG_EUNSUPPORTED,
+                "the two-stream pipeline needs a dense depth-4 plan with M %% 32 == 0, "
+                "N %% 64 == 0 and T %% 64 == 0");
   p->info.pipeline_parts = parts;
   return NWG_OK;
 }
 
 int nwg_plan_set_timing(nwg_plan* p, int enable) {
-  if (!p) {
-    set_error("NULL plan");
-    return NWG_EINVAL;
-  }
+  if (!p)
+    return fail(NWG_EINVAL, "NULL plan");
   p->timing = enable != 0;
   return NWG_OK;
 }
 
 int nwg_plan_get_timing(nwg_plan* p, double ms[4], long long count[4]) {
-  if (!p || !ms || !count) {
-    set_error("NULL argument to nwg_plan_get_timing");
-    return NWG_EINVAL;
-  }
+  if (!p || !ms || !count)
+    return fail(NWG_EINVAL, "NULL argument to nwg_plan_get_timing");
   int rc = NWG_OK;
   for (auto& r : p->pending) {
     float t = 0.0f;

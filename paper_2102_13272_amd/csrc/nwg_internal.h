@@ -8,6 +8,7 @@
 #include <cstdint>
 
 #include "../../include/nwg.h"
+#include "plan.h"
 
 namespace nwg {
 
@@ -260,12 +261,6 @@ struct ContractArgs {
   long long batch;
 };
 
-// mixed nest (NWG_TILE_MIX_F23_F33): F(3,3) levels above the two F(2,3)
-// levels, and the bytes of the depth-4 scratch (0 below depth 4) that the
-// input transform (level-4 blocks X4) and the output transform (level-3
-// blocks Z3) use in turn
-int mix_outer_levels(const nwg_plan_info& g);
-size_t mix_scratch_bytes(const nwg_plan_info& g);
 hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float* U,
                                    hipStream_t s);
 // X4, Z3: mix_scratch_bytes(g) of scratch at depth 4 (may be NULL at depth 3)
@@ -290,8 +285,6 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
                                  long long G, hipStream_t s, bool split = false, int ks = 1);
 // in place: every fp32 value of buf (n values) -> its packed bf16 (hi, lo) pair
 hipError_t launch_split_pairs(float* buf, size_t n, hipStream_t s);
-// depth 3-4 and N <= 2: x, U -> Z without forming V
-bool input_contract_applies(const nwg_plan_info& g);
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* U, float* Z,
                                  hipStream_t s);
 // the F(3,3) tile (depth 1-2): U [P][M][N], V [P][M][T], Z [P/25][9][N][T]
@@ -302,21 +295,12 @@ hipError_t launch_contract5(const nwg_plan_info& g, const float* U, const float*
 // parts > 1 / fold9: the fused kernel's partial Z9 buffers (see f33.hip)
 hipError_t launch_output_xform5(const nwg_plan_info& g, const float* Z, float* y, hipStream_t s,
                                 int parts = 1, bool fold9 = false);
-// fused x -> partial Z9 (depth 2, N = 1): applies / number of parts / bytes
-bool input_contract5_applies(const nwg_plan_info& g);
-int input_contract5_parts(const nwg_plan_info& g);
-size_t input_contract5_zbytes(const nwg_plan_info& g);
 hipError_t launch_input_contract5(const nwg_plan_info& g, const float* x, const float* U,
                                   float* Zp, hipStream_t s);
-// F(3,3) with M <= 2 (and not the fused N = 1 kernel): V -> y, the
-// contraction formed inside the output transform (no Z)
-bool contract_output5_applies(const nwg_plan_info& g);
 hipError_t launch_contract_output5(const nwg_plan_info& g, const float* V, const float* U,
                                    float* y, hipStream_t s);
 // Z[i] += Z[k n + i] for k = 1 .. parts-1 (n floats per part)
 hipError_t launch_sum_parts(float* Z, size_t n, int parts, hipStream_t s);
-// few channels at depth 1-2 (dense): x -> y in one kernel
-bool small_conv_applies(const nwg_plan_info& g);
 hipError_t launch_small_conv(const nwg_plan_info& g, const float* x, const float* U, float* y,
                              hipStream_t s);
 // depthwise: y = U[c] x (depth 0); x -> y in one kernel (depth 1-2);

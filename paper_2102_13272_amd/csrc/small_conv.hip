@@ -379,13 +379,6 @@ hipError_t launch_small_d2(const nwg_plan_info& g, const float* x, const float4*
 
 }  // namespace
 
-bool small_conv_applies(const nwg_plan_info& g) {
-  if (g.depthwise) return false;
-  if (g.n == 1) return g.M <= 8 && g.N <= 16;
-  if (g.n == 2) return g.M <= 2 && g.M * g.N <= 64;
-  return false;
-}
-
 hipError_t launch_small_conv(const nwg_plan_info& g, const float* x, const float* Uf, float* y,
                              hipStream_t s) {
   if (!small_conv_applies(g) || ((uintptr_t)Uf & 15)) return hipErrorInvalidValue;

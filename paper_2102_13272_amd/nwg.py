@@ -75,6 +75,7 @@ SIGNATURES = [
     ("nwg_plan_get_timing", _I, [_P, ctypes.POINTER(ctypes.c_double),
                                  ctypes.POINTER(ctypes.c_longlong)]),
     ("nwg_last_error", ctypes.c_char_p, []),
+    ("nwg_last_status", _I, []),
     ("nwg_version", ctypes.c_char_p, []),
 ]
 
@@ -128,8 +129,26 @@ def plan_geometry_depthwise(B, C, H, W, r, pad=0, tile=NWG_TILE_F2X2_3X3) -> dic
     return info.as_dict()
 
 
-def _ptr(t) -> int:
-    return int(t.data_ptr())
+def _ptr(t, numel: int, what: str) -> int:
+    """Device pointer of a tensor the library will read or write: a
+    contiguous float32 GPU tensor of at least `numel` elements, 16-byte
+    aligned.  Raises NwgError before any call into the library otherwise
+    (an undersized buffer would be read or written past its end)."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise NwgError(f"{what}: expected a torch tensor, got {type(t).__name__}")
+    if t.dtype != torch.float32:
+        raise NwgError(f"{what}: dtype {t.dtype}, the library computes in float32")
+    if not t.is_contiguous():
+        raise NwgError(f"{what}: not contiguous")
+    if t.numel() < numel:
+        raise NwgError(f"{what}: {t.numel()} elements, the plan needs {numel}")
+    if not t.is_cuda:
+        raise NwgError(f"{what}: a {t.device} tensor, the library takes GPU memory")
+    p = int(t.data_ptr())
+    if p % 16:
+        raise NwgError(f"{what}: address not 16-byte aligned")
+    return p
 
 
 def _stream(stream) -> int:
@@ -147,6 +166,7 @@ class Plan:
         over M = N channels (nwg_plan_create_depthwise)."""
         lib = load_library()
         self._lib = lib
+        self._w, self._w_version = None, None
         if depthwise:
             if M != N:
                 raise ValueError("a depthwise plan has M == N channels")
@@ -213,32 +233,72 @@ class Plan:
         i = self.info
         return (i["B"], i["N"], i["Ho"], i["Wo"])
 
+    # element counts of the tensors the calls take
+    @property
+    def _x_numel(self):
+        i = self.info
+        return i["B"] * i["M"] * i["H"] * i["W"]
+
+    @property
+    def _w_numel(self):
+        i = self.info
+        return i["N"] * (1 if i["depthwise"] else i["M"]) * i["r"] * i["r"]
+
+    @property
+    def _y_numel(self):
+        i = self.info
+        return i["B"] * i["N"] * i["Ho"] * i["Wo"]
+
+    def _buf_numel(self, which):
+        """U, V or Z of the stage calls (depth 0: V is x and Z is y)."""
+        i = self.info
+        if not i["n"] and which in ("V", "Z"):
+            return self._x_numel if which == "V" else self._y_numel
+        return i[{"U": "u_bytes", "V": "v_bytes", "Z": "yhat_bytes"}[which]] // 4
+
     def conv2d(self, x, w, y, stream=None):
-        _check(self._lib.nwg_conv2d(self.handle, _ptr(x), _ptr(w), _ptr(y), _stream(stream)),
-               "nwg_conv2d")
+        """y = conv(x, w).  The transformed weights are cached by the library
+        under w's address; the plan also keeps w itself (so that its memory
+        cannot be freed and handed to another weight tensor while cached) and
+        w's version counter, and transforms w again when either changes."""
+        xp = _ptr(x, self._x_numel, "x")
+        wp = _ptr(w, self._w_numel, "w")
+        yp = _ptr(y, self._y_numel, "y")
+        if self._w is not w or self._w_version != w._version:
+            self.set_weights(w, stream)
+        _check(self._lib.nwg_conv2d(self.handle, xp, wp, yp, _stream(stream)), "nwg_conv2d")
 
     def set_weights(self, w, stream=None):
-        _check(self._lib.nwg_plan_set_weights(self.handle, _ptr(w), _stream(stream)),
-               "nwg_plan_set_weights")
+        self._w, self._w_version = None, None
+        _check(self._lib.nwg_plan_set_weights(self.handle, _ptr(w, self._w_numel, "w"),
+                                              _stream(stream)), "nwg_plan_set_weights")
+        self._w, self._w_version = w, w._version
 
     def kernel_transform(self, w, U, stream=None):
-        _check(self._lib.nwg_kernel_transform(self.handle, _ptr(w), _ptr(U), _stream(stream)),
-               "nwg_kernel_transform")
+        _check(self._lib.nwg_kernel_transform(self.handle, _ptr(w, self._w_numel, "w"),
+                                              _ptr(U, self._buf_numel("U"), "U"),
+                                              _stream(stream)), "nwg_kernel_transform")
 
     def input_transform(self, x, V, stream=None):
-        _check(self._lib.nwg_input_transform(self.handle, _ptr(x), _ptr(V), _stream(stream)),
-               "nwg_input_transform")
+        _check(self._lib.nwg_input_transform(self.handle, _ptr(x, self._x_numel, "x"),
+                                             _ptr(V, self._buf_numel("V"), "V"),
+                                             _stream(stream)), "nwg_input_transform")
 
     def contract(self, U, V, Z, stream=None):
-        _check(self._lib.nwg_contract(self.handle, _ptr(U), _ptr(V), _ptr(Z), _stream(stream)),
+        _check(self._lib.nwg_contract(self.handle, _ptr(U, self._buf_numel("U"), "U"),
+                                      _ptr(V, self._buf_numel("V"), "V"),
+                                      _ptr(Z, self._buf_numel("Z"), "Z"), _stream(stream)),
                "nwg_contract")
 
     def input_contract(self, x, U, Z, stream=None):
-        _check(self._lib.nwg_input_contract(self.handle, _ptr(x), _ptr(U), _ptr(Z),
+        _check(self._lib.nwg_input_contract(self.handle, _ptr(x, self._x_numel, "x"),
+                                            _ptr(U, self._buf_numel("U"), "U"),
+                                            _ptr(Z, self._buf_numel("Z"), "Z"),
                                             _stream(stream)), "nwg_input_contract")
 
     def output_transform(self, Z, y, stream=None):
-        _check(self._lib.nwg_output_transform(self.handle, _ptr(Z), _ptr(y), _stream(stream)),
+        _check(self._lib.nwg_output_transform(self.handle, _ptr(Z, self._buf_numel("Z"), "Z"),
+                                              _ptr(y, self._y_numel, "y"), _stream(stream)),
                "nwg_output_transform")
 
     def set_pipeline(self, parts: int):
@@ -250,6 +310,7 @@ class Plan:
     def set_precision(self, precision: int):
         _check(self._lib.nwg_plan_set_precision(self.handle, int(precision)),
                "nwg_plan_set_precision")
+        self._w, self._w_version = None, None
         info = nwg_plan_info()
         _check(self._lib.nwg_plan_query(self.handle, ctypes.byref(info)), "nwg_plan_query")
         self.info = info.as_dict()

@@ -117,6 +117,42 @@ def test_null_arguments_are_rejected_without_a_device():
     assert lib.nwg_contract(None, None, None, None, None) == nwg.NWG_EINVAL
     assert lib.nwg_plan_set_timing(None, 1) == nwg.NWG_EINVAL
     lib.nwg_plan_destroy(None)                       # NULL-safe
+    # a NULL geometry output on every tile, the automatic choice included
+    for tile in (nwg.NWG_TILE_F2X2_3X3, nwg.NWG_TILE_F3X3_3X3, nwg.NWG_TILE_LD_F2X2_3X3,
+                 nwg.NWG_TILE_MIX_F23_F33, nwg.NWG_TILE_AUTO):
+        assert lib.nwg_plan_geometry(1, 4, 4, 16, 16, 4, 0, tile, None) == nwg.NWG_EINVAL
+        assert lib.nwg_last_status() == nwg.NWG_EINVAL
+        assert lib.nwg_plan_geometry(16, 128, 128, 56, 56, 31, 15, tile, None) == nwg.NWG_EINVAL
+        assert lib.nwg_plan_geometry_depthwise(1, 4, 16, 16, 4, 0, tile, None) == nwg.NWG_EINVAL
+        assert lib.nwg_last_status() == nwg.NWG_EINVAL
+
+
+def test_last_status_names_the_failure():
+    lib = nwg.load_library()
+    info = nwg.nwg_plan_info()
+    assert lib.nwg_plan_geometry(0, 4, 4, 16, 16, 4, 0, 0, ctypes.byref(info)) == nwg.NWG_EINVAL
+    assert lib.nwg_last_status() == nwg.NWG_EINVAL
+    assert lib.nwg_plan_geometry(1, 4, 4, 99, 99, 32, 0, 0, ctypes.byref(info)) == \
+        nwg.NWG_EUNSUPPORTED
+    assert lib.nwg_last_status() == nwg.NWG_EUNSUPPORTED and b"depth" in lib.nwg_last_error()
+    # maps of 2^31 values or more are refused before any size is formed
+    assert lib.nwg_plan_geometry(1, 1, 1, 65536, 65536, 3, 1, 0, ctypes.byref(info)) == \
+        nwg.NWG_EUNSUPPORTED
+
+
+def test_tensor_checks_reject_bad_buffers_before_the_library():
+    import torch
+    from paper_2102_13272_amd.nwg import _ptr
+    with pytest.raises(nwg.NwgError, match="float32"):
+        _ptr(torch.zeros(16, dtype=torch.float64), 16, "x")
+    with pytest.raises(nwg.NwgError, match="contiguous"):
+        _ptr(torch.zeros(4, 8).t(), 32, "x")
+    with pytest.raises(nwg.NwgError, match="elements"):
+        _ptr(torch.zeros(15), 16, "y")
+    with pytest.raises(nwg.NwgError, match="GPU"):
+        _ptr(torch.zeros(16), 16, "w")
+    with pytest.raises(nwg.NwgError, match="tensor"):
+        _ptr(np.zeros(16, np.float32), 16, "w")
 
 
 def test_no_silent_fallback_without_device():

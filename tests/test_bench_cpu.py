@@ -9,6 +9,7 @@ import os
 import subprocess
 import sys
 
+import numpy as np
 import pytest
 
 import bench
@@ -109,3 +110,20 @@ def test_committed_traffic_summaries_match_the_current_contraction_source():
     for tile in ("auto", "f23"):
         t = bench.measured_traffic("c5_r31", "contraction", tile)
         assert t is not None and t > 0
+
+
+def test_cpu_baseline_reports_parity_of_the_outputs_it_is_given():
+    """The oracle leg times whole images and compares every GPU output of the
+    same run on those images; a perturbation beyond the fp32 bar fails."""
+    from oracle.direct import direct_conv2d
+    from paper_2102_13272_amd.workloads import WORKLOADS, make_workload
+    x, (w,) = make_workload("c1_r4_valid")
+    y = direct_conv2d(x, w, WORKLOADS["c1_r4_valid"].layers[0].pad).astype(np.float32)
+    bad = y.copy()
+    bad[0, 1, 2, 3] += 0.01 * np.abs(y).max()
+    base, par = bench.cpu_baseline("c1_r4_valid", 0.0, {"good": y, "bad": bad})
+    assert base["kind"] == "oracle" and base["sample"].startswith("1 of 1 images")
+    assert base["cores"] >= 1 and base["host_nproc"] >= 1
+    assert par["good"]["ok"] and par["good"]["rel_l2"] < 1e-6
+    assert not par["bad"]["ok"] and par["bad"]["max_abs_over_max"] > 1e-3
+    assert par["good"]["outputs"] == y.size

@@ -11,11 +11,11 @@ import numpy as np
 import pytest
 import torch
 
-from oracle.direct import direct_conv2d, direct_conv2d_points
+from oracle.direct import direct_conv2d
 from oracle.mixed import input_matrix, kernel_matrix, mixed_levels, output_matrix
 from oracle.nested import ewmm
 from paper_2102_13272_amd import nwg
-from paper_2102_13272_amd.workloads import WORKLOADS, make_case, make_workload
+from paper_2102_13272_amd.workloads import make_case
 from tests.gpu_util import assert_close, dev
 from tests.layout import level1, mixed_chain, mixed_to_lib_points, quads
 
@@ -71,37 +71,20 @@ def test_mixed_conv2d_matches_direct_oracle(case):
     assert_close(_conv(x, w, pad), direct_conv2d(x, w, pad), what=str(case))
 
 
-def _sampled(x, w, pad, y, seed, edges):
-    """y against the direct oracle at 1500 random outputs plus the corners
-    and both sides of the tile edges given (rows and columns)."""
-    B, N, Ho, Wo = y.shape
-    rng = np.random.default_rng(seed)
-    pts = {(int(rng.integers(B)), int(rng.integers(N)), int(rng.integers(Ho)),
-            int(rng.integers(Wo))) for _ in range(1500)}
-    for b in (0, B - 1):
-        for n in (0, N - 1):
-            for i in edges + [0, Ho - 1]:
-                for j in edges + [0, Wo - 1]:
-                    if i < Ho and j < Wo:
-                        pts.add((b, n, i, j))
-    pts = sorted(pts)
-    ref = direct_conv2d_points(x, w, pad, pts)
-    got = np.array([y[p] for p in pts], dtype=np.float64)
-    assert_close(got, ref, what="sampled outputs")
-
-
 # the deep contraction at depth 4 (T = 64, 10000 groups: the persistent
-# form), 64 x 64 blocks (N = 64) and 128 x 64 blocks (N = 128); full outputs
-# are too slow for the CPU oracle here, so sampled outputs
+# form), 64 x 64 blocks (N = 64) and 128 x 64 blocks (N = 128), compared
+# output by output
 BIG = [(64, 32, 64, 36, 36, 31, 15), (64, 32, 128, 36, 36, 31, 15)]
 
 
 @pytest.mark.parametrize("case", BIG, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
-def test_mixed_conv2d_deep_contraction_sampled(case):
+def test_mixed_conv2d_deep_contraction_whole_output(case):
     B, M, N, H, W, r, pad = case
     L, x, w = make_case(B, M, N, H, W, r, pad, seed=7 * sum(case))
     print(f"mixed case {case}", flush=True)
-    _sampled(x, w, pad, _conv(x, w, pad), 13, [11, 12, 35])
+    with nwg.Plan(B, M, N, H, W, r, pad, tile=MIX) as plan:
+        assert (plan.info["n"], plan.info["T"]) == (4, 64)
+    assert_close(_conv(x, w, pad), direct_conv2d(x, w, pad), what=str(case))
 
 
 def _stage_refs(x, w, pad):
@@ -200,11 +183,12 @@ def test_mixed_plan_rejects_what_it_does_not_serve():
         assert plan.info["tile"] == nwg.NWG_TILE_F2X2_3X3
 
 
-def test_large_kernel_workload_sampled_on_the_mixed_nest():
-    name = "c5_r31"
-    L = WORKLOADS[name].layers[0]
-    x, (w,) = make_workload(name)
-    print(f"workload {name} mixed nest", flush=True)
+def test_large_kernel_workload_on_the_mixed_nest_at_tile_edges(c5_oracle):
+    """The 31x31 workload on the mixed nest (n = 4, 36 x 36 tiles, the second
+    ragged), whole output against the oracle, and on its own the outputs on
+    both sides of the 12-pixel level-3 blocks and the 36-pixel tile edge."""
+    L, x, w, ref = c5_oracle
+    print("workload c5_r31 mixed nest", flush=True)
     with nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, tile=MIX) as plan:
         assert (plan.info["n"], plan.info["Mn"], plan.info["T"]) == (4, 36, 64)
         y = torch.empty(plan.y_shape, device="cuda")
@@ -212,6 +196,7 @@ def test_large_kernel_workload_sampled_on_the_mixed_nest():
         torch.cuda.synchronize()
         yh = y.cpu().numpy()
     assert np.isfinite(yh).all()
-    # both sides of the 12-pixel level-3 blocks and the 36-pixel tile edge
-    # (a ragged second tile)
-    _sampled(x, w, L.pad, yh, 9, [11, 12, 23, 24, 35, 36])
+    assert_close(yh, ref, what="c5_r31 mixed")
+    edges = [0, 11, 12, 23, 24, 35, 36, 47, 48, L.Ho - 1]
+    sub = np.ix_(range(L.B), range(L.N), edges, edges)
+    assert_close(yh[sub], ref[sub], what="tile and block edges")

@@ -318,3 +318,62 @@ def test_single_kernel_small_channel_layers(case):
         ms, cnt = plan.get_timing()
         assert cnt == [1, 0, 1, 0]
     assert_close(y, direct_conv2d(x, w, pad), what=str(case))
+
+
+def test_weight_cache_survives_a_freed_weight_tensor():
+    """A weight tensor freed after use can hand its memory to the next one:
+    the binding keeps the tensor it transformed (and its version counter),
+    so a new tensor, or the same one changed in place, is transformed again."""
+    B, M, N, H, W, r, pad = 1, 4, 8, 20, 20, 9, 4
+    _, x, w1 = make_case(B, M, N, H, W, r, pad, seed=21)
+    _, _, w2 = make_case(B, M, N, H, W, r, pad, seed=22)
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        xd = dev(x)
+        y = torch.empty(plan.y_shape, device="cuda")
+        plan.conv2d(xd, dev(w1), y)                  # the weight tensor is a temporary
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w1, pad), what="w1")
+        wd2 = dev(w2)                                # may take the freed block's address
+        plan.conv2d(xd, wd2, y)
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w2, pad), what="w2 after w1 freed")
+        wd2.copy_(dev(w1))                           # in place, no set_weights
+        plan.conv2d(xd, wd2, y)
+        torch.cuda.synchronize()
+        assert_close(y.cpu().numpy(), direct_conv2d(x, w1, pad), what="w2 changed in place")
+
+
+def test_allocation_failure_reports_enomem():
+    """A plan whose workspace cannot fit on the device (V alone about 2.2 TB
+    here) fails with NWG_ENOMEM, releases what it took, and the next plan
+    works."""
+    lib = nwg.load_library()
+    g = nwg.plan_geometry(4096, 128, 128, 56, 56, 31, 15, nwg.NWG_TILE_F2X2_3X3)
+    assert g["workspace_bytes"] > 1e12
+    free0, _ = torch.cuda.mem_get_info()
+    with pytest.raises(nwg.NwgError, match="hipMalloc"):
+        nwg.Plan(4096, 128, 128, 56, 56, 31, 15, tile=nwg.NWG_TILE_F2X2_3X3)
+    assert lib.nwg_last_status() == nwg.NWG_ENOMEM
+    free1, _ = torch.cuda.mem_get_info()
+    assert free1 >= free0 - (64 << 20)               # U (4.3 GB) was released
+    _, x, w = make_case(1, 2, 3, 12, 12, 5, 2, seed=4)
+    with nwg.Plan(1, 2, 3, 12, 12, 5, 2) as plan:
+        assert_close(run_conv(x, w, 2, plan), direct_conv2d(x, w, 2), what="after ENOMEM")
+
+
+def test_bad_device_buffers_are_refused_before_the_library():
+    with nwg.Plan(1, 2, 3, 12, 12, 5, 2) as plan:
+        x = torch.zeros((1, 2, 12, 12), device="cuda")
+        w = torch.zeros((3, 2, 5, 5), device="cuda")
+        y = torch.zeros(plan.y_shape, device="cuda")
+        with pytest.raises(nwg.NwgError, match="float32"):
+            plan.conv2d(x.double(), w, y)
+        with pytest.raises(nwg.NwgError, match="contiguous"):
+            plan.conv2d(x, w, y.transpose(2, 3))
+        with pytest.raises(nwg.NwgError, match="elements"):
+            plan.conv2d(x, w, y.reshape(-1)[:-1])
+        with pytest.raises(nwg.NwgError, match="aligned"):
+            plan.conv2d(torch.zeros(x.numel() + 1, device="cuda")[1:], w, y)
+        U = torch.zeros(plan.u_shape, device="cuda")
+        with pytest.raises(nwg.NwgError, match="elements"):
+            plan.kernel_transform(w, U.reshape(-1)[:-4])

@@ -1,15 +1,14 @@
 """GPU parity on the five workloads at full size, in the launch configuration
 the benchmark times (one plan per layer, nwg_conv2d on torch's stream).
 
-Small workloads are compared with the full fp64 direct oracle; the 31x31
-workload with a sample of outputs computed one by one, plus checks that hold
-at any size (every output finite, the ragged tile edges included).
+Every workload is compared with the full fp64 direct oracle, output by
+output: the 31x31 workload too, on each path that serves it.
 """
 import numpy as np
 import pytest
 import torch
 
-from oracle.direct import direct_conv2d, direct_conv2d_points
+from oracle.direct import direct_conv2d
 from paper_2102_13272_amd import nwg
 from paper_2102_13272_amd.workloads import WORKLOADS, make_workload
 from tests.gpu_util import assert_close, dev
@@ -69,29 +68,28 @@ def test_sr_stack_per_layer_and_end_to_end(name, tile):
         p.close()
 
 
-@pytest.mark.parametrize("precision", [nwg.NWG_PRECISION_FP32, nwg.NWG_PRECISION_BF16_SPLIT],
-                         ids=["fp32", "bf16_split"])
-def test_large_kernel_workload_sampled(precision):
-    name = "c5_r31"
-    L = WORKLOADS[name].layers[0]
-    x, (w,) = make_workload(name)
-    print(f"workload {name} precision {precision}", flush=True)
-    with nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad) as plan:
+@pytest.mark.parametrize("tile,precision", [(nwg.NWG_TILE_AUTO, nwg.NWG_PRECISION_FP32),
+                                            (nwg.NWG_TILE_F2X2_3X3, nwg.NWG_PRECISION_FP32),
+                                            (nwg.NWG_TILE_F2X2_3X3, nwg.NWG_PRECISION_BF16_SPLIT)],
+                         ids=["auto_mixed_nest", "f23_fp32", "f23_bf16_split"])
+def test_large_kernel_workload_whole_output(c5_oracle, tile, precision):
+    """Every one of the 6.4 M outputs of the 31x31 workload against the fp64
+    direct oracle, on the three paths that serve it: the automatic tile (the
+    mixed nest the benchmark times), four F(2,3) levels, and four F(2,3)
+    levels with the bf16-split contraction."""
+    L, x, w, ref = c5_oracle
+    print(f"workload c5_r31 tile {tile} precision {precision}", flush=True)
+    with nwg.Plan(L.B, L.M, L.N, L.H, L.W, L.r, L.pad, tile=tile) as plan:
+        want_tile = nwg.NWG_TILE_MIX_F23_F33 if tile == nwg.NWG_TILE_AUTO else tile
+        assert plan.info["tile"] == want_tile and plan.info["n"] == 4
         plan.set_precision(precision)
-        y = _gpu_layer(plan, dev(x), w)
+        y = torch.full(plan.y_shape, float("nan"), device="cuda")
+        plan.conv2d(dev(x), dev(w), y)
         torch.cuda.synchronize()
-        yh = y.cpu().numpy()
-    assert np.isfinite(yh).all()
-    rng = np.random.default_rng(5)
-    pts = {(int(rng.integers(L.B)), int(rng.integers(L.N)), int(rng.integers(L.Ho)),
-            int(rng.integers(L.Wo))) for _ in range(1500)}
-    # corners and the last rows/columns of the ragged-free 4x4 tile grid
-    for b in (0, L.B - 1):
-        for n in (0, L.N - 1):
-            for i in (0, 15, 16, L.Ho - 1):
-                for j in (0, 15, 16, L.Wo - 1):
-                    pts.add((b, n, i, j))
-    pts = sorted(pts)
-    ref = direct_conv2d_points(x, w, L.pad, pts)
-    got = np.array([yh[p] for p in pts], dtype=np.float64)
-    assert_close(got, ref, what=name)
+        got = y.cpu().numpy()
+    assert np.isfinite(got).all()
+    rel, mabs = assert_close(got, ref, what="c5_r31")
+    per_image = [assert_close(got[b], ref[b], what=f"image {b}")[0] for b in range(L.B)]
+    print(f"c5_r31 tile {want_tile} precision {precision}: rel-L2 {rel:.3e}, max-abs "
+          f"{mabs / np.abs(ref).max():.3e} of max|y|, worst image rel-L2 {max(per_image):.3e}",
+          flush=True)
