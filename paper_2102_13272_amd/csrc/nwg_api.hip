@@ -173,6 +173,7 @@ float* mix_scratch(const nwg_plan* p) {
                                                    : nullptr;
 }
 
+
 // Input transform and contraction in `parts` pieces on two streams: part k's
 // contraction (on the plan's side stream) waits only for part k's input
 // transform, so part k+1's input transform (HBM-bound) overlaps it
@@ -224,6 +225,67 @@ int run_kernel_transform(nwg_plan* p, const nwg_plan_info& g, const float* w, fl
                [&] { return launch_kxform(g, w, U, s); });
 }
 
+// A plan's buffers: U (transformed weights), V and Z (with the partial sums
+// or the mixed nest's scratch after it); NULL where the plan holds none.
+struct Workspace {
+  const float* U;
+  float* V;
+  float* Yh;
+};
+
+float* mix_scratch_of(const nwg_plan_info& g, float* Yh) {
+  return Yh && nwg::mix_scratch_bytes(g) ? Yh + g.yhat_bytes / sizeof(float) : nullptr;
+}
+
+// Everything nwg_conv2d queues after the kernel transform: the kernels the
+// plan's geometry selects, on stream s.  p supplies the timing records and
+// the two-stream pipeline; NULL runs untimed (and needs pipeline_parts = 1).
+int run_steps(nwg_plan* p, const nwg_plan_info& g, const Workspace& ws, const float* x,
+              float* y, hipStream_t s) {
+  const float* U = ws.U;
+  if (g.n == 0) {
+    return timed(p, 2, s, "contraction launch", [&] { return launch_contract(g, U, x, y, s); });
+  }
+  if (g.fused_conv) {
+    // input transform, channel sum (or product) and output transform in one kernel
+    return timed(p, 2, s, "single-kernel convolution launch", [&] {
+      return g.depthwise ? nwg::launch_dw_small(g, x, U, y, s)
+                         : nwg::launch_small_conv(g, x, U, y, s);
+    });
+  }
+  int rc;
+  if (g.fused_input && g.tile == NWG_TILE_F3X3_3X3) {
+    // partial Z9 per input-channel group, summed by the output transform
+    const int parts = nwg::input_contract5_parts(g);
+    rc = timed(p, 2, s, "fused input transform + contraction launch", [&] {
+      const hipError_t e = nwg::launch_input_contract5(g, x, U, ws.Yh, s);
+      if (e != hipSuccess) return e;
+      return nwg::launch_sum_parts(ws.Yh, (size_t)(g.P / 25) * 9 * g.N * g.T, parts, s);
+    });
+    if (rc != NWG_OK) return rc;
+    return timed(p, 3, s, "output transform launch",
+                 [&] { return nwg::launch_output_xform5(g, ws.Yh, y, s, 1, true); });
+  } else if (g.fused_input) {
+    rc = timed(p, 2, s, "fused input transform + contraction launch",
+               [&] { return nwg::launch_input_contract(g, x, U, ws.Yh, s); });
+  } else if (g.pipeline_parts > 1) {
+    if (!p) return fail(NWG_EUNSUPPORTED, "the two-stream pipeline needs a plan");
+    rc = run_pipelined(p, x, s);
+  } else {
+    rc = timed(p, 1, s, "input transform launch",
+               [&] { return launch_ixform(g, x, ws.V, mix_scratch_of(g, ws.Yh), s); });
+    if (rc != NWG_OK) return rc;
+    if (g.fused_output)
+      return timed(p, 2, s, "contraction + output transform launch",
+                   [&] { return nwg::launch_contract_output5(g, ws.V, U, y, s); });
+    rc = timed(p, 2, s, "contraction launch",
+               [&] { return launch_contract(g, U, ws.V, ws.Yh, s, nwg::ld_kslices(g)); });
+  }
+  if (rc != NWG_OK) return rc;
+  return timed(p, 3, s, "output transform launch",
+               [&] { return launch_oxform(g, ws.Yh, y, mix_scratch_of(g, ws.Yh), s); });
+}
+
 }  // namespace
 
 
@@ -267,6 +329,21 @@ nwg_plan* create_plan(const nwg_plan_info& g) {
 }
 
 }  // namespace
+
+// The launch sequence of nwg_conv2d on caller-provided workspace, for entry
+// points that hold no plan (untimed, one stream).
+namespace nwg {
+
+int kernel_transform_into(const nwg_plan_info& g, const float* w, float* U, hipStream_t s) {
+  return check_launch(launch_kxform(g, w, U, s), "kernel transform launch", s);
+}
+
+int conv_steps(const nwg_plan_info& g, const float* U, float* V, float* Yh, const float* x,
+               float* y, hipStream_t s) {
+  return run_steps(nullptr, g, {U, V, Yh}, x, y, s);
+}
+
+}  // namespace nwg
 
 extern "C" {
 
@@ -370,53 +447,11 @@ int nwg_plan_set_weights(nwg_plan* p, const float* w, void* stream) {
 int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stream) {
   if (!p || !x || !w || !y)
     return fail(NWG_EINVAL, "NULL argument to nwg_conv2d");
-  hipStream_t s = (hipStream_t)stream;
-  const nwg_plan_info& g = p->info;
   if (!p->weights_valid || p->cached_w != w) {
     const int rc = nwg_plan_set_weights(p, w, stream);
     if (rc != NWG_OK) return rc;
   }
-  if (g.n == 0) {
-    return timed(p, 2, s, "contraction launch",
-                 [&] { return launch_contract(g, p->U, x, y, s); });
-  }
-  if (g.fused_conv) {
-    // input transform, channel sum (or product) and output transform in one kernel
-    return timed(p, 2, s, "single-kernel convolution launch", [&] {
-      return g.depthwise ? nwg::launch_dw_small(g, x, p->U, y, s)
-                         : nwg::launch_small_conv(g, x, p->U, y, s);
-    });
-  }
-  int rc;
-  if (g.fused_input && g.tile == NWG_TILE_F3X3_3X3) {
-    // partial Z9 per input-channel group, summed by the output transform
-    const int parts = nwg::input_contract5_parts(g);
-    rc = timed(p, 2, s, "fused input transform + contraction launch", [&] {
-      const hipError_t e = nwg::launch_input_contract5(g, x, p->U, p->Yh, s);
-      if (e != hipSuccess) return e;
-      return nwg::launch_sum_parts(p->Yh, (size_t)(g.P / 25) * 9 * g.N * g.T, parts, s);
-    });
-    if (rc != NWG_OK) return rc;
-    return timed(p, 3, s, "output transform launch",
-                 [&] { return nwg::launch_output_xform5(g, p->Yh, y, s, 1, true); });
-  } else if (g.fused_input) {
-    rc = timed(p, 2, s, "fused input transform + contraction launch",
-               [&] { return nwg::launch_input_contract(g, x, p->U, p->Yh, s); });
-  } else if (g.pipeline_parts > 1) {
-    rc = run_pipelined(p, x, s);
-  } else {
-    rc = timed(p, 1, s, "input transform launch",
-               [&] { return launch_ixform(g, x, p->V, mix_scratch(p), s); });
-    if (rc != NWG_OK) return rc;
-    if (g.fused_output)
-      return timed(p, 2, s, "contraction + output transform launch",
-                   [&] { return nwg::launch_contract_output5(g, p->V, p->U, y, s); });
-    rc = timed(p, 2, s, "contraction launch",
-               [&] { return launch_contract(g, p->U, p->V, p->Yh, s, nwg::ld_kslices(g)); });
-  }
-  if (rc != NWG_OK) return rc;
-  return timed(p, 3, s, "output transform launch",
-               [&] { return launch_oxform(g, p->Yh, y, mix_scratch(p), s); });
+  return run_steps(p, p->info, {p->U, p->V, p->Yh}, x, y, (hipStream_t)stream);
 }
 
 int nwg_plan_set_precision(nwg_plan* p, int precision) {

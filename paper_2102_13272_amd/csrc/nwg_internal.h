@@ -313,4 +313,12 @@ hipError_t launch_dw_contract(const nwg_plan_info& g, const float* U, const floa
                               hipStream_t s);
 hipError_t launch_output_xform(const nwg_plan_info& g, const float* Yh, float* y, hipStream_t s);
 
+// What nwg_conv2d queues, on workspace the caller provides (the plan's layout:
+// U; V when plan_holds_v; Z with its partial sums or scratch when
+// plan_holds_z): the kernel transform w -> U, and the steps after it.
+// NWG_OK or a status with its message (untimed; pipeline_parts must be 1).
+int kernel_transform_into(const nwg_plan_info& g, const float* w, float* U, hipStream_t s);
+int conv_steps(const nwg_plan_info& g, const float* U, float* V, float* Yh, const float* x,
+               float* y, hipStream_t s);
+
 }  // namespace nwg
