@@ -95,8 +95,13 @@ typedef struct nwg_plan nwg_plan;
  *     (its fused kernels; unless the F(2x2,3x3) plan runs the layer in one
  *     kernel), or M, N >= 32 and either r = 8..9 (one nesting level fewer)
  *     or r <= 3 --, the mixed nest NWG_TILE_MIX_F23_F33 (below) for dense
- *     plans with r = 16..31 and M, N >= 32, and F(2x2,3x3) otherwise
- *     (always for depthwise plans).  info.tile reports the tile taken. */
+ *     plans with r = 16..31 and M, N >= 32 when a roofline model of the two
+ *     plans' steps (their algorithmic bytes at 5 TB/s, their MFMA work on
+ *     whole 64-column tiles at 100 TFLOP/s) expects it to be faster -- it has
+ *     1.6x fewer contraction FLOPs per output but 2.4x the transformed
+ *     weights, and few 36 x 36 tiles leave its MFMA tiles mostly empty --,
+ *     and F(2x2,3x3) otherwise (always for depthwise plans).  info.tile
+ *     reports the tile taken. */
 /*   NWG_TILE_LD_F2X2_3X3: the linear decomposition of Sec. II.B (Fig. 2),
  *     the method the paper compares nesting with, on the same F(2x2,3x3)
  *     kernels: the r x r kernel is cut into c x c sub-kernels of 3 x 3

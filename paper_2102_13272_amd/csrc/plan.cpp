@@ -6,6 +6,7 @@
 #include "plan.h"
 
 #include <climits>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -336,11 +337,34 @@ int geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile, i
 
 }  // namespace
 
+namespace {
+
+// Step time of an unfused dense plan on MI355X, in seconds, from its
+// algorithmic bytes and FLOPs at the rates its kernels sustain at depth 4
+// (about 5 TB/s of HBM traffic, 100 TFLOP/s of fp32 MFMA): the transforms
+// move x + V and Z + y; the contraction takes the longer of its U + V + Z
+// traffic and its MFMA work on whole 64-column tiles and 64-row / 32-deep
+// channel blocks.  Used only to choose between nests.
+double unfused_step_seconds(const nwg_plan_info& g) {
+  constexpr double kBw = 5.0e12, kMfma = 100e12;
+  auto up = [](double v, double q) { return std::ceil(v / q) * q; };
+  const double flop = 2.0 * (double)g.P * up(g.M, 32) * up(g.N, 64) * up((double)g.T, 64);
+  const double x = 4.0 * g.B * g.M * g.H * g.W, y = 4.0 * g.B * g.N * (double)g.Ho * g.Wo;
+  const double cb = (double)g.u_bytes + g.v_bytes + g.yhat_bytes;
+  const double tc = flop / kMfma > cb / kBw ? flop / kMfma : cb / kBw;
+  return tc + (x + g.v_bytes) / kBw + (g.yhat_bytes + y) / kBw;
+}
+
+}  // namespace
+
 // NWG_TILE_AUTO: F(3x3,3x3) where it measured faster than F(2x2,3x3) --
 // the fused one-output-channel kernel at depth 2 (unless F(2,3) runs the
 // layer in one kernel), or both channel counts >= 32 and either a nesting
 // level saved (r = 8, 9) or depth 1 (r <= 3); the mixed nest for dense
-// layers at depth 4 with both channel counts >= 32; F(2x2,3x3) otherwise.
+// layers at depth 4 with both channel counts >= 32 when the step model
+// above expects it to be faster (it has 1.6x fewer contraction FLOPs per
+// output but 2.4x the transformed weights, and 36 x 36 tiles: few tiles
+// leave most of a 64-column MFMA tile empty); F(2x2,3x3) otherwise.
 int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile, int depthwise,
                      nwg_plan_info* g) {
   if (!g) return fail(NWG_EINVAL, "output pointer is NULL");
@@ -349,7 +373,7 @@ int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile
   const int ra = geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F2X2_3X3, depthwise, &a);
   if (ra == NWG_OK && !depthwise && a.n == 4 && M >= 32 && N >= 32) {
     if (geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_MIX_F23_F33, 0, &b) == NWG_OK) {
-      *g = b;
+      *g = unfused_step_seconds(b) < unfused_step_seconds(a) ? b : a;
       return NWG_OK;
     }
     clear_error();

@@ -249,6 +249,17 @@ def test_f33_geometry_matches_oracle_levels(r):
     ((4, 5, 5, 256, 256, 3, 1), 0),       # few channels
     ((16, 128, 128, 56, 56, 31, 15), 3),  # depth 4, wide channels: the mixed nest
     ((2, 16, 128, 56, 56, 31, 15), 0),    # depth 4, M < 32
+    # depth 4 with M, N >= 32: the nest measured faster on MI355X (ms per call,
+    # F(2,3) / mixed) -- the mixed nest needs enough 36 x 36 tiles to fill
+    # its 64-column MFMA tiles, and pays 2.4x the transformed weights
+    ((2, 128, 128, 56, 56, 31, 15), 0),   # 1.64 / 3.61 (8 tiles on the mixed nest)
+    ((4, 128, 128, 28, 28, 31, 15), 0),   # 1.57 / 3.57 (4 tiles)
+    ((1, 256, 256, 28, 28, 27, 13), 0),   # 5.25 / 13.12 (1 tile)
+    ((16, 32, 32, 56, 56, 31, 15), 3),    # 1.18 / 0.94
+    ((4, 64, 128, 112, 112, 23, 11), 3),  # 3.85 / 2.89
+    ((1, 32, 32, 224, 224, 31, 15), 3),   # 1.06 / 0.89
+    ((8, 64, 64, 56, 56, 17, 8), 3),      # 1.37 / 1.35
+    ((32, 32, 64, 32, 32, 19, 9), 3),     # 0.79 / 0.77
     ((8, 64, 64, 56, 56, 13, 6), 0),      # depth 3
     ((1, 32, 32, 64, 64, 1, 0), 0),       # 1x1
 ])

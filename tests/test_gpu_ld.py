@@ -99,5 +99,7 @@ def test_ld_is_rejected_for_depthwise_and_split():
         with pytest.raises(nwg.NwgError):
             plan.set_precision(nwg.NWG_PRECISION_BF16_SPLIT)
         x = torch.zeros((1, 32, 40, 40), device="cuda")
-        with pytest.raises(nwg.NwgError):
-            plan.input_contract(x, x, x)
+        U = torch.zeros(plan.u_shape, device="cuda")
+        Z = torch.zeros(plan.z_shape, device="cuda")
+        with pytest.raises(nwg.NwgError, match="N <= 2"):
+            plan.input_contract(x, U, Z)

@@ -144,16 +144,16 @@ def test_fused_input_contract_matches_cpu_nested_reference(case):
 
 
 def test_fused_input_contract_rejects_other_shapes():
-    with nwg.Plan(1, 2, 3, 20, 20, 9, 4) as plan:           # N = 3
-        assert plan.info["fused_input"] == 0
-        x = torch.zeros((1, 2, 20, 20), device="cuda")
-        with pytest.raises(nwg.NwgError, match="N <= 2"):
-            plan.input_contract(x, x, x)
-    with nwg.Plan(1, 2, 1, 20, 20, 7, 3) as plan:           # depth 2
-        assert plan.info["fused_input"] == 0
-        x = torch.zeros((1, 2, 20, 20), device="cuda")
-        with pytest.raises(nwg.NwgError):
-            plan.input_contract(x, x, x)
+    # buffers of the plan's sizes, so that the library itself refuses the shape
+    for shape in [(1, 2, 3, 20, 20, 9, 4),                   # N = 3
+                  (1, 2, 1, 20, 20, 7, 3)]:                  # depth 2
+        with nwg.Plan(*shape) as plan:
+            assert plan.info["fused_input"] == 0
+            x = torch.zeros((1, 2, 20, 20), device="cuda")
+            U = torch.zeros(plan.u_shape, device="cuda")
+            Z = torch.zeros(plan.z_shape, device="cuda")
+            with pytest.raises(nwg.NwgError, match="N <= 2"):
+                plan.input_contract(x, U, Z)
 
 
 @pytest.mark.parametrize("N,M,T,depth", [(1, 32, 4096, 1), (5, 5, 100, 1), (128, 128, 256, 1),
