@@ -325,6 +325,30 @@ int nwg_plan_set_precision(nwg_plan* plan, int precision);
 int nwg_plan_set_timing(nwg_plan* plan, int enable);
 int nwg_plan_get_timing(nwg_plan* plan, double ms[4], long long count[4]);
 
+/* --- Without allocation ----------------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ * nwg_conv2d_noalloc computes what nwg_conv2d computes on a plan created by
+ * nwg_plan_create_pad(B, M, N, H, W, r, pad, tile) (dense, fp32, no
+ * pipeline), with the same kernels, but takes that plan's workspace (U; V
+ * and Z where the plan holds them; each rounded up to 256 bytes) from a
+ * static device array of NWG_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends, and transforms w on every
+ * call (nothing is cached).  It calls no hipMalloc, hipFree or allocating
+ * routine; its first call on a device resolves that device's copy of the
+ * array (with that device current).  x, w, y as for nwg_conv2d (contiguous
+ * fp32 device buffers, 16-byte aligned).  Returns NWG_OK, queuing the work on
+ * `stream`; NWG_EINVAL / NWG_EUNSUPPORTED as nwg_plan_create_pad does for the
+ * shape; NWG_EUNSUPPORTED, queuing nothing, when the workspace does not fit
+ * (64 MiB: e.g. the 7x7 32->32 64x64 layer needs 11.6 MB, the 13x13 64->64
+ * B=8 56x56 layer 581 MB); NWG_EHIP when a launch fails.
+ * Every call on a GPU uses that GPU's one array and overwrites it: calls that
+ * overlap on one GPU (from two streams or two threads) race, so order them
+ * on one stream or serialise them. */
+#define NWG_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int nwg_conv2d_noalloc(int B, int M, int N, int H, int W, int r, int pad, int tile,
+                       const float* x, const float* w, float* y, void* stream);
+
 /* Message for the last error on the calling thread ("" if none). */
 const char* nwg_last_error(void);
 

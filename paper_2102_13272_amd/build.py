@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libnwg.so")
 SOURCES = ["plan.cpp", "nwg_api.hip", "kernel_xform.hip", "input_xform.hip", "contract_mfma.hip",
            "output_xform.hip", "fused_small.hip",
-           "depthwise.hip", "small_conv.hip", "f33.hip", "mixed.hip"]
+           "depthwise.hip", "small_conv.hip", "f33.hip", "mixed.hip", "noalloc.hip"]
 ARCH = "gfx950"
 CFLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

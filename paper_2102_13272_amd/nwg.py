@@ -74,6 +74,7 @@ SIGNATURES = [
     ("nwg_plan_set_timing", _I, [_P, _I]),
     ("nwg_plan_get_timing", _I, [_P, ctypes.POINTER(ctypes.c_double),
                                  ctypes.POINTER(ctypes.c_longlong)]),
+    ("nwg_conv2d_noalloc", _I, [_I] * 8 + [_P] * 4),
     ("nwg_last_error", ctypes.c_char_p, []),
     ("nwg_last_status", _I, []),
     ("nwg_version", ctypes.c_char_p, []),
@@ -156,6 +157,20 @@ def _stream(stream) -> int:
         import torch
         return int(torch.cuda.current_stream().cuda_stream)
     return int(getattr(stream, "cuda_stream", stream))
+
+
+NWG_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def conv2d_noalloc(x, w, y, pad=0, tile=NWG_TILE_F2X2_3X3, stream=None):
+    """y = conv(x, w) through nwg_conv2d_noalloc: no plan, no device allocation
+    (the library's static per-GPU scratch holds the workspace; see nwg.h)."""
+    B, M, H, W = x.shape
+    N, _, r, _ = w.shape
+    Ho, Wo = H + 2 * pad - r + 1, W + 2 * pad - r + 1
+    _check(load_library().nwg_conv2d_noalloc(
+        B, M, N, H, W, r, pad, tile, _ptr(x, B * M * H * W, "x"), _ptr(w, N * M * r * r, "w"),
+        _ptr(y, B * N * max(Ho, 0) * max(Wo, 0), "y"), _stream(stream)), "nwg_conv2d_noalloc")
 
 
 class Plan:
