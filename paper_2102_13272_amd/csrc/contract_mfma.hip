@@ -44,6 +44,9 @@
 #include "nwg_internal.h"
 
 #include <cstdlib>
+#include <map>
+#include <mutex>
+#include <utility>
 
 namespace nwg {
 namespace {
@@ -691,6 +694,25 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
   wait_vmcnt<0>();                          // the clamped tail loads land before exit
 }
 
+// Work-groups of a persistent kernel that fit on one CU of device dev, asked
+// once per (device, kernel) and kept; 0 if the query fails.  Safe to call
+// from several threads.
+int persist_occupancy(int dev, const void* kernel, int threads) {
+  static std::mutex mu;
+  static std::map<std::pair<int, const void*>, int> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_pair(dev, kernel);
+  const auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int b = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, kernel, threads, 0) != hipSuccess) {
+    hipGetLastError();
+    b = 0;
+  }
+  cache[key] = b;
+  return b;
+}
+
 // Columns [0, ncols) of V and Z rows of T quads (ncols < 0: all T; the
 // caller offsets V and Z to the first column it wants).  The last column
 // tile may be ragged: its loads clamp to column ncols - 1 and its extra
@@ -708,17 +730,14 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
   if (STAGES == 4 && ncols == T) {
     // one work-group per CU slot when every slot gets at least 4 items
-    static int occ = -1;
-    if (occ < 0) {
-      int b = 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-              &b, reinterpret_cast<const void*>(&contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT>),
-              64 * WM * WN, 0) != hipSuccess)
-        b = 0;
-      occ = b;
-    }
     int dev = 0, cus = 0;
-    if (occ > 0 && hipGetDevice(&dev) == hipSuccess &&
+    const int occ =
+        hipGetDevice(&dev) == hipSuccess
+            ? persist_occupancy(dev, reinterpret_cast<const void*>(
+                                         &contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT>),
+                                64 * WM * WN)
+            : 0;
+    if (occ > 0 &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
         cus >= 8) {
       const int wpx = cus / 8 * occ;
