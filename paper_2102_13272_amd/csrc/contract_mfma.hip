@@ -208,7 +208,7 @@ struct FusedTile {
 template <int BM, int BN, int WM, int WN, bool FULL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void contract_fused(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
-    int N, int T, int ncols, int ntb, int nnb) {
+    int N, int T, int ntb, int nnb) {
   using Tile = FusedTile<BM, BN, WM, WN, FULL>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4, "four waves");
@@ -246,7 +246,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     tile.db.init(T, c0);
   } else {
     tile.la.init(N, n0, N);
-    tile.lb.init(T, c0, ncols);
+    tile.lb.init(T, c0, T);
   }
 
   const int nk = (M + kBK - 1) / kBK;
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = c0 + wn * WTN + j * 16 + lr;
-        if (FULL || col < ncols)
+        if (FULL || col < T)
           Zg[(size_t)row * T + col] = make_float4(tile.out[0][i][j][v], tile.out[1][i][j][v],
                                                   tile.out[2][i][j][v], tile.out[3][i][j][v]);
       }
@@ -334,16 +334,6 @@ struct DeepLoader {
           (__attribute__((address_space(3))) void*)(flat + j * NT + wave * 64), 16, 0, 0);
   }
 };
-
-// One Z quad of the deep kernels' output tile: the four level-1 outputs of
-// element v of fragment (i, j).  (Nontemporal stores here measured the same
-// on the workloads: 3.41 ms on the 31x31 mixed-nest layer either way.)
-template <int FM, int FN>
-__device__ __forceinline__ void store_z(float4* dst, const floatx4 (&out)[4][FM][FN], int i, int j,
-                                        int v) {
-  *reinterpret_cast<floatx4*>(dst) =
-      floatx4{out[0][i][j][v], out[1][i][j][v], out[2][i][j][v], out[3][i][j][v]};
-}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -471,7 +461,7 @@ struct DeepTile {
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((BM / WM) * (BN / WN) > 1024 ? 1 : 2))) void contract_deep(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
-    int N, int T, int ncols, int ntb, int nnb, int ks) {
+    int N, int T, int ntb, int nnb, int ks) {
   using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
@@ -519,7 +509,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
         tile.acc[o][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
   tile.da.init(N, n0, N);
-  tile.db.init(T, c0, ncols);
+  tile.db.init(T, c0, T);
 
   // prologue: chunks 0 .. STAGES-2 (the K loop has nk % STAGES == 0 chunks per q1r)
   tile.request(0, A0, B0);
@@ -554,7 +544,9 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = c0 + tile.wn * WTN + j * 16 + tile.lr;
-        if (col < ncols) store_z(&Zg[(size_t)row * T + col], tile.out, i, j, v);
+        if (col < T)
+          Zg[(size_t)row * T + col] = make_float4(tile.out[0][i][j][v], tile.out[1][i][j][v],
+                                                  tile.out[2][i][j][v], tile.out[3][i][j][v]);
       }
     }
   }
@@ -680,7 +672,9 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
 #pragma unroll
         for (int jj = 0; jj < FN; ++jj) {
           const int col = c0 + tile.wn * WTN + jj * 16 + tile.lr;
-          if (col < T) store_z(&Zg[(size_t)row * T + col], tile.out, i, jj, v);
+          if (col < T)
+            Zg[(size_t)row * T + col] = make_float4(tile.out[0][i][jj][v], tile.out[1][i][jj][v],
+                                                    tile.out[2][i][jj][v], tile.out[3][i][jj][v]);
         }
       }
     }
@@ -713,22 +707,17 @@ int persist_occupancy(int dev, const void* kernel, int threads) {
   return b;
 }
 
-// Columns [0, ncols) of V and Z rows of T quads (ncols < 0: all T; the
-// caller offsets V and Z to the first column it wants).  The last column
-// tile may be ragged: its loads clamp to column ncols - 1 and its extra
-// columns are not stored.
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT = false>
 hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, int T,
-                       long long G, hipStream_t s, int ks = 1, int ncols = -1) {
-  if (ncols < 0) ncols = T;
-  const int ntb = (ncols + BN - 1) / BN, nnb = N / BM;
+                       long long G, hipStream_t s, int ks = 1) {
+  // T need not be a multiple of BN: the last column tile is ragged
+  const int ntb = (T + BN - 1) / BN, nnb = N / BM;
   const long long blocks = (long long)ntb * nnb * G * ks;
-  if (ks < 1 || ncols <= 0 || ncols > T || N % BM || M % (BKD * STAGES * ks) || blocks <= 0 ||
-      blocks > 0x7fffffffLL)
+  if (ks < 1 || N % BM || M % (BKD * STAGES * ks) || blocks <= 0 || blocks > 0x7fffffffLL)
     return hipErrorInvalidValue;
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
-  if (STAGES == 4 && ncols == T) {
+  if (STAGES == 4) {
     // one work-group per CU slot when every slot gets at least 4 items
     int dev = 0, cus = 0;
     const int occ =
@@ -751,31 +740,26 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
   }
   hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES, SPLIT>), dim3((unsigned)blocks),
                      dim3(64 * WM * WN), 0, s, (const float4*)U, (const float4*)V, (float4*)Z,
-                     M, N, T, ncols, ntb, nnb, ks);
+                     M, N, T, ntb, nnb, ks);
   return hipGetLastError();
 }
 
-// ncols < T: the columns [0, ncols) of a V and Z whose rows hold T quads
-// (the caller offsets V and Z to the first column it wants)
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                        long long G, hipStream_t s, int ncols = -1) {
-  if (ncols < 0) ncols = T;
-  const int ntb = (ncols + BN - 1) / BN;
+                        long long G, hipStream_t s) {
+  const int ntb = (T + BN - 1) / BN;
   const int nnb = (N + BM - 1) / BM;
   const long long blocks = (long long)ntb * nnb * G;
-  if (ncols <= 0 || ncols > T || blocks <= 0 || blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+  if (blocks <= 0 || blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
   if ((long long)M * (N > T ? N : T) > 0x7fffffffLL / 4) return hipErrorInvalidValue;
-  const bool full = N % BM == 0 && ncols % BN == 0 && M % kBK == 0;
+  const bool full = N % BM == 0 && T % BN == 0 && M % kBK == 0;
   if (full)
     hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN, true>), dim3((unsigned)blocks), dim3(256),
-                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ncols, ntb,
-                       nnb);
+                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
   else
     hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN, false>), dim3((unsigned)blocks), dim3(256),
-                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ncols, ntb,
-                       nnb);
+                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
   return hipGetLastError();
 }
 
@@ -952,31 +936,19 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
     if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s, ks);
     return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s, ks);
   }
-  // full 64-row tiles and whole 4-stage K sweeps: the deep pipeline
+  // full 64-row tiles and whole 4-stage K sweeps: the deep pipeline; a
+  // ragged T takes 64-column tiles (the last one partly recomputed)
   if (M % 32 == 0 && N % 64 == 0) {
     if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s);
     // T = 64 with N a multiple of 128 (e.g. the mixed nest's 31x31 layer):
     // 128 x 64 blocks, so that V is read once per group (3.52 -> 3.44 ms)
     if (T == 64 && N % 128 == 0)   // four wavefronts of 64 x 32 (one per SIMD): 3.43 -> 3.38 ms
       return launch_deep<128, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
-    if (T % 64 == 0) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
-    // a ragged T: the whole 64-column tiles on the deep pipeline, the last
-    // T % 64 columns in 16-column tiles, instead of a mostly empty last
-    // 64-column tile (13x13 layer, T = 392: 448 columns of MFMA work become
-    // 400, and 7 x 256 work-groups on 512 slots, 3.5 rounds, become 6 x 256
-    // in 3 rounds plus 256 narrow ones: 0.164 -> 0.150 ms)
-    if (T > 64) {
-      const int whole = T / 64 * 64;
-      const hipError_t e = launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s, 1, whole);
-      if (e != hipSuccess) return e;
-      // 64 x 16 blocks: one 16-column fragment per wavefront, 16-channel
-      // chunks (three in flight) where M allows, else the general kernel
-      if (M % 64 == 0)
-        return launch_deep<64, 16, 4, 1, 16, 4>(U, V + 4 * (size_t)whole, Z + 4 * (size_t)whole,
-                                                M, N, T, G, s, 1, T - whole);
-      return launch_fused<64, 16, 4, 1>(U, V + 4 * (size_t)whole, Z + 4 * (size_t)whole, M, N, T,
-                                        G, s, T - whole);
-    }
+    // a ragged T: 64-column tiles, the last one partly recomputed (on the
+    // 13x13 layer, T = 392, this measured 163 us against 173 us for the whole
+    // tiles plus a separate launch of 64 x 16 blocks for the last 8 columns,
+    // which re-reads all of U)
+    if (T >= 64) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
   }
   // small problems (fewer than 256 work-groups with the wide tiles, e.g.
   // 32 channels on 256 tiles at depth 2: 32 work-groups): 16 x 64 tiles

@@ -163,9 +163,7 @@ def test_fused_input_contract_rejects_other_shapes():
                                          # full tiles (direct global->LDS path) per tile shape
                                          (64, 32, 128, 1), (16, 16, 128, 2), (32, 48, 256, 1),
                                          (128, 64, 192, 1), (64, 96, 256, 1), (128, 32, 128, 2),
-                                         # ragged T: whole 64-column tiles on the deep
-                                         # path, the rest in 16-column tiles (deep for
-                                         # M % 64 == 0, else the general kernel)
+                                         # deep path with a ragged last column tile
                                          (64, 32, 100, 1), (128, 64, 200, 2), (64, 64, 65, 1),
                                          (64, 128, 130, 1), (64, 96, 150, 2), (128, 64, 392, 1),
                                          # persistent deep path (at least 4 tiles per CU slot):
