@@ -42,9 +42,11 @@
  * Z when info.fused_conv is set (the stage calls still work on caller
  * buffers).
  * Every call that takes a stream only queues work on it (`stream` is a
- * hipStream_t; NULL is the default stream) and never synchronises, except
- * nwg_plan_get_timing.  A plan is not thread-safe; one call in flight per
- * plan.
+ * hipStream_t; NULL is the default stream of the current device) and never
+ * synchronises, except nwg_plan_get_timing.  A call that uses a plan's
+ * workspace needs the device the plan was created on to be current and the
+ * stream to belong to it (NWG_EINVAL otherwise).  A plan is not thread-safe;
+ * one call in flight per plan.
  *
  * Errors: functions returning int give NWG_OK (0) or a negative status;
  * functions returning a pointer give NULL.  nwg_last_error() then returns a

@@ -73,6 +73,18 @@ extern "C" int nwg_conv2d_noalloc(int B, int M, int N, int H, int W, int r, int 
                      (size_t)NWG_NOALLOC_SCRATCH_BYTES);
   if ((((uintptr_t)x | (uintptr_t)w | (uintptr_t)y) & 15) != 0)
     return nwg::fail(NWG_EINVAL, "x, w and y must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (s) {
+    // the scratch is the current device's: the stream must run there
+    int sdev = -1, cur = -1;
+    if (hipStreamGetDevice(s, &sdev) != hipSuccess || hipGetDevice(&cur) != hipSuccess) {
+      hipGetLastError();
+      return nwg::fail(NWG_EHIP, "device of the stream or current device unknown");
+    }
+    if (sdev != cur)
+      return nwg::fail(NWG_EINVAL, "the stream runs on device %d, device %d is current", sdev,
+                       cur);
+  }
   unsigned char* base = nullptr;
   rc = scratch_of_current_device(&base);
   if (rc != NWG_OK) return rc;
@@ -81,7 +93,6 @@ extern "C" int nwg_conv2d_noalloc(int B, int M, int N, int H, int W, int r, int 
   float* U = ub ? reinterpret_cast<float*>(base) : nullptr;
   float* V = vb ? reinterpret_cast<float*>(base + round256(ub)) : nullptr;
   float* Z = zb ? reinterpret_cast<float*>(base + round256(ub) + round256(vb)) : nullptr;
-  hipStream_t s = static_cast<hipStream_t>(stream);
   rc = nwg::kernel_transform_into(g, w, U, s);
   if (rc != NWG_OK) return rc;
   return nwg::conv_steps(g, U, V, Z, x, y, s);

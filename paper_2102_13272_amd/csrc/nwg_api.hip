@@ -69,6 +69,32 @@ int check_launch(hipError_t e, const char* what, hipStream_t s) {
   return rc;
 }
 
+// The device a stream's work runs on: its own for a created stream, the
+// current device for the NULL stream.
+int stream_device(hipStream_t s, int* dev) {
+  const hipError_t e = s ? hipStreamGetDevice(s, dev) : hipGetDevice(dev);
+  if (e != hipSuccess) {
+    hipGetLastError();
+    return fail(NWG_EHIP, "device of the stream: %s", hipGetErrorString(e));
+  }
+  return NWG_OK;
+}
+
+// Work that touches a plan's workspace must run on the device that holds it,
+// with that device current (the plan's side stream and events are created
+// on the current device).
+int check_plan_device(const nwg_plan* p, hipStream_t s) {
+  int dev = -1, cur = -1;
+  int rc = stream_device(s, &dev);
+  if (rc == NWG_OK) rc = stream_device(nullptr, &cur);
+  if (rc != NWG_OK) return rc;
+  if (dev != p->device || cur != p->device)
+    return fail(NWG_EINVAL,
+                "the plan's workspace is on device %d; the stream runs on device %d and "
+                "device %d is current", p->device, dev, cur);
+  return NWG_OK;
+}
+
 hipEvent_t take_event(nwg_plan* p) {
   if (!p->event_pool.empty()) {
     hipEvent_t e = p->event_pool.back();
@@ -399,6 +425,10 @@ int nwg_input_transform(const nwg_plan* p, const float* x, float* V, void* strea
   if (p->info.n == 0)
     return fail(NWG_EINVAL, "depth 0 (r = 1) has no input transform");
   hipStream_t s = (hipStream_t)stream;
+  if (mix_scratch(p)) {   // the plan's scratch is part of this call
+    const int rd = check_plan_device(p, s);
+    if (rd != NWG_OK) return rd;
+  }
   return check_launch(launch_ixform(p->info, x, V, mix_scratch(p), s), "input transform launch", s);
 }
 
@@ -427,6 +457,10 @@ int nwg_output_transform(const nwg_plan* p, const float* Yh, float* y, void* str
   if (p->info.n == 0)
     return fail(NWG_EINVAL, "depth 0 (r = 1) has no output transform");
   hipStream_t s = (hipStream_t)stream;
+  if (mix_scratch(p)) {   // the plan's scratch is part of this call
+    const int rd = check_plan_device(p, s);
+    if (rd != NWG_OK) return rd;
+  }
   return check_launch(launch_oxform(p->info, Yh, y, mix_scratch(p), s), "output transform launch",
                       s);
 }
@@ -434,6 +468,8 @@ int nwg_output_transform(const nwg_plan* p, const float* Yh, float* y, void* str
 int nwg_plan_set_weights(nwg_plan* p, const float* w, void* stream) {
   if (!p || !w)
     return fail(NWG_EINVAL, "NULL argument to nwg_plan_set_weights");
+  const int rd = check_plan_device(p, (hipStream_t)stream);
+  if (rd != NWG_OK) return rd;
   const int rc = run_kernel_transform(p, p->info, w, p->U, (hipStream_t)stream);
   if (rc == NWG_OK) {
     p->cached_w = w;
@@ -447,6 +483,8 @@ int nwg_plan_set_weights(nwg_plan* p, const float* w, void* stream) {
 int nwg_conv2d(nwg_plan* p, const float* x, const float* w, float* y, void* stream) {
   if (!p || !x || !w || !y)
     return fail(NWG_EINVAL, "NULL argument to nwg_conv2d");
+  const int rd = check_plan_device(p, (hipStream_t)stream);
+  if (rd != NWG_OK) return rd;
   if (!p->weights_valid || p->cached_w != w) {
     const int rc = nwg_plan_set_weights(p, w, stream);
     if (rc != NWG_OK) return rc;

@@ -378,3 +378,21 @@ def test_bad_device_buffers_are_refused_before_the_library():
         U = torch.zeros(plan.u_shape, device="cuda")
         with pytest.raises(nwg.NwgError, match="elements"):
             plan.kernel_transform(w, U.reshape(-1)[:-4])
+
+
+def test_calls_on_a_created_stream_and_the_null_stream():
+    """The device check accepts the plan's own device, through a created
+    stream and through the NULL stream (the current device's)."""
+    B, M, N, H, W, r, pad = 1, 3, 5, 22, 18, 7, 3
+    _, x, w = make_case(B, M, N, H, W, r, pad, seed=31)
+    ref = direct_conv2d(x, w, pad)
+    side = torch.cuda.Stream()
+    with nwg.Plan(B, M, N, H, W, r, pad) as plan:
+        xd, wd = dev(x), dev(w)
+        torch.cuda.synchronize()
+        for stream in (side, 0):
+            y = torch.full(plan.y_shape, float("nan"), device="cuda")
+            torch.cuda.synchronize()
+            plan.conv2d(xd, wd, y, stream=stream)
+            torch.cuda.synchronize()
+            assert_close(y.cpu().numpy(), ref, what=f"stream {stream}")
