@@ -300,6 +300,8 @@ def run_workload(torch, nwg, name: str, tile: str, precision: str, steps: int, w
             del U2
         except nwg.NwgError:
             kx_ms += ms[0]      # no stage call (depth 0, depthwise): first call
+    # its algorithmic bytes (w read, U written), summed over layers
+    kx_bytes = float(sum(stage_bytes_flops(p.info)["kernel_transform"][0] for p in plans))
 
     # the timed steps run with the library's per-stage events off (recording
     # them puts work between the launches); a second pass of K steps with
@@ -421,7 +423,16 @@ def run_workload(torch, nwg, name: str, tile: str, precision: str, steps: int, w
     return {"plans": plans, "ms_step": ms_step, "ms_step_eager": ms_step_eager,
             "value": direct_flop / (ms_step * 1e-3) / 1e12, "direct_flop": direct_flop,
             "stages": detail, "roofline": roof, "config": cfg, "kx_ms": kx_ms,
+            "kx_bytes": kx_bytes,
             "kx_first_ms": kx_first_ms, "split": split, "y": y_timed}
+
+
+def kernel_transform_entry(ms: float, nbytes: float) -> dict:
+    """The cached kernel transform, timed apart from the step: its algorithmic
+    bytes (w + U) and their rate against the HBM peak."""
+    gbs = nbytes / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+    return {"ms_once": round(ms, 4), "bytes": nbytes, "GB_s": round(gbs, 1),
+            "hbm_frac": round(gbs / PEAK_HBM_GBS, 4), "bound": "hbm"}
 
 
 def close(res):
@@ -508,6 +519,7 @@ def main():
         "data": "synthetic", "config": cfg, "roofline": res["roofline"],
         "stages": res["stages"],
         "kernel_transform_ms_once": round(res["kx_ms"], 4),
+        "kernel_transform": kernel_transform_entry(res["kx_ms"], res["kx_bytes"]),
         "kernel_transform_ms_first_call": round(res["kx_first_ms"], 4),
         "value_incl_kernel_transform": round(
             res["direct_flop"] / ((res["ms_step"] + res["kx_ms"]) * 1e-3) / 1e12, 3),
@@ -529,7 +541,8 @@ def main():
             "roofline": {k: r2["roofline"][k] for k in ("bound", "frac", "kernel")},
             "stages": {k: {f: v[f] for f in ("ms_per_step", "GB_s", "hbm_frac", "TFLOP_s",
                                               "mfma_frac")}
-                       for k, v in r2["stages"].items()}}
+                       for k, v in r2["stages"].items()},
+            "kernel_transform": kernel_transform_entry(r2["kx_ms"], r2["kx_bytes"])}
         y_f23 = r2["y"]
         close(r2)
     failed = []
@@ -558,7 +571,8 @@ def main():
                                           "kernel", "avg_launch_us")},
                    "stages": {k: {f: v[f] for f in ("ms_per_step", "GB_s", "hbm_frac",
                                                      "TFLOP_s", "mfma_frac")}
-                              for k, v in rk["stages"].items()}}
+                              for k, v in rk["stages"].items()},
+                   "kernel_transform": kernel_transform_entry(rk["kx_ms"], rk["kx_bytes"])}
             y_k = rk["y"]
             close(rk)
             if not args.no_cpu_baseline:

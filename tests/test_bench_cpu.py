@@ -127,3 +127,15 @@ def test_cpu_baseline_reports_parity_of_the_outputs_it_is_given():
     assert par["good"]["ok"] and par["good"]["rel_l2"] < 1e-6
     assert not par["bad"]["ok"] and par["bad"]["max_abs_over_max"] > 1e-3
     assert par["good"]["outputs"] == y.size
+
+
+def test_kernel_transform_entry_is_its_bytes_over_its_time():
+    # the mixed nest's 31 x 31 layer: w (63 MB) + U (10.49 GB) in 2.25 ms
+    g = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15, nwg.NWG_TILE_MIX_F23_F33)
+    nbytes = bench.stage_bytes_flops(g)["kernel_transform"][0]
+    e = bench.kernel_transform_entry(2.25, nbytes)
+    assert e["bytes"] == 4 * 128 * 128 * 31 * 31 + g["u_bytes"]
+    assert e["GB_s"] == pytest.approx(nbytes / 2.25e-3 / 1e9, rel=1e-3)
+    assert e["hbm_frac"] == pytest.approx(e["GB_s"] / bench.PEAK_HBM_GBS, rel=1e-3)
+    assert e["bound"] == "hbm" and e["ms_once"] == 2.25
+    assert bench.kernel_transform_entry(0.0, nbytes)["GB_s"] == 0.0
