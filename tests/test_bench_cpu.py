@@ -107,8 +107,8 @@ def test_traffic_needs_the_copy_calibration(tmp_path, monkeypatch):
 def test_committed_traffic_summaries_match_the_current_contraction_source():
     """The default line's traffic comes from profiles/traffic_c5_r31_auto.json;
     its contraction entry must be the one taken on the current kernel source."""
-    for tile in ("auto", "f23"):
-        t = bench.measured_traffic("c5_r31", "contraction", tile)
+    for wl, tile in (("c5_r31", "auto"), ("c5_r31", "f23"), ("c3_r13", "auto")):
+        t = bench.measured_traffic(wl, "contraction", tile)
         assert t is not None and t > 0
 
 
