@@ -568,7 +568,8 @@ def main():
                    "unit": "TFLOP/s", "config": rk["config"],
                    "roofline": {k: rk["roofline"][k]
                                 for k in ("bound", "achieved", "peak", "unit", "frac",
-                                          "kernel", "avg_launch_us")},
+                                          "kernel", "avg_launch_us", "traffic",
+                                          "traffic_source")},
                    "stages": {k: {f: v[f] for f in ("ms_per_step", "GB_s", "hbm_frac",
                                                      "TFLOP_s", "mfma_frac")}
                               for k, v in rk["stages"].items()},
