@@ -190,6 +190,19 @@ typedef struct nwg_plan_info {
                                    contraction, index 2); the plan holds no Z */
   int outer33;                  /* NWG_TILE_MIX_F23_F33: F(3,3) levels above the two
                                    F(2,3) levels (1 or 2); else 0 */
+  /* Groups that need no work.  A group is the 16 points (4 x 4) sharing their
+   * digits above level 1; its place in Z is g = P/16 ordering of those digits.
+   * On the mixed nest the kernel taps split greedily over the levels leave
+   * some digit combinations with no tap (and the padded taps r..Kn-1 are
+   * zero), so the transformed kernel of a point is zero for every w when no
+   * real tap reaches it.  A group is dead when, along either axis, none of
+   * its points is reached; its Z is zero.  The library then neither writes
+   * nor reads its U, V and Z, and skips its contraction. */
+  int live_np;                  /* live digit prefixes per axis (levels 2..n) on the
+                                   mixed nest; 0 when every group is computed */
+  unsigned long long live_prefix[2];   /* bit i: prefix i of an axis is live (digits
+                                   q_n .. q_2, the outermost most significant) */
+  long long live_groups;        /* groups the contraction computes: live_np^2, or P/16 */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only): the

@@ -217,6 +217,58 @@ int ld_geometry(int B, int M, int N, int H, int W, int r, int pad, int depthwise
   return NWG_OK;
 }
 
+// Digits k_j of a tap's row in a level's kernel transform that the row of
+// point q reaches (bit k): G of F(2,3) (points 0, 1, -1, infinity) and of
+// F(3,3) (points 0, 1, -1, 2, infinity) has one nonzero entry in its first
+// and last rows and three in the others.
+unsigned g_row_digits(int l, int q) { return q == 0 ? 1u : q == l - 1 ? 4u : 7u; }
+
+// Mixed nest: which digit prefixes (q_n .. q_2) of an axis have a point whose
+// transformed kernel can be nonzero.  Tap k < r reaches point (q_n .. q_1)
+// when each digit of its greedy split (outermost first, each at most 2, as
+// the kernel transform splits it) is one that the point's G row reaches.
+void mix_liveness(nwg_plan_info* g) {
+  const int n = g->n;
+  int l[NWG_MAX_DEPTH];
+  for (int j = 0; j < n; ++j) l[j] = j < 2 ? 4 : 5;   // level j + 1
+  int npref = 1;
+  for (int j = 1; j < n; ++j) npref *= l[j];
+  if (npref > 128) return;                            // beyond the masks: all groups live
+  int live = 0;
+  unsigned long long mask[2] = {0, 0};
+  for (int pf = 0; pf < npref; ++pf) {
+    int q[NWG_MAX_DEPTH] = {0};
+    int rest = pf;
+    for (int j = 1; j < n; ++j) {                     // q_2 least significant
+      q[j] = rest % l[j];
+      rest /= l[j];
+    }
+    bool reached = false;
+    for (int q1 = 0; q1 < l[0] && !reached; ++q1) {
+      q[0] = q1;
+      for (int k = 0; k < g->r && !reached; ++k) {
+        int rem = k;
+        bool ok = true;
+        for (int j = n - 1; j >= 1 && ok; --j) {
+          const int d = rem / g->strides[j] < 2 ? rem / g->strides[j] : 2;
+          rem -= d * g->strides[j];
+          ok = (g_row_digits(l[j], q[j]) >> d) & 1u;
+        }
+        reached = ok && rem <= 2 && ((g_row_digits(l[0], q[0]) >> rem) & 1u);
+      }
+    }
+    if (reached) {
+      mask[pf >> 6] |= 1ULL << (pf & 63);
+      ++live;
+    }
+  }
+  if (live == npref) return;                        // nothing to skip
+  g->live_np = live;
+  g->live_prefix[0] = mask[0];
+  g->live_prefix[1] = mask[1];
+  g->live_groups = (long long)live * live;
+}
+
 // Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,
 // s_j = min(M_j, K_j), M_{j+1} = M_j + s_j (m_{j+1} - 1),
 // K_{j+1} = K_j + s_j (rb - 1); n is the smallest depth with K_n >= r, and
@@ -332,6 +384,8 @@ int geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile, i
   g->precision = NWG_PRECISION_FP32;
   g->workspace_bytes = g->u_bytes + (plan_holds_v(*g) ? g->v_bytes : 0) +
                        (plan_holds_z(*g) ? zalloc_bytes(*g) : 0);
+  g->live_groups = f33 || n == 0 ? 0 : g->P / 16;
+  if (mix && n >= 3) mix_liveness(g);
   return NWG_OK;
 }
 

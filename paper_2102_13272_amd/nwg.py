@@ -43,11 +43,14 @@ class nwg_plan_info(ctypes.Structure):
         ("depthwise", ctypes.c_int), ("fused_conv", ctypes.c_int),
         ("pipeline_parts", ctypes.c_int), ("precision", ctypes.c_int), ("ld_c", ctypes.c_int),
         ("fused_output", ctypes.c_int), ("outer33", ctypes.c_int),
+        ("live_np", ctypes.c_int), ("live_prefix", ctypes.c_ulonglong * 2),
+        ("live_groups", ctypes.c_longlong),
     ]
 
     def as_dict(self):
         d = {name: getattr(self, name) for name, _ in self._fields_}
         d["strides"] = list(self.strides)[: self.n]
+        d["live_prefix"] = list(self.live_prefix)
         return d
 
 

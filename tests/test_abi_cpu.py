@@ -368,3 +368,45 @@ def test_mixed_geometry_of_the_31x31_workload():
     # 1.64x fewer contraction FLOPs than four F(2,3) levels (65536 points x 256 tiles)
     f23 = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15)
     assert f23["P"] * f23["T"] / (g["P"] * g["T"]) == pytest.approx(1.6384)
+
+
+def _oracle_live_prefixes(r):
+    """Digit prefixes (q_n .. q_2, the outermost most significant) of the
+    mixed chain at kernel size r with a point whose row of the oracle's
+    kernel-transform matrix is nonzero over the r real taps."""
+    from oracle.mixed import mixed_levels, kernel_matrix, _digits
+    from oracle.nested import toom_cook_base
+    f23, f33 = base_f23(), toom_cook_base(3, 3, [0, 1, -1, 2])
+    n = nwg.plan_geometry(1, 1, 1, 64, 64, r, 0, nwg.NWG_TILE_MIX_F23_F33)["n"]
+    lv = mixed_levels([f23, f23] + [f33] * (n - 2), r)
+    KG = kernel_matrix(lv)
+    rad = [b.l for b in lv.bases]                 # level 1 .. n
+    live = set()
+    for p in range(lv.P1):
+        d = _digits(p, rad)                       # (q_1, ..., q_n), q_1 most significant
+        if any(KG[p, k] != 0 for k in range(r)):
+            idx = 0
+            for j in range(n - 1, 0, -1):         # q_n first
+                idx = idx * rad[j] + d[j]
+            live.add(idx)
+    npref = 1
+    for j in range(1, n):
+        npref *= rad[j]
+    return live, npref
+
+
+@pytest.mark.parametrize("r", [8, 9, 12, 13, 15, 16, 17, 24, 27, 31, 33, 35, 38, 39])
+def test_mixed_live_groups_are_the_oracle_kernel_rows_that_reach_a_real_tap(r):
+    """The library skips the mixed nest's groups whose transformed kernel is zero
+    for every w; its per-axis prefix mask must be the set of prefixes with a
+    nonzero row in the oracle's kernel-transform matrix (Sec. III.B's
+    reordering and G^(x)n, written independently)."""
+    g = nwg.plan_geometry(2, 8, 8, 64, 64, r, r // 2, nwg.NWG_TILE_MIX_F23_F33)
+    live, npref = _oracle_live_prefixes(r)
+    if g["live_np"] == 0:
+        assert len(live) == npref and g["live_groups"] == g["P"] // 16
+        return
+    mask = g["live_prefix"][0] | (g["live_prefix"][1] << 64)
+    lib = {i for i in range(npref) if (mask >> i) & 1}
+    assert lib == live
+    assert g["live_np"] == len(live) and g["live_groups"] == len(live) ** 2
