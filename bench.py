@@ -51,6 +51,10 @@ def stage_bytes_flops(info: dict):
     # Z: the contraction's output after (part of) the first output level: P/4
     # values per (n, t) on F(2x2,3x3), 3P/5 on F(3x3,3x3) (the plan's yhat_bytes)
     U, V, Yh = info["u_bytes"], info["v_bytes"], info["yhat_bytes"]
+    if info.get("live_np"):
+        # the mixed nest moves only its live groups' U, V and Z (16 points each)
+        G, live = P // 16, info["live_groups"]
+        U, V, Yh = U // G * live, V // G * live, Yh // G * live
     if info.get("fused_output"):
         # input transform, then the output transform that forms the contraction
         return {"kernel_transform": (w + U, 0.0), "input_transform": (x + V, 0.0),

@@ -168,9 +168,12 @@ typedef struct nwg_plan_info {
   long long T;                  /* B * th * tw */
   long long P;                  /* Winograd points per tile, l^(2n) */
   size_t u_bytes, v_bytes, yhat_bytes, workspace_bytes;   /* yhat_bytes: Z */
-  long long ewmm_mults;         /* general multiplications per call: P*T*M*N */
+  long long ewmm_mults;         /* general multiplications per call: P*T*M*N (every
+                                   point, dead groups included) */
   double direct_flop;           /* 2*B*N*M*Ho*Wo*r*r */
-  double contract_flop;         /* 2*P*M*N*T (n = 0: 2*B*N*M*Ho*Wo) */
+  double contract_flop;         /* FLOPs the contraction computes: 2*P*M*N*T, or
+                                   2*16*live_groups*M*N*T when live_np > 0
+                                   (n = 0: 2*B*N*M*Ho*Wo) */
   int fused_input;              /* 1: nwg_conv2d fuses the input transform into the
                                    contraction (F(2x2,3x3): nwg_input_contract, depth 3-4,
                                    N <= 2, or depthwise; F(3x3,3x3): depth 2, N = 1) and
@@ -191,7 +194,8 @@ typedef struct nwg_plan_info {
   int outer33;                  /* NWG_TILE_MIX_F23_F33: F(3,3) levels above the two
                                    F(2,3) levels (1 or 2); else 0 */
   /* Groups that need no work.  A group is the 16 points (4 x 4) sharing their
-   * digits above level 1; its place in Z is g = P/16 ordering of those digits.
+   * digits above level 1; it is Z's group index g, those digits read as one
+   * number (q_n^r, q_n^c, ..., q_2^r, q_2^c, most significant first).
    * On the mixed nest the kernel taps split greedily over the levels leave
    * some digit combinations with no tap (and the padded taps r..Kn-1 are
    * zero), so the transformed kernel of a point is zero for every w when no

@@ -208,7 +208,7 @@ struct FusedTile {
 template <int BM, int BN, int WM, int WN, bool FULL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void contract_fused(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
-    int N, int T, int ntb, int nnb) {
+    int N, int T, int ntb, int nnb, GroupMap gm) {
   using Tile = FusedTile<BM, BN, WM, WN, FULL>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4, "four waves");
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   const int tb = (int)(bid % ntb);
   bid /= ntb;
   const int nb = (int)(bid % nnb);
-  const long long g = bid / nnb;
+  const long long g = live_group(gm, bid / nnb);
   const int n0 = nb * BM, c0 = tb * BN;
   const size_t quadU = (size_t)M * N, quadV = (size_t)M * T;
   const float4* __restrict__ Ug = U + (size_t)(4 * g) * quadU;
@@ -461,7 +461,7 @@ struct DeepTile {
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((BM / WM) * (BN / WN) > 1024 ? 1 : 2))) void contract_deep(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
-    int N, int T, int ntb, int nnb, int ks) {
+    int N, int T, int ntb, int nnb, int ks, GroupMap gm) {
   using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
@@ -479,7 +479,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
   // K slices (ks > 1): slice sk takes channels [sk M/ks, (sk+1) M/ks) and
   // writes its partial Z to part sk (parts of G N T quads, back to back)
   const int sk = (int)(bid % ks);
-  const long long g = bid / ks;
+  const long long g = live_group(gm, bid / ks);   // ks > 1 only with every group live
   const long long G = (long long)gridDim.x / ((long long)ntb * nnb * ks);
   const int mk = M / ks;
   const int n0 = nb * BM, c0 = tb * BN;
@@ -563,7 +563,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((BM / WM) * (BN / WN) > 1024 ? 1 : 2))) void contract_deep_persist(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
-    int N, int T, int ntb, int nnb, int ks, long long G, int wpx) {
+    int N, int T, int ntb, int nnb, int ks, long long G, int wpx, GroupMap gm) {
   using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
@@ -615,7 +615,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
     const int nb = (int)(b % nnb);
     b /= nnb;
     const int sk = (int)(b % ks);
-    const long long g = b / ks;
+    const long long g = live_group(gm, b / ks);
     tile.Ug = U + (size_t)(4 * g) * tile.quadU + (size_t)sk * mk * N;
     tile.Vg = V + (size_t)(4 * g) * tile.quadV + (size_t)sk * mk * T;
     tile.da.init(N, nb * BM, N);
@@ -661,7 +661,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
     const int nb = (int)(b % nnb);
     b /= nnb;
     const int sk = (int)(b % ks);
-    const long long g = b / ks;
+    const long long g = live_group(gm, b / ks);
     const int n0 = nb * BM, c0 = tb * BN;
     float4* __restrict__ Zg = Z + (size_t)(sk * G + g) * N * T;
 #pragma unroll
@@ -709,7 +709,7 @@ int persist_occupancy(int dev, const void* kernel, int threads) {
 
 template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT = false>
 hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, int T,
-                       long long G, hipStream_t s, int ks = 1) {
+                       long long G, hipStream_t s, int ks, const GroupMap& gm) {
   // T need not be a multiple of BN: the last column tile is ragged
   const int ntb = (T + BN - 1) / BN, nnb = N / BM;
   const long long blocks = (long long)ntb * nnb * G * ks;
@@ -733,20 +733,20 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
       if (blocks >= 4LL * 8 * wpx) {
         hipLaunchKernelGGL((contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT>),
                            dim3((unsigned)(8 * wpx)), dim3(64 * WM * WN), 0, s, (const float4*)U,
-                           (const float4*)V, (float4*)Z, M, N, T, ntb, nnb, ks, G, wpx);
+                           (const float4*)V, (float4*)Z, M, N, T, ntb, nnb, ks, G, wpx, gm);
         return hipGetLastError();
       }
     }
   }
   hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES, SPLIT>), dim3((unsigned)blocks),
                      dim3(64 * WM * WN), 0, s, (const float4*)U, (const float4*)V, (float4*)Z,
-                     M, N, T, ntb, nnb, ks);
+                     M, N, T, ntb, nnb, ks, gm);
   return hipGetLastError();
 }
 
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                        long long G, hipStream_t s) {
+                        long long G, hipStream_t s, const GroupMap& gm) {
   const int ntb = (T + BN - 1) / BN;
   const int nnb = (N + BM - 1) / BM;
   const long long blocks = (long long)ntb * nnb * G;
@@ -756,10 +756,10 @@ hipError_t launch_fused(const float* U, const float* V, float* Z, int M, int N, 
   const bool full = N % BM == 0 && T % BN == 0 && M % kBK == 0;
   if (full)
     hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN, true>), dim3((unsigned)blocks), dim3(256),
-                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
+                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb, gm);
   else
     hipLaunchKernelGGL((contract_fused<BM, BN, WM, WN, false>), dim3((unsigned)blocks), dim3(256),
-                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb);
+                       0, s, (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, ntb, nnb, gm);
   return hipGetLastError();
 }
 
@@ -924,39 +924,42 @@ hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                                 long long G, hipStream_t s, bool split, int ks) {
+                                 long long G, hipStream_t s, bool split, int ks,
+                                 const GroupMap& gm) {
+  // a group list (live groups) needs whole groups per Z part
+  if (gm.np != 0 && (ks != 1 || G != (long long)gm.np * gm.np)) return hipErrorInvalidValue;
   // split precision and K slices: the deep pipeline only (full 64-row
   // tiles, whole sweeps)
   if (split || ks > 1) {
     if (M % (32 * ks) || N % 64 || T < 64) return hipErrorInvalidValue;
     if (split) {
-      if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4, true>(U, V, Z, M, N, T, G, s, ks);
-      return launch_deep<64, 64, 2, 2, 8, 4, true>(U, V, Z, M, N, T, G, s, ks);
+      if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4, true>(U, V, Z, M, N, T, G, s, ks, gm);
+      return launch_deep<64, 64, 2, 2, 8, 4, true>(U, V, Z, M, N, T, G, s, ks, gm);
     }
-    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s, ks);
-    return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s, ks);
+    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s, ks, gm);
+    return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s, ks, gm);
   }
   // full 64-row tiles and whole 4-stage K sweeps: the deep pipeline; a
   // ragged T takes 64-column tiles (the last one partly recomputed)
   if (M % 32 == 0 && N % 64 == 0) {
-    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s);
+    if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s, 1, gm);
     // T = 64 with N a multiple of 128 (e.g. the mixed nest's 31x31 layer):
     // 128 x 64 blocks, so that V is read once per group (3.52 -> 3.44 ms)
     if (T == 64 && N % 128 == 0)   // four wavefronts of 64 x 32 (one per SIMD): 3.43 -> 3.38 ms
-      return launch_deep<128, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
+      return launch_deep<128, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s, 1, gm);
     // a ragged T: 64-column tiles, the last one partly recomputed (on the
     // 13x13 layer, T = 392, this measured 163 us against 173 us for the whole
     // tiles plus a separate launch of 64 x 16 blocks for the last 8 columns,
     // which re-reads all of U)
-    if (T >= 64) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s);
+    if (T >= 64) return launch_deep<64, 64, 2, 2, 8, 4>(U, V, Z, M, N, T, G, s, 1, gm);
   }
   // small problems (fewer than 256 work-groups with the wide tiles, e.g.
   // 32 channels on 256 tiles at depth 2: 32 work-groups): 16 x 64 tiles
   const long long wide = (long long)((T + 127) / 128) * ((N + 31) / 32) * G;
-  if (N <= 32 && wide < 256) return launch_fused<16, 64, 1, 4>(U, V, Z, M, N, T, G, s);
-  if (N <= 16) return launch_fused<16, 128, 1, 4>(U, V, Z, M, N, T, G, s);
-  if (N <= 32) return launch_fused<32, 128, 1, 4>(U, V, Z, M, N, T, G, s);
-  return launch_fused<64, 64, 2, 2>(U, V, Z, M, N, T, G, s);
+  if (N <= 32 && wide < 256) return launch_fused<16, 64, 1, 4>(U, V, Z, M, N, T, G, s, gm);
+  if (N <= 16) return launch_fused<16, 128, 1, 4>(U, V, Z, M, N, T, G, s, gm);
+  if (N <= 32) return launch_fused<32, 128, 1, 4>(U, V, Z, M, N, T, G, s, gm);
+  return launch_fused<64, 64, 2, 2>(U, V, Z, M, N, T, G, s, gm);
 }
 
 }  // namespace nwg

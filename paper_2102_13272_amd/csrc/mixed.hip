@@ -37,6 +37,44 @@ namespace {
 
 constexpr int kStride3 = 4, kStride4 = 12;
 
+// The live groups (q2r, q2c) of outer branch (q4r, q4c, q3r, q3c) as a
+// 16-bit mask, bit 4 q2r + q2c (NO = 1: no level-4 digits).  A group is live
+// when its row prefix (q4r, q3r, q2r) and its column prefix (q4c, q3c, q2c)
+// are (masks m0, m1 of nwg_plan_info::live_prefix; all live when both are 0).
+template <int NO>
+__device__ __forceinline__ unsigned branch_live(unsigned long long m0, unsigned long long m1,
+                                                int q4r, int q4c, int q3r, int q3c) {
+  if ((m0 | m1) == 0) return 0xffffu;
+  const int br = (NO == 2 ? q4r * 5 + q3r : q3r) * 4, bc = (NO == 2 ? q4c * 5 + q3c : q3c) * 4;
+  unsigned lr = 0, lc = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    lr |= (prefix_live(m0, m1, br + q) ? 1u : 0u) << q;
+    lc |= (prefix_live(m0, m1, bc + q) ? 1u : 0u) << q;
+  }
+  unsigned live = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if ((lr >> q) & 1u) live |= lc << (4 * q);
+  return live;
+}
+
+// Stores of the live groups only, without a branch per group (branches
+// around the 64 stores of an unrolled branch transform make the compiler
+// spill): every quad goes through a raw buffer resource that spans the
+// wave's branches, and a dead group's lanes pass an offset past its range,
+// which the hardware drops with no memory traffic.
+constexpr unsigned kDrop = 0x80000000u;     // above every span (host checks)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t span_rsrc(float4* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ void drop_store(__amdgpu_buffer_rsrc_t r, unsigned off, float4 v) {
+  typedef unsigned u4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, (int)off, 0, 0);
+}
+
 // Tap of the axis multi-index (k4, k3, k2, k1) (digits < 3, strides 12, 4, 2,
 // 1), or -1 when the multi-index is not the greedy split of its tap
 // (outermost digit first, each as large as allowed).
@@ -76,10 +114,11 @@ __device__ __forceinline__ void bt5_row(int q, float (&c)[5]) {
 }
 
 // ---- kernel transform -------------------------------------------------------
-template <int NO>
+template <int NO, bool MASK>
 __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict__ w,
                                                         float* __restrict__ U, int M, int N,
-                                                        int r) {
+                                                        int r, unsigned long long m0,
+                                                        unsigned long long m1) {
   constexpr int K = NO == 2 ? 39 : 15;      // padded taps per axis (odd)
   constexpr int KS = K * K;
   constexpr int NA = NO == 2 ? 3 : 1;       // level-4 digits per axis
@@ -102,6 +141,9 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
   for (int b = slot; b < NB; b += 32) {
     const int q3c = b % 5, q3r = (b / 5) % 5;
     const int q4c = NO == 2 ? (b / 25) % 5 : 0, q4r = NO == 2 ? b / 125 : 0;
+    // the groups no real tap reaches are neither computed nor stored
+    const unsigned live = branch_live<NO>(m0, m1, q4r, q4c, q3r, q3c);
+    if (live == 0) continue;
     float c3r[3], c3c[3], c4r[3], c4c[3];
     g5_row(q3r, c3r);
     g5_row(q3c, c3c);
@@ -148,6 +190,12 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
         }
     // the two F(2,3) levels: 64 quads of this outer branch
     float4* ub = reinterpret_cast<float4*>(U) + (size_t)b * 64 * MN + (size_t)m * N + nn;
+    // MASK: the wave's four branches b0 .. b0 + 3 share a resource
+    const int b0 = __builtin_amdgcn_readfirstlane(b & ~3);
+    const auto rs = span_rsrc(reinterpret_cast<float4*>(U) + (size_t)b0 * 64 * MN +
+                                  (size_t)m * N + n0,
+                              (unsigned)(4 * 64 * MN * 16));
+    const unsigned lane0 = (unsigned)(((size_t)(b - b0) * 64 * MN + cl) * 16);
 #pragma unroll
     for (int rho = 0; rho < 16; ++rho) {
       const int q2r = rho >> 2, q1r = rho & 3;
@@ -167,8 +215,11 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
 #pragma unroll
       for (int q2c = 0; q2c < 4; ++q2c) {
         const int quad = q2r * 16 + q2c * 4 + q1r;
-        ub[(size_t)quad * MN] =
-            make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+        const float4 v = make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
+        if constexpr (MASK)
+          drop_store(rs, (live >> (quad >> 2)) & 1u ? lane0 + (unsigned)(quad * MN * 16) : kDrop, v);
+        else
+          ub[(size_t)quad * MN] = v;
       }
     }
   }
@@ -267,10 +318,11 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
 // threads, one work-group per CU) write each point's V row in 512-byte runs:
 // 1.394 -> 1.372 ms on the 31 x 31 layer against 16 tiles.  Work-group ->
 // (level-4 branch q4 (NO = 2), TPW-tile chunk, channel m).
-template <int NO>
+template <int NO, bool MASK>
 __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix(
     const float* __restrict__ x, const float* __restrict__ X4, float4* __restrict__ V, int M,
-    int H, int W, int pad, int th, int tw, int T, long long qstride) {
+    int H, int W, int pad, int th, int tw, int T, long long qstride, unsigned long long m0,
+    unsigned long long m1) {
   constexpr int Mn = NO == 2 ? 36 : 12;
   constexpr int KK = kL3 * kL3;
   constexpr int TPW = NO == 2 ? 32 : 16, NT = 16 * TPW;   // tiles, threads per work-group
@@ -348,6 +400,9 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
   // a row of B^T of F(3,3) has its nonzero taps among 4 consecutive ones,
   // from tap 0 for row 0 and from tap 1 otherwise
   const int q3r = slot / 5, q3c = slot - 5 * q3r;
+  // V of the groups no real tap reaches is neither computed nor stored
+  const unsigned live = branch_live<NO>(m0, m1, q4 / 5, q4 % 5, q3r, q3c);
+  if (live == 0) continue;
   const int lr = q3r == 0 ? 0 : 1, lc = q3c == 0 ? 0 : 1;
   float ca5[5], cb5[5], ca[4], cb[4];
   bt5_row(q3r, ca5);
@@ -389,7 +444,20 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
     __builtin_amdgcn_sched_barrier(0);
   }
   const int ob = q4 * 25 + slot;
-  inner2_store<false>(S, V + (size_t)ob * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+  if constexpr (MASK) {
+    // the wave's 64 / TPW consecutive slots share a resource
+    constexpr int SPW = 64 / TPW;
+    const int slot0 = __builtin_amdgcn_readfirstlane(slot & ~(SPW - 1));
+    const auto rs = span_rsrc(V + (size_t)(q4 * 25 + slot0) * 64 * qstride + (size_t)m * T + t0,
+                              (unsigned)(SPW * 64 * qstride * 16));
+    const unsigned lane0 = (unsigned)(((size_t)(slot - slot0) * 64 * qstride + tl) * 16);
+    inner2_xform<false>(S, [&](int quad, float4 v) {
+      drop_store(rs, (live >> (quad >> 2)) & 1u ? lane0 + (unsigned)(quad * qstride * 16) : kDrop,
+                 v);
+    });
+  } else {
+    inner2_store<false>(S, V + (size_t)ob * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+  }
   }
 }
 
@@ -401,7 +469,8 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
 // Z3[q4][n][t][e], e = 12 row + column (depth 4).
 __global__ __launch_bounds__(64) void output_xform_mix23(const float4* __restrict__ Z,
                                                          float* __restrict__ out, int N, int T,
-                                                         long long gstride) {
+                                                         long long gstride, unsigned long long m0,
+                                                         unsigned long long m1) {
   // grid (tile block, n, q4): consecutive work-groups read adjacent channels
   // of the same Z rows (0.317 -> 0.305 ms per step for the pair on the
   // 31 x 31 layer against q4 before n)
@@ -423,8 +492,11 @@ __global__ __launch_bounds__(64) void output_xform_mix23(const float4* __restric
   for (int q3 = 0; q3 < 25; ++q3) {
     const int q3r = q3 / 5, q3c = q3 - 5 * q3r;
     const int ob = q4 * 25 + q3;
+    // the dead groups' Z is zero and is not read (uniform over the work-group)
+    const unsigned live = branch_live<2>(m0, m1, q4 / 5, q4 % 5, q3r, q3c);
+    if (live == 0) continue;
     float po[4][4];
-    level2_reduce(zt + (size_t)ob * 16 * gstride, (size_t)gstride, po);
+    level2_reduce(zt + (size_t)ob * 16 * gstride, (size_t)gstride, po, live);
     float cr[3], cc[3];
 #pragma unroll
     for (int i = 0; i < 3; ++i) {
@@ -464,7 +536,8 @@ __global__ __launch_bounds__(64) void output_xform_mix23(const float4* __restric
 __global__ __launch_bounds__(64) void output_xform_mix3(const float4* __restrict__ Z,
                                                         float* __restrict__ y, int N, int Ho,
                                                         int Wo, int th, int tw, int T,
-                                                        long long gstride) {
+                                                        long long gstride, unsigned long long m0,
+                                                        unsigned long long m1) {
   const int t = blockIdx.x * 64 + threadIdx.x;
   const int blk = blockIdx.y;               // 3 i3r + i3c
   const int n = blockIdx.z;
@@ -479,8 +552,10 @@ __global__ __launch_bounds__(64) void output_xform_mix3(const float4* __restrict
     const int q3r = q3 / 5, q3c = q3 - 5 * q3r;
     const float c = at5(i3r, q3r) * at5(i3c, q3c);
     if (c == 0.0f) continue;                // uniform over the work-group
+    const unsigned live = branch_live<1>(m0, m1, 0, 0, q3r, q3c);
+    if (live == 0) continue;
     float po[4][4];
-    level2_reduce(zt + (size_t)q3 * 16 * gstride, (size_t)gstride, po);
+    level2_reduce(zt + (size_t)q3 * 16 * gstride, (size_t)gstride, po, live);
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[e] = fmaf(c, po[e >> 2][e & 3], acc[e]);
   }
@@ -563,14 +638,17 @@ hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float
   const int K = no == 2 ? 39 : 15;
   const size_t lds = (size_t)16 * K * K * sizeof(float);
   dim3 grid((unsigned)((g.N + 15) / 16), (unsigned)g.M);
-  const void* fn = no == 2 ? reinterpret_cast<const void*>(&kernel_xform_mix<2>)
-                           : reinterpret_cast<const void*>(&kernel_xform_mix<1>);
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  // the dead groups' stores are dropped when a wave's four branches fit one
+  // buffer resource; otherwise every group of a live branch is stored
+  const bool mask = (g.live_prefix[0] | g.live_prefix[1]) != 0 &&
+                    4LL * 64 * g.M * g.N * 16 < (long long)kDrop;
+  const auto fn = no == 2 ? (mask ? &kernel_xform_mix<2, true> : &kernel_xform_mix<2, false>)
+                          : (mask ? &kernel_xform_mix<1, true> : &kernel_xform_mix<1, false>);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  if (no == 2)
-    hipLaunchKernelGGL(kernel_xform_mix<2>, grid, dim3(512), lds, s, w, U, g.M, g.N, g.r);
-  else
-    hipLaunchKernelGGL(kernel_xform_mix<1>, grid, dim3(512), lds, s, w, U, g.M, g.N, g.r);
+  hipLaunchKernelGGL(fn, grid, dim3(512), lds, s, w, U, g.M, g.N, g.r, g.live_prefix[0],
+                     g.live_prefix[1]);
   return hipGetLastError();
 }
 
@@ -585,21 +663,25 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
   const long long nwg = (g.T + tpw - 1) / tpw * g.M * (no == 2 ? 25 : 1);
   if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
   const size_t lds = (size_t)tpw * kWS * sizeof(float);
+  // dead groups' stores dropped when a wave's 64 / TPW branches fit one
+  // buffer resource
+  const bool mask = (g.live_prefix[0] | g.live_prefix[1]) != 0 &&
+                    (64LL / tpw) * 64 * qstride * 16 < (long long)kDrop;
+  const auto fn = no == 2 ? (mask ? &input_xform_mix<2, true> : &input_xform_mix<2, false>)
+                          : (mask ? &input_xform_mix<1, true> : &input_xform_mix<1, false>);
   if (no == 2) {
     if (g.M > 65535) return hipErrorInvalidValue;
     hipLaunchKernelGGL(input_mix_l4, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x, X4,
                        g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_mix<2>),
+    const hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (ea != hipSuccess) return ea;
-    hipLaunchKernelGGL(input_xform_mix<2>, dim3((unsigned)nwg), dim3(512), lds, s, x, X4, V, g.M,
-                       g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride);
-  } else {
-    hipLaunchKernelGGL(input_xform_mix<1>, dim3((unsigned)nwg), dim3(256), lds, s, x, X4, V, g.M,
-                       g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride);
   }
+  hipLaunchKernelGGL(fn, dim3((unsigned)nwg), dim3(no == 2 ? 512 : 256), lds, s, x, X4, V, g.M,
+                     g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride, g.live_prefix[0],
+                     g.live_prefix[1]);
   return hipGetLastError();
 }
 
@@ -612,12 +694,13 @@ hipError_t launch_output_xform_mix(const nwg_plan_info& g, const float* Zf, floa
   const unsigned tb = (unsigned)((g.T + 63) / 64);
   if (no == 1) {
     hipLaunchKernelGGL(output_xform_mix3, dim3(tb, 9, (unsigned)g.N), dim3(64), 0, s, Z, y, g.N,
-                       g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride);
+                       g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride, g.live_prefix[0],
+                       g.live_prefix[1]);
     return hipGetLastError();
   }
   if (!Z3) return hipErrorInvalidValue;
   hipLaunchKernelGGL(output_xform_mix23, dim3(tb, (unsigned)g.N, 25), dim3(64), 0, s, Z, Z3, g.N,
-                     (int)g.T, gstride);
+                     (int)g.T, gstride, g.live_prefix[0], g.live_prefix[1]);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const long long total = 144LL * g.N * g.T;

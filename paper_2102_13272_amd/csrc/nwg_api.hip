@@ -165,8 +165,11 @@ hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* 
   if (g.tile == NWG_TILE_F3X3_3X3) return nwg::launch_contract5(g, U, V, Z, s);
   // linear decomposition: the contraction runs over M c^2 channels
   const int mk = g.ld_c > 0 ? g.M * g.ld_c * g.ld_c : g.M;
-  const hipError_t e = nwg::launch_contract_fused(U, V, Z, mk, g.N, (int)g.T, g.P / 16, s,
-                                                  g.precision == NWG_PRECISION_BF16_SPLIT, ks);
+  // the mixed nest contracts its live groups only (the others' Z is zero)
+  const nwg::GroupMap gm = nwg::group_map(g);
+  const long long G = gm.np > 0 ? g.live_groups : g.P / 16;
+  const hipError_t e = nwg::launch_contract_fused(U, V, Z, mk, g.N, (int)g.T, G, s,
+                                                  g.precision == NWG_PRECISION_BF16_SPLIT, ks, gm);
   if (e != hipSuccess || ks == 1) return e;
   return nwg::launch_sum_parts(Z, (size_t)(g.P / 4) * g.N * g.T, ks, s);
 }

@@ -29,6 +29,51 @@ __device__ __forceinline__ long long xcd_remap(long long i, long long G) {
   return xcd < rem ? xcd * (q + 1) + slot : rem * (q + 1) + (xcd - rem) * q + slot;
 }
 
+// Position of the k-th set bit (k from 0) of the 128-bit mask (w1:w0).
+__device__ __forceinline__ int select_bit(unsigned long long w0, unsigned long long w1, int k) {
+  const int c0 = __popcll(w0);
+  unsigned long long w = k < c0 ? w0 : w1;
+  int pos = k < c0 ? 0 : 64;
+  k = k < c0 ? k : k - c0;
+#pragma unroll
+  for (int sh = 32; sh >= 1; sh >>= 1) {
+    const unsigned long long low = w & ((1ULL << sh) - 1);
+    const int c = __popcll(low);
+    if (k >= c) {
+      k -= c;
+      w >>= sh;
+      pos += sh;
+    } else {
+      w = low;
+    }
+  }
+  return pos;
+}
+
+// Entry i of a plan's group list (GroupMap): the group the contraction
+// computes as its i-th.
+__device__ __forceinline__ long long live_group(const GroupMap& m, long long i) {
+  if (m.np == 0) return i;
+  const int ir = (int)(i / m.np), ic = (int)(i - (long long)ir * m.np);
+  int pr = select_bit(m.mask0, m.mask1, ir), pc = select_bit(m.mask0, m.mask1, ic);
+  long long g = 0;
+#pragma unroll
+  for (int d = 0; d < 3; ++d) {
+    if (d < m.nd) {
+      g += (long long)(pr % m.rad[d]) * m.wr[d] + (long long)(pc % m.rad[d]) * m.wc[d];
+      pr /= m.rad[d];
+      pc /= m.rad[d];
+    }
+  }
+  return g;
+}
+
+// Whether prefix i of an axis is live (every prefix when the masks are 0).
+__device__ __forceinline__ bool prefix_live(unsigned long long m0, unsigned long long m1, int i) {
+  if ((m0 | m1) == 0) return true;
+  return ((i < 64 ? m0 >> i : m1 >> (i - 64)) & 1ULL) != 0;
+}
+
 // Wait until at most N vector-memory loads of this wavefront are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -151,13 +196,17 @@ __device__ __forceinline__ void g_inner2(const float (&v)[9], float (&out)[16]) 
 // Level 2 for one branch: 16 quads (q2r, q2c) -> 4x4 partial tile
 // po[rr][cc], rr = i1r + 2*i2r, cc = i1c + 2*i2c.  zb points at the branch's
 // first quad for this (n, t); gstride is the distance between groups.
+// live: bit q2r * 4 + q2c set for the groups whose Z is read (the others
+// are zero and not read).
 __device__ __forceinline__ void level2_reduce(const float4* __restrict__ zb, size_t gstride,
-                                              float (&po)[4][4]) {
+                                              float (&po)[4][4], unsigned live = 0xffffu) {
   float4 v[4][4];
 #pragma unroll
   for (int q2r = 0; q2r < 4; ++q2r)
 #pragma unroll
-    for (int q2c = 0; q2c < 4; ++q2c) v[q2r][q2c] = zb[(size_t)(q2r * 4 + q2c) * gstride];
+    for (int q2c = 0; q2c < 4; ++q2c)
+      v[q2r][q2c] = (live >> (q2r * 4 + q2c)) & 1u ? zb[(size_t)(q2r * 4 + q2c) * gstride]
+                                                    : make_float4(0.f, 0.f, 0.f, 0.f);
   // along columns: h[q2r][i2c] (float4 over (i1r, i1c))
   float4 h[4][2];
 #pragma unroll
@@ -176,13 +225,12 @@ __device__ __forceinline__ void level2_reduce(const float4* __restrict__ zb, siz
   }
 }
 
-// 2D inner transform (two levels per axis) of a 10 x 10 sub-window S and
-// store of its 256 points as 64 quads.  Point digits (q2r, q2c, q1r, q1c),
-// most significant first; vb points at the branch's first quad for this
-// (m, t), qstride is the distance between quads (M*T float4).
-template <bool SPLIT>
-__device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* __restrict__ vb,
-                                             size_t qstride) {
+// 2D inner transform (two levels per axis) of a 10 x 10 sub-window S into
+// its 256 points as 64 quads.  Point digits (q2r, q2c, q1r, q1c), most
+// significant first; put(quad, value) stores quad q2r * 16 + q2c * 4 + q1r
+// (q1c over the four lanes of the value).
+template <bool SPLIT, class Put>
+__device__ __forceinline__ void inner2_xform(const float (&S)[10][10], Put&& put) {
 #pragma unroll
   for (int q2r = 0; q2r < 4; ++q2r) {
     // level 2 along rows (stride 2): Z[u][j], u = 0..3
@@ -204,13 +252,19 @@ __device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* _
       float o[16];
       bt_inner2(R, o);  // columns: index q2c*4 + q1c
 #pragma unroll
-      for (int q2c = 0; q2c < 4; ++q2c) {
-        const int quad = q2r * 16 + q2c * 4 + q1r;
-        vb[(size_t)quad * qstride] =
-            store_quad<SPLIT>(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
-      }
+      for (int q2c = 0; q2c < 4; ++q2c)
+        put(q2r * 16 + q2c * 4 + q1r,
+            store_quad<SPLIT>(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]));
     }
   }
+}
+
+// inner2_xform stored to vb, the branch's first quad for this (m, t);
+// qstride is the distance between quads (M*T float4).
+template <bool SPLIT>
+__device__ __forceinline__ void inner2_store(const float (&S)[10][10], float4* __restrict__ vb,
+                                             size_t qstride) {
+  inner2_xform<SPLIT>(S, [&](int quad, float4 v) { vb[(size_t)quad * qstride] = v; });
 }
 
 // ---- F(3,3): B^T, G, A^T (Toom-Cook points 0, 1, -1, 2, infinity) ----------
@@ -281,8 +335,10 @@ hipError_t launch_kernel_xform_ld(const nwg_plan_info& g, const float* w, float*
 // split = true: U, V hold bf16 (hi, lo) pairs (precision NWG_PRECISION_BF16_SPLIT).
 // ks > 1: K slices of M / ks channels (deep path: M % (32 ks) == 0, N % 64 == 0,
 // T >= 64), slice k writing its partial Z to Z + k G N T 4 floats.
+// gm: the plan's group list (G = gm.np^2 entries when gm.np > 0, then ks = 1).
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
-                                 long long G, hipStream_t s, bool split = false, int ks = 1);
+                                 long long G, hipStream_t s, bool split = false, int ks = 1,
+                                 const GroupMap& gm = GroupMap{});
 // in place: every fp32 value of buf (n values) -> its packed bf16 (hi, lo) pair
 hipError_t launch_split_pairs(float* buf, size_t n, hipStream_t s);
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* U, float* Z,

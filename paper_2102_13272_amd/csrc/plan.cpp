@@ -151,6 +151,24 @@ bool split_allowed(const nwg_plan_info& g) {
          !g.fused_conv && g.pipeline_parts <= 1 && g.M % 32 == 0 && g.N % 64 == 0 && g.T >= 64;
 }
 
+GroupMap group_map(const nwg_plan_info& g) {
+  GroupMap m{};
+  if (g.live_np <= 0 || g.tile != NWG_TILE_MIX_F23_F33 || g.n < 3 || g.n - 1 > 3) return m;
+  m.np = g.live_np;
+  m.nd = g.n - 1;
+  m.mask0 = g.live_prefix[0];
+  m.mask1 = g.live_prefix[1];
+  // groups are ordered by (q_n^r, q_n^c, ..., q_2^r, q_2^c), each radix l_j
+  int wc = 1;
+  for (int d = 0; d < m.nd; ++d) {
+    m.rad[d] = d == 0 ? 4 : 5;                       // q_2: F(2,3); above: F(3,3)
+    m.wc[d] = wc;
+    m.wr[d] = wc * m.rad[d];
+    wc = m.wr[d] * m.rad[d];
+  }
+  return m;
+}
+
 namespace {
 
 // Output size and the limits every tile shares: each map (input and output)
@@ -267,6 +285,7 @@ void mix_liveness(nwg_plan_info* g) {
   g->live_prefix[0] = mask[0];
   g->live_prefix[1] = mask[1];
   g->live_groups = (long long)live * live;
+  g->contract_flop = 2.0 * 16 * g->live_groups * g->M * g->N * g->T;
 }
 
 // Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,

@@ -63,4 +63,17 @@ bool pipeline_allowed(const nwg_plan_info& g);
 // Plans that can take NWG_PRECISION_BF16_SPLIT.
 bool split_allowed(const nwg_plan_info& g);
 
+// The contraction's list of groups (nwg_plan_info::live_np): entry i is the
+// group with row prefix p_r = the (i / np)-th live prefix and column prefix
+// p_c = the (i % np)-th, at g = sum_d digit_d(p_r) wr[d] + digit_d(p_c) wc[d]
+// (digit d = q_{d+2}, the least significant first).  np = 0: entry i is
+// group i.
+struct GroupMap {
+  int np;                       // live prefixes per axis; 0: every group
+  int nd;                       // digits of a prefix (levels 2..n), at most 3
+  unsigned long long mask0, mask1;   // live prefixes (bit i: prefix i)
+  int rad[3], wr[3], wc[3];     // radix of digit d, its weight in g for rows and columns
+};
+GroupMap group_map(const nwg_plan_info& g);
+
 }  // namespace nwg

@@ -101,3 +101,27 @@ def mixed_to_lib_points(a, radices):
         rows = rows * radices[j] + idx[k]
         cols = cols * radices[j] + idx[k + 1]
     return a[..., rows, cols]
+
+
+def live_group_mask(info):
+    """Per group (P/16, the library's order) whether it is live for the plan
+    (nwg_plan_info live_np, live_prefix): its row prefix (q_n^r .. q_2^r) and
+    its column prefix are both live.  A prefix's bit index has q_2 least
+    significant (radix 4), then q_3, ... (radix 5).  Every group when live_np
+    is 0."""
+    G = info["P"] // 16
+    if info["live_np"] == 0:
+        return np.ones(G, dtype=bool)
+    mask = int(info["live_prefix"][0]) | (int(info["live_prefix"][1]) << 64)
+    radix = [4] + [5] * (info["n"] - 2)             # levels 2 .. n
+    out = np.empty(G, dtype=bool)
+    for g in range(G):
+        rest, pr, pc, mul = g, 0, 0, 1
+        for l in radix:                             # group digits (row, col) per level, q_2 last
+            pc += (rest % l) * mul
+            rest //= l
+            pr += (rest % l) * mul
+            rest //= l
+            mul *= l
+        out[g] = bool((mask >> pr) & 1) and bool((mask >> pc) & 1)
+    return out
