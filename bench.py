@@ -32,6 +32,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 PEAK_BF16_MFMA_TFLOPS = 2500.0  # MI355X dense bf16 matrix
 METRIC = "direct-conv-equiv TFLOP/s & fraction of fp32 MFMA/HBM roofline, 1 MI355X"
 STAGES = ["kernel_transform", "input_transform", "contraction", "output_transform"]
+NWG_TILE_MIX = 3               # the mixed F(2,3)/F(3,3) nest (include/nwg.h)
 CSRC = os.path.join(ROOT, "paper_2102_13272_amd", "csrc")
 
 
@@ -51,10 +52,13 @@ def stage_bytes_flops(info: dict):
     # Z: the contraction's output after (part of) the first output level: P/4
     # values per (n, t) on F(2x2,3x3), 3P/5 on F(3x3,3x3) (the plan's yhat_bytes)
     U, V, Yh = info["u_bytes"], info["v_bytes"], info["yhat_bytes"]
-    if info.get("live_np"):
-        # the mixed nest moves only its live groups' U, V and Z (16 points each)
+    if info.get("tile") == NWG_TILE_MIX and info["n"] >= 3:
+        # the mixed nest moves only its live groups' U, V and Z, and of U and
+        # V only the quads whose level-1 row digit is live (3 of 4 when digit
+        # 3 is dead; a quad's float4 still carries its dead fourth point)
         G, live = P // 16, info["live_groups"]
-        U, V, Yh = U // G * live, V // G * live, Yh // G * live
+        nq = 3 if info.get("level1_live") == 0x7 else 4
+        U, V, Yh = U // G * live * nq // 4, V // G * live * nq // 4, Yh // G * live
     if info.get("fused_output"):
         # input transform, then the output transform that forms the contraction
         return {"kernel_transform": (w + U, 0.0), "input_transform": (x + V, 0.0),

@@ -171,9 +171,10 @@ typedef struct nwg_plan_info {
   long long ewmm_mults;         /* general multiplications per call: P*T*M*N (every
                                    point, dead groups included) */
   double direct_flop;           /* 2*B*N*M*Ho*Wo*r*r */
-  double contract_flop;         /* FLOPs the contraction computes: 2*P*M*N*T, or
-                                   2*16*live_groups*M*N*T when live_np > 0
-                                   (n = 0: 2*B*N*M*Ho*Wo) */
+  double contract_flop;         /* FLOPs of the contraction's nonzero points: 2*P*M*N*T,
+                                   or on the mixed nest 2*L^2*live_groups*M*N*T with L
+                                   the live level-1 digits (3 or 4; n = 0:
+                                   2*B*N*M*Ho*Wo) */
   int fused_input;              /* 1: nwg_conv2d fuses the input transform into the
                                    contraction (F(2x2,3x3): nwg_input_contract, depth 3-4,
                                    N <= 2, or depthwise; F(3x3,3x3): depth 2, N = 1) and
@@ -207,6 +208,13 @@ typedef struct nwg_plan_info {
   unsigned long long live_prefix[2];   /* bit i: prefix i of an axis is live (digits
                                    q_n .. q_2, the outermost most significant) */
   long long live_groups;        /* groups the contraction computes: live_np^2, or P/16 */
+  int level1_live;              /* bit q: level-1 digit q is live along each axis (0xf,
+                                   or 0x7 on the mixed nest when no tap k < r splits to
+                                   level-1 digit 2, i.e. r below the nest's Kn: then the
+                                   points with q_1^r = 3 or q_1^c = 3 are zero, quads
+                                   q_1^r = 3 are neither written nor read, and the
+                                   contraction takes 3 x 3 points per group); 0 on
+                                   F(3x3,3x3) and at depth 0 */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only): the

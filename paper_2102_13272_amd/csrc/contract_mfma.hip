@@ -250,7 +250,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   }
 
   const int nk = (M + kBK - 1) / kBK;
-  const int total = 4 * nk;                 // (q1r, K chunk) pairs, one pipeline
+  // (q1r, K chunk) pairs, one pipeline; q1r = 3 is skipped where level-1
+  // digit 3 is dead (its U is zero and its V is not written)
+  const int total = (gm.q3 ? 3 : 4) * nk;
   tile.prefetch(Ug, Vg, N, T, 0, M, A0, B0);
   tile.commit(A0, B0);
   __syncthreads();
@@ -338,8 +340,11 @@ struct DeepLoader {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
+// Q3: level-1 digit 3 is dead (GroupMap::q3): quads q1r = 0..2 only, and
+// the fourth point of each quad (q1c = 3, its U zero) is not multiplied.
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT, bool Q3>
 struct DeepTile {
+  static constexpr int NQ = Q3 ? 3 : 4;     // quads (q1r) per group
   static constexpr int NT = 64 * WM * WN;
   static constexpr int WTM = BM / WM, WTN = BN / WN;
   static constexpr int FM = WTM / 16, FN = WTN / 16;
@@ -378,7 +383,8 @@ struct DeepTile {
           acc[0][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].x, bf[j].x, acc[0][i][j], 0, 0, 0);
           acc[1][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].y, bf[j].y, acc[1][i][j], 0, 0, 0);
           acc[2][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].z, bf[j].z, acc[2][i][j], 0, 0, 0);
-          acc[3][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].w, bf[j].w, acc[3][i][j], 0, 0, 0);
+          if constexpr (!Q3)
+            acc[3][i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i].w, bf[j].w, acc[3][i][j], 0, 0, 0);
         }
     }
   }
@@ -432,13 +438,14 @@ struct DeepTile {
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const floatx4 z0 = acc[0][i][j] + acc[1][i][j] + acc[2][i][j];
-        const floatx4 z1 = acc[1][i][j] - acc[2][i][j] - acc[3][i][j];
+        const floatx4 z1 = Q3 ? acc[1][i][j] - acc[2][i][j]
+                              : acc[1][i][j] - acc[2][i][j] - acc[3][i][j];
         out[0][i][j] += r0 * z0;
         out[1][i][j] += r0 * z1;
         out[2][i][j] += r1 * z0;
         out[3][i][j] += r1 * z1;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[c][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < NQ; ++c) acc[c][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
   }
 
@@ -458,11 +465,11 @@ struct DeepTile {
 
 // Two wavefronts per SIMD for 32 x 32 wavefront tiles; a 64 x 32 tile (eight
 // accumulator sets of 8 floatx4) needs the whole register file, one per SIMD.
-template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT, bool Q3>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((BM / WM) * (BN / WN) > 1024 ? 1 : 2))) void contract_deep(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
     int N, int T, int ntb, int nnb, int ks, GroupMap gm) {
-  using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
+  using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT, Q3>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
   static_assert(STAGES >= 2 && STAGES <= 4, "2 to 4 stages");
@@ -492,7 +499,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
   tile.N = N;
   tile.T = T;
   tile.nk = mk / BKD;
-  tile.total = 4 * tile.nk;
+  tile.total = Tile::NQ * tile.nk;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   tile.wm = wave / WN;
@@ -515,7 +522,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
   tile.request(0, A0, B0);
   if (STAGES > 2) tile.request(1, A1, B1);
   if (STAGES > 3) tile.request(2, A2, B2);
-  for (int q1r = 0; q1r < 4; ++q1r) {
+  for (int q1r = 0; q1r < Tile::NQ; ++q1r) {
     for (int kb = 0; kb < tile.nk; kb += STAGES) {
       const int c = q1r * tile.nk + kb;
       if (STAGES == 2) {
@@ -560,11 +567,11 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
 // in contract_deep; XCD x takes a contiguous range of them (the split of
 // xcd_remap) and its wpx work-groups stride through that range, so the
 // tiles that share a group's U and V run together on one L2.
-template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT>
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT, bool Q3>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((BM / WM) * (BN / WN) > 1024 ? 1 : 2))) void contract_deep_persist(
     const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
     int N, int T, int ntb, int nnb, int ks, long long G, int wpx, GroupMap gm) {
-  using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT>;
+  using Tile = DeepTile<BM, BN, WM, WN, BKD, STAGES, SPLIT, Q3>;
   constexpr int WTM = Tile::WTM, WTN = Tile::WTN, FM = Tile::FM, FN = Tile::FN;
   static_assert(WM * WN == 4 || WM * WN == 8, "four or eight waves");
   static_assert(STAGES == 4, "4 stages");
@@ -588,7 +595,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
   tile.N = N;
   tile.T = T;
   tile.nk = mk / BKD;
-  tile.total = 4 * tile.nk;
+  tile.total = Tile::NQ * tile.nk;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   tile.wm = wave / WN;
@@ -646,7 +653,7 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
   request_next(A1, B1);
   request_next(A2, B2);
   for (int it = 0; it < mine; ++it) {
-    for (int q1r = 0; q1r < 4; ++q1r) {
+    for (int q1r = 0; q1r < Tile::NQ; ++q1r) {
       for (int kb = 0; kb < tile.nk; kb += STAGES) {
         step(A0, B0, A3, B3);
         step(A1, B1, A0, B0);
@@ -707,7 +714,8 @@ int persist_occupancy(int dev, const void* kernel, int threads) {
   return b;
 }
 
-template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT = false>
+template <int BM, int BN, int WM, int WN, int BKD, int STAGES, bool SPLIT = false,
+          bool Q3 = false>
 hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, int T,
                        long long G, hipStream_t s, int ks, const GroupMap& gm) {
   // T need not be a multiple of BN: the last column tile is ragged
@@ -723,7 +731,7 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
     const int occ =
         hipGetDevice(&dev) == hipSuccess
             ? persist_occupancy(dev, reinterpret_cast<const void*>(
-                                         &contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT>),
+                                         &contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT, Q3>),
                                 64 * WM * WN)
             : 0;
     if (occ > 0 &&
@@ -731,14 +739,14 @@ hipError_t launch_deep(const float* U, const float* V, float* Z, int M, int N, i
         cus >= 8) {
       const int wpx = cus / 8 * occ;
       if (blocks >= 4LL * 8 * wpx) {
-        hipLaunchKernelGGL((contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT>),
+        hipLaunchKernelGGL((contract_deep_persist<BM, BN, WM, WN, BKD, 4, SPLIT, Q3>),
                            dim3((unsigned)(8 * wpx)), dim3(64 * WM * WN), 0, s, (const float4*)U,
                            (const float4*)V, (float4*)Z, M, N, T, ntb, nnb, ks, G, wpx, gm);
         return hipGetLastError();
       }
     }
   }
-  hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES, SPLIT>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((contract_deep<BM, BN, WM, WN, BKD, STAGES, SPLIT, Q3>), dim3((unsigned)blocks),
                      dim3(64 * WM * WN), 0, s, (const float4*)U, (const float4*)V, (float4*)Z,
                      M, N, T, ntb, nnb, ks, gm);
   return hipGetLastError();
@@ -928,6 +936,7 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
                                  const GroupMap& gm) {
   // a group list (live groups) needs whole groups per Z part
   if (gm.np != 0 && (ks != 1 || G != (long long)gm.np * gm.np)) return hipErrorInvalidValue;
+  if (gm.q3 && (split || ks != 1)) return hipErrorInvalidValue;
   // split precision and K slices: the deep pipeline only (full 64-row
   // tiles, whole sweeps)
   if (split || ks > 1) {
@@ -942,6 +951,14 @@ hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M
   // full 64-row tiles and whole 4-stage K sweeps: the deep pipeline; a
   // ragged T takes 64-column tiles (the last one partly recomputed)
   if (M % 32 == 0 && N % 64 == 0) {
+    if (gm.q3) {
+      if (T % 128 == 0)
+        return launch_deep<64, 128, 2, 4, 8, 4, false, true>(U, V, Z, M, N, T, G, s, 1, gm);
+      if (T == 64 && N % 128 == 0)
+        return launch_deep<128, 64, 2, 2, 8, 4, false, true>(U, V, Z, M, N, T, G, s, 1, gm);
+      if (T >= 64)
+        return launch_deep<64, 64, 2, 2, 8, 4, false, true>(U, V, Z, M, N, T, G, s, 1, gm);
+    }
     if (T % 128 == 0) return launch_deep<64, 128, 2, 4, 8, 4>(U, V, Z, M, N, T, G, s, 1, gm);
     // T = 64 with N a multiple of 128 (e.g. the mixed nest's 31x31 layer):
     // 128 x 64 blocks, so that V is read once per group (3.52 -> 3.44 ms)

@@ -59,10 +59,11 @@ __device__ __forceinline__ unsigned branch_live(unsigned long long m0, unsigned 
   return live;
 }
 
-// Stores of the live groups only, without a branch per group (branches
+// Stores of the live quads only, without a branch per quad (branches
 // around the 64 stores of an unrolled branch transform make the compiler
 // spill): every quad goes through a raw buffer resource that spans the
-// wave's branches, and a dead group's lanes pass an offset past its range,
+// wave's branches, and the lanes of a dead quad (its group dead, or its
+// level-1 row digit q1r = 3 when q3 is set) pass an offset past the range,
 // which the hardware drops with no memory traffic.
 constexpr unsigned kDrop = 0x80000000u;     // above every span (host checks)
 
@@ -73,6 +74,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t span_rsrc(float4* base, unsign
 __device__ __forceinline__ void drop_store(__amdgpu_buffer_rsrc_t r, unsigned off, float4 v) {
   typedef unsigned u4 __attribute__((ext_vector_type(4)));
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, (int)off, 0, 0);
+}
+
+// Whether quad q2r * 16 + q2c * 4 + q1r of a branch with live-group mask
+// live is stored.
+__device__ __forceinline__ bool quad_live(unsigned live, int q3, int quad) {
+  return ((live >> (quad >> 2)) & 1u) && !(q3 && (quad & 3) == 3);
 }
 
 // Tap of the axis multi-index (k4, k3, k2, k1) (digits < 3, strides 12, 4, 2,
@@ -118,7 +125,7 @@ template <int NO, bool MASK>
 __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict__ w,
                                                         float* __restrict__ U, int M, int N,
                                                         int r, unsigned long long m0,
-                                                        unsigned long long m1) {
+                                                        unsigned long long m1, int q3) {
   constexpr int K = NO == 2 ? 39 : 15;      // padded taps per axis (odd)
   constexpr int KS = K * K;
   constexpr int NA = NO == 2 ? 3 : 1;       // level-4 digits per axis
@@ -217,7 +224,7 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
         const int quad = q2r * 16 + q2c * 4 + q1r;
         const float4 v = make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
         if constexpr (MASK)
-          drop_store(rs, (live >> (quad >> 2)) & 1u ? lane0 + (unsigned)(quad * MN * 16) : kDrop, v);
+          drop_store(rs, quad_live(live, q3, quad) ? lane0 + (unsigned)(quad * MN * 16) : kDrop, v);
         else
           ub[(size_t)quad * MN] = v;
       }
@@ -322,7 +329,7 @@ template <int NO, bool MASK>
 __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix(
     const float* __restrict__ x, const float* __restrict__ X4, float4* __restrict__ V, int M,
     int H, int W, int pad, int th, int tw, int T, long long qstride, unsigned long long m0,
-    unsigned long long m1) {
+    unsigned long long m1, int q3) {
   constexpr int Mn = NO == 2 ? 36 : 12;
   constexpr int KK = kL3 * kL3;
   constexpr int TPW = NO == 2 ? 32 : 16, NT = 16 * TPW;   // tiles, threads per work-group
@@ -452,7 +459,7 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
                               (unsigned)(SPW * 64 * qstride * 16));
     const unsigned lane0 = (unsigned)(((size_t)(slot - slot0) * 64 * qstride + tl) * 16);
     inner2_xform<false>(S, [&](int quad, float4 v) {
-      drop_store(rs, (live >> (quad >> 2)) & 1u ? lane0 + (unsigned)(quad * qstride * 16) : kDrop,
+      drop_store(rs, quad_live(live, q3, quad) ? lane0 + (unsigned)(quad * qstride * 16) : kDrop,
                  v);
     });
   } else {
@@ -638,9 +645,10 @@ hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float
   const int K = no == 2 ? 39 : 15;
   const size_t lds = (size_t)16 * K * K * sizeof(float);
   dim3 grid((unsigned)((g.N + 15) / 16), (unsigned)g.M);
-  // the dead groups' stores are dropped when a wave's four branches fit one
-  // buffer resource; otherwise every group of a live branch is stored
-  const bool mask = (g.live_prefix[0] | g.live_prefix[1]) != 0 &&
+  // the dead quads' stores are dropped when a wave's four branches fit one
+  // buffer resource; otherwise every quad of a live branch is stored
+  const int q3 = g.level1_live == 0x7 ? 1 : 0;
+  const bool mask = ((g.live_prefix[0] | g.live_prefix[1]) != 0 || q3) &&
                     4LL * 64 * g.M * g.N * 16 < (long long)kDrop;
   const auto fn = no == 2 ? (mask ? &kernel_xform_mix<2, true> : &kernel_xform_mix<2, false>)
                           : (mask ? &kernel_xform_mix<1, true> : &kernel_xform_mix<1, false>);
@@ -648,7 +656,7 @@ hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(fn, grid, dim3(512), lds, s, w, U, g.M, g.N, g.r, g.live_prefix[0],
-                     g.live_prefix[1]);
+                     g.live_prefix[1], q3);
   return hipGetLastError();
 }
 
@@ -663,9 +671,10 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
   const long long nwg = (g.T + tpw - 1) / tpw * g.M * (no == 2 ? 25 : 1);
   if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
   const size_t lds = (size_t)tpw * kWS * sizeof(float);
-  // dead groups' stores dropped when a wave's 64 / TPW branches fit one
+  // dead quads' stores dropped when a wave's 64 / TPW branches fit one
   // buffer resource
-  const bool mask = (g.live_prefix[0] | g.live_prefix[1]) != 0 &&
+  const int q3 = g.level1_live == 0x7 ? 1 : 0;
+  const bool mask = ((g.live_prefix[0] | g.live_prefix[1]) != 0 || q3) &&
                     (64LL / tpw) * 64 * qstride * 16 < (long long)kDrop;
   const auto fn = no == 2 ? (mask ? &input_xform_mix<2, true> : &input_xform_mix<2, false>)
                           : (mask ? &input_xform_mix<1, true> : &input_xform_mix<1, false>);
@@ -681,7 +690,7 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
   }
   hipLaunchKernelGGL(fn, dim3((unsigned)nwg), dim3(no == 2 ? 512 : 256), lds, s, x, X4, V, g.M,
                      g.H, g.W, g.pad, g.th, g.tw, (int)g.T, qstride, g.live_prefix[0],
-                     g.live_prefix[1]);
+                     g.live_prefix[1], q3);
   return hipGetLastError();
 }
 

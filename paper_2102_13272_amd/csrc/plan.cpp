@@ -153,7 +153,9 @@ bool split_allowed(const nwg_plan_info& g) {
 
 GroupMap group_map(const nwg_plan_info& g) {
   GroupMap m{};
-  if (g.live_np <= 0 || g.tile != NWG_TILE_MIX_F23_F33 || g.n < 3 || g.n - 1 > 3) return m;
+  if (g.tile != NWG_TILE_MIX_F23_F33 || g.n < 3 || g.n - 1 > 3) return m;
+  m.q3 = g.level1_live == 0x7 ? 1 : 0;
+  if (g.live_np <= 0) return m;
   m.np = g.live_np;
   m.nd = g.n - 1;
   m.mask0 = g.live_prefix[0];
@@ -242,9 +244,10 @@ int ld_geometry(int B, int M, int N, int H, int W, int r, int pad, int depthwise
 unsigned g_row_digits(int l, int q) { return q == 0 ? 1u : q == l - 1 ? 4u : 7u; }
 
 // Mixed nest: which digit prefixes (q_n .. q_2) of an axis have a point whose
-// transformed kernel can be nonzero.  Tap k < r reaches point (q_n .. q_1)
-// when each digit of its greedy split (outermost first, each at most 2, as
-// the kernel transform splits it) is one that the point's G row reaches.
+// transformed kernel can be nonzero, and which level-1 digits q_1 any point
+// has that for.  Tap k < r reaches point (q_n .. q_1) when each digit of its
+// greedy split (outermost first, each at most 2, as the kernel transform
+// splits it) is one that the point's G row reaches.
 void mix_liveness(nwg_plan_info* g) {
   const int n = g->n;
   int l[NWG_MAX_DEPTH];
@@ -253,6 +256,7 @@ void mix_liveness(nwg_plan_info* g) {
   for (int j = 1; j < n; ++j) npref *= l[j];
   if (npref > 128) return;                            // beyond the masks: all groups live
   int live = 0;
+  unsigned q1mask = 0;
   unsigned long long mask[2] = {0, 0};
   for (int pf = 0; pf < npref; ++pf) {
     int q[NWG_MAX_DEPTH] = {0};
@@ -261,10 +265,10 @@ void mix_liveness(nwg_plan_info* g) {
       q[j] = rest % l[j];
       rest /= l[j];
     }
-    bool reached = false;
-    for (int q1 = 0; q1 < l[0] && !reached; ++q1) {
+    unsigned reached = 0;                             // bit q_1
+    for (int q1 = 0; q1 < l[0]; ++q1) {
       q[0] = q1;
-      for (int k = 0; k < g->r && !reached; ++k) {
+      for (int k = 0; k < g->r && !((reached >> q1) & 1u); ++k) {
         int rem = k;
         bool ok = true;
         for (int j = n - 1; j >= 1 && ok; --j) {
@@ -272,20 +276,26 @@ void mix_liveness(nwg_plan_info* g) {
           rem -= d * g->strides[j];
           ok = (g_row_digits(l[j], q[j]) >> d) & 1u;
         }
-        reached = ok && rem <= 2 && ((g_row_digits(l[0], q[0]) >> rem) & 1u);
+        if (ok && rem <= 2 && ((g_row_digits(l[0], q[0]) >> rem) & 1u)) reached |= 1u << q1;
       }
     }
     if (reached) {
       mask[pf >> 6] |= 1ULL << (pf & 63);
       ++live;
+      q1mask |= reached;
     }
   }
-  if (live == npref) return;                        // nothing to skip
-  g->live_np = live;
-  g->live_prefix[0] = mask[0];
-  g->live_prefix[1] = mask[1];
-  g->live_groups = (long long)live * live;
-  g->contract_flop = 2.0 * 16 * g->live_groups * g->M * g->N * g->T;
+  // the kernels skip level-1 digit 3 only (the F(2,3) row that reaches tap
+  // digit 2 alone: no tap k < r has it when r is below the nest's taps)
+  g->level1_live = q1mask == 0x7u ? 0x7 : 0xf;
+  const int lq = g->level1_live == 0x7 ? 3 : 4;
+  if (live < npref) {
+    g->live_np = live;
+    g->live_prefix[0] = mask[0];
+    g->live_prefix[1] = mask[1];
+    g->live_groups = (long long)live * live;
+  }
+  g->contract_flop = 2.0 * lq * lq * g->live_groups * g->M * g->N * g->T;
 }
 
 // Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,
@@ -404,6 +414,7 @@ int geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile, i
   g->workspace_bytes = g->u_bytes + (plan_holds_v(*g) ? g->v_bytes : 0) +
                        (plan_holds_z(*g) ? zalloc_bytes(*g) : 0);
   g->live_groups = f33 || n == 0 ? 0 : g->P / 16;
+  g->level1_live = f33 || n == 0 ? 0 : 0xf;
   if (mix && n >= 3) mix_liveness(g);
   return NWG_OK;
 }

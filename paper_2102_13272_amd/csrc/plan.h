@@ -73,6 +73,8 @@ struct GroupMap {
   int nd;                       // digits of a prefix (levels 2..n), at most 3
   unsigned long long mask0, mask1;   // live prefixes (bit i: prefix i)
   int rad[3], wr[3], wc[3];     // radix of digit d, its weight in g for rows and columns
+  int q3;                       // 1: level-1 digit 3 is dead (nwg_plan_info::level1_live
+                                // = 0x7): quads q1r = 0..2 of a group only
 };
 GroupMap group_map(const nwg_plan_info& g);
 

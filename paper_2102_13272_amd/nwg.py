@@ -44,7 +44,7 @@ class nwg_plan_info(ctypes.Structure):
         ("pipeline_parts", ctypes.c_int), ("precision", ctypes.c_int), ("ld_c", ctypes.c_int),
         ("fused_output", ctypes.c_int), ("outer33", ctypes.c_int),
         ("live_np", ctypes.c_int), ("live_prefix", ctypes.c_ulonglong * 2),
-        ("live_groups", ctypes.c_longlong),
+        ("live_groups", ctypes.c_longlong), ("level1_live", ctypes.c_int),
     ]
 
     def as_dict(self):

@@ -381,7 +381,7 @@ def _oracle_live_prefixes(r):
     lv = mixed_levels([f23, f23] + [f33] * (n - 2), r)
     KG = kernel_matrix(lv)
     rad = [b.l for b in lv.bases]                 # level 1 .. n
-    live = set()
+    live, q1 = set(), set()
     for p in range(lv.P1):
         d = _digits(p, rad)                       # (q_1, ..., q_n), q_1 most significant
         if any(KG[p, k] != 0 for k in range(r)):
@@ -389,10 +389,11 @@ def _oracle_live_prefixes(r):
             for j in range(n - 1, 0, -1):         # q_n first
                 idx = idx * rad[j] + d[j]
             live.add(idx)
+            q1.add(d[0])
     npref = 1
     for j in range(1, n):
         npref *= rad[j]
-    return live, npref
+    return live, npref, q1
 
 
 @pytest.mark.parametrize("r", [8, 9, 12, 13, 15, 16, 17, 24, 27, 31, 33, 35, 38, 39])
@@ -402,7 +403,11 @@ def test_mixed_live_groups_are_the_oracle_kernel_rows_that_reach_a_real_tap(r):
     nonzero row in the oracle's kernel-transform matrix (Sec. III.B's
     reordering and G^(x)n, written independently)."""
     g = nwg.plan_geometry(2, 8, 8, 64, 64, r, r // 2, nwg.NWG_TILE_MIX_F23_F33)
-    live, npref = _oracle_live_prefixes(r)
+    live, npref, q1 = _oracle_live_prefixes(r)
+    # level-1 digits: the library skips digit 3 exactly when no point with it
+    # has a nonzero kernel row (r below the nest's 39 or 15 taps)
+    assert g["level1_live"] == sum(1 << q for q in q1)
+    assert (g["level1_live"] == 0x7) == (r < g["Kn"])
     if g["live_np"] == 0:
         assert len(live) == npref and g["live_groups"] == g["P"] // 16
         return

@@ -34,17 +34,21 @@ def test_stage_bytes_are_the_plan_buffers_and_the_layer_tensors(tile):
     x, y, w = 4 * B * M * H * W, 4 * B * N * H * W, 4 * N * M * r * r
     # the contraction moves 4 bytes per U and V value once, and one Z value
     # per four points (the level-1 output fold), over the groups it computes:
-    # every group on F(2x2,3x3), the 72^2 live ones of 100^2 on the mixed nest
-    G = g["live_groups"]
-    assert G == (72 * 72 if tile == nwg.NWG_TILE_MIX_F23_F33 else g["P"] // 16)
-    U, V, Z = 4 * 16 * G * M * N, 4 * 16 * G * M * g["T"], 4 * 4 * G * N * g["T"]
+    # every group on F(2x2,3x3); on the mixed nest the 72^2 live ones of
+    # 100^2, three of their four quads (level-1 row digit 3 is dead at
+    # r = 31), and 3 x 3 of their 16 points multiplied
+    mix = tile == nwg.NWG_TILE_MIX_F23_F33
+    G, nq, npt = g["live_groups"], 3 if mix else 4, 9 if mix else 16
+    assert G == (72 * 72 if mix else g["P"] // 16)
+    assert g["level1_live"] == (0x7 if mix else 0xf)
+    U, V, Z = 4 * 4 * nq * G * M * N, 4 * 4 * nq * G * M * g["T"], 4 * 4 * G * N * g["T"]
     assert (g["u_bytes"], g["v_bytes"], g["yhat_bytes"]) == (
         4 * g["P"] * M * N, 4 * g["P"] * M * g["T"], 4 * (g["P"] // 4) * N * g["T"])
     assert sb["kernel_transform"] == (w + U, 0.0)
     assert sb["input_transform"] == (x + V, 0.0)
     assert sb["output_transform"] == (Z + y, 0.0)
     b, f = sb["contraction"]
-    assert b == U + V + Z and f == g["contract_flop"] == 2.0 * 16 * G * M * N * g["T"]
+    assert b == U + V + Z and f == g["contract_flop"] == 2.0 * npt * G * M * N * g["T"]
 
 
 def test_depth0_stage_bytes_are_a_channel_gemm():
@@ -133,12 +137,12 @@ def test_cpu_baseline_reports_parity_of_the_outputs_it_is_given():
 
 
 def test_kernel_transform_entry_is_its_bytes_over_its_time():
-    # the mixed nest's 31 x 31 layer: w (63 MB) + the live groups' U (5184 of
-    # 10000 groups of 16 points: 5.44 GB) in 2.25 ms
+    # the mixed nest's 31 x 31 layer: w (63 MB) + the live quads' U (three of
+    # four in 5184 of 10000 groups: 4.08 GB) in 2.25 ms
     g = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15, nwg.NWG_TILE_MIX_F23_F33)
     nbytes = bench.stage_bytes_flops(g)["kernel_transform"][0]
     e = bench.kernel_transform_entry(2.25, nbytes)
-    assert e["bytes"] == 4 * 128 * 128 * 31 * 31 + 4 * 16 * 5184 * 128 * 128
+    assert e["bytes"] == 4 * 128 * 128 * 31 * 31 + 4 * 4 * 3 * 5184 * 128 * 128
     assert e["GB_s"] == pytest.approx(nbytes / 2.25e-3 / 1e9, rel=1e-3)
     assert e["hbm_frac"] == pytest.approx(e["GB_s"] / bench.PEAK_HBM_GBS, rel=1e-3)
     assert e["bound"] == "hbm" and e["ms_once"] == 2.25
