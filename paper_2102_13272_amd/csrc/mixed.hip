@@ -325,7 +325,7 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
 // threads, one work-group per CU) write each point's V row in 512-byte runs:
 // 1.394 -> 1.372 ms on the 31 x 31 layer against 16 tiles.  Work-group ->
 // (level-4 branch q4 (NO = 2), TPW-tile chunk, channel m).
-template <int NO, bool MASK>
+template <int NO, bool MASK, bool Q3>
 __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix(
     const float* __restrict__ x, const float* __restrict__ X4, float4* __restrict__ V, int M,
     int H, int W, int pad, int th, int tw, int T, long long qstride, unsigned long long m0,
@@ -423,9 +423,11 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
   // the column taps need (from column 4 lc), read as float2, then the
   // columns' taps
   const float* wb = win + kStride3 * lr * kL3 + kStride3 * lc;
+  // Q3 (level-1 digit 3 dead): the inner transform reads S[0..8][0..8]
+  constexpr int NS = Q3 ? 9 : 10;
   float S[10][10];
 #pragma unroll
-  for (int i = 0; i < 10; ++i) {
+  for (int i = 0; i < NS; ++i) {
     float tr[22];
 #pragma unroll
     for (int c = 0; c < 22; c += 2) {
@@ -440,7 +442,7 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
       tr[c + 1] = s1;
     }
 #pragma unroll
-    for (int j = 0; j < 10; ++j) {
+    for (int j = 0; j < NS; ++j) {
       float sacc = 0.0f;
 #pragma unroll
       for (int u = 0; u < 4; ++u) sacc = fmaf(cb[u], tr[j + kStride3 * u], sacc);
@@ -458,12 +460,13 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
     const auto rs = span_rsrc(V + (size_t)(q4 * 25 + slot0) * 64 * qstride + (size_t)m * T + t0,
                               (unsigned)(SPW * 64 * qstride * 16));
     const unsigned lane0 = (unsigned)(((size_t)(slot - slot0) * 64 * qstride + tl) * 16);
-    inner2_xform<false>(S, [&](int quad, float4 v) {
+    inner2_xform<false, Q3>(S, [&](int quad, float4 v) {
       drop_store(rs, quad_live(live, q3, quad) ? lane0 + (unsigned)(quad * qstride * 16) : kDrop,
                  v);
     });
   } else {
-    inner2_store<false>(S, V + (size_t)ob * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+    float4* vb = V + (size_t)ob * 64 * qstride + (size_t)m * T + t;
+    inner2_xform<false, Q3>(S, [&](int quad, float4 v) { vb[(size_t)quad * qstride] = v; });
   }
   }
 }
@@ -676,8 +679,11 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
   const int q3 = g.level1_live == 0x7 ? 1 : 0;
   const bool mask = ((g.live_prefix[0] | g.live_prefix[1]) != 0 || q3) &&
                     (64LL / tpw) * 64 * qstride * 16 < (long long)kDrop;
-  const auto fn = no == 2 ? (mask ? &input_xform_mix<2, true> : &input_xform_mix<2, false>)
-                          : (mask ? &input_xform_mix<1, true> : &input_xform_mix<1, false>);
+  const auto fn =
+      no == 2 ? (q3 ? (mask ? &input_xform_mix<2, true, true> : &input_xform_mix<2, false, true>)
+                    : (mask ? &input_xform_mix<2, true, false> : &input_xform_mix<2, false, false>))
+              : (q3 ? (mask ? &input_xform_mix<1, true, true> : &input_xform_mix<1, false, true>)
+                    : (mask ? &input_xform_mix<1, true, false> : &input_xform_mix<1, false, false>));
   if (no == 2) {
     if (g.M > 65535) return hipErrorInvalidValue;
     hipLaunchKernelGGL(input_mix_l4, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x, X4,

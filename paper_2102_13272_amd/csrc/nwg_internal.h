@@ -131,15 +131,20 @@ __device__ __forceinline__ void bt_level(const float* v, float (*out)[LEN]) {
 
 // Two inner levels of the nested input transform on a length-10 vector:
 // level 2 (stride 2) then level 1 (stride 1); out index = q2*4 + q1.
+// Q3: level-1 digit 3 is not needed (its output is set to 0), nor v[9].
+template <bool Q3 = false>
 __device__ __forceinline__ void bt_inner2(const float (&v)[10], float (&out)[16]) {
-  float z[4][4];
-  bt_level<2, 4>(v, z);
+  float z[4][Q3 ? 3 : 4];
+  bt_level<2, Q3 ? 3 : 4>(v, z);
 #pragma unroll
   for (int q2 = 0; q2 < 4; ++q2) {
     out[q2 * 4 + 0] = z[q2][0] - z[q2][2];
     out[q2 * 4 + 1] = z[q2][1] + z[q2][2];
     out[q2 * 4 + 2] = z[q2][2] - z[q2][1];
-    out[q2 * 4 + 3] = z[q2][1] - z[q2][3];
+    if constexpr (Q3)
+      out[q2 * 4 + 3] = 0.0f;
+    else
+      out[q2 * 4 + 3] = z[q2][1] - z[q2][3];
   }
 }
 
@@ -228,9 +233,13 @@ __device__ __forceinline__ void level2_reduce(const float4* __restrict__ zb, siz
 // 2D inner transform (two levels per axis) of a 10 x 10 sub-window S into
 // its 256 points as 64 quads.  Point digits (q2r, q2c, q1r, q1c), most
 // significant first; put(quad, value) stores quad q2r * 16 + q2c * 4 + q1r
-// (q1c over the four lanes of the value).
-template <bool SPLIT, class Put>
+// (q1c over the four lanes of the value).  Q3: level-1 digit 3 is dead, so
+// quads q1r = 3 are not formed (put is not called for them), the q1c = 3
+// lanes are 0, and S's row and column 9 are not read (rows and columns 1..3
+// of B^T of F(2,3) at level 1 take taps 0..2 only).
+template <bool SPLIT, bool Q3 = false, class Put>
 __device__ __forceinline__ void inner2_xform(const float (&S)[10][10], Put&& put) {
+  constexpr int NR = Q3 ? 3 : 4, NJ = Q3 ? 9 : 10;
 #pragma unroll
   for (int q2r = 0; q2r < 4; ++q2r) {
     // level 2 along rows (stride 2): Z[u][j], u = 0..3
@@ -238,19 +247,19 @@ __device__ __forceinline__ void inner2_xform(const float (&S)[10][10], Put&& put
     const int a0 = 2 * bt_tap0(q2r), a1 = 2 * bt_tap1(q2r);
     const float s0 = bt_sign0(q2r), s1 = bt_sign1(q2r);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < NR; ++u)
 #pragma unroll
-      for (int j = 0; j < 10; ++j) Z[u][j] = s0 * S[u + a0][j] + s1 * S[u + a1][j];
+      for (int j = 0; j < NJ; ++j) Z[u][j] = s0 * S[u + a0][j] + s1 * S[u + a1][j];
 #pragma unroll
-    for (int q1r = 0; q1r < 4; ++q1r) {
+    for (int q1r = 0; q1r < NR; ++q1r) {
       // level 1 along rows (stride 1)
       float R[10];
       const int b0 = bt_tap0(q1r), b1 = bt_tap1(q1r);
       const float t0 = bt_sign0(q1r), t1 = bt_sign1(q1r);
 #pragma unroll
-      for (int j = 0; j < 10; ++j) R[j] = t0 * Z[b0][j] + t1 * Z[b1][j];
+      for (int j = 0; j < NJ; ++j) R[j] = t0 * Z[b0][j] + t1 * Z[b1][j];
       float o[16];
-      bt_inner2(R, o);  // columns: index q2c*4 + q1c
+      bt_inner2<Q3>(R, o);  // columns: index q2c*4 + q1c
 #pragma unroll
       for (int q2c = 0; q2c < 4; ++q2c)
         put(q2r * 16 + q2c * 4 + q1r,

@@ -160,8 +160,12 @@ def test_mixed_stages_match_cpu_oracle_chain(case):
         plan.input_transform(dev(x), V)
         torch.cuda.synchronize()
         # fp32 rounding of B^T's thirds and sixths and G's 4s over the levels
-        assert_close(U.cpu().numpy()[lq], quads(U_lib)[lq], rel_tol=1e-6, abs_frac=1e-6, what="U")
-        assert_close(V.cpu().numpy()[lq], quads(V_lib)[lq], rel_tol=1e-6, abs_frac=1e-6, what="V")
+        # the live lanes (q1c = 3 is a dead point too when digit 3 is dead)
+        nl = 3 if i["level1_live"] == 0x7 else 4
+        assert_close(U.cpu().numpy()[lq][..., :nl], quads(U_lib)[lq][..., :nl],
+                     rel_tol=1e-6, abs_frac=1e-6, what="U")
+        assert_close(V.cpu().numpy()[lq][..., :nl], quads(V_lib)[lq][..., :nl],
+                     rel_tol=1e-6, abs_frac=1e-6, what="V")
         Vq = quads(V_lib)
         Vq[~lq] = np.nan                            # never read
         plan.contract(dev(quads(U_lib)), dev(Vq), Z)
