@@ -53,12 +53,15 @@ def stage_bytes_flops(info: dict):
     # values per (n, t) on F(2x2,3x3), 3P/5 on F(3x3,3x3) (the plan's yhat_bytes)
     U, V, Yh = info["u_bytes"], info["v_bytes"], info["yhat_bytes"]
     if info.get("tile") == NWG_TILE_MIX and info["n"] >= 3:
-        # the mixed nest moves only its live groups' U, V and Z, and of U and
-        # V only the quads whose level-1 row digit is live (3 of 4 when digit
-        # 3 is dead; a quad's float4 still carries its dead fourth point)
+        # the mixed nest moves only its live groups' U, V and Z; of U and V
+        # the planar layout holds just the 3 x 3 live points of a group, the
+        # quad layout the quads whose level-1 row digit is live (3 of 4 when
+        # digit 3 is dead, each float4 still carrying its dead fourth point)
         G, live = P // 16, info["live_groups"]
         nq = 3 if info.get("level1_live") == 0x7 else 4
-        U, V, Yh = U // G * live * nq // 4, V // G * live * nq // 4, Yh // G * live
+        if not info.get("mix_planar"):      # planar: U and V hold the live points only
+            U, V = U // G * live * nq // 4, V // G * live * nq // 4
+        Yh = Yh // G * live
     if info.get("fused_output"):
         # input transform, then the output transform that forms the contraction
         return {"kernel_transform": (w + U, 0.0), "input_transform": (x + V, 0.0),

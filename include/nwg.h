@@ -215,6 +215,16 @@ typedef struct nwg_plan_info {
                                    q_1^r = 3 are neither written nor read, and the
                                    contraction takes 3 x 3 points per group); 0 on
                                    F(3x3,3x3) and at depth 0 */
+  int mix_planar;               /* 1: U and V are in the mixed nest's planar layout (depth
+                                   4, level1_live = 0x7, live_np > 0, M % 128 == 0,
+                                   N % 128 == 0, T % 64 == 0): only the live groups'
+                                   9 live points, U[i][p][M][N] and V[i][p][M][T] with
+                                   i the group's place in the live list (row-prefix
+                                   rank * live_np + column-prefix rank, ranks among
+                                   the live prefixes in prefix order) and
+                                   p = 3 q_1^r + q_1^c; u_bytes and v_bytes are those
+                                   sizes.  0: the quad layouts described at the stage
+                                   calls. */
 } nwg_plan_info;
 
 /* Geometry of a convolution without touching any device (host-only): the

@@ -695,6 +695,189 @@ __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu((B
   wait_vmcnt<0>();                          // the clamped tail loads land before exit
 }
 
+// ---------------------------------------------------------------------------
+// Planar contraction of the mixed nest (nwg_plan_info::mix_planar).  U and V
+// hold each live group's 9 live points (3 x 3 level-1 digits, the fourth
+// digit dead) as plain matrices, U[i][p][M][N] and V[i][p][M][T], so that
+// no dead point is loaded.  An item is a 128 x 64 block of (n, t) of one
+// group; four wavefronts of 64 x 32.  A chunk is 32 channels of one point,
+// loaded straight to LDS as float4 along n (A) and t (B).  A lane's float4
+// of A (n = 4 r + c) feeds four MFMA row blocks c and its float2 of B
+// (t = 2 r + b) two column blocks b, so every MFMA block takes every fourth
+// row and every second column of the wavefront's tile.  After a point's
+// channel sweep its products are folded into the four level-1 outputs with
+// A^T[i1r][q1r] A^T[i1c][q1c].  Persistent like contract_deep_persist.
+// ---------------------------------------------------------------------------
+constexpr int kPlBM = 128, kPlBN = 64, kPlBK = 32;   // n rows, t columns, channels per chunk
+
+struct PlanarTile {
+  using LA = DeepLoader<kPlBK, kPlBM / 4, 256>;
+  using LB = DeepLoader<kPlBK, kPlBN / 4, 256>;
+  static constexpr int LPC = LA::PER + LB::PER;     // loads per thread per chunk
+  floatx4 acc[4][2];        // [c][b]: rows 4 r + c, columns 2 r' + b of the wave's tile
+  floatx4 out[4][4][2];     // level-1 outputs 2 i1r + i1c
+  LA da;
+  LB db;
+  const float4* Ug;
+  const float4* Vg;
+  size_t ptU, ptV;          // float4 between points: M N / 4, M T / 4
+  int ldU, ldV, nk, total, wm, wn, lr, lk;
+
+  __device__ __forceinline__ void request(int c, float4 (*An)[kPlBM / 4],
+                                          float4 (*Bn)[kPlBN / 4]) {
+    const int p = c / nk, k0 = (c % nk) * kPlBK;
+    da.load(Ug + (size_t)p * ptU, ldU, k0, An);
+    db.load(Vg + (size_t)p * ptV, ldV, k0, Bn);
+  }
+
+  __device__ __forceinline__ void compute(const float4 (*Ac)[kPlBM / 4],
+                                          const float4 (*Bc)[kPlBN / 4]) {
+#pragma unroll
+    for (int kk = 0; kk < kPlBK / 4; ++kk) {
+      const float4 a = Ac[kk * 4 + lk][wm * 16 + lr];
+      const float2 b = reinterpret_cast<const float2*>(&Bc[kk * 4 + lk][0])[wn * 16 + lr];
+      const float av[4] = {a.x, a.y, a.z, a.w}, bv[2] = {b.x, b.y};
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[c][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], bv[j], acc[c][j], 0, 0, 0);
+    }
+  }
+
+  // point p = 3 q1r + q1c done: out[2 i1r + i1c] += A^T[i1r][q1r] A^T[i1c][q1c] acc
+  __device__ __forceinline__ void fold(int p) {
+    const int q1r = p / 3, q1c = p - 3 * q1r;
+    const float r1 = at_coef(1, q1r), c1 = at_coef(1, q1c);   // A^T[0][q] = 1 for q < 3
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const floatx4 a = acc[c][j];
+        out[0][c][j] += a;
+        out[1][c][j] += c1 * a;
+        out[2][c][j] += r1 * a;
+        out[3][c][j] += (r1 * c1) * a;
+        acc[c][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+  }
+};
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1))) void contract_planar_persist(
+    const float4* __restrict__ U, const float4* __restrict__ V, float4* __restrict__ Z, int M,
+    int N, int T, int ntb, int nnb, long long G, int wpx, GroupMap gm) {
+  constexpr int CA = kPlBM / 4, CB = kPlBN / 4;
+  __shared__ float4 A0[kPlBK][CA], A1[kPlBK][CA], A2[kPlBK][CA], A3[kPlBK][CA];
+  __shared__ float4 B0[kPlBK][CB], B1[kPlBK][CB], B2[kPlBK][CB], B3[kPlBK][CB];
+
+  // this work-group's items: first + i * wpx, i < mine (as contract_deep_persist)
+  const long long items = (long long)ntb * nnb * G;
+  const int xcd = blockIdx.x % 8, j = blockIdx.x / 8;
+  const long long q = items / 8, rem = items % 8;
+  const long long xstart = xcd < rem ? xcd * (q + 1) : rem * (q + 1) + (xcd - rem) * q;
+  const long long xcount = q + (xcd < rem ? 1 : 0);
+  const int mine = xcount > j ? (int)((xcount - 1 - j) / wpx + 1) : 0;
+  if (mine == 0) return;                    // uniform over the work-group
+  const long long first = xstart + j;
+
+  PlanarTile tile;
+  tile.ptU = (size_t)M * (N / 4);
+  tile.ptV = (size_t)M * (T / 4);
+  tile.ldU = N / 4;
+  tile.ldV = T / 4;
+  tile.nk = M / kPlBK;
+  tile.total = 9 * tile.nk;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  tile.wm = wave / 2;
+  tile.wn = wave % 2;
+  tile.lr = lane & 15;
+  tile.lk = lane >> 4;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      tile.acc[c][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int o = 0; o < 4; ++o) tile.out[o][c][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+
+  // request cursor: item ri, chunk rc
+  int ri = 0, rc = 0;
+  auto set_req_item = [&](int i) {
+    long long b = first + (long long)i * wpx;
+    const int tb = (int)(b % ntb);
+    b /= ntb;
+    const int nb = (int)(b % nnb);
+    const long long li = b / nnb;             // place in the live list
+    tile.Ug = U + (size_t)li * 9 * tile.ptU;
+    tile.Vg = V + (size_t)li * 9 * tile.ptV;
+    tile.da.init(tile.ldU, nb * CA, tile.ldU);
+    tile.db.init(tile.ldV, tb * CB, tile.ldV);
+  };
+  // past the last item the last chunk is requested again, into a buffer
+  // that is never read, so every step issues the same loads
+  auto request_next = [&](float4 (*An)[CA], float4 (*Bn)[CB]) {
+    tile.request(rc, An, Bn);
+    if (rc + 1 < tile.total) {
+      ++rc;
+    } else if (ri + 1 < mine) {
+      ++ri;
+      rc = 0;
+      set_req_item(ri);
+    }
+  };
+  auto step = [&](const float4 (*Ac)[CA], const float4 (*Bc)[CB], float4 (*An)[CA],
+                  float4 (*Bn)[CB]) {
+    wait_vmcnt<2 * PlanarTile::LPC>();
+    __builtin_amdgcn_s_barrier();
+    request_next(An, Bn);
+    tile.compute(Ac, Bc);
+  };
+
+  set_req_item(0);
+  request_next(A0, B0);
+  request_next(A1, B1);
+  request_next(A2, B2);
+  for (int it = 0; it < mine; ++it) {
+    for (int p = 0; p < 9; ++p) {
+      for (int kb = 0; kb < tile.nk; kb += 4) {
+        step(A0, B0, A3, B3);
+        step(A1, B1, A0, B0);
+        step(A2, B2, A1, B1);
+        step(A3, B3, A2, B2);
+      }
+      tile.fold(p);
+    }
+    long long b = first + (long long)it * wpx;
+    const int tb = (int)(b % ntb);
+    b /= ntb;
+    const int nb = (int)(b % nnb);
+    const long long g = live_group(gm, b / nnb);
+    float4* __restrict__ Zg = Z + (size_t)g * N * T;
+    const int n0 = nb * kPlBM + tile.wm * 64, t0 = tb * kPlBN + tile.wn * 32;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = n0 + 4 * (4 * tile.lk + v) + c;
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int col = t0 + 2 * tile.lr + jj;
+          Zg[(size_t)row * T + col] = make_float4(tile.out[0][c][jj][v], tile.out[1][c][jj][v],
+                                                  tile.out[2][c][jj][v], tile.out[3][c][jj][v]);
+        }
+      }
+#pragma unroll
+    for (int o = 0; o < 4; ++o)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) tile.out[o][c][jj] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  wait_vmcnt<0>();                          // the clamped tail loads land before exit
+}
+
 // Work-groups of a persistent kernel that fit on one CU of device dev, asked
 // once per (device, kernel) and kept; 0 if the query fails.  Safe to call
 // from several threads.
@@ -922,6 +1105,29 @@ hipError_t launch_gemm(const ContractArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_contract_planar(const float* U, const float* V, float* Z, int M, int N, int T,
+                                  long long G, const GroupMap& gm, hipStream_t s) {
+  if (M <= 0 || N <= 0 || T <= 0 || G <= 0 || gm.np <= 0 || G != (long long)gm.np * gm.np)
+    return hipErrorInvalidValue;
+  if (M % (4 * kPlBK) || N % kPlBM || T % kPlBN) return hipErrorInvalidValue;
+  if (((uintptr_t)U | (uintptr_t)V | (uintptr_t)Z) & 15) return hipErrorInvalidValue;
+  const long long items = (long long)(T / kPlBN) * (N / kPlBM) * G;
+  if (items > 0x7fffffffLL) return hipErrorInvalidValue;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  const int occ =
+      persist_occupancy(dev, reinterpret_cast<const void*>(&contract_planar_persist), 256);
+  if (occ <= 0 || cus < 8) return hipErrorInvalidValue;
+  const int wpx = cus / 8 * occ;            // work-groups per XCD, one per CU slot
+  hipLaunchKernelGGL(contract_planar_persist, dim3((unsigned)(8 * wpx)), dim3(256), 0, s,
+                     (const float4*)U, (const float4*)V, (float4*)Z, M, N, T, T / kPlBN,
+                     N / kPlBM, G, wpx, gm);
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm_depth0(const ContractArgs& a, hipStream_t s) {
   const int N = a.Nrows;

@@ -76,6 +76,30 @@ __device__ __forceinline__ void drop_store(__amdgpu_buffer_rsrc_t r, unsigned of
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, (int)off, 0, 0);
 }
 
+__device__ __forceinline__ void drop_store1(__amdgpu_buffer_rsrc_t r, unsigned off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
+}
+
+// How a transform stores its points: every quad of a live branch, the live
+// quads only (quad layout), or the live points of the live groups in the
+// planar layout (nwg_plan_info::mix_planar).
+enum { kStoreAll = 0, kStoreMasked = 1, kStorePlanar = 2 };
+
+// Rank of axis prefix i among the live prefixes (the live ones below it),
+// branch-free over the four 32-bit words (a 64-bit shift by a lane-varying
+// amount became control flow that stopped the transforms' unrolling).
+__device__ __forceinline__ int prefix_rank(unsigned long long m0, unsigned long long m1, int i) {
+  const unsigned wd[4] = {(unsigned)m0, (unsigned)(m0 >> 32), (unsigned)m1, (unsigned)(m1 >> 32)};
+  int r = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int k = i - 32 * q;
+    const unsigned below = k <= 0 ? 0u : (k >= 32 ? 0xffffffffu : (1u << k) - 1u);
+    r += __popc(wd[q] & below);
+  }
+  return r;
+}
+
 // Whether quad q2r * 16 + q2c * 4 + q1r of a branch with live-group mask
 // live is stored.
 __device__ __forceinline__ bool quad_live(unsigned live, int q3, int quad) {
@@ -121,7 +145,8 @@ __device__ __forceinline__ void bt5_row(int q, float (&c)[5]) {
 }
 
 // ---- kernel transform -------------------------------------------------------
-template <int NO, bool MASK>
+// STORE = kStorePlanar: depth 4 only, U [live group][3 q1r + q1c][M][N].
+template <int NO, int STORE>
 __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict__ w,
                                                         float* __restrict__ U, int M, int N,
                                                         int r, unsigned long long m0,
@@ -197,15 +222,40 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
         }
     // the two F(2,3) levels: 64 quads of this outer branch
     float4* ub = reinterpret_cast<float4*>(U) + (size_t)b * 64 * MN + (size_t)m * N + nn;
-    // MASK: the wave's four branches b0 .. b0 + 3 share a resource
+    // kStoreMasked: the wave's four branches b0 .. b0 + 3 share a resource
     const int b0 = __builtin_amdgcn_readfirstlane(b & ~3);
     const auto rs = span_rsrc(reinterpret_cast<float4*>(U) + (size_t)b0 * 64 * MN +
                                   (size_t)m * N + n0,
                               (unsigned)(4 * 64 * MN * 16));
     const unsigned lane0 = (unsigned)(((size_t)(b - b0) * 64 * MN + cl) * 16);
+    // kStorePlanar: groups at their live-list places; the wave's resource
+    // starts at the lowest row-prefix block (q4r, q3r) of its four branches,
+    // and a group's place is at most 20 live row prefixes above it
+    unsigned irp = 0, icp = 0;                // ranks of the 4 row / column prefixes, 8 bits each
+    int lbase = 0, np = 0;
+    __amdgpu_buffer_rsrc_t pr = rs;
+    if constexpr (STORE == kStorePlanar) {
+      np = __popcll(m0) + __popcll(m1);
+      int smin = 1 << 20;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int bi = b0 + i;
+        const int si = ((bi / 125) * 5 + (bi / 5) % 5) * 4;
+        if (bi < NB && si < smin) smin = si;
+      }
+      lbase = prefix_rank(m0, m1, smin) * np;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        irp |= (unsigned)prefix_rank(m0, m1, (q4r * 5 + q3r) * 4 + q) << (8 * q);
+        icp |= (unsigned)prefix_rank(m0, m1, (q4c * 5 + q3c) * 4 + q) << (8 * q);
+      }
+      pr = span_rsrc(reinterpret_cast<float4*>(U + (size_t)lbase * 9 * MN + (size_t)m * N + n0),
+                     (unsigned)(20 * np * 9 * MN * 4));
+    }
 #pragma unroll
     for (int rho = 0; rho < 16; ++rho) {
       const int q2r = rho >> 2, q1r = rho & 3;
+      if (STORE == kStorePlanar && q1r == 3) continue;   // dead level-1 digit
       float rowv[9];
 #pragma unroll
       for (int ic = 0; ic < 9; ++ic) {
@@ -223,10 +273,19 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
       for (int q2c = 0; q2c < 4; ++q2c) {
         const int quad = q2r * 16 + q2c * 4 + q1r;
         const float4 v = make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
-        if constexpr (MASK)
+        if constexpr (STORE == kStorePlanar) {
+          const bool on = (live >> (quad >> 2)) & 1u;
+          const int ir = (irp >> (8 * q2r)) & 0xff, ic = (icp >> (8 * q2c)) & 0xff;
+          const unsigned rel = (unsigned)((ir * np + ic - lbase) * 9 + 3 * q1r);
+          const unsigned o0 = (unsigned)(rel * MN + cl) * 4u, ps = (unsigned)MN * 4u;
+          drop_store1(pr, on ? o0 : kDrop, v.x);
+          drop_store1(pr, on ? o0 + ps : kDrop, v.y);
+          drop_store1(pr, on ? o0 + 2 * ps : kDrop, v.z);
+        } else if constexpr (STORE == kStoreMasked) {
           drop_store(rs, quad_live(live, q3, quad) ? lane0 + (unsigned)(quad * MN * 16) : kDrop, v);
-        else
+        } else {
           ub[(size_t)quad * MN] = v;
+        }
       }
     }
   }
@@ -325,7 +384,8 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
 // threads, one work-group per CU) write each point's V row in 512-byte runs:
 // 1.394 -> 1.372 ms on the 31 x 31 layer against 16 tiles.  Work-group ->
 // (level-4 branch q4 (NO = 2), TPW-tile chunk, channel m).
-template <int NO, bool MASK, bool Q3>
+// STORE = kStorePlanar: depth 4 and Q3 only, V [live group][3 q1r + q1c][M][T].
+template <int NO, int STORE, bool Q3>
 __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix(
     const float* __restrict__ x, const float* __restrict__ X4, float4* __restrict__ V, int M,
     int H, int W, int pad, int th, int tw, int T, long long qstride, unsigned long long m0,
@@ -453,7 +513,36 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
     __builtin_amdgcn_sched_barrier(0);
   }
   const int ob = q4 * 25 + slot;
-  if constexpr (MASK) {
+  if constexpr (STORE == kStorePlanar) {
+    static_assert(NO == 2 && Q3, "planar V: depth 4, level-1 digit 3 dead");
+    // groups at their live-list places; the work-group's resource starts at
+    // its level-4 row block (q4r), 20 row prefixes
+    const int np = __popcll(m0) + __popcll(m1);
+    const int q4r = q4 / 5, q4c = q4 - 5 * q4r;
+    const int lbase = prefix_rank(m0, m1, q4r * 20) * np;
+    const size_t plane = (size_t)M * T;
+    const auto pr = span_rsrc(reinterpret_cast<float4*>(reinterpret_cast<float*>(V) +
+                                                        (size_t)lbase * 9 * plane +
+                                                        (size_t)m * T + t0),
+                              (unsigned)(20 * np * 9 * plane * 4));
+    unsigned irp = 0, icp = 0;                // ranks of the 4 row / column prefixes, 8 bits each
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      irp |= (unsigned)prefix_rank(m0, m1, (q4r * 5 + q3r) * 4 + q) << (8 * q);
+      icp |= (unsigned)prefix_rank(m0, m1, (q4c * 5 + q3c) * 4 + q) << (8 * q);
+    }
+    const unsigned ps = (unsigned)plane * 4u;
+    inner2_xform<false, true>(S, [=](int quad, float4 v) {
+      const int q2r = quad >> 4, q2c = (quad >> 2) & 3, q1r = quad & 3;
+      const bool on = (live >> (quad >> 2)) & 1u;
+      const int ir = (irp >> (8 * q2r)) & 0xff, ic = (icp >> (8 * q2c)) & 0xff;
+      const unsigned rel = (unsigned)((ir * np + ic - lbase) * 9 + 3 * q1r);
+      const unsigned o0 = rel * ps + (unsigned)tl * 4u;
+      drop_store1(pr, on ? o0 : kDrop, v.x);
+      drop_store1(pr, on ? o0 + ps : kDrop, v.y);
+      drop_store1(pr, on ? o0 + 2 * ps : kDrop, v.z);
+    });
+  } else if constexpr (STORE == kStoreMasked) {
     // the wave's 64 / TPW consecutive slots share a resource
     constexpr int SPW = 64 / TPW;
     const int slot0 = __builtin_amdgcn_readfirstlane(slot & ~(SPW - 1));
@@ -653,8 +742,11 @@ hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float
   const int q3 = g.level1_live == 0x7 ? 1 : 0;
   const bool mask = ((g.live_prefix[0] | g.live_prefix[1]) != 0 || q3) &&
                     4LL * 64 * g.M * g.N * 16 < (long long)kDrop;
-  const auto fn = no == 2 ? (mask ? &kernel_xform_mix<2, true> : &kernel_xform_mix<2, false>)
-                          : (mask ? &kernel_xform_mix<1, true> : &kernel_xform_mix<1, false>);
+  const auto fn = g.mix_planar ? &kernel_xform_mix<2, kStorePlanar>
+                  : no == 2    ? (mask ? &kernel_xform_mix<2, kStoreMasked>
+                                       : &kernel_xform_mix<2, kStoreAll>)
+                               : (mask ? &kernel_xform_mix<1, kStoreMasked>
+                                       : &kernel_xform_mix<1, kStoreAll>);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
@@ -679,11 +771,13 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
   const int q3 = g.level1_live == 0x7 ? 1 : 0;
   const bool mask = ((g.live_prefix[0] | g.live_prefix[1]) != 0 || q3) &&
                     (64LL / tpw) * 64 * qstride * 16 < (long long)kDrop;
+  constexpr int A = kStoreAll, K = kStoreMasked;
   const auto fn =
-      no == 2 ? (q3 ? (mask ? &input_xform_mix<2, true, true> : &input_xform_mix<2, false, true>)
-                    : (mask ? &input_xform_mix<2, true, false> : &input_xform_mix<2, false, false>))
-              : (q3 ? (mask ? &input_xform_mix<1, true, true> : &input_xform_mix<1, false, true>)
-                    : (mask ? &input_xform_mix<1, true, false> : &input_xform_mix<1, false, false>));
+      g.mix_planar ? &input_xform_mix<2, kStorePlanar, true>
+      : no == 2    ? (q3 ? (mask ? &input_xform_mix<2, K, true> : &input_xform_mix<2, A, true>)
+                         : (mask ? &input_xform_mix<2, K, false> : &input_xform_mix<2, A, false>))
+                   : (q3 ? (mask ? &input_xform_mix<1, K, true> : &input_xform_mix<1, A, true>)
+                         : (mask ? &input_xform_mix<1, K, false> : &input_xform_mix<1, A, false>));
   if (no == 2) {
     if (g.M > 65535) return hipErrorInvalidValue;
     hipLaunchKernelGGL(input_mix_l4, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x, X4,

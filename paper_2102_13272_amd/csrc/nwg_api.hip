@@ -167,6 +167,8 @@ hipError_t launch_contract(const nwg_plan_info& g, const float* U, const float* 
   const int mk = g.ld_c > 0 ? g.M * g.ld_c * g.ld_c : g.M;
   // the mixed nest contracts its live groups only (the others' Z is zero)
   const nwg::GroupMap gm = nwg::group_map(g);
+  if (g.mix_planar)
+    return nwg::launch_contract_planar(U, V, Z, g.M, g.N, (int)g.T, g.live_groups, gm, s);
   const long long G = gm.np > 0 ? g.live_groups : g.P / 16;
   const hipError_t e = nwg::launch_contract_fused(U, V, Z, mk, g.N, (int)g.T, G, s,
                                                   g.precision == NWG_PRECISION_BF16_SPLIT, ks, gm);

@@ -348,6 +348,11 @@ hipError_t launch_kernel_xform_ld(const nwg_plan_info& g, const float* w, float*
 hipError_t launch_contract_fused(const float* U, const float* V, float* Z, int M, int N, int T,
                                  long long G, hipStream_t s, bool split = false, int ks = 1,
                                  const GroupMap& gm = GroupMap{});
+// Planar contraction of the mixed nest (mix_planar plans): U [G][9][M][N],
+// V [G][9][M][T] over the G = gm.np^2 live groups, Z [P/16][N][T][4] at the
+// groups' places; M % 128 == 0, N % 128 == 0, T % 64 == 0.
+hipError_t launch_contract_planar(const float* U, const float* V, float* Z, int M, int N, int T,
+                                  long long G, const GroupMap& gm, hipStream_t s);
 // in place: every fp32 value of buf (n values) -> its packed bf16 (hi, lo) pair
 hipError_t launch_split_pairs(float* buf, size_t n, hipStream_t s);
 hipError_t launch_input_contract(const nwg_plan_info& g, const float* x, const float* U, float* Z,

@@ -298,6 +298,22 @@ void mix_liveness(nwg_plan_info* g) {
   g->contract_flop = 2.0 * lq * lq * g->live_groups * g->M * g->N * g->T;
 }
 
+// Depth-4 mixed plans with dead groups and level-1 digit 3 dead, on shapes
+// the planar contraction tiles evenly (128 x 64 blocks of (n, t), 128-deep
+// channel sweeps): U and V hold only the live groups' 3 x 3 live points,
+// point by point.  The transforms address a level-4 row block (20 row
+// prefixes) of groups through one buffer resource, which must stay below
+// 2 GiB.
+void mix_layout(nwg_plan_info* g) {
+  if (g->n != 4 || g->level1_live != 0x7 || g->live_np <= 0) return;
+  if (g->M % 128 || g->N % 128 || g->T % 64) return;
+  const double span = 20.0 * g->live_np * 9 * g->M * (double)(g->N > g->T ? g->N : g->T) * 4;
+  if (span >= 2147483648.0) return;
+  g->mix_planar = 1;
+  g->u_bytes = (size_t)9 * g->live_groups * g->M * g->N * sizeof(float);
+  g->v_bytes = (size_t)9 * g->live_groups * g->M * g->T * sizeof(float);
+}
+
 // Level recurrence on the base F(m, rb): s_0 = 1, M_1 = m, K_1 = rb,
 // s_j = min(M_j, K_j), M_{j+1} = M_j + s_j (m_{j+1} - 1),
 // K_{j+1} = K_j + s_j (rb - 1); n is the smallest depth with K_n >= r, and
@@ -415,7 +431,11 @@ int geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile, i
                        (plan_holds_z(*g) ? zalloc_bytes(*g) : 0);
   g->live_groups = f33 || n == 0 ? 0 : g->P / 16;
   g->level1_live = f33 || n == 0 ? 0 : 0xf;
-  if (mix && n >= 3) mix_liveness(g);
+  if (mix && n >= 3) {
+    mix_liveness(g);
+    mix_layout(g);
+    g->workspace_bytes = g->u_bytes + g->v_bytes + zalloc_bytes(*g);
+  }
   return NWG_OK;
 }
 

@@ -45,6 +45,7 @@ class nwg_plan_info(ctypes.Structure):
         ("fused_output", ctypes.c_int), ("outer33", ctypes.c_int),
         ("live_np", ctypes.c_int), ("live_prefix", ctypes.c_ulonglong * 2),
         ("live_groups", ctypes.c_longlong), ("level1_live", ctypes.c_int),
+        ("mix_planar", ctypes.c_int),
     ]
 
     def as_dict(self):
@@ -232,11 +233,15 @@ class Plan:
         mk = 1 if i["depthwise"] else self._mv
         if not i["n"]:
             return (mk, i["N"])
+        if i["mix_planar"]:
+            return (i["live_groups"], 9, mk, i["N"])
         return (i["P"], mk, i["N"]) if self._f33 else (i["P"] // 4, mk, i["N"], 4)
 
     @property
     def v_shape(self):
         i = self.info
+        if i["mix_planar"]:
+            return (i["live_groups"], 9, i["M"], i["T"])
         return (i["P"], i["M"], i["T"]) if self._f33 else (i["P"] // 4, self._mv, i["T"], 4)
 
     @property

@@ -125,3 +125,48 @@ def live_group_mask(info):
             mul *= l
         out[g] = bool((mask >> pr) & 1) and bool((mask >> pc) & 1)
     return out
+
+
+def live_prefixes(info):
+    """The live axis prefixes of a mixed plan, in prefix order (bit i of
+    live_prefix: i = (q_4 * 5 + q_3) * 4 + q_2 at depth 4)."""
+    mask = int(info["live_prefix"][0]) | (int(info["live_prefix"][1]) << 64)
+    return [i for i in range(128) if (mask >> i) & 1]
+
+
+def mixed_axis_index(q1, prefix):
+    """Depth-4 mixed nest: the oracle's per-axis point index (level 1 most
+    significant, radices 4, 4, 5, 5) of level-1 digit q1 under axis prefix
+    (q_4 * 5 + q_3) * 4 + q_2."""
+    q2, q3, q4 = prefix % 4, (prefix // 4) % 5, prefix // 20
+    return ((q1 * 4 + q2) * 5 + q3) * 5 + q4
+
+
+def planar_points(info):
+    """Row and column oracle axis indices [live_groups][9] of the planar
+    layout's points: group i = (row rank, column rank) = divmod(i, live_np),
+    point p = 3 q1r + q1c."""
+    pre = live_prefixes(info)
+    np_ = info["live_np"]
+    rows = np.empty((np_ * np_, 9), dtype=np.int64)
+    cols = np.empty_like(rows)
+    for i in range(np_ * np_):
+        pr, pc = pre[i // np_], pre[i % np_]
+        for p in range(9):
+            rows[i, p] = mixed_axis_index(p // 3, pr)
+            cols[i, p] = mixed_axis_index(p % 3, pc)
+    return rows, cols
+
+
+def planar_group_index(info, i):
+    """Z's group index g of the planar layout's group i."""
+    pre = live_prefixes(info)
+    np_ = info["live_np"]
+    pr, pc = pre[i // np_], pre[i % np_]
+    g = 0
+    for d, (wr, wc) in enumerate([(4, 1), (80, 16), (2000, 400)]):   # q_2, q_3, q_4
+        rad = 4 if d == 0 else 5
+        g += (pr % rad) * wr + (pc % rad) * wc
+        pr //= rad
+        pc //= rad
+    return g

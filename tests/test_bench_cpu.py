@@ -38,12 +38,13 @@ def test_stage_bytes_are_the_plan_buffers_and_the_layer_tensors(tile):
     # 100^2, three of their four quads (level-1 row digit 3 is dead at
     # r = 31), and 3 x 3 of their 16 points multiplied
     mix = tile == nwg.NWG_TILE_MIX_F23_F33
-    G, nq, npt = g["live_groups"], 3 if mix else 4, 9 if mix else 16
+    G, npt = g["live_groups"], 9 if mix else 16
     assert G == (72 * 72 if mix else g["P"] // 16)
-    assert g["level1_live"] == (0x7 if mix else 0xf)
-    U, V, Z = 4 * 4 * nq * G * M * N, 4 * 4 * nq * G * M * g["T"], 4 * 4 * G * N * g["T"]
+    assert g["level1_live"] == (0x7 if mix else 0xf) and g["mix_planar"] == int(mix)
+    # the mixed nest's planar U and V hold the 9 live points of each live group
+    U, V, Z = 4 * npt * G * M * N, 4 * npt * G * M * g["T"], 4 * 4 * G * N * g["T"]
     assert (g["u_bytes"], g["v_bytes"], g["yhat_bytes"]) == (
-        4 * g["P"] * M * N, 4 * g["P"] * M * g["T"], 4 * (g["P"] // 4) * N * g["T"])
+        U, V, 4 * (g["P"] // 4) * N * g["T"])
     assert sb["kernel_transform"] == (w + U, 0.0)
     assert sb["input_transform"] == (x + V, 0.0)
     assert sb["output_transform"] == (Z + y, 0.0)
@@ -137,12 +138,12 @@ def test_cpu_baseline_reports_parity_of_the_outputs_it_is_given():
 
 
 def test_kernel_transform_entry_is_its_bytes_over_its_time():
-    # the mixed nest's 31 x 31 layer: w (63 MB) + the live quads' U (three of
-    # four in 5184 of 10000 groups: 4.08 GB) in 2.25 ms
+    # the mixed nest's 31 x 31 layer: w (63 MB) + the planar U (the 9 live
+    # points of 5184 live groups of 10000: 3.06 GB) in 2.25 ms
     g = nwg.plan_geometry(16, 128, 128, 56, 56, 31, 15, nwg.NWG_TILE_MIX_F23_F33)
     nbytes = bench.stage_bytes_flops(g)["kernel_transform"][0]
     e = bench.kernel_transform_entry(2.25, nbytes)
-    assert e["bytes"] == 4 * 128 * 128 * 31 * 31 + 4 * 4 * 3 * 5184 * 128 * 128
+    assert e["bytes"] == 4 * 128 * 128 * 31 * 31 + 4 * 9 * 5184 * 128 * 128
     assert e["GB_s"] == pytest.approx(nbytes / 2.25e-3 / 1e9, rel=1e-3)
     assert e["hbm_frac"] == pytest.approx(e["GB_s"] / bench.PEAK_HBM_GBS, rel=1e-3)
     assert e["bound"] == "hbm" and e["ms_once"] == 2.25

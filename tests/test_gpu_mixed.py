@@ -17,7 +17,8 @@ from oracle.nested import ewmm
 from paper_2102_13272_amd import nwg
 from paper_2102_13272_amd.workloads import make_case
 from tests.gpu_util import assert_close, dev
-from tests.layout import level1, live_group_mask, mixed_chain, mixed_to_lib_points, quads
+from tests.layout import (level1, live_group_mask, mixed_chain, mixed_to_lib_points,
+                          planar_group_index, planar_points, quads)
 
 pytestmark = pytest.mark.gpu
 MIX = nwg.NWG_TILE_MIX_F23_F33
@@ -180,6 +181,87 @@ def test_mixed_stages_match_cpu_oracle_chain(case):
         # fp32 sums over A^T entries up to 4 at the F(3,3) levels (rows and
         # columns, two levels at depth 4): ~1e-6 of the output's norm
         assert_close(y.cpu().numpy(), y_ref, rel_tol=1e-5, abs_frac=1e-5, what="y")
+
+
+# the planar layout (mix_planar: depth 4, level-1 digit 3 dead, M % 128,
+# N % 128, T % 64): one 36 x 36 tile per image, T = 64 or 128, 128 x 64
+# blocks in one or two rows, r = 31, 27 and 23
+PLANAR = [(64, 128, 128, 36, 36, 31, 15), (64, 128, 256, 36, 36, 31, 15),
+          (128, 128, 128, 36, 36, 23, 11), (16, 128, 128, 72, 72, 27, 13)]
+
+
+@pytest.mark.parametrize("case", PLANAR, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
+def test_mixed_planar_conv2d_sampled_outputs(case):
+    """Whole layers on the planar layout against the direct oracle on sampled
+    images and output channels (every output position of those)."""
+    B, M, N, H, W, r, pad = case
+    L, x, w = make_case(B, M, N, H, W, r, pad, seed=3 * sum(case))
+    print(f"mixed planar case {case}", flush=True)
+    with nwg.Plan(B, M, N, H, W, r, pad, tile=MIX) as plan:
+        assert plan.info["mix_planar"] == 1
+    y = _conv(x, w, pad)
+    bs = sorted({0, B // 2, B - 1})
+    ns = sorted({0, 1, N // 2 + 3, N - 1})
+    ref = direct_conv2d(x[bs], w[ns], pad)
+    assert_close(y[np.ix_(bs, ns)], ref, what=str(case))
+
+
+def test_mixed_planar_stages_sampled():
+    """Stage by stage on the planar layout: U and V at sampled (channel, tile)
+    against the oracle's kernel and input matrices at every live point; the
+    contraction on seeded random U and V against an fp64 sum on sampled
+    groups, the dead groups' Z untouched."""
+    B, M, N, H, W, r, pad = PLANAR[0]
+    L, x, w = make_case(B, M, N, H, W, r, pad, seed=5)
+    print(f"mixed planar stages {PLANAR[0]}", flush=True)
+    lv = mixed_levels(mixed_chain(), r)
+    KG = np.asarray(kernel_matrix(lv), dtype=np.float64)
+    IB = np.asarray(input_matrix(lv), dtype=np.float64)
+    with nwg.Plan(B, M, N, H, W, r, pad, tile=MIX) as plan:
+        i = plan.info
+        G = i["live_groups"]
+        assert i["mix_planar"] == 1 and (i["T"], i["th"], i["tw"]) == (B, 1, 1)
+        assert plan.u_shape == (G, 9, M, N) and plan.v_shape == (G, 9, M, B)
+        rows, cols = planar_points(i)
+        U = torch.full(plan.u_shape, float("nan"), device="cuda")
+        V = torch.full(plan.v_shape, float("nan"), device="cuda")
+        plan.kernel_transform(dev(w), U)
+        plan.input_transform(dev(x), V)
+        torch.cuda.synchronize()
+        Uh, Vh = U.cpu().numpy(), V.cpu().numpy()
+        del U, V
+        for n, m in [(0, 0), (N - 1, M - 1), (37, 101)]:
+            wp = np.zeros((lv.Kn, lv.Kn))
+            wp[:r, :r] = w[n, m]
+            Uo = KG @ wp @ KG.T
+            assert_close(Uh[:, :, m, n], Uo[rows, cols], rel_tol=1e-6, abs_frac=1e-6,
+                         what=f"U n={n} m={m}")
+        for b, m in [(0, 0), (B - 1, M - 1), (20, 77)]:
+            X = np.zeros((lv.Ln, lv.Ln))
+            X[pad:pad + H, pad:pad + W] = x[b, m, :lv.Ln - pad, :lv.Ln - pad]
+            Vo = IB @ X @ IB.T
+            assert_close(Vh[:, :, m, b], Vo[rows, cols], rel_tol=1e-6, abs_frac=1e-6,
+                         what=f"V b={b} m={m}")
+        del Uh, Vh
+        rng = np.random.default_rng(3)
+        Ur = rng.standard_normal(plan.u_shape, dtype=np.float32)
+        Vr = rng.standard_normal(plan.v_shape, dtype=np.float32)
+        Z = torch.full(plan.z_shape, float("nan"), device="cuda")
+        plan.contract(dev(Ur), dev(Vr), Z)
+        torch.cuda.synchronize()
+        Zh = Z.cpu().numpy()
+    assert np.isnan(Zh[~live_group_mask(i)]).all()     # dead groups: not written
+    AT = np.array([[1.0, 1.0, 1.0], [0.0, 1.0, -1.0]])  # A^T of F(2,3) on digits 0..2
+    for li in [0, 1, 1234, G // 2, G - 1]:
+        prod = np.einsum("pmn,pmt->pnt", Ur[li].astype(np.float64), Vr[li].astype(np.float64))
+        zr = np.zeros((N, B, 4))
+        for p in range(9):
+            q1r, q1c = divmod(p, 3)
+            for i1r in range(2):
+                for i1c in range(2):
+                    zr[..., 2 * i1r + i1c] += AT[i1r, q1r] * AT[i1c, q1c] * prod[p]
+        assert_close(Zh[planar_group_index(i, li)], zr, rel_tol=1e-5, abs_frac=1e-5,
+                     what=f"Z group {li}")
 
 
 def test_mixed_plan_rejects_what_it_does_not_serve():
