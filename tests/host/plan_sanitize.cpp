@@ -56,7 +56,15 @@ void check_plan(const nwg_plan_info& g) {
     expect(g.n == 0 || (Mj == g.Mn && Kj == g.Kn), "M_n, K_n", g);
     expect(g.P == P1 * P1, "P", g);
     const int Mk = g.depthwise ? 1 : g.M;
-    if (g.n > 0) {
+    if (g.n > 0 && g.mix_planar) {
+      // planar mixed layout: the 9 live points of each live group
+      expect(g.tile == NWG_TILE_MIX_F23_F33 && g.n == 4 && g.level1_live == 0x7 &&
+                 g.live_np > 0 && g.live_groups == (long long)g.live_np * g.live_np,
+             "planar conditions", g);
+      expect(g.u_bytes == (size_t)(36.0 * (double)g.live_groups * Mk * g.N), "u_bytes", g);
+      expect(g.v_bytes == (size_t)(36.0 * (double)g.live_groups * g.M * (double)g.T),
+             "v_bytes", g);
+    } else if (g.n > 0) {
       expect(g.u_bytes == (size_t)(4.0 * (double)g.P * Mk * g.N), "u_bytes", g);
       expect(g.v_bytes == (size_t)(4.0 * (double)g.P * g.M * (double)g.T), "v_bytes", g);
     }
