@@ -443,20 +443,41 @@ int geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile, i
 
 namespace {
 
-// Step time of an unfused dense plan on MI355X, in seconds, from its
-// algorithmic bytes and FLOPs at the rates its kernels sustain at depth 4
-// (about 5 TB/s of HBM traffic, 100 TFLOP/s of fp32 MFMA): the transforms
-// move x + V and Z + y; the contraction takes the longer of its U + V + Z
-// traffic and its MFMA work on whole 64-column tiles and 64-row / 32-deep
-// channel blocks.  Used only to choose between nests.
+// Step time of an unfused dense plan on MI355X, in seconds, from the bytes
+// and FLOPs its kernels move and compute, at the rates they sustain at depth
+// 4 (about 5 TB/s of HBM traffic, 100 TFLOP/s of fp32 MFMA): the transforms
+// move x + V and Z + y (and the mixed nest's depth-4 scratch both ways); the
+// contraction takes the longer of its U + V + Z traffic and its MFMA work on
+// whole 64-column tiles and 64-row / 32-deep channel blocks.  On the mixed
+// nest only the live groups count, and of them the live points (planar
+// layout) or quads (quad layout).  Its kernels fall short of these rates
+// more than the F(2,3) ones do: its estimate is scaled by 1.47 at depth 4
+// and 1.3 at depth 3, the factors that order the two nests as measured on
+// the fifteen layers of the automatic-choice test (ties within 3 % either
+// way).  Used only to choose between nests.
 double unfused_step_seconds(const nwg_plan_info& g) {
   constexpr double kBw = 5.0e12, kMfma = 100e12;
   auto up = [](double v, double q) { return std::ceil(v / q) * q; };
-  const double flop = 2.0 * (double)g.P * up(g.M, 32) * up(g.N, 64) * up((double)g.T, 64);
+  double pts = (double)g.P, U = (double)g.u_bytes, V = (double)g.v_bytes,
+         Z = (double)g.yhat_bytes, scratch = 0.0, scale = 1.0;
+  if (g.tile == NWG_TILE_MIX_F23_F33 && g.n >= 3) {
+    const double G = (double)(g.P / 16), live = (double)g.live_groups;
+    const bool q3 = g.level1_live == 0x7;
+    pts = live * (q3 ? 9.0 : 16.0);
+    if (!g.mix_planar) {
+      U = U / G * live * (q3 ? 0.75 : 1.0);
+      V = V / G * live * (q3 ? 0.75 : 1.0);
+    }
+    Z = Z / G * live;
+    if (g.n == 4)   // X4 (level-4 input blocks) and Z3 (level-3 output blocks), each written and read
+      scratch = 2.0 * 4.0 * 25.0 * (double)g.T * ((double)kMixL3 * kMixL3 * g.M + 144.0 * g.N);
+    scale = g.n == 4 ? 1.47 : 1.3;
+  }
+  const double flop = 2.0 * pts * up(g.M, 32) * up(g.N, 64) * up((double)g.T, 64);
   const double x = 4.0 * g.B * g.M * g.H * g.W, y = 4.0 * g.B * g.N * (double)g.Ho * g.Wo;
-  const double cb = (double)g.u_bytes + g.v_bytes + g.yhat_bytes;
+  const double cb = U + V + Z;
   const double tc = flop / kMfma > cb / kBw ? flop / kMfma : cb / kBw;
-  return tc + (x + g.v_bytes) / kBw + (g.yhat_bytes + y) / kBw;
+  return scale * (tc + (x + V) / kBw + (Z + y) / kBw + scratch / kBw);
 }
 
 }  // namespace
@@ -465,17 +486,18 @@ double unfused_step_seconds(const nwg_plan_info& g) {
 // the fused one-output-channel kernel at depth 2 (unless F(2,3) runs the
 // layer in one kernel), or both channel counts >= 32 and either a nesting
 // level saved (r = 8, 9) or depth 1 (r <= 3); the mixed nest for dense
-// layers at depth 4 with both channel counts >= 32 when the step model
-// above expects it to be faster (it has 1.6x fewer contraction FLOPs per
-// output but 2.4x the transformed weights, and 36 x 36 tiles: few tiles
-// leave most of a 64-column MFMA tile empty); F(2x2,3x3) otherwise.
+// layers at depth 3 (r = 10..15) or 4 with both channel counts >= 32 when
+// the step model above expects it to be faster (with its dead groups and
+// points skipped it has 2.5x to 5.6x fewer contraction FLOPs per output,
+// but its 12 x 12 and 36 x 36 tiles leave few tiles on small images, and
+// its transformed weights are up to 2x larger); F(2x2,3x3) otherwise.
 int compute_geometry(int B, int M, int N, int H, int W, int r, int pad, int tile, int depthwise,
                      nwg_plan_info* g) {
   if (!g) return fail(NWG_EINVAL, "output pointer is NULL");
   if (tile != NWG_TILE_AUTO) return geometry_tile(B, M, N, H, W, r, pad, tile, depthwise, g);
   nwg_plan_info a, b;
   const int ra = geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_F2X2_3X3, depthwise, &a);
-  if (ra == NWG_OK && !depthwise && a.n == 4 && M >= 32 && N >= 32) {
+  if (ra == NWG_OK && !depthwise && (a.n == 4 || (a.n == 3 && r > 9)) && M >= 32 && N >= 32) {
     if (geometry_tile(B, M, N, H, W, r, pad, NWG_TILE_MIX_F23_F33, 0, &b) == NWG_OK) {
       *g = unfused_step_seconds(b) < unfused_step_seconds(a) ? b : a;
       return NWG_OK;
