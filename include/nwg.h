@@ -34,6 +34,12 @@
  * q_1^col), most significant first, q_j being the level-j Winograd index.
  * At depth 0 (r = 1) there is no transform: U is [M][N] and the contraction
  * maps x to y directly.  All buffers must be 16-byte aligned.
+ * Mixed-nest plans (NWG_TILE_MIX_F23_F33) compute only the points whose
+ * transformed kernel can be nonzero (nwg_plan_info live_np, live_prefix,
+ * level1_live): the stage calls neither write nor read the dead groups'
+ * U, V and Z, nor the quads of a dead level-1 row digit; with mix_planar
+ * set, U and V hold only the live points, in the planar layout described
+ * at that field.  Z keeps the layout above.
  *
  * Ownership: the caller owns x, w, y, U/V/Z passed to stage calls, and
  * the stream; they must stay valid until the work queued on the stream has
