@@ -37,6 +37,41 @@ namespace {
 
 constexpr int kStride3 = 4, kStride4 = 12;
 
+// Rank of axis prefix i among the live prefixes (the live ones below it),
+// branch-free over the four 32-bit words (a 64-bit shift by a lane-varying
+// amount became control flow that stopped the transforms' unrolling).
+__device__ __forceinline__ int prefix_rank(unsigned long long m0, unsigned long long m1, int i) {
+  const unsigned wd[4] = {(unsigned)m0, (unsigned)(m0 >> 32), (unsigned)m1, (unsigned)(m1 >> 32)};
+  int r = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int k = i - 32 * q;
+    const unsigned below = k <= 0 ? 0u : (k >= 32 ? 0xffffffffu : (1u << k) - 1u);
+    r += __popc(wd[q] & below);
+  }
+  return r;
+}
+
+// Live bits of the four axis prefixes 4 b .. 4 b + 3 (level-2 digit q2 =
+// 0..3 under level-3 block b = 5 q4 + q3 at depth 4, b = q3 at depth 3): a
+// nibble, which never straddles two 32-bit words of the mask.
+__device__ __forceinline__ unsigned prefix_nibble(unsigned long long m0, unsigned long long m1,
+                                                  int b) {
+  const int i = 4 * b;
+  const unsigned long long w = i < 64 ? m0 : m1;
+  const unsigned h = (i & 63) < 32 ? (unsigned)w : (unsigned)(w >> 32);
+  return (h >> (i & 31)) & 0xfu;
+}
+
+// The live groups (q2r, q2c) of a branch from its row and column nibbles,
+// as a 16-bit mask, bit 4 q2r + q2c.
+__device__ __forceinline__ unsigned nibble_live(unsigned nr, unsigned nc) {
+  unsigned live = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) live |= ((nr >> q) & 1u) ? nc << (4 * q) : 0u;
+  return live;
+}
+
 // The live groups (q2r, q2c) of outer branch (q4r, q4c, q3r, q3c) as a
 // 16-bit mask, bit 4 q2r + q2c (NO = 1: no level-4 digits).  A group is live
 // when its row prefix (q4r, q3r, q2r) and its column prefix (q4c, q3c, q2c)
@@ -45,18 +80,8 @@ template <int NO>
 __device__ __forceinline__ unsigned branch_live(unsigned long long m0, unsigned long long m1,
                                                 int q4r, int q4c, int q3r, int q3c) {
   if ((m0 | m1) == 0) return 0xffffu;
-  const int br = (NO == 2 ? q4r * 5 + q3r : q3r) * 4, bc = (NO == 2 ? q4c * 5 + q3c : q3c) * 4;
-  unsigned lr = 0, lc = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    lr |= (prefix_live(m0, m1, br + q) ? 1u : 0u) << q;
-    lc |= (prefix_live(m0, m1, bc + q) ? 1u : 0u) << q;
-  }
-  unsigned live = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q)
-    if ((lr >> q) & 1u) live |= lc << (4 * q);
-  return live;
+  return nibble_live(prefix_nibble(m0, m1, NO == 2 ? q4r * 5 + q3r : q3r),
+                     prefix_nibble(m0, m1, NO == 2 ? q4c * 5 + q3c : q3c));
 }
 
 // Stores of the live quads only, without a branch per quad (branches
@@ -76,29 +101,17 @@ __device__ __forceinline__ void drop_store(__amdgpu_buffer_rsrc_t r, unsigned of
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, (int)off, 0, 0);
 }
 
-__device__ __forceinline__ void drop_store1(__amdgpu_buffer_rsrc_t r, unsigned off, float v) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, 0, 0);
+// soff: a wave-uniform byte offset added to off (kDrop + soff stays past
+// every span: the host keeps spans and soff below 2^30)
+__device__ __forceinline__ void drop_store1(__amdgpu_buffer_rsrc_t r, unsigned off, float v,
+                                            unsigned soff = 0) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, (int)soff, 0);
 }
 
 // How a transform stores its points: every quad of a live branch, the live
 // quads only (quad layout), or the live points of the live groups in the
 // planar layout (nwg_plan_info::mix_planar).
 enum { kStoreAll = 0, kStoreMasked = 1, kStorePlanar = 2 };
-
-// Rank of axis prefix i among the live prefixes (the live ones below it),
-// branch-free over the four 32-bit words (a 64-bit shift by a lane-varying
-// amount became control flow that stopped the transforms' unrolling).
-__device__ __forceinline__ int prefix_rank(unsigned long long m0, unsigned long long m1, int i) {
-  const unsigned wd[4] = {(unsigned)m0, (unsigned)(m0 >> 32), (unsigned)m1, (unsigned)(m1 >> 32)};
-  int r = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int k = i - 32 * q;
-    const unsigned below = k <= 0 ? 0u : (k >= 32 ? 0xffffffffu : (1u << k) - 1u);
-    r += __popc(wd[q] & below);
-  }
-  return r;
-}
 
 // Whether quad q2r * 16 + q2c * 4 + q1r of a branch with live-group mask
 // live is stored.
@@ -231,8 +244,8 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
     // kStorePlanar: groups at their live-list places; the wave's resource
     // starts at the lowest row-prefix block (q4r, q3r) of its four branches,
     // and a group's place is at most 20 live row prefixes above it
-    unsigned irp = 0, icp = 0;                // ranks of the 4 row / column prefixes, 8 bits each
-    int lbase = 0, np = 0;
+    unsigned nr = 0, nc = 0;                  // live nibbles of the row / column prefixes
+    int lbase = 0, np = 0, r0 = 0, c0 = 0;     // ranks of the first row / column prefix
     __amdgpu_buffer_rsrc_t pr = rs;
     if constexpr (STORE == kStorePlanar) {
       np = __popcll(m0) + __popcll(m1);
@@ -244,11 +257,10 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
         if (bi < NB && si < smin) smin = si;
       }
       lbase = prefix_rank(m0, m1, smin) * np;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        irp |= (unsigned)prefix_rank(m0, m1, (q4r * 5 + q3r) * 4 + q) << (8 * q);
-        icp |= (unsigned)prefix_rank(m0, m1, (q4c * 5 + q3c) * 4 + q) << (8 * q);
-      }
+      nr = prefix_nibble(m0, m1, q4r * 5 + q3r);
+      nc = prefix_nibble(m0, m1, q4c * 5 + q3c);
+      r0 = prefix_rank(m0, m1, (q4r * 5 + q3r) * 4);
+      c0 = prefix_rank(m0, m1, (q4c * 5 + q3c) * 4);
       pr = span_rsrc(reinterpret_cast<float4*>(U + (size_t)lbase * 9 * MN + (size_t)m * N + n0),
                      (unsigned)(20 * np * 9 * MN * 4));
     }
@@ -275,9 +287,11 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
         const float4 v = make_float4(o[q2c * 4 + 0], o[q2c * 4 + 1], o[q2c * 4 + 2], o[q2c * 4 + 3]);
         if constexpr (STORE == kStorePlanar) {
           const bool on = (live >> (quad >> 2)) & 1u;
-          const int ir = (irp >> (8 * q2r)) & 0xff, ic = (icp >> (8 * q2c)) & 0xff;
+          const int ir = r0 + __popc(nr & ((1u << q2r) - 1u));
+          const int ic = c0 + __popc(nc & ((1u << q2c) - 1u));
           const unsigned rel = (unsigned)((ir * np + ic - lbase) * 9 + 3 * q1r);
-          const unsigned o0 = (unsigned)(rel * MN + cl) * 4u, ps = (unsigned)MN * 4u;
+          const unsigned ps = (unsigned)MN * 4u;
+          const unsigned o0 = (unsigned)(rel * MN + cl) * 4u;
           drop_store1(pr, on ? o0 : kDrop, v.x);
           drop_store1(pr, on ? o0 + ps : kDrop, v.y);
           drop_store1(pr, on ? o0 + 2 * ps : kDrop, v.z);
@@ -525,22 +539,23 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
                                                         (size_t)lbase * 9 * plane +
                                                         (size_t)m * T + t0),
                               (unsigned)(20 * np * 9 * plane * 4));
-    unsigned irp = 0, icp = 0;                // ranks of the 4 row / column prefixes, 8 bits each
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      irp |= (unsigned)prefix_rank(m0, m1, (q4r * 5 + q3r) * 4 + q) << (8 * q);
-      icp |= (unsigned)prefix_rank(m0, m1, (q4c * 5 + q3c) * 4 + q) << (8 * q);
-    }
+    // ranks of the branch's first row and column prefixes; the other three
+    // follow from the live nibbles
+    const int br = q4r * 5 + q3r, bc = q4c * 5 + q3c;
+    const unsigned nr = prefix_nibble(m0, m1, br), nc = prefix_nibble(m0, m1, bc);
+    const int r0 = prefix_rank(m0, m1, 4 * br), c0 = prefix_rank(m0, m1, 4 * bc);
     const unsigned ps = (unsigned)plane * 4u;
+    // byte offset of group (q2r, q2c)'s first point plane, for this lane
+    const unsigned gbase = (unsigned)(((r0 * np + c0 - lbase) * 9) * plane) * 4u + (unsigned)tl * 4u;
     inner2_xform<false, true>(S, [=](int quad, float4 v) {
       const int q2r = quad >> 4, q2c = (quad >> 2) & 3, q1r = quad & 3;
       const bool on = (live >> (quad >> 2)) & 1u;
-      const int ir = (irp >> (8 * q2r)) & 0xff, ic = (icp >> (8 * q2c)) & 0xff;
-      const unsigned rel = (unsigned)((ir * np + ic - lbase) * 9 + 3 * q1r);
-      const unsigned o0 = rel * ps + (unsigned)tl * 4u;
-      drop_store1(pr, on ? o0 : kDrop, v.x);
-      drop_store1(pr, on ? o0 + ps : kDrop, v.y);
-      drop_store1(pr, on ? o0 + 2 * ps : kDrop, v.z);
+      const int ir = __popc(nr & ((1u << q2r) - 1u)), ic = __popc(nc & ((1u << q2c) - 1u));
+      const unsigned o0 = gbase + (unsigned)((ir * np + ic) * 9 + 3 * q1r) * ps;
+      const unsigned off = on ? o0 : kDrop;
+      drop_store1(pr, off, v.x);
+      drop_store1(pr, off, v.y, ps);
+      drop_store1(pr, off, v.z, 2 * ps);
     });
   } else if constexpr (STORE == kStoreMasked) {
     // the wave's 64 / TPW consecutive slots share a resource
