@@ -68,12 +68,6 @@ __device__ __forceinline__ long long live_group(const GroupMap& m, long long i) 
   return g;
 }
 
-// Whether prefix i of an axis is live (every prefix when the masks are 0).
-__device__ __forceinline__ bool prefix_live(unsigned long long m0, unsigned long long m1, int i) {
-  if ((m0 | m1) == 0) return true;
-  return ((i < 64 ? m0 >> i : m1 >> (i - 64)) & 1ULL) != 0;
-}
-
 // Wait until at most N vector-memory loads of this wavefront are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
