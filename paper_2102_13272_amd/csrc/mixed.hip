@@ -648,16 +648,23 @@ __global__ __launch_bounds__(64) void output_xform_mix23(const float4* __restric
 // work-group-uniform test), level2_reduce gives the branch's 4 x 4 block and
 // the thread accumulates its own 4 x 4 output block.  Nine times the threads
 // of a (tile, channel) split (the 144 accumulators of output_xform_mix23 leave
-// one wavefront per CU on layers of a few hundred tiles).
+// one wavefront per CU on layers of a few hundred tiles).  A block's
+// branches overlap its neighbours' (each Z value is read by up to nine
+// blocks), so the work-groups are numbered per XCD (xcd_remap), tile block
+// fastest, then output block, then channel: the 9 ntb work-groups of a
+// channel run together on one XCD and share its Z through that XCD's L2.
 __global__ __launch_bounds__(64) void output_xform_mix3(const float4* __restrict__ Z,
                                                         float* __restrict__ y, int N, int Ho,
                                                         int Wo, int th, int tw, int T,
                                                         long long gstride, unsigned long long m0,
                                                         unsigned long long m1) {
-  const int t = blockIdx.x * 64 + threadIdx.x;
-  const int blk = blockIdx.y;               // 3 i3r + i3c
-  const int n = blockIdx.z;
-  if (t >= T) return;
+  const int ntb = (T + 63) / 64;
+  const long long lid = xcd_remap(blockIdx.x, gridDim.x);
+  const int tb = (int)(lid % ntb);
+  const int blk = (int)((lid / ntb) % 9);   // 3 i3r + i3c
+  const int n = (int)(lid / (9LL * ntb));
+  const int t = tb * 64 + threadIdx.x;
+  if (t >= T || n >= N) return;
   const int i3r = blk / 3, i3c = blk - 3 * i3r;
   float acc[16];
 #pragma unroll
@@ -819,7 +826,9 @@ hipError_t launch_output_xform_mix(const nwg_plan_info& g, const float* Zf, floa
   const long long gstride = (long long)g.N * g.T;
   const unsigned tb = (unsigned)((g.T + 63) / 64);
   if (no == 1) {
-    hipLaunchKernelGGL(output_xform_mix3, dim3(tb, 9, (unsigned)g.N), dim3(64), 0, s, Z, y, g.N,
+    const long long nwg = 9LL * tb * g.N;
+    if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(output_xform_mix3, dim3((unsigned)nwg), dim3(64), 0, s, Z, y, g.N,
                        g.Ho, g.Wo, g.th, g.tw, (int)g.T, gstride, g.live_prefix[0],
                        g.live_prefix[1]);
     return hipGetLastError();
