@@ -398,6 +398,14 @@ def run_workload(torch, nwg, name: str, tile: str, precision: str, steps: int, w
                          "TFLOP_s": round(tfs, 2),
                          "mfma_frac": round(flop_x * tfs / peak_mm, 4),
                          "per_layer": st["per_layer"]}
+        # the bytes the stage's kernels really move (committed counter
+        # summary of the same sources and tile), at this run's stage time:
+        # scratch round trips and re-reads count here, not in GB_s
+        tb = measured_traffic(name, sname, tile) if len(plans) == 1 and not split else None
+        if tb is not None:
+            tgbs = tb * st["launches"] / sec / 1e9
+            detail[sname]["traffic_GB_s"] = round(tgbs, 1)
+            detail[sname]["traffic_hbm_frac"] = round(tgbs / PEAK_HBM_GBS, 4)
 
     # dominant kernel: largest time share of the step
     dom = max(stages, key=lambda k: stages[k]["ms_total"])
@@ -551,7 +559,8 @@ def main():
             "ms_per_step": round(r2["ms_step"], 4), "value": round(r2["value"], 3),
             "roofline": {k: r2["roofline"][k] for k in ("bound", "frac", "kernel")},
             "stages": {k: {f: v[f] for f in ("ms_per_step", "GB_s", "hbm_frac", "TFLOP_s",
-                                              "mfma_frac")}
+                                              "mfma_frac", "traffic_GB_s", "traffic_hbm_frac")
+                           if f in v}
                        for k, v in r2["stages"].items()},
             "kernel_transform": kernel_transform_entry(r2["kx_ms"], r2["kx_bytes"])}
         y_f23 = r2["y"]
@@ -582,7 +591,8 @@ def main():
                                           "kernel", "avg_launch_us", "traffic",
                                           "traffic_source")},
                    "stages": {k: {f: v[f] for f in ("ms_per_step", "GB_s", "hbm_frac",
-                                                     "TFLOP_s", "mfma_frac")}
+                                                     "TFLOP_s", "mfma_frac", "traffic_GB_s",
+                                                     "traffic_hbm_frac") if f in v}
                               for k, v in rk["stages"].items()},
                    "kernel_transform": kernel_transform_entry(rk["kx_ms"], rk["kx_bytes"])}
             y_k = rk["y"]
