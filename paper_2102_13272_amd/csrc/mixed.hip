@@ -308,31 +308,33 @@ __global__ __launch_bounds__(512) void kernel_xform_mix(const float* __restrict_
 // Planar plans (depth 4, level-1 digit 3 dead): the same transform with the
 // outer column fold shared.  The fold of a kernel row over the column digits
 // (k4c, k3c) depends on the column branch (q4c, q3c) only, so per column
-// branch the work-group first folds every row of its 16 kernels into
+// branch the work-group first folds every row of its NW kernels into
 // C[row tap][column inner digits] in LDS (one thread per (channel, row)),
 // and then one thread per (channel, row branch (q4r, q3r)) folds C's rows
 // into the 9 x 9 sub-kernel and runs the two F(2,3) levels as above: the
 // column fold is computed once per column branch instead of once per outer
-// branch.  U [live group][3 q1r + q1c][M][N].
-constexpr int kKX = 39;                      // padded taps per axis at depth 4
-constexpr int kKXP = 40;                     // LDS row of w (16-byte aligned rows)
-constexpr int kCP = 12;                      // LDS row of C (9 used, 16-byte aligned)
-__global__ __launch_bounds__(512) void kernel_xform_mix_sep(const float* __restrict__ w,
-                                                            float* __restrict__ U, int M, int N,
-                                                            int r, unsigned long long m0,
-                                                            unsigned long long m1) {
+// branch.  NW output channels per work-group (32 when their r x r kernels
+// fit in LDS, r <= 31): a wavefront's lanes store U in NW-float runs.
+// U [live group][3 q1r + q1c][M][N].
+template <int NW>
+__global__ __launch_bounds__(NW * 32) void kernel_xform_mix_sep(const float* __restrict__ w,
+                                                                float* __restrict__ U, int M,
+                                                                int N, int r,
+                                                                unsigned long long m0,
+                                                                unsigned long long m1) {
+  constexpr int NT = NW * 32;                // threads
+  constexpr int RB = 64 / NW;                // row branches per wavefront
   extern __shared__ float sm[];
-  float* wl = sm;                            // [16][kKX][kKXP], zero past r
-  float* cl = sm + 16 * kKX * kKXP;          // [16][kKX][kCP], rows >= r stay zero
+  float* wl = sm;                            // [NW][r][r]
+  float* cl = sm + NW * r * r;               // [NW][r][9]
   const int m = blockIdx.y;
-  const int n0 = blockIdx.x * 16;
-  for (int e = threadIdx.x; e < 16 * kKX * kKXP; e += 512) {
-    const int c = e / (kKX * kKXP), k = e - c * (kKX * kKXP);
-    const int u = k / kKXP, v = k - u * kKXP;
+  const int n0 = blockIdx.x * NW;
+  const int rr = r * r;
+  for (int e = threadIdx.x; e < NW * rr; e += NT) {
+    const int c = e / rr;
     const int nn = n0 + c;
-    wl[e] = (nn < N && u < r && v < r) ? w[((size_t)nn * M + m) * r * r + u * r + v] : 0.0f;
+    wl[e] = nn < N ? w[((size_t)nn * M + m) * rr + (e - c * rr)] : 0.0f;
   }
-  for (int e = threadIdx.x; e < 16 * kKX * kCP; e += 512) cl[e] = 0.0f;
   __syncthreads();
   const int np = __popcll(m0) + __popcll(m1);
   const size_t MN = (size_t)M * N;
@@ -343,12 +345,13 @@ __global__ __launch_bounds__(512) void kernel_xform_mix_sep(const float* __restr
     const unsigned nc = prefix_nibble(m0, m1, q4c * 5 + q3c);
     if ((m0 | m1) != 0 && nc == 0) continue;   // no live group in this column branch
     // C[c][tr][ic] = sum over (k4c, k3c) of G rows (q4c, q3c) times w[tr][tap]
+    // (taps >= r are the kernel's zero padding)
     float c4c[3], c3c[3];
     g5_row(q4c, c4c);
     g5_row(q3c, c3c);
-    for (int task = threadIdx.x; task < 16 * r; task += 512) {
+    for (int task = threadIdx.x; task < NW * r; task += NT) {
       const int c = task / r, tr = task - c * r;
-      const float* wr = wl + (c * kKX + tr) * kKXP;
+      const float* wr = wl + (c * r + tr) * r;
       float cv[9];
 #pragma unroll
       for (int ic = 0; ic < 9; ++ic) cv[ic] = 0.0f;
@@ -361,20 +364,20 @@ __global__ __launch_bounds__(512) void kernel_xform_mix_sep(const float* __restr
           for (int ic = 0; ic < 9; ++ic) {
             const int tc = mix_tap<2>(b4, b3, ic / 3, ic % 3);
             if (tc < 0) continue;
-            cv[ic] = fmaf(cc, wr[tc], cv[ic]);
+            if (tc < r) cv[ic] = fmaf(cc, wr[tc], cv[ic]);
           }
         }
-      float* cr = cl + (c * kKX + tr) * kCP;
+      float* cr = cl + (c * r + tr) * 9;
 #pragma unroll
       for (int ic = 0; ic < 9; ++ic) cr[ic] = cv[ic];
     }
     __syncthreads();
     // one thread per (channel, row branch): lanes on channels, so that the
-    // 16 lanes of a row branch store 64 contiguous bytes
-    for (int task = threadIdx.x; task < 16 * 25; task += 512) {
-      const int cl16 = task & 15, br = task >> 4;    // br = 5 q4r + q3r
+    // NW lanes of a row branch store NW contiguous floats
+    for (int task = threadIdx.x; task < NW * 25; task += NT) {
+      const int cln = task % NW, br = task / NW;    // br = 5 q4r + q3r
       const int q4r = br / 5, q3r = br - 5 * q4r;
-      const int nn = n0 + cl16;
+      const int nn = n0 + cln;
       const unsigned live = branch_live<2>(m0, m1, q4r, q4c, q3r, q3c);
       if (nn >= N || live == 0) continue;
       float c4r[3], c3r[3];
@@ -385,7 +388,7 @@ __global__ __launch_bounds__(512) void kernel_xform_mix_sep(const float* __restr
       for (int i = 0; i < 9; ++i)
 #pragma unroll
         for (int j = 0; j < 9; ++j) S[i][j] = 0.0f;
-      const float* cb = cl + cl16 * kKX * kCP;
+      const float* cb = cl + cln * r * 9;
 #pragma unroll
       for (int a4 = 0; a4 < 3; ++a4)
 #pragma unroll
@@ -394,21 +397,17 @@ __global__ __launch_bounds__(512) void kernel_xform_mix_sep(const float* __restr
 #pragma unroll
           for (int ir = 0; ir < 9; ++ir) {
             const int tr = mix_tap<2>(a4, a3, ir / 3, ir % 3);
-            if (tr < 0) continue;
-            const float4 x0 = *reinterpret_cast<const float4*>(cb + tr * kCP);
-            const float4 x1 = *reinterpret_cast<const float4*>(cb + tr * kCP + 4);
-            const float x8 = cb[tr * kCP + 8];
-            const float cv[9] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w, x8};
+            if (tr < 0 || tr >= r) continue;   // rows >= r: zero padding
+            const float* cv = cb + tr * 9;
 #pragma unroll
             for (int ic = 0; ic < 9; ++ic) S[ir][ic] = fmaf(crr, cv[ic], S[ir][ic]);
           }
         }
-      // planar places: the wave's four row branches (readfirstlane of the
+      // planar places: the wave's RB row branches (readfirstlane of the
       // lowest) share a resource from the lowest row-prefix block; a
       // group's place is at most 20 live row prefixes above it
-      const int br0 = __builtin_amdgcn_readfirstlane(br & ~3);
-      const int smin = ((br0 / 5) * 5 + br0 % 5) * 4;
-      const int lbase = prefix_rank(m0, m1, smin) * np;
+      const int br0 = __builtin_amdgcn_readfirstlane(br & ~(RB - 1));
+      const int lbase = prefix_rank(m0, m1, br0 * 4) * np;
       const unsigned nr = prefix_nibble(m0, m1, q4r * 5 + q3r);
       const int r0 = prefix_rank(m0, m1, (q4r * 5 + q3r) * 4);
       const int c0 = prefix_rank(m0, m1, (q4c * 5 + q3c) * 4);
@@ -438,7 +437,7 @@ __global__ __launch_bounds__(512) void kernel_xform_mix_sep(const float* __restr
           const int ir = r0 + __popc(nr & ((1u << q2r) - 1u));
           const int ic = c0 + __popc(nc & ((1u << q2c) - 1u));
           const unsigned rel = (unsigned)((ir * np + ic - lbase) * 9 + 3 * q1r);
-          const unsigned o0 = (unsigned)(rel * MN + cl16) * 4u;
+          const unsigned o0 = (unsigned)(rel * MN + cln) * 4u;
           drop_store1(pr, on ? o0 : kDrop, o[q2c * 4 + 0]);
           drop_store1(pr, on ? o0 + ps : kDrop, o[q2c * 4 + 1]);
           drop_store1(pr, on ? o0 + 2 * ps : kDrop, o[q2c * 4 + 2]);
@@ -911,13 +910,18 @@ hipError_t launch_kernel_xform_mix(const nwg_plan_info& g, const float* w, float
   const bool mask = ((g.live_prefix[0] | g.live_prefix[1]) != 0 || q3) &&
                     4LL * 64 * g.M * g.N * 16 < (long long)kDrop;
   if (g.mix_planar) {
-    if (no != 2) return hipErrorInvalidValue;
-    const size_t ldsp = (size_t)16 * kKX * (kKXP + kCP) * sizeof(float);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&kernel_xform_mix_sep),
+    // 32 output channels per work-group when their kernels and C fit in LDS
+    if (no != 2 || g.r > 39) return hipErrorInvalidValue;
+    const auto lds_of = [&](int nw) { return (size_t)nw * (g.r * g.r + 9 * g.r) * sizeof(float); };
+    const bool wide = g.N % 32 == 0 && lds_of(32) <= 160 * 1024;
+    const int nw = wide ? 32 : 16;
+    const size_t ldsp = lds_of(nw);
+    const auto fk = wide ? &kernel_xform_mix_sep<32> : &kernel_xform_mix_sep<16>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fk),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)ldsp);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kernel_xform_mix_sep, grid, dim3(512), ldsp, s, w, U, g.M, g.N, g.r,
-                       g.live_prefix[0], g.live_prefix[1]);
+    hipLaunchKernelGGL(fk, dim3((unsigned)((g.N + nw - 1) / nw), (unsigned)g.M), dim3(nw * 32),
+                       ldsp, s, w, U, g.M, g.N, g.r, g.live_prefix[0], g.live_prefix[1]);
     return hipGetLastError();
   }
   const auto fn = no == 2 ? (mask ? &kernel_xform_mix<2, kStoreMasked>

@@ -187,7 +187,8 @@ def test_mixed_stages_match_cpu_oracle_chain(case):
 # N % 128, T % 64): one 36 x 36 tile per image, T = 64 or 128, 128 x 64
 # blocks in one or two rows, r = 31, 27 and 23
 PLANAR = [(64, 128, 128, 36, 36, 31, 15), (64, 128, 256, 36, 36, 31, 15),
-          (128, 128, 128, 36, 36, 23, 11), (16, 128, 128, 72, 72, 27, 13)]
+          (128, 128, 128, 36, 36, 23, 11), (16, 128, 128, 72, 72, 27, 13),
+          (64, 128, 128, 36, 36, 35, 17)]
 
 
 @pytest.mark.parametrize("case", PLANAR, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
@@ -262,6 +263,37 @@ def test_mixed_planar_stages_sampled():
                     zr[..., 2 * i1r + i1c] += AT[i1r, q1r] * AT[i1c, q1c] * prod[p]
         assert_close(Zh[planar_group_index(i, li)], zr, rel_tol=1e-5, abs_frac=1e-5,
                      what=f"Z group {li}")
+
+
+@pytest.mark.parametrize("r,N", [(17, 128), (31, 256), (32, 128), (35, 128), (38, 128)])
+def test_mixed_planar_kernel_transform_matches_oracle(r, N):
+    """The planar kernel transform at both of its work-group widths (32
+    output channels when their kernels fit in LDS, r <= 31; 16 above): every
+    place of U written, and U at every live point for sampled (n, m) against
+    the oracle's kernel matrix."""
+    B, M, H = 64, 128, 36
+    pad = (r - 1) // 2
+    rng = np.random.default_rng(r * 1000 + N)
+    w = (rng.standard_normal((N, M, r, r)) / np.sqrt(M * r * r)).astype(np.float32)
+    lv = mixed_levels(mixed_chain(), r)
+    KG = np.asarray(kernel_matrix(lv), dtype=np.float64)
+    print(f"mixed planar kernel transform r={r} N={N}", flush=True)
+    with nwg.Plan(B, M, N, H, H, r, pad, tile=MIX) as plan:
+        i = plan.info
+        assert i["mix_planar"] == 1
+        rows, cols = planar_points(i)
+        U = torch.full(plan.u_shape, float("nan"), device="cuda")
+        plan.kernel_transform(dev(w), U)
+        torch.cuda.synchronize()
+        Uh = U.cpu().numpy()
+        del U
+    assert np.isfinite(Uh).all()
+    for n, m in [(0, 0), (N - 1, M - 1), (31, 5), (32, 77), (N // 2 + 15, 64)]:
+        wp = np.zeros((lv.Kn, lv.Kn))
+        wp[:r, :r] = w[n, m]
+        Uo = KG @ wp @ KG.T
+        assert_close(Uh[:, :, m, n], Uo[rows, cols], rel_tol=1e-6, abs_frac=1e-6,
+                     what=f"U r={r} n={n} m={m}")
 
 
 def test_mixed_plan_rejects_what_it_does_not_serve():
