@@ -463,12 +463,15 @@ constexpr int kL3 = kMixL3;                 // window side left for levels 1..3
 // start on 32 different even banks
 constexpr int kWS = kL3 * kL3 + 2;
 
+// BS = 26 keeps every level-3 input row and column; BS = 25 (planar plans,
+// level-1 digit 3 dead) drops row and column 25, which no live point reads.
+template <int BS>
 __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
                                                     float* __restrict__ X4, int M, int H, int W,
                                                     int pad, int th, int tw, int T) {
   // work-group (tile t, channel m): the 74 x 74 window, then per level-4
-  // row branch the B^T along the rows (26 x 74), then along the columns (5
-  // branches of 26 x 26), separably through LDS
+  // row branch the B^T along the rows (BS x 74), then along the columns (5
+  // branches of BS x BS), separably through LDS
   constexpr int LW = 74, LS = 75;           // window side, odd LDS stride
   __shared__ float win[LW * LS];
   __shared__ float rw[kL3 * LS];
@@ -502,12 +505,12 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
   // one level-4 row branch at a time, so that rw holds 26 rows: 30 KB of LDS
   // in all, five work-groups per CU to hide the window loads (0.17 -> 0.14
   // ms on the 31 x 31 layer against all five row branches at once)
-  const size_t bstride = (size_t)M * T * kL3 * kL3;   // between level-4 branches
-  float* __restrict__ dst = X4 + ((size_t)m * T + t) * kL3 * kL3;
+  const size_t bstride = (size_t)M * T * BS * BS;     // between level-4 branches
+  float* __restrict__ dst = X4 + ((size_t)m * T + t) * BS * BS;
 #pragma unroll
   for (int q4r = 0; q4r < 5; ++q4r) {
     // rows: rw[i][c] = sum_a B^T[q4r][a] win[i + 12 a][c]
-    for (int e = threadIdx.x; e < kL3 * LW; e += 256) {
+    for (int e = threadIdx.x; e < BS * LW; e += 256) {
       const int i = e / LW, c = e - i * LW;
       float sacc = 0.0f;
 #pragma unroll
@@ -517,8 +520,8 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
     }
     __syncthreads();
     // columns: X4[5 q4r + q4c][m][t][i][j] = sum_b B^T[q4c][b] rw[i][j + 12 b]
-    for (int k = threadIdx.x; k < kL3 * kL3; k += 256) {
-      const int i = k / kL3, j = k - i * kL3;
+    for (int k = threadIdx.x; k < BS * BS; k += 256) {
+      const int i = k / BS, j = k - i * BS;
       float v[5];
 #pragma unroll
       for (int bb = 0; bb < 5; ++bb) v[bb] = rw[i * LS + j + kStride4 * bb];
@@ -532,6 +535,127 @@ __global__ __launch_bounds__(256) void input_mix_l4(const float* __restrict__ x,
       }
     }
     if (q4r < 4) __syncthreads();             // rw is rewritten next
+  }
+}
+
+// One level-3 branch (slot = 5 q3r + q3c under level-4 branch q4) of one
+// tile (lane tl of a TPW-tile chunk starting at t0, channel m): its level-3
+// block win in LDS (rows ROW floats apart) -> the branch's points of V.
+template <int NO, int STORE, bool Q3, int TPW, int ROW>
+__device__ __forceinline__ void mix_branch(const float* win, int slot, int q4, int m, int t0,
+                                           int tl, float4* __restrict__ V, int M, int T,
+                                           long long qstride, unsigned long long m0,
+                                           unsigned long long m1, int q3) {
+  const int t = t0 + tl;
+  // a row of B^T of F(3,3) has its nonzero taps among 4 consecutive ones,
+  // from tap 0 for row 0 and from tap 1 otherwise
+  const int q3r = slot / 5, q3c = slot - 5 * q3r;
+  // V of the groups no real tap reaches is neither computed nor stored
+  const unsigned live = branch_live<NO>(m0, m1, q4 / 5, q4 % 5, q3r, q3c);
+  if (live == 0) return;
+  const int lr = q3r == 0 ? 0 : 1, lc = q3c == 0 ? 0 : 1;
+  float ca5[5], cb5[5], ca[4], cb[4];
+  bt5_row(q3r, ca5);
+  bt5_row(q3c, cb5);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    ca[u] = lr ? ca5[u + 1] : ca5[u];
+    cb[u] = lc ? cb5[u + 1] : cb5[u];
+    if constexpr (TPW == 64) {
+      // one branch per wavefront: the coefficients are uniform, keep them
+      // in scalar registers
+      ca[u] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(ca[u])));
+      cb[u] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(cb[u])));
+    }
+  }
+  // level 3 (stride 4): per output row, the rows' taps over the 22 columns
+  // the column taps need (from column 4 lc), read as float2, then the
+  // columns' taps
+  const float* wb = win + kStride3 * lr * ROW + kStride3 * lc;
+  // Q3 (level-1 digit 3 dead): the inner transform reads S[0..8][0..8], so
+  // the column taps reach columns 4 lc .. 4 lc + 20 (NC = 21) of the block
+  constexpr int NS = Q3 ? 9 : 10, NC = NS + 3 * kStride3;
+  float S[10][10];
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    float tr[22];
+#pragma unroll
+    for (int c = 0; c < 22; c += 2) {
+      float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float* p = wb + (i + kStride3 * u) * ROW + c;
+        float2 v;
+        if constexpr (ROW % 2 == 0) {
+          v = *reinterpret_cast<const float2*>(p);
+        } else {
+          v.x = p[0];                       // odd rows: pairs not 8-byte aligned
+          v.y = c + 1 < NC ? p[1] : 0.0f;   // (a 25-wide block has no column 25)
+        }
+        s0 = fmaf(ca[u], v.x, s0);
+        s1 = fmaf(ca[u], v.y, s1);
+      }
+      tr[c] = s0;
+      tr[c + 1] = s1;
+    }
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+      float sacc = 0.0f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sacc = fmaf(cb[u], tr[j + kStride3 * u], sacc);
+      S[i][j] = sacc;
+    }
+    // one output row at a time: keeps the row's LDS reads from being
+    // hoisted across rows (register pressure); with level-1 digit 3 dead the
+    // kernel has the registers to let them overlap (0.714 -> 0.672 ms for
+    // the stage on the 31 x 31 layer)
+    if constexpr (!Q3) __builtin_amdgcn_sched_barrier(0);
+  }
+  const int ob = q4 * 25 + slot;
+  if constexpr (STORE == kStorePlanar) {
+    static_assert(NO == 2 && Q3, "planar V: depth 4, level-1 digit 3 dead");
+    // groups at their live-list places; the work-group's resource starts at
+    // its level-4 row block (q4r), 20 row prefixes
+    const int np = __popcll(m0) + __popcll(m1);
+    const int q4r = q4 / 5, q4c = q4 - 5 * q4r;
+    const int lbase = prefix_rank(m0, m1, q4r * 20) * np;
+    const size_t plane = (size_t)M * T;
+    const auto pr = span_rsrc(reinterpret_cast<float4*>(reinterpret_cast<float*>(V) +
+                                                        (size_t)lbase * 9 * plane +
+                                                        (size_t)m * T + t0),
+                              (unsigned)(20 * np * 9 * plane * 4));
+    // ranks of the branch's first row and column prefixes; the other three
+    // follow from the live nibbles
+    const int br = q4r * 5 + q3r, bc = q4c * 5 + q3c;
+    const unsigned nr = prefix_nibble(m0, m1, br), nc = prefix_nibble(m0, m1, bc);
+    const int r0 = prefix_rank(m0, m1, 4 * br), c0 = prefix_rank(m0, m1, 4 * bc);
+    const unsigned ps = (unsigned)plane * 4u;
+    // byte offset of group (q2r, q2c)'s first point plane, for this lane
+    const unsigned gbase = (unsigned)(((r0 * np + c0 - lbase) * 9) * plane) * 4u + (unsigned)tl * 4u;
+    inner2_xform<false, true>(S, [=](int quad, float4 v) {
+      const int q2r = quad >> 4, q2c = (quad >> 2) & 3, q1r = quad & 3;
+      const bool on = (live >> (quad >> 2)) & 1u;
+      const int ir = __popc(nr & ((1u << q2r) - 1u)), ic = __popc(nc & ((1u << q2c) - 1u));
+      const unsigned o0 = gbase + (unsigned)((ir * np + ic) * 9 + 3 * q1r) * ps;
+      const unsigned off = on ? o0 : kDrop;
+      drop_store1(pr, off, v.x);
+      drop_store1(pr, off, v.y, ps);
+      drop_store1(pr, off, v.z, 2 * ps);
+    });
+  } else if constexpr (STORE == kStoreMasked) {
+    // the wave's 64 / TPW consecutive slots share a resource
+    constexpr int SPW = 64 / TPW;
+    const int slot0 = __builtin_amdgcn_readfirstlane(slot & ~(SPW - 1));
+    const auto rs = span_rsrc(V + (size_t)(q4 * 25 + slot0) * 64 * qstride + (size_t)m * T + t0,
+                              (unsigned)(SPW * 64 * qstride * 16));
+    const unsigned lane0 = (unsigned)(((size_t)(slot - slot0) * 64 * qstride + tl) * 16);
+    inner2_xform<false, Q3>(S, [&](int quad, float4 v) {
+      drop_store(rs, quad_live(live, q3, quad) ? lane0 + (unsigned)(quad * qstride * 16) : kDrop,
+                 v);
+    });
+  } else {
+    float4* vb = V + (size_t)ob * 64 * qstride + (size_t)m * T + t;
+    inner2_xform<false, Q3>(S, [&](int quad, float4 v) { vb[(size_t)quad * qstride] = v; });
   }
 }
 
@@ -621,103 +745,49 @@ __global__ __launch_bounds__(NO == 2 ? 512 : 256) __attribute__((amdgpu_waves_pe
   if (t >= T) return;                       // no barrier below
   const float* win = lds + tl * kWS;
   for (int slot = threadIdx.x / TPW; slot < 25; slot += 16) {   // slot = 5 q3r + q3c
-  // a row of B^T of F(3,3) has its nonzero taps among 4 consecutive ones,
-  // from tap 0 for row 0 and from tap 1 otherwise
-  const int q3r = slot / 5, q3c = slot - 5 * q3r;
-  // V of the groups no real tap reaches is neither computed nor stored
-  const unsigned live = branch_live<NO>(m0, m1, q4 / 5, q4 % 5, q3r, q3c);
-  if (live == 0) continue;
-  const int lr = q3r == 0 ? 0 : 1, lc = q3c == 0 ? 0 : 1;
-  float ca5[5], cb5[5], ca[4], cb[4];
-  bt5_row(q3r, ca5);
-  bt5_row(q3c, cb5);
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    ca[u] = lr ? ca5[u + 1] : ca5[u];
-    cb[u] = lc ? cb5[u + 1] : cb5[u];
+    mix_branch<NO, STORE, Q3, TPW, kL3>(win, slot, q4, m, t0, tl, V, M, T, qstride, m0, m1, q3);
   }
-  // level 3 (stride 4): per output row, the rows' taps over the 22 columns
-  // the column taps need (from column 4 lc), read as float2, then the
-  // columns' taps
-  const float* wb = win + kStride3 * lr * kL3 + kStride3 * lc;
-  // Q3 (level-1 digit 3 dead): the inner transform reads S[0..8][0..8]
-  constexpr int NS = Q3 ? 9 : 10;
-  float S[10][10];
-#pragma unroll
-  for (int i = 0; i < NS; ++i) {
-    float tr[22];
-#pragma unroll
-    for (int c = 0; c < 22; c += 2) {
-      float s0 = 0.0f, s1 = 0.0f;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float2 v = *reinterpret_cast<const float2*>(wb + (i + kStride3 * u) * kL3 + c);
-        s0 = fmaf(ca[u], v.x, s0);
-        s1 = fmaf(ca[u], v.y, s1);
-      }
-      tr[c] = s0;
-      tr[c + 1] = s1;
+}
+
+// Planar plans (depth 4, level-1 digit 3 dead, T a multiple of 64): 64 tiles
+// per work-group, one wavefront per level-3 branch at a time (its lanes on
+// the 64 tiles), so every V store of a wavefront writes 256 contiguous
+// bytes and the branch's B^T coefficients are uniform.  The 64 tiles' X4
+// blocks are kept 25 x 25 (input_mix_l4<kPB>), one contiguous 160 KB run
+// that direct global->LDS loads copy as is.  Work-group -> (64-tile chunk,
+// channel m, level-4 branch q4), the chunk fastest.
+constexpr int kPB = kL3 - 1, kPKB = kPB * kPB;   // planar X4 block side, floats
+constexpr int kPT = 64;                          // tiles per work-group
+constexpr int kPRun4 = kPT * kPKB / 4;           // float4 of a work-group's X4 run
+constexpr int kPBlk = (kPRun4 + 63) / 64;        // 64-lane load blocks (the last partial)
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2))) void input_xform_mix_p64(
+    const float* __restrict__ X4, float4* __restrict__ V, int M, int T, unsigned long long m0,
+    unsigned long long m1) {
+  extern __shared__ float4 lds4[];           // [kPBlk * 64]: [64][625] floats and a pad
+  const int nchunk = T / kPT;
+  long long lid = blockIdx.x;
+  const int t0 = (int)(lid % nchunk) * kPT;
+  lid /= nchunk;
+  const int m = (int)(lid % M), q4 = (int)(lid / M);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  {
+    // wave w copies 64-float4 blocks w, w + 8, ...; the last block's lanes
+    // past the run re-read its last float4 into the pad
+    const float4* src =
+        reinterpret_cast<const float4*>(X4 + (((size_t)q4 * M + m) * T + t0) * kPKB);
+    for (int blk = wave; blk < kPBlk; blk += 8) {
+      const int e = blk * 64 + lane;
+      __builtin_amdgcn_global_load_lds((const void*)(src + (e < kPRun4 ? e : kPRun4 - 1)),
+                                       (__attribute__((address_space(3))) void*)(lds4 + blk * 64),
+                                       16, 0, 0);
     }
-#pragma unroll
-    for (int j = 0; j < NS; ++j) {
-      float sacc = 0.0f;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) sacc = fmaf(cb[u], tr[j + kStride3 * u], sacc);
-      S[i][j] = sacc;
-    }
-    // one output row at a time: keeps the row's LDS reads from being
-    // hoisted across rows (register pressure); with level-1 digit 3 dead the
-    // kernel has the registers to let them overlap (0.714 -> 0.672 ms for
-    // the stage on the 31 x 31 layer)
-    if constexpr (!Q3) __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<0>();
   }
-  const int ob = q4 * 25 + slot;
-  if constexpr (STORE == kStorePlanar) {
-    static_assert(NO == 2 && Q3, "planar V: depth 4, level-1 digit 3 dead");
-    // groups at their live-list places; the work-group's resource starts at
-    // its level-4 row block (q4r), 20 row prefixes
-    const int np = __popcll(m0) + __popcll(m1);
-    const int q4r = q4 / 5, q4c = q4 - 5 * q4r;
-    const int lbase = prefix_rank(m0, m1, q4r * 20) * np;
-    const size_t plane = (size_t)M * T;
-    const auto pr = span_rsrc(reinterpret_cast<float4*>(reinterpret_cast<float*>(V) +
-                                                        (size_t)lbase * 9 * plane +
-                                                        (size_t)m * T + t0),
-                              (unsigned)(20 * np * 9 * plane * 4));
-    // ranks of the branch's first row and column prefixes; the other three
-    // follow from the live nibbles
-    const int br = q4r * 5 + q3r, bc = q4c * 5 + q3c;
-    const unsigned nr = prefix_nibble(m0, m1, br), nc = prefix_nibble(m0, m1, bc);
-    const int r0 = prefix_rank(m0, m1, 4 * br), c0 = prefix_rank(m0, m1, 4 * bc);
-    const unsigned ps = (unsigned)plane * 4u;
-    // byte offset of group (q2r, q2c)'s first point plane, for this lane
-    const unsigned gbase = (unsigned)(((r0 * np + c0 - lbase) * 9) * plane) * 4u + (unsigned)tl * 4u;
-    inner2_xform<false, true>(S, [=](int quad, float4 v) {
-      const int q2r = quad >> 4, q2c = (quad >> 2) & 3, q1r = quad & 3;
-      const bool on = (live >> (quad >> 2)) & 1u;
-      const int ir = __popc(nr & ((1u << q2r) - 1u)), ic = __popc(nc & ((1u << q2c) - 1u));
-      const unsigned o0 = gbase + (unsigned)((ir * np + ic) * 9 + 3 * q1r) * ps;
-      const unsigned off = on ? o0 : kDrop;
-      drop_store1(pr, off, v.x);
-      drop_store1(pr, off, v.y, ps);
-      drop_store1(pr, off, v.z, 2 * ps);
-    });
-  } else if constexpr (STORE == kStoreMasked) {
-    // the wave's 64 / TPW consecutive slots share a resource
-    constexpr int SPW = 64 / TPW;
-    const int slot0 = __builtin_amdgcn_readfirstlane(slot & ~(SPW - 1));
-    const auto rs = span_rsrc(V + (size_t)(q4 * 25 + slot0) * 64 * qstride + (size_t)m * T + t0,
-                              (unsigned)(SPW * 64 * qstride * 16));
-    const unsigned lane0 = (unsigned)(((size_t)(slot - slot0) * 64 * qstride + tl) * 16);
-    inner2_xform<false, Q3>(S, [&](int quad, float4 v) {
-      drop_store(rs, quad_live(live, q3, quad) ? lane0 + (unsigned)(quad * qstride * 16) : kDrop,
-                 v);
-    });
-  } else {
-    float4* vb = V + (size_t)ob * 64 * qstride + (size_t)m * T + t;
-    inner2_xform<false, Q3>(S, [&](int quad, float4 v) { vb[(size_t)quad * qstride] = v; });
-  }
-  }
+  __syncthreads();
+  const float* win = reinterpret_cast<const float*>(lds4) + lane * kPKB;
+  for (int slot = wave; slot < 25; slot += 8)
+    mix_branch<2, kStorePlanar, true, kPT, kPB>(win, slot, q4, m, t0, lane, V, M, T, 0, m0, m1,
+                                                1);
 }
 
 // ---- output transform -------------------------------------------------------
@@ -954,15 +1024,31 @@ hipError_t launch_input_xform_mix(const nwg_plan_info& g, const float* x, float*
                     (64LL / tpw) * 64 * qstride * 16 < (long long)kDrop;
   constexpr int A = kStoreAll, K = kStoreMasked;
   const auto fn =
-      g.mix_planar ? &input_xform_mix<2, kStorePlanar, true>
-      : no == 2    ? (q3 ? (mask ? &input_xform_mix<2, K, true> : &input_xform_mix<2, A, true>)
-                         : (mask ? &input_xform_mix<2, K, false> : &input_xform_mix<2, A, false>))
-                   : (q3 ? (mask ? &input_xform_mix<1, K, true> : &input_xform_mix<1, A, true>)
-                         : (mask ? &input_xform_mix<1, K, false> : &input_xform_mix<1, A, false>));
+      no == 2 ? (q3 ? (mask ? &input_xform_mix<2, K, true> : &input_xform_mix<2, A, true>)
+                    : (mask ? &input_xform_mix<2, K, false> : &input_xform_mix<2, A, false>))
+              : (q3 ? (mask ? &input_xform_mix<1, K, true> : &input_xform_mix<1, A, true>)
+                    : (mask ? &input_xform_mix<1, K, false> : &input_xform_mix<1, A, false>));
+  if (g.mix_planar) {
+    // 25 x 25 level-4 blocks, then 64 tiles per work-group
+    if (no != 2 || !q3 || g.M > 65535 || g.T % kPT) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(input_mix_l4<kPB>, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x,
+                       X4, g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t ldsp = (size_t)kPBlk * 64 * sizeof(float4);
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&input_xform_mix_p64),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)ldsp);
+    if (e != hipSuccess) return e;
+    const long long nwgp = (long long)(g.T / kPT) * g.M * 25;
+    if (nwgp > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(input_xform_mix_p64, dim3((unsigned)nwgp), dim3(512), ldsp, s, X4, V, g.M,
+                       (int)g.T, g.live_prefix[0], g.live_prefix[1]);
+    return hipGetLastError();
+  }
   if (no == 2) {
     if (g.M > 65535) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(input_mix_l4, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x, X4,
-                       g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T);
+    hipLaunchKernelGGL(input_mix_l4<kL3>, dim3((unsigned)g.T, (unsigned)g.M), dim3(256), 0, s, x,
+                       X4, g.M, g.H, g.W, g.pad, g.th, g.tw, (int)g.T);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
