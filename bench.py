@@ -504,7 +504,7 @@ def main():
         print(json.dumps(res, indent=1))
         return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); the path "
+        print(f"bench.py: the library runs on one GPU only (got --gpus {args.gpus}); the path "
               f"shards over output tiles or Winograd points, which is not built here.",
               file=sys.stderr)
         sys.exit(2)

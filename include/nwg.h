@@ -146,7 +146,7 @@ enum {
   NWG_EINVAL = -1,       /* bad argument (NULL pointer, bad shape) */
   NWG_ENOMEM = -2,       /* device allocation failed */
   NWG_EHIP = -3,         /* a HIP runtime call or kernel launch failed */
-  NWG_EUNSUPPORTED = -4  /* valid request this build does not handle */
+  NWG_EUNSUPPORTED = -4  /* valid request the library does not serve */
 };
 
 #define NWG_MAX_DEPTH 4   /* r <= 31 */
