@@ -505,7 +505,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py: the library runs on one GPU only (got --gpus {args.gpus}); the path "
-              f"shards over output tiles or Winograd points, which is not built here.",
+              f"would shard over output tiles or Winograd points, which the library does not do.",
               file=sys.stderr)
         sys.exit(2)
 
