@@ -185,10 +185,10 @@ def test_mixed_stages_match_cpu_oracle_chain(case):
 
 # the planar layout (mix_planar: depth 4, level-1 digit 3 dead, M % 128,
 # N % 128, T % 64): one 36 x 36 tile per image, T = 64 or 128, 128 x 64
-# blocks in one or two rows, r = 31, 27 and 23
+# blocks in one or two rows, r = 23 to 35, 128 or 256 input channels
 PLANAR = [(64, 128, 128, 36, 36, 31, 15), (64, 128, 256, 36, 36, 31, 15),
           (128, 128, 128, 36, 36, 23, 11), (16, 128, 128, 72, 72, 27, 13),
-          (64, 128, 128, 36, 36, 35, 17)]
+          (64, 128, 128, 36, 36, 35, 17), (64, 256, 128, 36, 36, 31, 15)]
 
 
 @pytest.mark.parametrize("case", PLANAR, ids=lambda c: "B%d_M%d_N%d_%dx%d_r%d_p%d" % c)
