@@ -62,6 +62,14 @@ def stage_bytes_flops(info: dict):
         if not info.get("mix_planar"):      # planar: U and V hold the live points only
             U, V = U // G * live * nq // 4, V // G * live * nq // 4
         Yh = Yh // G * live
+    # a dense F(2x2,3x3) chain with dead groups: its transforms write every
+    # group, the contraction reads and writes the live ones only, and the
+    # output transform reads only their Z
+    Uc, Vc, Zc = U, V, Yh
+    if (info.get("tile") == 0 and not dw and info["n"] >= 3 and info.get("live_np", 0) > 0
+            and not (info.get("fused_input") or info.get("fused_conv") or info.get("fused_output"))):
+        G, live = P // 16, info["live_groups"]
+        Uc, Vc, Zc = U // G * live, V // G * live, Yh // G * live
     if info.get("fused_output"):
         # input transform, then the output transform that forms the contraction
         return {"kernel_transform": (w + U, 0.0), "input_transform": (x + V, 0.0),
@@ -76,8 +84,8 @@ def stage_bytes_flops(info: dict):
                 "output_transform": (Yh + y, 0.0)}
     return {"kernel_transform": (w + U, 0.0),
             "input_transform": (x + V, 0.0),
-            "contraction": (U + V + Yh, flop),
-            "output_transform": (Yh + y, 0.0)}
+            "contraction": (Uc + Vc + Zc, flop),
+            "output_transform": (Zc + y, 0.0)}
 
 
 def source_hash(files):

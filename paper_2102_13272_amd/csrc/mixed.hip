@@ -52,26 +52,6 @@ __device__ __forceinline__ int prefix_rank(unsigned long long m0, unsigned long 
   return r;
 }
 
-// Live bits of the four axis prefixes 4 b .. 4 b + 3 (level-2 digit q2 =
-// 0..3 under level-3 block b = 5 q4 + q3 at depth 4, b = q3 at depth 3): a
-// nibble, which never straddles two 32-bit words of the mask.
-__device__ __forceinline__ unsigned prefix_nibble(unsigned long long m0, unsigned long long m1,
-                                                  int b) {
-  const int i = 4 * b;
-  const unsigned long long w = i < 64 ? m0 : m1;
-  const unsigned h = (i & 63) < 32 ? (unsigned)w : (unsigned)(w >> 32);
-  return (h >> (i & 31)) & 0xfu;
-}
-
-// The live groups (q2r, q2c) of a branch from its row and column nibbles,
-// as a 16-bit mask, bit 4 q2r + q2c.
-__device__ __forceinline__ unsigned nibble_live(unsigned nr, unsigned nc) {
-  unsigned live = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) live |= ((nr >> q) & 1u) ? nc << (4 * q) : 0u;
-  return live;
-}
-
 // The live groups (q2r, q2c) of outer branch (q4r, q4c, q3r, q3c) as a
 // 16-bit mask, bit 4 q2r + q2c (NO = 1: no level-4 digits).  A group is live
 // when its row prefix (q4r, q3r, q2r) and its column prefix (q4c, q3c, q2c)

@@ -50,6 +50,27 @@ __device__ __forceinline__ int select_bit(unsigned long long w0, unsigned long l
   return pos;
 }
 
+// Live bits of the four axis prefixes 4 b .. 4 b + 3 (level-2 digit q2 =
+// 0..3 under the block b of the digits above it: b = 5 q4 + q3 on the mixed
+// nest at depth 4, 4 q4 + q3 on four F(2,3) levels, q3 at depth 3): a
+// nibble, which never straddles two 32-bit words of the mask.
+__device__ __forceinline__ unsigned prefix_nibble(unsigned long long m0, unsigned long long m1,
+                                                  int b) {
+  const int i = 4 * b;
+  const unsigned long long w = i < 64 ? m0 : m1;
+  const unsigned h = (i & 63) < 32 ? (unsigned)w : (unsigned)(w >> 32);
+  return (h >> (i & 31)) & 0xfu;
+}
+
+// The live groups (q2r, q2c) of a branch from its row and column nibbles,
+// as a 16-bit mask, bit 4 q2r + q2c.
+__device__ __forceinline__ unsigned nibble_live(unsigned nr, unsigned nc) {
+  unsigned live = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) live |= ((nr >> q) & 1u) ? nc << (4 * q) : 0u;
+  return live;
+}
+
 // Entry i of a plan's group list (GroupMap): the group the contraction
 // computes as its i-th.
 __device__ __forceinline__ long long live_group(const GroupMap& m, long long i) {

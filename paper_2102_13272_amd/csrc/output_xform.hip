@@ -73,10 +73,13 @@ __global__ __launch_bounds__(256) void output_xform_tile(
 // (a_q = C of row q, for column half k).  Step 2 (partner q3r ^ 2):
 //   q3r < 2: y3[0] = u + u(partner)   q3r >= 2: y3[1] = w(partner) - w
 // which are the two A^T rows (1, 1, 1, 0) and (0, 1, -1, -1).
+// m0, m1: the plan's live digit prefixes (nwg_plan_info::live_prefix; both 0
+// when every group is live): the groups no tap reaches are not read (the
+// contraction does not write them; their Z is zero).
 template <int NLEV>
 __global__ __launch_bounds__(64) void output_xform_shfl(
     const float4* __restrict__ Z, float* __restrict__ y, int N, int Ho, int Wo, int th, int tw,
-    int T, long long gstride, int vec) {
+    int T, long long gstride, int vec, unsigned long long m0, unsigned long long m1) {
   constexpr int Mn = 1 << NLEV;
   constexpr int PASSES = NLEV == 4 ? 16 : 1;
   constexpr int NI4 = NLEV == 4 ? 2 : 1;
@@ -110,11 +113,16 @@ __global__ __launch_bounds__(64) void output_xform_shfl(
       // depth 4: two branches' 32 quad loads in flight at a time (240
       // registers, two wavefronts per SIMD); depth 3 has one pass and keeps
       // all four branches in flight
+      const int p4r = pass >> 2, p4c = pass & 3;
+      const unsigned nr = prefix_nibble(m0, m1, NLEV == 4 ? p4r * 4 + q3r : q3r);
 #pragma unroll (NLEV == 3 ? 4 : 2)
       for (int q3c = 0; q3c < 4; ++q3c) {
         const int branch = pass * 16 + q3r * 4 + q3c;
+        const unsigned live = (m0 | m1) == 0
+            ? 0xffffu
+            : nibble_live(nr, prefix_nibble(m0, m1, NLEV == 4 ? p4c * 4 + q3c : q3c));
         float po[4][4];
-        level2_reduce(zt + (size_t)branch * 16 * gstride, (size_t)gstride, po);
+        level2_reduce(zt + (size_t)branch * 16 * gstride, (size_t)gstride, po, live);
         const float c0 = at_coef(0, q3c), c1 = at_coef(1, q3c);
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
@@ -189,13 +197,16 @@ hipError_t launch_output_xform(const nwg_plan_info& g, const float* Zf, float* y
   if (g.n >= 3) {
     // float4 stores of y rows need 16-byte aligned rows
     const int vec = (g.Wo % 4 == 0 && ((uintptr_t)y & 15) == 0) ? 1 : 0;
+    // the dead groups of a dense F(2,3) chain (none elsewhere)
+    const bool dead = g.tile == NWG_TILE_F2X2_3X3 && !g.depthwise && g.live_np > 0;
+    const unsigned long long m0 = dead ? g.live_prefix[0] : 0, m1 = dead ? g.live_prefix[1] : 0;
     dim3 grid((unsigned)((g.T + 15) / 16), (unsigned)g.N);
     if (g.n == 3)
       hipLaunchKernelGGL(output_xform_shfl<3>, grid, dim3(64), 0, s, Z, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, gstride, vec);
+                         g.th, g.tw, T, gstride, vec, m0, m1);
     else
       hipLaunchKernelGGL(output_xform_shfl<4>, grid, dim3(64), 0, s, Z, y, g.N, g.Ho, g.Wo,
-                         g.th, g.tw, T, gstride, vec);
+                         g.th, g.tw, T, gstride, vec, m0, m1);
   } else {
     dim3 grid((unsigned)((g.T + 255) / 256), (unsigned)g.N);
     if (g.n == 2)

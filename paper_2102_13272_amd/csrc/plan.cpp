@@ -153,7 +153,8 @@ bool split_allowed(const nwg_plan_info& g) {
 
 GroupMap group_map(const nwg_plan_info& g) {
   GroupMap m{};
-  if (g.tile != NWG_TILE_MIX_F23_F33 || g.n < 3 || g.n - 1 > 3) return m;
+  const bool mix = g.tile == NWG_TILE_MIX_F23_F33;
+  if ((!mix && g.tile != NWG_TILE_F2X2_3X3) || g.depthwise || g.n < 3 || g.n - 1 > 3) return m;
   m.q3 = g.level1_live == 0x7 ? 1 : 0;
   if (g.live_np <= 0) return m;
   m.np = g.live_np;
@@ -163,7 +164,7 @@ GroupMap group_map(const nwg_plan_info& g) {
   // groups are ordered by (q_n^r, q_n^c, ..., q_2^r, q_2^c), each radix l_j
   int wc = 1;
   for (int d = 0; d < m.nd; ++d) {
-    m.rad[d] = d == 0 ? 4 : 5;                       // q_2: F(2,3); above: F(3,3)
+    m.rad[d] = mix && d > 0 ? 5 : 4;                 // F(2,3) digits; the mixed nest's F(3,3) above q_2
     m.wc[d] = wc;
     m.wr[d] = wc * m.rad[d];
     wc = m.wr[d] * m.rad[d];
@@ -243,15 +244,16 @@ int ld_geometry(int B, int M, int N, int H, int W, int r, int pad, int depthwise
 // and last rows and three in the others.
 unsigned g_row_digits(int l, int q) { return q == 0 ? 1u : q == l - 1 ? 4u : 7u; }
 
-// Mixed nest: which digit prefixes (q_n .. q_2) of an axis have a point whose
+// Which digit prefixes (q_n .. q_2) of an axis have a point whose
 // transformed kernel can be nonzero, and which level-1 digits q_1 any point
-// has that for.  Tap k < r reaches point (q_n .. q_1) when each digit of its
-// greedy split (outermost first, each at most 2, as the kernel transform
-// splits it) is one that the point's G row reaches.
-void mix_liveness(nwg_plan_info* g) {
+// has that for (the mixed nest, mix = true, or a chain of F(2,3) levels).
+// Tap k < r reaches point (q_n .. q_1) when each digit of its greedy split
+// (outermost first, each at most 2, as the kernel transform splits it) is
+// one that the point's G row reaches.
+void nest_liveness(nwg_plan_info* g, bool mix) {
   const int n = g->n;
   int l[NWG_MAX_DEPTH];
-  for (int j = 0; j < n; ++j) l[j] = j < 2 ? 4 : 5;   // level j + 1
+  for (int j = 0; j < n; ++j) l[j] = mix && j >= 2 ? 5 : 4;   // level j + 1
   int npref = 1;
   for (int j = 1; j < n; ++j) npref *= l[j];
   if (npref > 128) return;                            // beyond the masks: all groups live
@@ -285,9 +287,10 @@ void mix_liveness(nwg_plan_info* g) {
       q1mask |= reached;
     }
   }
-  // the kernels skip level-1 digit 3 only (the F(2,3) row that reaches tap
-  // digit 2 alone: no tap k < r has it when r is below the nest's taps)
-  g->level1_live = q1mask == 0x7u ? 0x7 : 0xf;
+  // the mixed nest's kernels skip level-1 digit 3 (the F(2,3) row that
+  // reaches tap digit 2 alone: no tap k < r has it when r is below the
+  // nest's taps); F(2,3) chains keep every level-1 digit and skip groups only
+  if (mix) g->level1_live = q1mask == 0x7u ? 0x7 : 0xf;
   const int lq = g->level1_live == 0x7 ? 3 : 4;
   if (live < npref) {
     g->live_np = live;
@@ -432,9 +435,14 @@ int geometry_tile(int B, int M, int N, int H, int W, int r, int pad, int tile, i
   g->live_groups = f33 || n == 0 ? 0 : g->P / 16;
   g->level1_live = f33 || n == 0 ? 0 : 0xf;
   if (mix && n >= 3) {
-    mix_liveness(g);
+    nest_liveness(g, true);
     mix_layout(g);
     g->workspace_bytes = g->u_bytes + g->v_bytes + zalloc_bytes(*g);
+  } else if (!mix && !f33 && !depthwise && n >= 3 && !g->fused_input && !g->fused_conv &&
+             !g->fused_output) {
+    // unfused dense F(2,3) chains: the contraction and the output transform
+    // skip the groups no tap reaches (their U is zero for every weight)
+    nest_liveness(g, false);
   }
   return NWG_OK;
 }

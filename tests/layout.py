@@ -107,13 +107,15 @@ def live_group_mask(info):
     """Per group (P/16, the library's order) whether it is live for the plan
     (nwg_plan_info live_np, live_prefix): its row prefix (q_n^r .. q_2^r) and
     its column prefix are both live.  A prefix's bit index has q_2 least
-    significant (radix 4), then q_3, ... (radix 5).  Every group when live_np
-    is 0."""
+    significant (radix 4), then q_3, ... (radix 5 on the mixed nest, 4 on a
+    chain of F(2x2,3x3) levels).  Every group when live_np is 0."""
+    from paper_2102_13272_amd import nwg
     G = info["P"] // 16
     if info["live_np"] == 0:
         return np.ones(G, dtype=bool)
     mask = int(info["live_prefix"][0]) | (int(info["live_prefix"][1]) << 64)
-    radix = [4] + [5] * (info["n"] - 2)             # levels 2 .. n
+    up = 5 if info["tile"] == nwg.NWG_TILE_MIX_F23_F33 else 4
+    radix = [4] + [up] * (info["n"] - 2)            # levels 2 .. n
     out = np.empty(G, dtype=bool)
     for g in range(G):
         rest, pr, pc, mul = g, 0, 0, 1

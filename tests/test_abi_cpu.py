@@ -374,15 +374,17 @@ def test_mixed_geometry_of_the_31x31_workload():
     assert f23["P"] * f23["T"] / (g["P"] * g["T"]) == pytest.approx(1.6384)
 
 
-def _oracle_live_prefixes(r):
+def _oracle_live_prefixes(r, tile=nwg.NWG_TILE_MIX_F23_F33):
     """Digit prefixes (q_n .. q_2, the outermost most significant) of the
-    mixed chain at kernel size r with a point whose row of the oracle's
-    kernel-transform matrix is nonzero over the r real taps."""
+    mixed chain (or the chain of F(2,3) levels) at kernel size r with a point
+    whose row of the oracle's kernel-transform matrix is nonzero over the r
+    real taps."""
     from oracle.mixed import mixed_levels, kernel_matrix, _digits
     from oracle.nested import toom_cook_base
     f23, f33 = base_f23(), toom_cook_base(3, 3, [0, 1, -1, 2])
-    n = nwg.plan_geometry(1, 1, 1, 64, 64, r, 0, nwg.NWG_TILE_MIX_F23_F33)["n"]
-    lv = mixed_levels([f23, f23] + [f33] * (n - 2), r)
+    n = nwg.plan_geometry(1, 1, 1, 64, 64, r, 0, tile)["n"]
+    up = f33 if tile == nwg.NWG_TILE_MIX_F23_F33 else f23
+    lv = mixed_levels([f23, f23] + [up] * (n - 2), r)
     KG = kernel_matrix(lv)
     rad = [b.l for b in lv.bases]                 # level 1 .. n
     live, q1 = set(), set()
@@ -412,6 +414,27 @@ def test_mixed_live_groups_are_the_oracle_kernel_rows_that_reach_a_real_tap(r):
     # has a nonzero kernel row (r below the nest's 39 or 15 taps)
     assert g["level1_live"] == sum(1 << q for q in q1)
     assert (g["level1_live"] == 0x7) == (r < g["Kn"])
+    if g["live_np"] == 0:
+        assert len(live) == npref and g["live_groups"] == g["P"] // 16
+        return
+    mask = g["live_prefix"][0] | (g["live_prefix"][1] << 64)
+    lib = {i for i in range(npref) if (mask >> i) & 1}
+    assert lib == live
+    assert g["live_np"] == len(live) and g["live_groups"] == len(live) ** 2
+
+
+@pytest.mark.parametrize("r", [5, 6, 7, 8, 9, 11, 13, 15, 16, 17, 20, 23, 29, 31])
+def test_f23_chain_live_groups_are_the_oracle_kernel_rows_that_reach_a_real_tap(r):
+    """Unfused dense chains of F(2x2,3x3) levels (depth 3 and 4) skip the
+    groups whose transformed kernel is zero for every w; the prefix mask must
+    be the set of prefixes with a nonzero row of the oracle's kernel-transform
+    matrix, and every level-1 digit stays (F(2,3) chains skip groups only)."""
+    g = nwg.plan_geometry(2, 8, 8, 64, 64, r, r // 2)
+    assert g["tile"] == nwg.NWG_TILE_F2X2_3X3 and g["level1_live"] == 0xf
+    if g["n"] < 3 or g["fused_conv"] or g["fused_input"] or g["fused_output"]:
+        assert g["live_np"] == 0 and g["live_groups"] == g["P"] // 16
+        return
+    live, npref, _ = _oracle_live_prefixes(r, nwg.NWG_TILE_F2X2_3X3)
     if g["live_np"] == 0:
         assert len(live) == npref and g["live_groups"] == g["P"] // 16
         return

@@ -33,23 +33,28 @@ def test_stage_bytes_are_the_plan_buffers_and_the_layer_tensors(tile):
     sb = bench.stage_bytes_flops(g)
     x, y, w = 4 * B * M * H * W, 4 * B * N * H * W, 4 * N * M * r * r
     # the contraction moves 4 bytes per U and V value once, and one Z value
-    # per four points (the level-1 output fold), over the groups it computes:
-    # every group on F(2x2,3x3); on the mixed nest the 72^2 live ones of
-    # 100^2, three of their four quads (level-1 row digit 3 is dead at
-    # r = 31), and 3 x 3 of their 16 points multiplied
+    # per four points (the level-1 output fold), over the groups it computes,
+    # the live ones (a tap reaches them): on four F(2x2,3x3) levels 54^2 of
+    # 64^2, every point of each multiplied; on the mixed nest 72^2 of 100^2,
+    # three of their four quads (level-1 row digit 3 is dead at r = 31), and
+    # 3 x 3 of their 16 points multiplied
     mix = tile == nwg.NWG_TILE_MIX_F23_F33
     G, npt = g["live_groups"], 9 if mix else 16
-    assert G == (72 * 72 if mix else g["P"] // 16)
+    assert G == (72 * 72 if mix else 54 * 54) and g["P"] // 16 == (100 * 100 if mix else 64 * 64)
     assert g["level1_live"] == (0x7 if mix else 0xf) and g["mix_planar"] == int(mix)
-    # the mixed nest's planar U and V hold the 9 live points of each live group
-    U, V, Z = 4 * npt * G * M * N, 4 * npt * G * M * g["T"], 4 * 4 * G * N * g["T"]
+    # the mixed nest's planar U and V hold the 9 live points of each live
+    # group; the F(2,3) plan's U and V hold every group, its transforms write
+    # them all
+    Ga = G if mix else g["P"] // 16
+    U, V = 4 * npt * Ga * M * N, 4 * npt * Ga * M * g["T"]
+    Uc, Vc, Z = 4 * npt * G * M * N, 4 * npt * G * M * g["T"], 4 * 4 * G * N * g["T"]
     assert (g["u_bytes"], g["v_bytes"], g["yhat_bytes"]) == (
         U, V, 4 * (g["P"] // 4) * N * g["T"])
     assert sb["kernel_transform"] == (w + U, 0.0)
     assert sb["input_transform"] == (x + V, 0.0)
     assert sb["output_transform"] == (Z + y, 0.0)
     b, f = sb["contraction"]
-    assert b == U + V + Z and f == g["contract_flop"] == 2.0 * npt * G * M * N * g["T"]
+    assert b == Uc + Vc + Z and f == g["contract_flop"] == 2.0 * npt * G * M * N * g["T"]
 
 
 def test_depth0_stage_bytes_are_a_channel_gemm():
