@@ -468,6 +468,16 @@ double unfused_step_seconds(const nwg_plan_info& g) {
   auto up = [](double v, double q) { return std::ceil(v / q) * q; };
   double pts = (double)g.P, U = (double)g.u_bytes, V = (double)g.v_bytes,
          Z = (double)g.yhat_bytes, scratch = 0.0, scale = 1.0;
+  double Vc = V;                                      // V as the contraction reads it
+  if (g.tile == NWG_TILE_F2X2_3X3 && g.live_np > 0) {
+    // the contraction and the output transform visit the live groups only;
+    // the transforms write every group's U and V
+    const double live = (double)g.live_groups / (double)(g.P / 16);
+    pts *= live;
+    U *= live;
+    Vc *= live;
+    Z *= live;
+  }
   if (g.tile == NWG_TILE_MIX_F23_F33 && g.n >= 3) {
     const double G = (double)(g.P / 16), live = (double)g.live_groups;
     const bool q3 = g.level1_live == 0x7;
@@ -476,14 +486,15 @@ double unfused_step_seconds(const nwg_plan_info& g) {
       U = U / G * live * (q3 ? 0.75 : 1.0);
       V = V / G * live * (q3 ? 0.75 : 1.0);
     }
+    Vc = V;
     Z = Z / G * live;
     if (g.n == 4)   // X4 (level-4 input blocks) and Z3 (level-3 output blocks), each written and read
       scratch = 2.0 * 4.0 * 25.0 * (double)g.T * ((double)kMixL3 * kMixL3 * g.M + 144.0 * g.N);
-    scale = g.n == 4 ? 1.47 : 1.3;
+    scale = g.n == 4 ? 1.47 : 1.22;
   }
   const double flop = 2.0 * pts * up(g.M, 32) * up(g.N, 64) * up((double)g.T, 64);
   const double x = 4.0 * g.B * g.M * g.H * g.W, y = 4.0 * g.B * g.N * (double)g.Ho * g.Wo;
-  const double cb = U + V + Z;
+  const double cb = U + Vc + Z;
   const double tc = flop / kMfma > cb / kBw ? flop / kMfma : cb / kBw;
   return scale * (tc + (x + V) / kBw + (Z + y) / kBw + scratch / kBw);
 }
