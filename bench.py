@@ -62,14 +62,18 @@ def stage_bytes_flops(info: dict):
         if not info.get("mix_planar"):      # planar: U and V hold the live points only
             U, V = U // G * live * nq // 4, V // G * live * nq // 4
         Yh = Yh // G * live
-    # a dense F(2x2,3x3) chain with dead groups: its transforms write every
-    # group, the contraction reads and writes the live ones only, and the
-    # output transform reads only their Z
-    Uc, Vc, Zc = U, V, Yh
+    # a dense F(2x2,3x3) chain with dead groups: the kernel transform writes
+    # every group, the input transform the live ones (while a wavefront's
+    # four level-3 branches of V span at most 2^30 bytes), the contraction
+    # reads and writes the live ones only, and the output transform reads
+    # only their Z
+    Uc, Vc, Zc, Vw = U, V, Yh, V
     if (info.get("tile") == 0 and not dw and info["n"] >= 3 and info.get("live_np", 0) > 0
             and not (info.get("fused_input") or info.get("fused_conv") or info.get("fused_output"))):
         G, live = P // 16, info["live_groups"]
         Uc, Vc, Zc = U // G * live, V // G * live, Yh // G * live
+        if 256 * info["M"] * info["T"] * 16 <= 1 << 30:
+            Vw = Vc
     if info.get("fused_output"):
         # input transform, then the output transform that forms the contraction
         return {"kernel_transform": (w + U, 0.0), "input_transform": (x + V, 0.0),
@@ -83,7 +87,7 @@ def stage_bytes_flops(info: dict):
                 "contraction": (x + U + Yh, flop),
                 "output_transform": (Yh + y, 0.0)}
     return {"kernel_transform": (w + U, 0.0),
-            "input_transform": (x + V, 0.0),
+            "input_transform": (x + Vw, 0.0),
             "contraction": (Uc + Vc + Zc, flop),
             "output_transform": (Zc + y, 0.0)}
 

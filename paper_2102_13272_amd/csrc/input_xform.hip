@@ -166,7 +166,7 @@ __global__ __launch_bounds__(256) void input_xform_d2(
 template <int NLEV, bool SPLIT>
 __global__ __launch_bounds__(256) void input_xform_tiles(
     const float* __restrict__ x, float4* __restrict__ V, int M, int H, int W, int pad, int th,
-    int tw, int T, long long qstride, int q4_0, int nq4) {
+    int tw, int T, long long qstride, int q4_0, int nq4, unsigned long long live) {
   constexpr int Mn = 1 << NLEV;
   constexpr int L3 = 22;                     // window side left for levels 1..3
   constexpr int WS = L3 * L3 + 1;            // odd window stride: 16 tiles -> 16 banks
@@ -285,7 +285,24 @@ __global__ __launch_bounds__(256) void input_xform_tiles(
     }
   // 256-point block of this branch: (q4r, q4c, q3r, q3c) at depth 4, (q3r, q3c) at depth 3
   const int branch = q4 * 16 + slot;
-  inner2_store<SPLIT>(S, V + (size_t)branch * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+  if (live == 0) {
+    inner2_store<SPLIT>(S, V + (size_t)branch * 64 * qstride + (size_t)m * T + t, (size_t)qstride);
+    return;
+  }
+  // only the live groups (q2r, q2c) of the branch are written (the groups
+  // no tap reaches are never read): one buffer resource over the wave's
+  // four branches, (q3r, q3c = 0..3), dead quads' lanes sent past its range
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const unsigned g16 = nibble_live(prefix_nibble(live, 0, NLEV == 4 ? 4 * q4r + q3r : q3r),
+                                   prefix_nibble(live, 0, NLEV == 4 ? 4 * q4c + q3c : q3c));
+  const __amdgpu_buffer_rsrc_t rs =
+      span_rsrc(V + (size_t)(q4 * 16 + 4 * wv) * 64 * qstride, (unsigned)(256 * qstride * 16));
+  const unsigned lane0 = (unsigned)((((size_t)(slot & 3) * 64) * qstride + (size_t)m * T + t) * 16);
+  const unsigned qs = (unsigned)(qstride * 16);
+  inner2_xform<SPLIT>(S, [&](int quad, float4 v) {
+    const int grp = (quad >> 4) * 4 + ((quad >> 2) & 3);      // 4 q2r + q2c
+    drop_store(rs, ((g16 >> grp) & 1u) ? lane0 + (unsigned)quad * qs : kDrop, v);
+  });
 }
 
 }  // namespace
@@ -314,9 +331,16 @@ hipError_t launch_input_xform(const nwg_plan_info& g, const float* x, float* Vf,
     const long long nwg = (g.T + 15) / 16 * g.M * nq4;
     if (nwg > 0x7fffffffLL) return hipErrorInvalidValue;
     dim3 grid((unsigned)nwg);
+    // dense F(2,3) chains write the live groups only, when a wave's four
+    // branches (256 quads of M T float4) span at most 2^30 bytes
+    const unsigned long long live =
+        g.tile == NWG_TILE_F2X2_3X3 && g.live_np > 0 && g.ld_c == 0 &&
+                256.0 * (double)qstride * 16.0 <= (double)(1u << 30)
+            ? g.live_prefix[0]
+            : 0ull;
 #define NWG_TILES(L, SP)                                                                       \
   hipLaunchKernelGGL((input_xform_tiles<L, SP>), grid, dim3(256), lds, s, x, V, g.M, g.H, g.W,  \
-                     g.pad, g.th, g.tw, T, qstride, q4_0, nq4)
+                     g.pad, g.th, g.tw, T, qstride, q4_0, nq4, live)
     if (g.n == 3) {
       if (split) NWG_TILES(3, true); else NWG_TILES(3, false);
     } else {

@@ -64,30 +64,6 @@ __device__ __forceinline__ unsigned branch_live(unsigned long long m0, unsigned 
                      prefix_nibble(m0, m1, NO == 2 ? q4c * 5 + q3c : q3c));
 }
 
-// Stores of the live quads only, without a branch per quad (branches
-// around the 64 stores of an unrolled branch transform make the compiler
-// spill): every quad goes through a raw buffer resource that spans the
-// wave's branches, and the lanes of a dead quad (its group dead, or its
-// level-1 row digit q1r = 3 when q3 is set) pass an offset past the range,
-// which the hardware drops with no memory traffic.
-constexpr unsigned kDrop = 0x80000000u;     // above every span (host checks)
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t span_rsrc(float4* base, unsigned bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)bytes, 0x00020000);
-}
-
-__device__ __forceinline__ void drop_store(__amdgpu_buffer_rsrc_t r, unsigned off, float4 v) {
-  typedef unsigned u4 __attribute__((ext_vector_type(4)));
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4, v), r, (int)off, 0, 0);
-}
-
-// soff: a wave-uniform byte offset added to off (kDrop + soff stays past
-// every span: the host keeps spans and soff below 2^30)
-__device__ __forceinline__ void drop_store1(__amdgpu_buffer_rsrc_t r, unsigned off, float v,
-                                            unsigned soff = 0) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)off, (int)soff, 0);
-}
-
 // How a transform stores its points: every quad of a live branch, the live
 // quads only (quad layout), or the live points of the live groups in the
 // planar layout (nwg_plan_info::mix_planar).

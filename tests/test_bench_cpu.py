@@ -43,15 +43,15 @@ def test_stage_bytes_are_the_plan_buffers_and_the_layer_tensors(tile):
     assert G == (72 * 72 if mix else 54 * 54) and g["P"] // 16 == (100 * 100 if mix else 64 * 64)
     assert g["level1_live"] == (0x7 if mix else 0xf) and g["mix_planar"] == int(mix)
     # the mixed nest's planar U and V hold the 9 live points of each live
-    # group; the F(2,3) plan's U and V hold every group, its transforms write
-    # them all
+    # group; the F(2,3) plan's U and V hold every group, its kernel transform
+    # writes them all and its input transform the live groups' V
     Ga = G if mix else g["P"] // 16
     U, V = 4 * npt * Ga * M * N, 4 * npt * Ga * M * g["T"]
     Uc, Vc, Z = 4 * npt * G * M * N, 4 * npt * G * M * g["T"], 4 * 4 * G * N * g["T"]
     assert (g["u_bytes"], g["v_bytes"], g["yhat_bytes"]) == (
         U, V, 4 * (g["P"] // 4) * N * g["T"])
     assert sb["kernel_transform"] == (w + U, 0.0)
-    assert sb["input_transform"] == (x + V, 0.0)
+    assert sb["input_transform"] == (x + Vc, 0.0)
     assert sb["output_transform"] == (Z + y, 0.0)
     b, f = sb["contraction"]
     assert b == Uc + Vc + Z and f == g["contract_flop"] == 2.0 * npt * G * M * N * g["T"]
