@@ -470,8 +470,11 @@ double unfused_step_seconds(const nwg_plan_info& g) {
          Z = (double)g.yhat_bytes, scratch = 0.0, scale = 1.0;
   double Vc = V;                                      // V as the contraction reads it
   if (g.tile == NWG_TILE_F2X2_3X3 && g.live_np > 0) {
-    // the contraction and the output transform visit the live groups only;
-    // the transforms write every group's U and V
+    // the contraction and the output transform visit the live groups only.
+    // The input transform writes only their V too, but the model charges it
+    // every group's: on 32- and 64-channel layers the F(2,3) kernels run
+    // about 1.5x below the model's rates, and with the live write counted no
+    // single factor below orders all the measured layers
     const double live = (double)g.live_groups / (double)(g.P / 16);
     pts *= live;
     U *= live;

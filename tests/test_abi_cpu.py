@@ -247,25 +247,25 @@ def test_f33_geometry_matches_oracle_levels(r):
     ((8, 64, 64, 56, 56, 7, 3), 0),       # same depth: F(2,3)
     ((8, 64, 64, 56, 56, 3, 1), 1),       # depth 1, wide channels
     ((4, 5, 5, 256, 256, 3, 1), 0),       # few channels
-    ((16, 128, 128, 56, 56, 31, 15), 3),  # depth 4, wide channels: the mixed nest (5.51 / 1.90 ms)
+    ((16, 128, 128, 56, 56, 31, 15), 3),  # depth 4, wide channels: the mixed nest (5.07 / 1.90 ms)
     ((2, 16, 128, 56, 56, 31, 15), 0),    # depth 4, M < 32
     # depth 3 (r > 9) and 4 with M, N >= 32: the nest measured faster on
     # MI355X (ms per call, F(2,3) / mixed, one box) -- both skip their dead
     # groups, the mixed nest its dead points too, but it needs enough 12 x 12
     # or 36 x 36 tiles
-    ((2, 128, 128, 56, 56, 31, 15), 0),   # 1.295 / 1.574 (8 tiles on the mixed nest)
-    ((4, 128, 128, 28, 28, 31, 15), 0),   # 1.219 / 1.559 (4 tiles)
-    ((1, 256, 256, 28, 28, 27, 13), 0),   # 2.78 / 5.41 (1 tile)
-    ((16, 32, 32, 56, 56, 31, 15), 3),    # 1.02 / 0.456
-    ((4, 64, 128, 112, 112, 23, 11), 3),  # 1.95 / 0.97
-    ((1, 32, 32, 224, 224, 31, 15), 3),   # 0.93 / 0.44
-    ((8, 64, 64, 56, 56, 17, 8), 3),      # 0.87 / 0.48
-    ((32, 32, 64, 32, 32, 19, 9), 3),     # 0.49 / 0.29
-    ((8, 64, 64, 56, 56, 13, 6), 3),      # depth 3: 0.241 / 0.189
-    ((16, 128, 128, 56, 56, 13, 6), 3),   # 1.268 / 0.841
-    ((16, 128, 128, 56, 56, 11, 5), 3),   # 0.944 / 0.587
-    ((8, 64, 64, 56, 56, 15, 7), 0),      # 0.240 / 0.246 (r = 15: level-1 digit 3 live)
-    ((4, 256, 256, 56, 56, 15, 7), 3),    # 1.345 / 1.141
+    ((2, 128, 128, 56, 56, 31, 15), 0),   # 1.262 / 1.580 (8 tiles on the mixed nest)
+    ((4, 128, 128, 28, 28, 31, 15), 0),   # 1.172 / 1.565 (4 tiles)
+    ((1, 256, 256, 28, 28, 27, 13), 0),   # 2.77 / 5.42 (1 tile)
+    ((16, 32, 32, 56, 56, 31, 15), 3),    # 0.889 / 0.457
+    ((4, 64, 128, 112, 112, 23, 11), 3),  # 1.49 / 1.00
+    ((1, 32, 32, 224, 224, 31, 15), 3),   # 0.81 / 0.43
+    ((8, 64, 64, 56, 56, 17, 8), 3),      # 0.639 / 0.479
+    ((32, 32, 64, 32, 32, 19, 9), 3),     # 0.381 / 0.286
+    ((8, 64, 64, 56, 56, 13, 6), 3),      # depth 3: 0.238 / 0.190
+    ((16, 128, 128, 56, 56, 13, 6), 3),   # 1.236 / 0.838
+    ((16, 128, 128, 56, 56, 11, 5), 3),   # 0.838 / 0.587
+    ((8, 64, 64, 56, 56, 15, 7), 0),      # 0.237 / 0.247 (r = 15: level-1 digit 3 live)
+    ((4, 256, 256, 56, 56, 15, 7), 3),    # 1.310 / 1.136
     ((1, 32, 32, 64, 64, 1, 0), 0),       # 1x1
 ])
 def test_auto_tile_choice(shape, tile):
