@@ -39,7 +39,13 @@
  * level1_live): the stage calls neither write nor read the dead groups'
  * U, V and Z, nor the quads of a dead level-1 row digit; with mix_planar
  * set, U and V hold only the live points, in the planar layout described
- * at that field.  Z keeps the layout above.
+ * at that field.  Z keeps the layout above.  Unfused dense F(2x2,3x3)
+ * plans at depth 3 and 4 with live_np > 0 skip their dead groups the same
+ * way, keeping the layout above: the kernel transform writes every group
+ * of U, the input transform writes only the live groups of V (every group
+ * when 256 M T quads of 16 bytes exceed 2^30 bytes), the contraction reads
+ * only the live groups of U and V and writes only their Z, and the output
+ * transform reads only their Z.
  *
  * Ownership: the caller owns x, w, y, U/V/Z passed to stage calls, and
  * the stream; they must stay valid until the work queued on the stream has
